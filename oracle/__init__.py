@@ -1,0 +1,277 @@
+"""fp64 CPU oracle for the Two-Bit Networks hot path (arXiv 1701.00485).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the CPU-baseline leg of
+the benchmark may import this package; the product library never does.  The oracle
+shares no code with the GPU library.  The numerics live in ``tbn_oracle.c`` (plain fp64
+loops, one function per step of the method, each citing the passage it follows); this
+module only marshals numpy arrays through ctypes.
+
+Sections cited: Sec. 2 Eq. (1) approximate convolution, Eq. (3) discretisation,
+Eq. (4)-(5) optimal scale; Sec. 3 Algorithm 1 (quantise, forward, backward, update);
+Sec. 4 optimiser settings.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tbn_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (fp64, OpenMP, no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+             "-fno-fast-math", "-ffp-contract=off", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    p = ctypes.c_void_p
+    i64 = ctypes.c_int64
+    lib.orc_round_bf16.argtypes = [p, i64, p]
+    lib.orc_round_bf16.restype = None
+    lib.orc_quantize.argtypes = [p, i64, i64, p, p, p, p, p, p, p]
+    lib.orc_quantize.restype = ctypes.c_int
+    lib.orc_packed_words.argtypes = [i64, i64]
+    lib.orc_packed_words.restype = i64
+    lib.orc_pack.argtypes = [p, i64, i64, p]
+    lib.orc_pack.restype = ctypes.c_int
+    lib.orc_unpack.argtypes = [p, i64, i64, p]
+    lib.orc_unpack.restype = ctypes.c_int
+    lib.orc_out_dims.argtypes = [p, p, p]
+    lib.orc_out_dims.restype = ctypes.c_int
+    lib.orc_conv_fwd.argtypes = [p, p, p, p, ctypes.c_int, p]
+    lib.orc_conv_fwd.restype = ctypes.c_int
+    lib.orc_conv_bwd_data.argtypes = [p, p, p, p, p]
+    lib.orc_conv_bwd_data.restype = ctypes.c_int
+    lib.orc_conv_bwd_weight.argtypes = [p, p, p, p]
+    lib.orc_conv_bwd_weight.restype = ctypes.c_int
+    for name in ("orc_conv_fwd_sampled_bf16", "orc_conv_bwd_data_sampled_bf16"):
+        getattr(lib, name).argtypes = [p, p, p, p, p, i64, p]
+        getattr(lib, name).restype = ctypes.c_int
+    lib.orc_conv_bwd_weight_sampled_bf16.argtypes = [p, p, p, p, i64, p]
+    lib.orc_conv_bwd_weight_sampled_bf16.restype = ctypes.c_int
+    lib.orc_sgd.argtypes = [p, p, p, i64, ctypes.c_double, ctypes.c_double, ctypes.c_double]
+    lib.orc_sgd.restype = None
+    _lib = lib
+    return lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+class ConvDesc:
+    """Geometry of one convolution (NHWC activations, [K][R][S][C] filters)."""
+
+    __slots__ = ("n", "h", "w", "c", "k", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w")
+
+    def __init__(self, n, h, w, c, k, r, s, stride=1, pad=0, stride_w=None, pad_w=None):
+        self.n, self.h, self.w, self.c, self.k, self.r, self.s = n, h, w, c, k, r, s
+        self.stride_h = stride
+        self.stride_w = stride if stride_w is None else stride_w
+        self.pad_h = pad
+        self.pad_w = pad if pad_w is None else pad_w
+
+    def as_array(self) -> np.ndarray:
+        return np.array([self.n, self.h, self.w, self.c, self.k, self.r, self.s,
+                         self.stride_h, self.stride_w, self.pad_h, self.pad_w], dtype=np.int32)
+
+    def out_dims(self):
+        d = self.as_array()
+        p = np.zeros(1, np.int32)
+        q = np.zeros(1, np.int32)
+        if _load().orc_out_dims(_ptr(d), _ptr(p), _ptr(q)) != 0:
+            raise OracleError("invalid convolution geometry")
+        return int(p[0]), int(q[0])
+
+
+# --------------------------------------------------------------------------------------
+# bf16 rounding of fp32 inputs (IEEE round-to-nearest-even on the dropped 16 bits)
+# --------------------------------------------------------------------------------------
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    x = _c(x, np.float32)
+    out = np.empty(x.shape, np.float64)
+    _load().orc_round_bf16(_ptr(x), x.size, _ptr(out))
+    return out
+
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Exact widening of raw bf16 bit patterns (uint16) to float64."""
+    b = np.asarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+# --------------------------------------------------------------------------------------
+# Sec. 2, Eq. (3)-(5): quantisation
+# --------------------------------------------------------------------------------------
+class Quantized:
+    __slots__ = ("codes", "alpha64", "alpha", "b1_size", "b2_size", "b1_sum", "b2_sum")
+
+
+def quantize(w: np.ndarray) -> Quantized:
+    """w: [K][n] fp32 real weights (one filter per row)."""
+    w = _c(w, np.float32)
+    if w.ndim != 2:
+        raise OracleError("quantize expects [K][n]")
+    K, n = w.shape
+    out = Quantized()
+    out.codes = np.zeros((K, n), np.int8)
+    out.alpha64 = np.zeros(K, np.float64)
+    out.alpha = np.zeros(K, np.float32)
+    out.b1_size = np.zeros(K, np.int64)
+    out.b2_size = np.zeros(K, np.int64)
+    out.b1_sum = np.zeros(K, np.float64)
+    out.b2_sum = np.zeros(K, np.float64)
+    st = _load().orc_quantize(_ptr(w), K, n, _ptr(out.codes), _ptr(out.alpha64),
+                              _ptr(out.alpha), _ptr(out.b1_size), _ptr(out.b2_size),
+                              _ptr(out.b1_sum), _ptr(out.b2_sum))
+    if st == 1:
+        raise OracleError("non-finite weight: outside the method's domain")
+    if st != 0:
+        raise OracleError("quantize: bad shape")
+    return out
+
+
+def packed_words(K: int, n: int) -> int:
+    return int(_load().orc_packed_words(K, n))
+
+
+def pack(codes: np.ndarray) -> np.ndarray:
+    codes = _c(codes, np.int8)
+    K, n = codes.shape
+    words = np.zeros(packed_words(K, n), np.uint32)
+    if _load().orc_pack(_ptr(codes), K, n, _ptr(words)) != 0:
+        raise OracleError("pack: codes outside {-2,-1,1,2} or bad shape")
+    return words
+
+
+def unpack(words: np.ndarray, K: int, n: int) -> np.ndarray:
+    words = _c(words, np.uint32)
+    if words.size != packed_words(K, n):
+        raise OracleError("unpack: wrong word count")
+    codes = np.zeros((K, n), np.int8)
+    if _load().orc_unpack(_ptr(words), K, n, _ptr(codes)) != 0:
+        raise OracleError("unpack: bad shape")
+    return codes
+
+
+# --------------------------------------------------------------------------------------
+# Sec. 2 Eq. (1) and Sec. 3 Algorithm 1: convolutions with the two-bit filters
+# --------------------------------------------------------------------------------------
+def conv_fwd(desc: ConvDesc, x: np.ndarray, codes: np.ndarray, alpha: np.ndarray,
+             form: int = 0) -> np.ndarray:
+    """x NHWC fp64 (exact values the GPU consumed); codes [K][R][S][C] (or [K][n])."""
+    P, Q = desc.out_dims()
+    x = _c(x, np.float64)
+    codes = _c(codes, np.int8)
+    alpha = _c(alpha, np.float64)
+    if x.size != desc.n * desc.h * desc.w * desc.c or codes.size != desc.k * desc.r * desc.s * desc.c:
+        raise OracleError("conv_fwd: operand sizes do not match the geometry")
+    y = np.zeros((desc.n, P, Q, desc.k), np.float64)
+    d = desc.as_array()
+    if _load().orc_conv_fwd(_ptr(d), _ptr(x), _ptr(codes), _ptr(alpha), form, _ptr(y)) != 0:
+        raise OracleError("conv_fwd failed")
+    return y
+
+
+def conv_bwd_data(desc: ConvDesc, dy: np.ndarray, codes: np.ndarray, alpha: np.ndarray) -> np.ndarray:
+    P, Q = desc.out_dims()
+    dy = _c(dy, np.float64)
+    codes = _c(codes, np.int8)
+    alpha = _c(alpha, np.float64)
+    if dy.size != desc.n * P * Q * desc.k:
+        raise OracleError("conv_bwd_data: dy size does not match the geometry")
+    dx = np.zeros((desc.n, desc.h, desc.w, desc.c), np.float64)
+    d = desc.as_array()
+    if _load().orc_conv_bwd_data(_ptr(d), _ptr(dy), _ptr(codes), _ptr(alpha), _ptr(dx)) != 0:
+        raise OracleError("conv_bwd_data failed")
+    return dx
+
+
+def conv_bwd_weight(desc: ConvDesc, x: np.ndarray, dy: np.ndarray) -> np.ndarray:
+    P, Q = desc.out_dims()
+    x = _c(x, np.float64)
+    dy = _c(dy, np.float64)
+    if dy.size != desc.n * P * Q * desc.k or x.size != desc.n * desc.h * desc.w * desc.c:
+        raise OracleError("conv_bwd_weight: operand sizes do not match the geometry")
+    dw = np.zeros((desc.k, desc.r, desc.s, desc.c), np.float64)
+    d = desc.as_array()
+    if _load().orc_conv_bwd_weight(_ptr(d), _ptr(x), _ptr(dy), _ptr(dw)) != 0:
+        raise OracleError("conv_bwd_weight failed")
+    return dw
+
+
+def conv_fwd_sampled(desc, x_bits, codes, alpha, idx):
+    x_bits = _c(x_bits, np.uint16)
+    codes = _c(codes, np.int8)
+    alpha = _c(alpha, np.float64)
+    idx = _c(idx, np.int64)
+    out = np.zeros(idx.size, np.float64)
+    d = desc.as_array()
+    if _load().orc_conv_fwd_sampled_bf16(_ptr(d), _ptr(x_bits), _ptr(codes), _ptr(alpha),
+                                         _ptr(idx), idx.size, _ptr(out)) != 0:
+        raise OracleError("conv_fwd_sampled failed")
+    return out
+
+
+def conv_bwd_data_sampled(desc, dy_bits, codes, alpha, idx):
+    dy_bits = _c(dy_bits, np.uint16)
+    codes = _c(codes, np.int8)
+    alpha = _c(alpha, np.float64)
+    idx = _c(idx, np.int64)
+    out = np.zeros(idx.size, np.float64)
+    d = desc.as_array()
+    if _load().orc_conv_bwd_data_sampled_bf16(_ptr(d), _ptr(dy_bits), _ptr(codes), _ptr(alpha),
+                                              _ptr(idx), idx.size, _ptr(out)) != 0:
+        raise OracleError("conv_bwd_data_sampled failed")
+    return out
+
+
+def conv_bwd_weight_sampled(desc, x_bits, dy_bits, idx):
+    x_bits = _c(x_bits, np.uint16)
+    dy_bits = _c(dy_bits, np.uint16)
+    idx = _c(idx, np.int64)
+    out = np.zeros(idx.size, np.float64)
+    d = desc.as_array()
+    if _load().orc_conv_bwd_weight_sampled_bf16(_ptr(d), _ptr(x_bits), _ptr(dy_bits),
+                                                _ptr(idx), idx.size, _ptr(out)) != 0:
+        raise OracleError("conv_bwd_weight_sampled failed")
+    return out
+
+
+# --------------------------------------------------------------------------------------
+# Algorithm 1 update step with the Sec. 4 optimiser
+# --------------------------------------------------------------------------------------
+def sgd(w, v, g, eta, mu=0.9, lam=1e-4):
+    """Returns (w_new, v_new) in fp64; inputs are not modified."""
+    w = np.array(w, dtype=np.float64, copy=True).ravel()
+    v = np.array(v, dtype=np.float64, copy=True).ravel()
+    g = _c(g, np.float64).ravel()
+    _load().orc_sgd(_ptr(w), _ptr(v), _ptr(g), w.size, float(eta), float(mu), float(lam))
+    return w, v

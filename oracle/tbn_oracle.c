@@ -1,0 +1,430 @@
+/*
+ * tbn_oracle.c -- plain, slow, fp64 CPU oracle for the Two-Bit Networks hot path
+ * (Meng, Gu, Zhang, Wu, "Two-Bit Networks for Deep Learning on Resource-Constrained
+ * Embedded Devices", arXiv 1701.00485).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the checker, not the product: only the test
+ * suite, the smoke check and the CPU-baseline leg of the benchmark may load it.  It
+ * shares no code, header, table or helper with the GPU library; the only thing both
+ * sides see is the seeded input arrays.
+ *
+ * Every routine is the plain definition of what it computes, written with direct loops
+ * in double precision, in the order the paper states the steps:
+ *   - discretisation                      : Sec. 2, Eq. (3)
+ *   - optimal per-filter scale            : Sec. 2, Eq. (4)-(5)
+ *   - approximate convolution             : Sec. 2, Eq. (1); Sec. 3, Algorithm 1 (forward)
+ *   - backward passes through the approximate filters, gradient w.r.t. the approximate
+ *     filter used as the real-weight gradient : Sec. 3 (text) and Algorithm 1 (backward,
+ *     update)
+ *   - SGD with momentum and weight decay  : Sec. 4 (training set-up)
+ * The 2-bit packed layout is this project's own storage format (the paper only says the
+ * four values fit in two bits, abstract and Sec. 1); its definition is restated next to
+ * the packer below.
+ *
+ * Pins: every function here is checked by the CPU test suite against something other
+ * than itself (closed forms, library routines on special cases, brute force, adjoint
+ * identities); none is "parity unpinned".
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_ERR_NONFINITE 1
+#define ORC_ERR_SHAPE 2
+
+/* ------------------------------------------------------------------------------------ */
+/* Rounding of an fp32 value to bf16, round-to-nearest-even on the 16 dropped bits      */
+/* (IEEE 754 rounding rule applied to the bfloat16 format: 1 sign, 8 exponent, 7        */
+/* fraction bits).  Used where a GPU operand is an fp32 input rounded to bf16 on load.   */
+/* ------------------------------------------------------------------------------------ */
+static double orc_round_bf16_one(float f) {
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu) != 0) {
+        return (double)f; /* NaN stays NaN */
+    }
+    uint32_t keep = u >> 16;
+    uint32_t dropped = u & 0xFFFFu;
+    if (dropped > 0x8000u || (dropped == 0x8000u && (keep & 1u))) keep += 1u;
+    uint32_t r = keep << 16;
+    float out;
+    memcpy(&out, &r, 4);
+    return (double)out;
+}
+
+void orc_round_bf16(const float* in, int64_t count, double* out) {
+    for (int64_t i = 0; i < count; ++i) out[i] = orc_round_bf16_one(in[i]);
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Sec. 2, Eq. (3): deterministic discretisation of one real weight.                    */
+/*   -2 if W < -1;  -1 if -1 <= W <= 0;  1 if 0 < W <= 1;  2 if W > 1.                  */
+/* ------------------------------------------------------------------------------------ */
+static int orc_discretize_one(double w) {
+    if (w < -1.0) return -2;
+    if (w <= 0.0) return -1; /* here -1 <= w <= 0 */
+    if (w <= 1.0) return 1;  /* here 0 < w <= 1 */
+    return 2;                /* here w > 1 */
+}
+
+/*
+ * Quantise K filters of n real weights each (w is [K][n], row k = filter k).
+ * Writes codes [K][n] in {-2,-1,1,2}, the optimal scale alpha [K] (fp64, and its
+ * single round-to-nearest fp32 value), the sizes |B1|, |B2| and the sums over B1 and
+ * B2 of |W_i| for every filter.
+ *   Eq. (3) gives the codes; Eq. (4) names the sets B1 = {|W_i| <= 1}, B2 = {|W_i| > 1};
+ *   Eq. (5): alpha* = (sum_{B1}|W_i| + 2 sum_{B2}|W_i|) / (|B1| + 4|B2|).
+ * Non-finite weights are outside the method's domain: the call returns
+ * ORC_ERR_NONFINITE and writes nothing for that filter.
+ * The sums run in index order in fp64.
+ */
+int orc_quantize(const float* w, int64_t K, int64_t n, int8_t* codes, double* alpha64,
+                 float* alpha32, int64_t* b1_size, int64_t* b2_size, double* b1_sum,
+                 double* b2_sum) {
+    if (K < 0 || n <= 0) return ORC_ERR_SHAPE;
+    int status = ORC_OK;
+    for (int64_t k = 0; k < K; ++k) {
+        const float* wk = w + k * n;
+        int finite = 1;
+        for (int64_t i = 0; i < n; ++i)
+            if (!isfinite(wk[i])) finite = 0;
+        if (!finite) {
+            status = ORC_ERR_NONFINITE;
+            continue;
+        }
+        /* Step 1 (Eq. 3): the two-bit filter. */
+        for (int64_t i = 0; i < n; ++i) codes[k * n + i] = (int8_t)orc_discretize_one((double)wk[i]);
+        /* Step 2 (Eq. 4-5): the optimal scale given the two-bit filter. */
+        int64_t nb1 = 0, nb2 = 0;
+        double s1 = 0.0, s2 = 0.0;
+        for (int64_t i = 0; i < n; ++i) {
+            double mag = fabs((double)wk[i]);
+            if (mag <= 1.0) {
+                nb1 += 1;
+                s1 += mag;
+            } else {
+                nb2 += 1;
+                s2 += mag;
+            }
+        }
+        double a = (s1 + 2.0 * s2) / (double)(nb1 + 4 * nb2);
+        if (alpha64) alpha64[k] = a;
+        if (alpha32) alpha32[k] = (float)a; /* one round-to-nearest-even to fp32 */
+        if (b1_size) b1_size[k] = nb1;
+        if (b2_size) b2_size[k] = nb2;
+        if (b1_sum) b1_sum[k] = s1;
+        if (b2_sum) b2_sum[k] = s2;
+    }
+    return status;
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Two-bit packed storage (this project's format; the paper fixes only that the four     */
+/* values fit in two bits).                                                              */
+/*   Filters are grouped in blocks of 64, reduction elements (index i of W^k_i, ordered  */
+/*   (r, s, c) with c fastest) in blocks of 64.  With NB = ceil(n/64) and                */
+/*   KB = ceil(K/64) the array holds KB*NB*64*4 words; element (k, i) lives in word      */
+/*        ((k/64 * NB + i/64) * 64 + k%64) * 4 + (i%64)/16.                              */
+/*   Inside a word, element e = i%16 uses j = e/2 and h = e%2:                           */
+/*        bit 16h + j      = 1 iff |code| = 2  (the "magnitude" plane)                   */
+/*        bit 16h + 8 + j  = 1 iff code < 0    (the "sign" plane).                       */
+/*   Bits of filters k >= K and of elements i >= n are zero.                             */
+/* ------------------------------------------------------------------------------------ */
+int64_t orc_packed_words(int64_t K, int64_t n) {
+    int64_t kb = (K + 63) / 64, nb = (n + 63) / 64;
+    return kb * nb * 64 * 4;
+}
+
+int orc_pack(const int8_t* codes, int64_t K, int64_t n, uint32_t* words) {
+    if (K <= 0 || n <= 0) return ORC_ERR_SHAPE;
+    int64_t nb = (n + 63) / 64;
+    memset(words, 0, (size_t)orc_packed_words(K, n) * sizeof(uint32_t));
+    for (int64_t k = 0; k < K; ++k) {
+        for (int64_t i = 0; i < n; ++i) {
+            int c = codes[k * n + i];
+            if (c != -2 && c != -1 && c != 1 && c != 2) return ORC_ERR_SHAPE;
+            int64_t widx = ((k / 64 * nb + i / 64) * 64 + k % 64) * 4 + (i % 64) / 16;
+            int e = (int)(i % 16), j = e / 2, h = e % 2;
+            uint32_t bits = 0;
+            if (c == 2 || c == -2) bits |= 1u << (16 * h + j);
+            if (c < 0) bits |= 1u << (16 * h + 8 + j);
+            words[widx] |= bits;
+        }
+    }
+    return ORC_OK;
+}
+
+int orc_unpack(const uint32_t* words, int64_t K, int64_t n, int8_t* codes) {
+    if (K <= 0 || n <= 0) return ORC_ERR_SHAPE;
+    int64_t nb = (n + 63) / 64;
+    for (int64_t k = 0; k < K; ++k) {
+        for (int64_t i = 0; i < n; ++i) {
+            int64_t widx = ((k / 64 * nb + i / 64) * 64 + k % 64) * 4 + (i % 64) / 16;
+            int e = (int)(i % 16), j = e / 2, h = e % 2;
+            int mag = (words[widx] >> (16 * h + j)) & 1u;
+            int neg = (words[widx] >> (16 * h + 8 + j)) & 1u;
+            int v = mag ? 2 : 1;
+            codes[k * n + i] = (int8_t)(neg ? -v : v);
+        }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Convolution geometry.  d[] = {N, H, W, C, K, R, S, stride_h, stride_w, pad_h, pad_w}. */
+/* Cross-correlation with zero padding, dilation 1, one group; output size               */
+/* P = floor((H + 2 pad_h - R) / stride_h) + 1, likewise Q.  Activations are NHWC,       */
+/* filters are [K][R][S][C] (so filter element i = (r*S + s)*C + c).                     */
+/* ------------------------------------------------------------------------------------ */
+enum { DN, DH, DW, DC, DK, DR, DS, DSH, DSW, DPH, DPW };
+
+int orc_out_dims(const int32_t* d, int32_t* P, int32_t* Q) {
+    for (int i = 0; i < 7; ++i)
+        if (d[i] <= 0) return ORC_ERR_SHAPE;
+    if (d[DSH] <= 0 || d[DSW] <= 0 || d[DPH] < 0 || d[DPW] < 0) return ORC_ERR_SHAPE;
+    int32_t p = (d[DH] + 2 * d[DPH] - d[DR]) / d[DSH] + 1;
+    int32_t q = (d[DW] + 2 * d[DPW] - d[DS]) / d[DSW] + 1;
+    if (d[DH] + 2 * d[DPH] < d[DR] || d[DW] + 2 * d[DPW] < d[DS]) return ORC_ERR_SHAPE;
+    *P = p;
+    *Q = q;
+    return ORC_OK;
+}
+
+/*
+ * Forward pass of one two-bit layer: Eq. (1), I * (alpha W~) = (alpha I) (+) W~, and
+ * Algorithm 1's forward step.  x is NHWC [N][H][W][C], codes [K][R][S][C] in
+ * {-2,-1,1,2}, alpha [K]; y is NHWC [N][P][Q][K].
+ *   form 0: y = alpha_k * sum x * W~           (scale after the multiplication-free sum)
+ *   form 1: y = sum (alpha_k x) * W~           (the literal right-hand side of Eq. 1)
+ *   form 2: y = sum x * (alpha_k W~)           (the approximate filter W^ of Algorithm 1)
+ * All three are equal in exact arithmetic; the tests check they agree in fp64.
+ */
+int orc_conv_fwd(const int32_t* d, const double* x, const int8_t* codes, const double* alpha,
+                 int form, double* y) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t N = d[DN], H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t nn = 0; nn < N; ++nn) {
+        for (int64_t p = 0; p < P; ++p) {
+            for (int64_t q = 0; q < Q; ++q) {
+                for (int64_t k = 0; k < K; ++k) {
+                    double acc = 0.0;
+                    for (int64_t r = 0; r < R; ++r) {
+                        int64_t h = p * sh - ph + r;
+                        if (h < 0 || h >= H) continue; /* zero padding */
+                        for (int64_t s = 0; s < S; ++s) {
+                            int64_t w = q * sw - pw + s;
+                            if (w < 0 || w >= W) continue;
+                            const double* xp = x + ((nn * H + h) * W + w) * C;
+                            const int8_t* cp = codes + ((k * R + r) * S + s) * C;
+                            for (int64_t c = 0; c < C; ++c) {
+                                if (form == 1)
+                                    acc += (alpha[k] * xp[c]) * (double)cp[c];
+                                else if (form == 2)
+                                    acc += xp[c] * (alpha[k] * (double)cp[c]);
+                                else
+                                    acc += xp[c] * (double)cp[c];
+                            }
+                        }
+                    }
+                    y[((nn * P + p) * Q + q) * K + k] = (form == 0) ? alpha[k] * acc : acc;
+                }
+            }
+        }
+    }
+    return ORC_OK;
+}
+
+/*
+ * Backward pass to the layer input through the approximate filters W^ = alpha W~
+ * (Sec. 3: both passes use the approximate filters; Algorithm 1, backward step).
+ * By the chain rule through y[n,p,q,k] = sum x[n, p*sh-ph+r, q*sw-pw+s, c] W^[k,r,s,c]:
+ *   dx[n,h,w,c] = sum over (p,q,k,r,s) with p*sh-ph+r = h, q*sw-pw+s = w of
+ *                 W^[k,r,s,c] * dy[n,p,q,k]
+ * written here as the scatter over every (n,p,q,k,r,s,c) term.
+ */
+int orc_conv_bwd_data(const int32_t* d, const double* dy, const int8_t* codes,
+                      const double* alpha, double* dx) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t N = d[DN], H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+#pragma omp parallel for schedule(static)
+    for (int64_t nn = 0; nn < N; ++nn) {
+        double* dxn = dx + nn * H * W * C;
+        for (int64_t i = 0; i < H * W * C; ++i) dxn[i] = 0.0;
+        for (int64_t p = 0; p < P; ++p)
+            for (int64_t q = 0; q < Q; ++q)
+                for (int64_t k = 0; k < K; ++k) {
+                    double g = dy[((nn * P + p) * Q + q) * K + k];
+                    for (int64_t r = 0; r < R; ++r) {
+                        int64_t h = p * sh - ph + r;
+                        if (h < 0 || h >= H) continue;
+                        for (int64_t s = 0; s < S; ++s) {
+                            int64_t w = q * sw - pw + s;
+                            if (w < 0 || w >= W) continue;
+                            const int8_t* cp = codes + ((k * R + r) * S + s) * C;
+                            double* o = dxn + (h * W + w) * C;
+                            for (int64_t c = 0; c < C; ++c) o[c] += (alpha[k] * (double)cp[c]) * g;
+                        }
+                    }
+                }
+    }
+    return ORC_OK;
+}
+
+/*
+ * Gradient with respect to the approximate filter W^ (Algorithm 1, backward step):
+ *   dW^[k,r,s,c] = sum_{n,p,q} dy[n,p,q,k] * x[n, p*sh-ph+r, q*sw-pw+s, c].
+ * Sec. 3 updates the real-valued filters with this gradient unchanged (the real weights
+ * are kept only to accumulate small updates), so it is also the real-weight gradient.
+ */
+int orc_conv_bwd_weight(const int32_t* d, const double* x, const double* dy, double* dw) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t N = d[DN], H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+#pragma omp parallel for schedule(static)
+    for (int64_t k = 0; k < K; ++k) {
+        double* dwk = dw + k * R * S * C;
+        for (int64_t i = 0; i < R * S * C; ++i) dwk[i] = 0.0;
+        for (int64_t nn = 0; nn < N; ++nn)
+            for (int64_t p = 0; p < P; ++p)
+                for (int64_t q = 0; q < Q; ++q) {
+                    double g = dy[((nn * P + p) * Q + q) * K + k];
+                    for (int64_t r = 0; r < R; ++r) {
+                        int64_t h = p * sh - ph + r;
+                        if (h < 0 || h >= H) continue;
+                        for (int64_t s = 0; s < S; ++s) {
+                            int64_t w = q * sw - pw + s;
+                            if (w < 0 || w >= W) continue;
+                            const double* xp = x + ((nn * H + h) * W + w) * C;
+                            double* o = dwk + (r * S + s) * C;
+                            for (int64_t c = 0; c < C; ++c) o[c] += g * xp[c];
+                        }
+                    }
+                }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Sampled forms for layers too large for the full loops: each requested element is      */
+/* computed on its own from the same definitions.  Index arrays are flat element         */
+/* indices into the NHWC / KRSC output tensors.  The bf16-valued inputs arrive as        */
+/* their raw 16-bit patterns (exact in fp64), so a full-size tensor need not be widened. */
+/* ------------------------------------------------------------------------------------ */
+static double orc_bf16_bits_to_double(uint16_t b) {
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return (double)f;
+}
+
+int orc_conv_fwd_sampled_bf16(const int32_t* d, const uint16_t* x, const int8_t* codes,
+                              const double* alpha, const int64_t* idx, int64_t count,
+                              double* out) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < count; ++t) {
+        int64_t e = idx[t];
+        int64_t k = e % K, q = (e / K) % Q, p = (e / (K * Q)) % P, nn = e / (K * Q * P);
+        double acc = 0.0;
+        for (int64_t r = 0; r < R; ++r) {
+            int64_t h = p * sh - ph + r;
+            if (h < 0 || h >= H) continue;
+            for (int64_t s = 0; s < S; ++s) {
+                int64_t w = q * sw - pw + s;
+                if (w < 0 || w >= W) continue;
+                const uint16_t* xp = x + ((nn * H + h) * W + w) * C;
+                const int8_t* cp = codes + ((k * R + r) * S + s) * C;
+                for (int64_t c = 0; c < C; ++c) acc += orc_bf16_bits_to_double(xp[c]) * (double)cp[c];
+            }
+        }
+        out[t] = alpha[k] * acc;
+    }
+    return ORC_OK;
+}
+
+/* dx at chosen (n,h,w,c): the gather over every (k,r,s) whose output position
+ * p = (h + ph - r)/sh, q = (w + pw - s)/sw is integral and inside the output. */
+int orc_conv_bwd_data_sampled_bf16(const int32_t* d, const uint16_t* dy, const int8_t* codes,
+                                   const double* alpha, const int64_t* idx, int64_t count,
+                                   double* out) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < count; ++t) {
+        int64_t e = idx[t];
+        int64_t c = e % C, w = (e / C) % W, h = (e / (C * W)) % H, nn = e / (C * W * H);
+        double acc = 0.0;
+        for (int64_t r = 0; r < R; ++r) {
+            int64_t ph_ = h + ph - r;
+            if (ph_ < 0 || ph_ % sh != 0) continue;
+            int64_t p = ph_ / sh;
+            if (p >= P) continue;
+            for (int64_t s = 0; s < S; ++s) {
+                int64_t qw_ = w + pw - s;
+                if (qw_ < 0 || qw_ % sw != 0) continue;
+                int64_t q = qw_ / sw;
+                if (q >= Q) continue;
+                const uint16_t* g = dy + ((nn * P + p) * Q + q) * K;
+                for (int64_t k = 0; k < K; ++k)
+                    acc += (alpha[k] * (double)codes[((k * R + r) * S + s) * C + c]) *
+                           orc_bf16_bits_to_double(g[k]);
+            }
+        }
+        out[t] = acc;
+    }
+    return ORC_OK;
+}
+
+int orc_conv_bwd_weight_sampled_bf16(const int32_t* d, const uint16_t* x, const uint16_t* dy,
+                                     const int64_t* idx, int64_t count, double* out) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t N = d[DN], H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int64_t t = 0; t < count; ++t) {
+        int64_t e = idx[t];
+        int64_t c = e % C, s = (e / C) % S, r = (e / (C * S)) % R, k = e / (C * S * R);
+        double acc = 0.0;
+        for (int64_t nn = 0; nn < N; ++nn)
+            for (int64_t p = 0; p < P; ++p) {
+                int64_t h = p * sh - ph + r;
+                if (h < 0 || h >= H) continue;
+                for (int64_t q = 0; q < Q; ++q) {
+                    int64_t w = q * sw - pw + s;
+                    if (w < 0 || w >= W) continue;
+                    acc += orc_bf16_bits_to_double(dy[((nn * P + p) * Q + q) * K + k]) *
+                           orc_bf16_bits_to_double(x[((nn * H + h) * W + w) * C + c]);
+                }
+            }
+        out[t] = acc;
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Algorithm 1, parameter update, with the optimiser of Sec. 4: SGD with momentum mu and */
+/* weight decay lambda (no dampening, no Nesterov term):                                 */
+/*   v <- mu v + (g + lambda w);   w <- w - eta v.                                      */
+/* g is the gradient with respect to the approximate filter, applied to the real weights.*/
+/* ------------------------------------------------------------------------------------ */
+void orc_sgd(double* w, double* v, const double* g, int64_t count, double eta, double mu,
+             double lambda) {
+    for (int64_t i = 0; i < count; ++i) {
+        v[i] = mu * v[i] + (g[i] + lambda * w[i]);
+        w[i] = w[i] - eta * v[i];
+    }
+}
