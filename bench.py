@@ -1,0 +1,219 @@
+"""Benchmark of the Two-Bit Networks hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch (Algorithm 1 on one large
+layer): quantise the real weights (Sec. 2 Eq. 3-5) -> forward (Eq. 1) -> backward to the
+input and to the approximate filter (Sec. 3) -> SGD update of the real weights (Sec. 4).
+Workload: conv 3x3, 256 -> 256 channels, 56 x 56, pad 1, batch 128, bf16 activations
+N(0,1), upstream gradient N(0,1), real weights N(0, 0.05^2), lr 0.1, momentum 0.9, weight
+decay 1e-4.  Inputs are seeded synthetic tensors already resident in HBM.
+
+Prints one JSON line: the effective TFLOP/s of the step (2 FLOP per multiply-add of the
+three dense contractions, the count of the full-precision layer), the roofline of the
+dominant kernel (timed live with HIP events on the stream it runs on), and the fp64 CPU
+oracle timed on a bounded slice of the same step.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+LAYER = dict(n=128, h=56, w=56, c=256, k=256, r=3, s=3, stride=1, pad=1)
+LR, MOMENTUM, WD = 0.1, 0.9, 1e-4
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle sample")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain device copy of known size (HBM counter calibration)")
+    return ap.parse_args()
+
+
+def layer_flops():
+    """FLOP of one dense contraction of the layer (2 per multiply-add)."""
+    L = LAYER
+    P = (L["h"] + 2 * L["pad"] - L["r"]) // L["stride"] + 1
+    Q = (L["w"] + 2 * L["pad"] - L["s"]) // L["stride"] + 1
+    M = L["n"] * P * Q
+    kred = L["r"] * L["s"] * L["c"]
+    return 2.0 * M * L["k"] * kred, P, Q
+
+
+def cpu_baseline(budget_s: float):
+    """The fp64 oracle on a bounded slice of the same step: the three convolutions on one
+    image of the batch (the work is linear in the batch, scaled by 128), plus quantise and
+    SGD over the whole layer."""
+    import oracle
+    import synth
+
+    L = LAYER
+    threads = len(os.sched_getaffinity(0))
+    os.environ.setdefault("OMP_NUM_THREADS", str(threads))
+    d = oracle.ConvDesc(1, L["h"], L["w"], L["c"], L["k"], L["r"], L["s"], L["stride"], L["pad"])
+    P, Q = d.out_dims()
+    n = L["r"] * L["s"] * L["c"]
+    x = oracle.bf16_bits_to_f64(synth.normal_bf16(5, "x1", (1, L["h"], L["w"], L["c"])))
+    dy = oracle.bf16_bits_to_f64(synth.normal_bf16(5, "dy1", (1, P, Q, L["k"])))
+    w = synth.normal(5, "w", (L["k"], n), 0.05)
+    v = np.zeros_like(w)
+    t0 = time.perf_counter()
+    q = oracle.quantize(w)
+    a64 = q.alpha.astype(np.float64)
+    t1 = time.perf_counter()
+    oracle.conv_fwd(d, x, q.codes, a64)
+    t2 = time.perf_counter()
+    oracle.conv_bwd_data(d, dy, q.codes, a64)
+    t3 = time.perf_counter()
+    g = oracle.conv_bwd_weight(d, x, dy).reshape(L["k"], n)
+    t4 = time.perf_counter()
+    oracle.sgd(w, v, g, LR, MOMENTUM, WD)
+    t5 = time.perf_counter()
+    per_image = (t2 - t1) + (t3 - t2) + (t4 - t3)
+    step_s = (t1 - t0) + (t5 - t4) + per_image * L["n"]
+    conv_flops, _, _ = layer_flops()
+    return {
+        "value": round(3 * conv_flops / step_s / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": int(os.environ.get("OMP_NUM_THREADS", threads)),
+        "kind": "oracle",
+        "sample": "fp64 oracle: quantise + SGD over the full 256x3x3x256 layer, fwd/bwd_data/bwd_weight "
+                  "on 1 of 128 images (scaled x128); measured %.1f s, extrapolated %.0f s per step" %
+                  (t5 - t0, step_s),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (got --gpus %d)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_1701_00485_amd as tbn
+    import synth
+
+    tbn.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L = LAYER
+    conv_flops, P, Q = layer_flops()
+    flops = 3 * conv_flops  # forward, backward-data and backward-weight contractions
+    n = L["r"] * L["s"] * L["c"]
+    desc = tbn.ConvDesc(L["n"], L["h"], L["w"], L["c"], L["k"], L["r"], L["s"], L["stride"], L["pad"])
+
+    def dev_bf16(bits):
+        return torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
+
+    x = dev_bf16(synth.normal_bf16(5, "x", (L["n"], L["h"], L["w"], L["c"])))
+    dy = dev_bf16(synth.normal_bf16(5, "dy", (L["n"], P, Q, L["k"])))
+    w = torch.from_numpy(synth.normal(5, "w", (L["k"], n), 0.05)).to(dev)
+    v = torch.zeros_like(w)
+    codes = torch.empty(tbn.packed_words(L["k"], n), dtype=torch.int32, device=dev)
+    alpha = torch.empty(L["k"], dtype=torch.float32, device=dev)
+    y = torch.empty((L["n"], P, Q, L["k"]), dtype=torch.bfloat16, device=dev)
+    dx = torch.empty_like(x)
+    dw = torch.empty((L["k"], L["r"], L["s"], L["c"]), dtype=torch.float32, device=dev)
+    ws_bd = tbn.workspace(tbn.OP_BWD_DATA, desc, dev)
+    ws_bw = tbn.workspace(tbn.OP_BWD_WEIGHT, desc, dev)
+    stream = torch.cuda.current_stream()
+
+    names = ["quantize", "fwd", "bwd_data", "bwd_weight", "sgd"]
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record(stream)
+        mark(0)
+        tbn.quantize(w, codes, alpha, want_counts=False)
+        mark(1)
+        tbn.conv2d_fwd(desc, x, codes, alpha, y=y)
+        mark(2)
+        tbn.conv2d_bwd_data(desc, dy, codes, alpha, dx=dx, ws=ws_bd)
+        mark(3)
+        tbn.conv2d_bwd_weight(desc, x, dy, dw=dw, ws=ws_bw)
+        mark(4)
+        tbn.sgd_step(w, v, dw, LR, MOMENTUM, WD)
+        mark(5)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        step(events[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_step = total_ms / args.steps
+    per_kernel = {nm: float(np.mean([events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]))
+                  for j, nm in enumerate(names)}
+
+    if args.copy_probe:
+        a = torch.empty(256 * 1024 * 1024, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    conv_names = ["fwd", "bwd_data", "bwd_weight"]
+    dom = max(conv_names, key=lambda nm: per_kernel[nm])
+    achieved = conv_flops / (per_kernel[dom] * 1e-3) / 1e12
+    result = {
+        "metric": "2-bit-weight conv effective TFLOP/s + ResNet-18-shape fwd images/sec, 1 GPU",
+        "value": round(flops / (ms_step * 1e-3) / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) activations and gradients, N(0,0.05^2) real weights)",
+        "config": {
+            "workload": "two-bit conv3x3 training step: quantise -> fwd -> bwd_data -> bwd_weight -> SGD, "
+                        "256->256 ch, 56x56, pad 1, batch 128",
+            "global_batch": L["n"],
+            "flop_per_step": flops,
+            "parallelism": "none (1 GPU)",
+        },
+        "per_kernel_ms": {k: round(v_, 4) for k, v_ in per_kernel.items()},
+        "roofline": {
+            "bound": "mfma",
+            "kernel": dom,
+            "achieved": round(achieved, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

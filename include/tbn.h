@@ -1,0 +1,172 @@
+/*
+ * tbn.h -- C ABI of the Two-Bit Networks hot path on MI355X (gfx950).
+ *
+ * Method: Meng, Gu, Zhang, Wu, "Two-Bit Networks for Deep Learning on Resource-
+ * Constrained Embedded Devices", arXiv 1701.00485.  Each real-valued filter W (n = c*w*h
+ * elements) is approximated by alpha * W~ with W~_i in {-2,-1,1,2} (Sec. 2, Eq. 1-2),
+ * W~ from the deterministic rule of Eq. (3) and alpha from Eq. (5).  Training follows
+ * Algorithm 1 (Sec. 3): quantise every filter, run the forward and backward passes with
+ * the approximate filters, and update the real weights with the gradient taken with
+ * respect to the approximate filters.
+ *
+ * Conventions shared by every call
+ *   - Activations are NHWC, dense, element (n,h,w,c) at ((n*H + h)*W + w)*C + c.
+ *   - Real weights are [K][R][S][C] fp32 (filter k is row k of a [K][n] matrix with
+ *     n = R*S*C, element i = (r*S + s)*C + c).
+ *   - Convolution is cross-correlation with zero padding, dilation 1, one group;
+ *     P = (H + 2*pad_h - R)/stride_h + 1 (floor), Q likewise.  A fully-connected layer is
+ *     the 1x1 convolution over a 1x1 map (or the R x S "valid" convolution over the last
+ *     map), as the paper's Sec. 3 allows.
+ *   - Every pointer is a device pointer owned by the caller, 16-byte aligned, and must
+ *     stay valid until the work queued on `stream` has finished.  The library allocates
+ *     no memory and keeps no mutable global state; calls may come from any host thread.
+ *   - Every call validates its arguments before queuing anything and returns a status;
+ *     on an error nothing has been queued.  TBN_ERR_HIP reports a failed launch.  Faults
+ *     during execution surface at the caller's next synchronisation of `stream`.
+ *   - All work is queued asynchronously on `stream` (0 = the null stream).
+ *
+ * Two-bit packed codes ("TBN2" layout, this library's storage format; the paper fixes
+ * only that the four values fit in two bits):
+ *   filters are grouped in blocks of 64 and filter elements in blocks of 64.  With
+ *   NB = ceil(n/64), KB = ceil(K/64) the array holds KB*NB*256 uint32 words and
+ *   element (k, i) lives in word ((k/64*NB + i/64)*64 + k%64)*4 + (i%64)/16.  Inside a
+ *   word, element e = i%16 uses j = e/2, h = e%2: bit 16h+j is set iff |W~| = 2 and bit
+ *   16h+8+j is set iff W~ < 0.  Bits of padding filters and padding elements are zero.
+ *   A 64-filter x 64-element block is 1 KiB and contiguous, so one wave reads it with
+ *   one 16-byte load per lane, and the bf16 pair of elements (2j, 2j+1) of a word is
+ *   ((word >> j) & 0x01010101) << 7 plus 0x3F803F80 -- two integer operations.
+ */
+#ifndef TBN_H
+#define TBN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum tbn_status {
+    TBN_OK = 0,
+    TBN_ERR_NULL = 1,        /* a required pointer is NULL */
+    TBN_ERR_SHAPE = 2,       /* a size or geometry is invalid (<= 0, empty output, overflow) */
+    TBN_ERR_UNSUPPORTED = 3, /* valid request this build does not implement */
+    TBN_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
+    TBN_ERR_WORKSPACE = 5,   /* workspace missing or smaller than tbn_workspace_size() */
+    TBN_ERR_HIP = 6          /* a HIP launch failed; see tbn_last_error() */
+} tbn_status;
+
+typedef enum tbn_dtype { TBN_BF16 = 0, TBN_F32 = 1 } tbn_dtype;
+
+typedef enum tbn_op { TBN_OP_FWD = 0, TBN_OP_BWD_DATA = 1, TBN_OP_BWD_WEIGHT = 2 } tbn_op;
+
+/* Geometry of one layer: input N x H x W x C, K filters of R x S x C. */
+typedef struct tbn_conv_desc {
+    int32_t n, h, w, c, k, r, s, stride_h, stride_w, pad_h, pad_w;
+} tbn_conv_desc;
+
+/* Optional fused output transform of the forward pass, applied per output element
+ * (n,p,q,k) after the scale alpha_k:  y = act(alpha_k * scale[k] * acc + bias[k]
+ * + residual[n,p,q,k]).  Any pointer may be NULL (scale 1, bias 0, no residual);
+ * `residual` is NHWC [N][P][Q][K] with the output's dtype.  relu != 0 applies
+ * max(., 0).  Used for inference-mode batch normalisation folded into scale and bias,
+ * the residual add of a basic block, and ReLU. */
+typedef struct tbn_epilogue {
+    const float* scale;
+    const float* bias;
+    const void* residual;
+    int32_t relu;
+} tbn_epilogue;
+
+/* Human-readable name of a status. Never NULL. */
+const char* tbn_status_str(tbn_status status);
+
+/* Detail of the last error raised on the calling thread ("" if none). */
+const char* tbn_last_error(void);
+
+/* Output spatial size of a geometry (see conventions). TBN_ERR_SHAPE if invalid. */
+tbn_status tbn_conv_out_dims(const tbn_conv_desc* desc, int32_t* p, int32_t* q);
+
+/* Number of uint32 words of the packed codes of K filters of n elements
+ * (ceil(K/64) * ceil(n/64) * 256), or -1 if K or n <= 0. */
+int64_t tbn_packed_words(int64_t k, int64_t n);
+
+/* Bytes of caller-provided workspace `op` needs for `desc` (0 = none needed).
+ * Pass the same op and geometry to the corresponding call. */
+tbn_status tbn_workspace_size(tbn_op op, const tbn_conv_desc* desc, size_t* bytes);
+
+/*
+ * Quantise K real-valued filters (Sec. 2 Eq. 3 and Eq. 5; Algorithm 1, quantisation).
+ *   w      [K][n] fp32, one filter per row.
+ *   codes  out, tbn_packed_words(K, n) words in the TBN2 layout; every padding bit is
+ *          written as zero.  W~_i = -2 if W_i < -1; -1 if -1 <= W_i <= 0 (both signed
+ *          zeros); 1 if 0 < W_i <= 1; 2 if W_i > 1.  A NaN weight gets code -1.
+ *   alpha  out, [K] fp32: (sum_{|W_i|<=1} |W_i| + 2 sum_{|W_i|>1} |W_i|) /
+ *          (|B1| + 4|B2|) accumulated in fp64 and rounded once to fp32.  An all-zero
+ *          filter gets alpha = 0 (the infimum of the paper's alpha > 0).
+ *   counts out, optional (NULL to skip), [K][2] int32: |B1| = #{|W_i| <= 1} and
+ *          |B2| = #{|W_i| > 1} (the index sets of Eq. 4).
+ */
+tbn_status tbn_quantize(const float* w, int64_t k, int64_t n, uint32_t* codes, float* alpha,
+                        int32_t* counts, hipStream_t stream);
+
+/*
+ * Forward pass of a two-bit layer (Sec. 2 Eq. 1, I * (alpha W~) = (alpha I) (+) W~;
+ * Algorithm 1, forward step):  y[n,p,q,k] = alpha_k * sum_{r,s,c} x[n, p*sh-ph+r,
+ * q*sw-pw+s, c] * W~[k,r,s,c], then the optional epilogue.  The products with the codes
+ * are exact; accumulation is fp32 on bf16 operands; alpha is applied in fp32.
+ *   x      NHWC [N][H][W][C], dtype xt (TBN_F32 input is rounded to bf16, nearest-even).
+ *   codes  TBN2 packed codes of the K filters (n = R*S*C); alpha [K] fp32.
+ *   ep     optional epilogue (NULL = none).
+ *   y      NHWC [N][P][Q][K], dtype yt.
+ *   ws     workspace of tbn_workspace_size(TBN_OP_FWD) bytes (currently 0: may be NULL).
+ */
+tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt,
+                          const uint32_t* codes, const float* alpha, const tbn_epilogue* ep,
+                          void* y, tbn_dtype yt, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Backward pass to the layer input through the approximate filters W^ = alpha W~
+ * (Sec. 3: both passes use the approximate filters; Algorithm 1, backward step):
+ *   dx[n,h,w,c] = sum over (p,q,k,r,s) with p*sh-ph+r = h, q*sw-pw+s = w of
+ *                 alpha_k W~[k,r,s,c] dy[n,p,q,k].
+ * alpha_k W~ is formed exactly from bf16(alpha_k) (the codes only flip the sign and add
+ * one to the exponent), so the only rounding beyond fp32 accumulation is alpha to bf16.
+ *   dy     NHWC [N][P][Q][K] bf16.   dx  NHWC [N][H][W][C], dtype dxt (overwritten).
+ *   ws     tbn_workspace_size(TBN_OP_BWD_DATA) bytes: the codes re-packed for the
+ *          transposed, flipped filter and the bf16 scales.
+ * Requires stride 1 in both directions (TBN_ERR_UNSUPPORTED otherwise) and K even.
+ */
+tbn_status tbn_conv2d_bwd_data(const tbn_conv_desc* desc, const void* dy, const uint32_t* codes,
+                               const float* alpha, void* dx, tbn_dtype dxt, void* ws,
+                               size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Gradient with respect to the approximate filter (Algorithm 1, backward step), which
+ * Sec. 3 applies unchanged to the real-valued filter (straight-through):
+ *   dw[k,r,s,c] (+)= sum_{n,p,q} dy[n,p,q,k] * x[n, p*sh-ph+r, q*sw-pw+s, c].
+ *   x   NHWC [N][H][W][C] bf16.   dy  NHWC [N][P][Q][K] bf16.
+ *   dw  [K][R][S][C] fp32; overwritten, or added to when accumulate != 0.
+ *   ws  tbn_workspace_size(TBN_OP_BWD_WEIGHT) bytes of fp32 split-reduction partials.
+ * The result is deterministic: partial sums are combined in a fixed order.
+ */
+tbn_status tbn_conv2d_bwd_weight(const tbn_conv_desc* desc, const void* x, const void* dy,
+                                 float* dw, int32_t accumulate, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
+/*
+ * Update of the real weights (Algorithm 1, update step) with the optimiser of Sec. 4,
+ * SGD with momentum and weight decay, no dampening, no Nesterov term:
+ *   v = momentum * v + (g + weight_decay * w);   w = w - lr * v        (fp32, in place)
+ *   w, v, g  [count] fp32.
+ */
+tbn_status tbn_sgd_step(float* w, float* v, const float* g, int64_t count, float lr,
+                        float momentum, float weight_decay, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TBN_H */

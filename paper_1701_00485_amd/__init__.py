@@ -1,0 +1,238 @@
+"""Two-Bit Networks (arXiv 1701.00485) hot path on MI355X: Python binding of libtbn.
+
+A thin ctypes layer over the C ABI in ``include/tbn.h``.  It only marshals arguments:
+torch supplies device memory and the current stream, and every step of the computation
+runs in the library's HIP kernels.  If ``libtbn.so`` is missing or does not load, every
+call raises; there is no fallback.
+
+Calls (same names as the C ABI, without the ``tbn_`` prefix):
+  quantize(w)                      Sec. 2 Eq. (3)-(5)   -> packed codes, alpha, counts
+  conv2d_fwd(desc, x, codes, alpha) Sec. 2 Eq. (1)       -> y
+  conv2d_bwd_data(desc, dy, codes, alpha)  Sec. 3        -> dx
+  conv2d_bwd_weight(desc, x, dy)    Sec. 3 (straight-through) -> dW
+  sgd_step(w, v, g, lr, momentum, weight_decay)  Sec. 4 optimiser
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtbn.so")
+
+TBN_BF16, TBN_F32 = 0, 1
+OP_FWD, OP_BWD_DATA, OP_BWD_WEIGHT = 0, 1, 2
+
+_lib = None
+
+
+class TbnError(RuntimeError):
+    def __init__(self, status: int, call: str, detail: str):
+        self.status = status
+        super().__init__("%s failed: %s (%s)" % (call, _status_name(status), detail))
+
+
+class ConvDesc(ctypes.Structure):
+    """Layer geometry: input N x H x W x C (NHWC), K filters of R x S x C."""
+
+    _fields_ = [(f, ctypes.c_int32) for f in
+                ("n", "h", "w", "c", "k", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w")]
+
+    def __init__(self, n, h, w, c, k, r, s, stride=1, pad=0, stride_w=None, pad_w=None):
+        super().__init__(n, h, w, c, k, r, s, stride, stride if stride_w is None else stride_w,
+                         pad, pad if pad_w is None else pad_w)
+
+    def out_dims(self):
+        p, q = ctypes.c_int32(), ctypes.c_int32()
+        _call("tbn_conv_out_dims", ctypes.byref(self), ctypes.byref(p), ctypes.byref(q))
+        return p.value, q.value
+
+    def __repr__(self):
+        return "ConvDesc(n=%d,h=%d,w=%d,c=%d,k=%d,r=%d,s=%d,stride=%d/%d,pad=%d/%d)" % (
+            self.n, self.h, self.w, self.c, self.k, self.r, self.s, self.stride_h, self.stride_w,
+            self.pad_h, self.pad_w)
+
+
+class Epilogue(ctypes.Structure):
+    _fields_ = [("scale", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("residual", ctypes.c_void_p),
+                ("relu", ctypes.c_int32)]
+
+
+def load():
+    """Load libtbn.so (built in-tree by build.py); raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libtbn.so not built: run `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    sigs = {
+        "tbn_status_str": ([i32], ctypes.c_char_p),
+        "tbn_last_error": ([], ctypes.c_char_p),
+        "tbn_conv_out_dims": ([vp, vp, vp], i32),
+        "tbn_packed_words": ([i64, i64], i64),
+        "tbn_workspace_size": ([i32, vp, vp], i32),
+        "tbn_quantize": ([vp, i64, i64, vp, vp, vp, vp], i32),
+        "tbn_conv2d_fwd": ([vp, vp, i32, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
+        "tbn_conv2d_bwd_data": ([vp, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
+        "tbn_conv2d_bwd_weight": ([vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
+        "tbn_sgd_step": ([vp, vp, vp, i64, f32, f32, f32, vp], i32),
+    }
+    for name, (args, res) in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def exported_symbols():
+    return ["tbn_status_str", "tbn_last_error", "tbn_conv_out_dims", "tbn_packed_words",
+            "tbn_workspace_size", "tbn_quantize", "tbn_conv2d_fwd", "tbn_conv2d_bwd_data",
+            "tbn_conv2d_bwd_weight", "tbn_sgd_step"]
+
+
+def _status_name(s: int) -> str:
+    try:
+        return load().tbn_status_str(s).decode()
+    except Exception:
+        return str(s)
+
+
+def _call(name, *args):
+    lib = load()
+    st = getattr(lib, name)(*args)
+    if st != 0:
+        raise TbnError(st, name, lib.tbn_last_error().decode())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtypes=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("%s must be a CUDA (HIP) tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous (NHWC order for activations)" % name)
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError("%s has dtype %s, expected one of %s" % (name, t.dtype, dtypes))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(dt):
+    if dt == torch.bfloat16:
+        return TBN_BF16
+    if dt == torch.float32:
+        return TBN_F32
+    raise TypeError("unsupported dtype %s" % dt)
+
+
+def packed_words(k: int, n: int) -> int:
+    return int(load().tbn_packed_words(k, n))
+
+
+def workspace_size(op: int, desc: ConvDesc) -> int:
+    b = ctypes.c_size_t()
+    _call("tbn_workspace_size", op, ctypes.byref(desc), ctypes.byref(b))
+    return b.value
+
+
+def workspace(op: int, desc: ConvDesc, device="cuda"):
+    n = workspace_size(op, desc)
+    return torch.empty(max(n, 16), dtype=torch.uint8, device=device)
+
+
+def _numel(t, expect, name):
+    if t.numel() != expect:
+        raise ValueError("%s has %d elements, expected %d" % (name, t.numel(), expect))
+
+
+def quantize(w: torch.Tensor, codes=None, alpha=None, counts=None, want_counts=True):
+    """w: [K][n] fp32 (or [K][R][S][C]).  Returns (codes int32 words, alpha fp32, counts)."""
+    K = w.shape[0]
+    n = w.numel() // K
+    pw = _dev(w, "w", (torch.float32,))
+    if codes is None:
+        codes = torch.empty(packed_words(K, n), dtype=torch.int32, device=w.device)
+    if alpha is None:
+        alpha = torch.empty(K, dtype=torch.float32, device=w.device)
+    if counts is None and want_counts:
+        counts = torch.empty((K, 2), dtype=torch.int32, device=w.device)
+    _numel(codes, packed_words(K, n), "codes")
+    _numel(alpha, K, "alpha")
+    pc = _dev(counts, "counts", (torch.int32,)) if counts is not None else None
+    _call("tbn_quantize", pw, K, n, _dev(codes, "codes", (torch.int32,)),
+          _dev(alpha, "alpha", (torch.float32,)), pc, _stream())
+    return codes, alpha, counts
+
+
+def conv2d_fwd(desc: ConvDesc, x, codes, alpha, y=None, out_dtype=torch.bfloat16, scale=None, bias=None,
+               residual=None, relu=False):
+    """y = act(alpha_k * scale_k * (x conv W~) + bias_k + residual), NHWC."""
+    P, Q = desc.out_dims()
+    _numel(x, desc.n * desc.h * desc.w * desc.c, "x")
+    _numel(codes, packed_words(desc.k, desc.r * desc.s * desc.c), "codes")
+    _numel(alpha, desc.k, "alpha")
+    if y is None:
+        y = torch.empty((desc.n, P, Q, desc.k), dtype=out_dtype, device=x.device)
+    _numel(y, desc.n * P * Q * desc.k, "y")
+    ep = None
+    if scale is not None or bias is not None or residual is not None or relu:
+        if residual is not None:
+            _numel(residual, y.numel(), "residual")
+            if residual.dtype != y.dtype:
+                raise TypeError("residual must have y's dtype")
+        ep = Epilogue(_dev(scale, "scale", (torch.float32,)).value if scale is not None else None,
+                      _dev(bias, "bias", (torch.float32,)).value if bias is not None else None,
+                      _dev(residual, "residual").value if residual is not None else None,
+                      1 if relu else 0)
+    _call("tbn_conv2d_fwd", ctypes.byref(desc), _dev(x, "x", (torch.bfloat16, torch.float32)),
+          _dtype_code(x.dtype), _dev(codes, "codes", (torch.int32,)), _dev(alpha, "alpha", (torch.float32,)),
+          ctypes.byref(ep) if ep is not None else None, _dev(y, "y", (torch.bfloat16, torch.float32)),
+          _dtype_code(y.dtype), None, 0, _stream())
+    return y
+
+
+def conv2d_bwd_data(desc: ConvDesc, dy, codes, alpha, dx=None, out_dtype=torch.bfloat16, ws=None):
+    P, Q = desc.out_dims()
+    _numel(dy, desc.n * P * Q * desc.k, "dy")
+    _numel(codes, packed_words(desc.k, desc.r * desc.s * desc.c), "codes")
+    _numel(alpha, desc.k, "alpha")
+    if dx is None:
+        dx = torch.empty((desc.n, desc.h, desc.w, desc.c), dtype=out_dtype, device=dy.device)
+    _numel(dx, desc.n * desc.h * desc.w * desc.c, "dx")
+    if ws is None:
+        ws = workspace(OP_BWD_DATA, desc, dy.device)
+    _call("tbn_conv2d_bwd_data", ctypes.byref(desc), _dev(dy, "dy", (torch.bfloat16,)),
+          _dev(codes, "codes", (torch.int32,)), _dev(alpha, "alpha", (torch.float32,)),
+          _dev(dx, "dx", (torch.bfloat16, torch.float32)), _dtype_code(dx.dtype), _dev(ws, "ws"),
+          ws.numel() * ws.element_size(), _stream())
+    return dx
+
+
+def conv2d_bwd_weight(desc: ConvDesc, x, dy, dw=None, accumulate=False, ws=None):
+    P, Q = desc.out_dims()
+    _numel(x, desc.n * desc.h * desc.w * desc.c, "x")
+    _numel(dy, desc.n * P * Q * desc.k, "dy")
+    if dw is None:
+        dw = torch.empty((desc.k, desc.r, desc.s, desc.c), dtype=torch.float32, device=x.device)
+    _numel(dw, desc.k * desc.r * desc.s * desc.c, "dw")
+    if ws is None:
+        ws = workspace(OP_BWD_WEIGHT, desc, x.device)
+    _call("tbn_conv2d_bwd_weight", ctypes.byref(desc), _dev(x, "x", (torch.bfloat16,)),
+          _dev(dy, "dy", (torch.bfloat16,)), _dev(dw, "dw", (torch.float32,)), 1 if accumulate else 0,
+          _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream())
+    return dw
+
+
+def sgd_step(w, v, g, lr, momentum=0.9, weight_decay=1e-4):
+    n = w.numel()
+    _numel(v, n, "v")
+    _numel(g, n, "g")
+    _call("tbn_sgd_step", _dev(w, "w", (torch.float32,)), _dev(v, "v", (torch.float32,)),
+          _dev(g, "g", (torch.float32,)), n, float(lr), float(momentum), float(weight_decay), _stream())
+    return w, v

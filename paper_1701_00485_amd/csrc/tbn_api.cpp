@@ -1,0 +1,263 @@
+// tbn_api.cpp -- the C ABI of libtbn (declared in include/tbn.h): argument validation,
+// shape arithmetic, workspace sizing and kernel launches on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "tbn.h"
+#include "tbn_kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+tbn_status fail(tbn_status s, const char* what) {
+    g_last_error = what;
+    return s;
+}
+
+tbn_status hip_fail(hipError_t e, const char* where) {
+    g_last_error = std::string(where) + ": " + hipGetErrorString(e);
+    return TBN_ERR_HIP;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+constexpr int64_t kI32Max = 0x7FFFFFFF;
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+struct Geometry {
+    int64_t N, H, W, C, K, R, S, sh, sw, ph, pw, P, Q;
+};
+
+tbn_status check_desc(const tbn_conv_desc* d, Geometry* g) {
+    if (!d) return fail(TBN_ERR_NULL, "desc is NULL");
+    if (d->n <= 0 || d->h <= 0 || d->w <= 0 || d->c <= 0 || d->k <= 0 || d->r <= 0 || d->s <= 0)
+        return fail(TBN_ERR_SHAPE, "every size must be positive");
+    if (d->stride_h <= 0 || d->stride_w <= 0) return fail(TBN_ERR_SHAPE, "strides must be positive");
+    if (d->pad_h < 0 || d->pad_w < 0) return fail(TBN_ERR_SHAPE, "padding must be non-negative");
+    const int64_t hp = (int64_t)d->h + 2 * (int64_t)d->pad_h, wp = (int64_t)d->w + 2 * (int64_t)d->pad_w;
+    if (hp < d->r || wp < d->s) return fail(TBN_ERR_SHAPE, "filter larger than the padded input");
+    g->N = d->n; g->H = d->h; g->W = d->w; g->C = d->c; g->K = d->k; g->R = d->r; g->S = d->s;
+    g->sh = d->stride_h; g->sw = d->stride_w; g->ph = d->pad_h; g->pw = d->pad_w;
+    g->P = (hp - d->r) / d->stride_h + 1;
+    g->Q = (wp - d->s) / d->stride_w + 1;
+    // index arithmetic inside the kernels is 32-bit for pixels and filter elements
+    if (g->N * g->P * g->Q > kI32Max || g->N * g->H * g->W > kI32Max)
+        return fail(TBN_ERR_SHAPE, "more than 2^31 - 1 pixels");
+    if (g->R * g->S * g->C > kI32Max / 2 || g->R * g->S * g->K > kI32Max / 2)
+        return fail(TBN_ERR_SHAPE, "filter has more than 2^30 elements");
+    return TBN_OK;
+}
+
+// bwd_weight: number of reduction splits for a geometry (shared by sizing and launch)
+int wgrad_splits(const Geometry& g) {
+    const int64_t J = g.R * g.S * g.C;
+    const int64_t tiles = ((g.K + 127) / 128) * ((J + 127) / 128);
+    const int64_t chunks = (g.N * g.P * g.Q + 63) / 64;
+    int64_t splits = (1024 + tiles - 1) / tiles;
+    const int64_t max_by_len = chunks / 16 > 0 ? chunks / 16 : 1;  // >= 16 chunks per split
+    if (splits > max_by_len) splits = max_by_len;
+    if (splits > 256) splits = 256;
+    if (splits < 1) splits = 1;
+    return (int)splits;
+}
+
+struct BwdDataWs {
+    int64_t codes_bytes, apair_off, apair_bytes, total;
+};
+
+BwdDataWs bwd_data_ws(const Geometry& g) {
+    BwdDataWs w;
+    const int64_t nt = g.R * g.S * g.K;
+    const int64_t nbt = (nt + 63) / 64;
+    w.codes_bytes = ((g.C + 63) / 64) * nbt * 256 * 4;
+    w.apair_off = round_up(w.codes_bytes, 256);
+    w.apair_bytes = nbt * 32 * 4;
+    w.total = w.apair_off + round_up(w.apair_bytes, 256);
+    return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tbn_status_str(tbn_status s) {
+    switch (s) {
+        case TBN_OK: return "TBN_OK";
+        case TBN_ERR_NULL: return "TBN_ERR_NULL";
+        case TBN_ERR_SHAPE: return "TBN_ERR_SHAPE";
+        case TBN_ERR_UNSUPPORTED: return "TBN_ERR_UNSUPPORTED";
+        case TBN_ERR_ALIGN: return "TBN_ERR_ALIGN";
+        case TBN_ERR_WORKSPACE: return "TBN_ERR_WORKSPACE";
+        case TBN_ERR_HIP: return "TBN_ERR_HIP";
+    }
+    return "TBN_ERR_UNKNOWN";
+}
+
+const char* tbn_last_error(void) { return g_last_error.c_str(); }
+
+tbn_status tbn_conv_out_dims(const tbn_conv_desc* desc, int32_t* p, int32_t* q) {
+    Geometry g;
+    tbn_status st = check_desc(desc, &g);
+    if (st != TBN_OK) return st;
+    if (!p || !q) return fail(TBN_ERR_NULL, "output pointer is NULL");
+    *p = (int32_t)g.P;
+    *q = (int32_t)g.Q;
+    return TBN_OK;
+}
+
+int64_t tbn_packed_words(int64_t k, int64_t n) {
+    if (k <= 0 || n <= 0) return -1;
+    return ((k + 63) / 64) * ((n + 63) / 64) * 256;
+}
+
+tbn_status tbn_workspace_size(tbn_op op, const tbn_conv_desc* desc, size_t* bytes) {
+    Geometry g;
+    tbn_status st = check_desc(desc, &g);
+    if (st != TBN_OK) return st;
+    if (!bytes) return fail(TBN_ERR_NULL, "bytes is NULL");
+    switch (op) {
+        case TBN_OP_FWD: *bytes = 0; return TBN_OK;
+        case TBN_OP_BWD_DATA: *bytes = (size_t)bwd_data_ws(g).total; return TBN_OK;
+        case TBN_OP_BWD_WEIGHT: {
+            const int splits = wgrad_splits(g);
+            *bytes = splits > 1 ? (size_t)splits * (size_t)(g.K * g.R * g.S * g.C) * 4 : 0;
+            return TBN_OK;
+        }
+    }
+    return fail(TBN_ERR_UNSUPPORTED, "unknown op");
+}
+
+tbn_status tbn_quantize(const float* w, int64_t k, int64_t n, uint32_t* codes, float* alpha, int32_t* counts,
+                        hipStream_t stream) {
+    if (!w || !codes || !alpha) return fail(TBN_ERR_NULL, "w, codes and alpha are required");
+    if (k <= 0 || n <= 0) return fail(TBN_ERR_SHAPE, "k and n must be positive");
+    if (n > kI32Max || k > kI32Max / 2) return fail(TBN_ERR_SHAPE, "k or n too large");
+    if (!aligned4(w) || !aligned16(codes) || !aligned4(alpha) || (counts && !aligned4(counts)))
+        return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    hipError_t e = tbn::launch_quantize(w, k, n, codes, alpha, counts, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_quantize");
+}
+
+tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt, const uint32_t* codes,
+                          const float* alpha, const tbn_epilogue* ep, void* y, tbn_dtype yt, void* ws,
+                          size_t ws_bytes, hipStream_t stream) {
+    (void)ws;
+    (void)ws_bytes;
+    Geometry g;
+    tbn_status st = check_desc(desc, &g);
+    if (st != TBN_OK) return st;
+    if (!x || !codes || !alpha || !y) return fail(TBN_ERR_NULL, "x, codes, alpha and y are required");
+    if ((xt != TBN_BF16 && xt != TBN_F32) || (yt != TBN_BF16 && yt != TBN_F32))
+        return fail(TBN_ERR_UNSUPPORTED, "unknown dtype");
+    if (!aligned16(x) || !aligned16(codes) || !aligned16(y) || !aligned4(alpha))
+        return fail(TBN_ERR_ALIGN, "x, codes and y must be 16-byte aligned");
+    tbn::ConvGemmArgs a = {};
+    a.x = x;
+    a.codes = codes;
+    a.apair = nullptr;
+    a.colscale = alpha;
+    if (ep) {
+        if ((ep->scale && !aligned4(ep->scale)) || (ep->bias && !aligned4(ep->bias)) ||
+            (ep->residual && !aligned16(ep->residual)))
+            return fail(TBN_ERR_ALIGN, "misaligned epilogue pointer");
+        a.scale = ep->scale;
+        a.bias = ep->bias;
+        a.residual = ep->residual;
+        a.relu = ep->relu ? 1 : 0;
+    }
+    a.y = y;
+    a.N = (int32_t)g.N; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.C = (int32_t)g.C; a.Kf = (int32_t)g.K;
+    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = (int32_t)g.sh; a.sw = (int32_t)g.sw;
+    a.ph = (int32_t)g.ph; a.pw = (int32_t)g.pw; a.P = (int32_t)g.P; a.Q = (int32_t)g.Q;
+    a.x_f32 = xt == TBN_F32;
+    a.y_f32 = yt == TBN_F32;
+    hipError_t e = tbn::launch_conv_gemm(a, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_fwd");
+}
+
+tbn_status tbn_conv2d_bwd_data(const tbn_conv_desc* desc, const void* dy, const uint32_t* codes, const float* alpha,
+                               void* dx, tbn_dtype dxt, void* ws, size_t ws_bytes, hipStream_t stream) {
+    Geometry g;
+    tbn_status st = check_desc(desc, &g);
+    if (st != TBN_OK) return st;
+    if (!dy || !codes || !alpha || !dx) return fail(TBN_ERR_NULL, "dy, codes, alpha and dx are required");
+    if (dxt != TBN_BF16 && dxt != TBN_F32) return fail(TBN_ERR_UNSUPPORTED, "unknown dtype");
+    if (g.sh != 1 || g.sw != 1) return fail(TBN_ERR_UNSUPPORTED, "backward-data supports stride 1 only");
+    if (!aligned16(dy) || !aligned16(codes) || !aligned16(dx) || !aligned4(alpha))
+        return fail(TBN_ERR_ALIGN, "dy, codes and dx must be 16-byte aligned");
+    const BwdDataWs w = bwd_data_ws(g);
+    if (!ws || ws_bytes < (size_t)w.total) return fail(TBN_ERR_WORKSPACE, "workspace too small");
+    if (!aligned16(ws)) return fail(TBN_ERR_ALIGN, "workspace must be 16-byte aligned");
+    uint32_t* codes_t = reinterpret_cast<uint32_t*>(ws);
+    uint32_t* apair = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + w.apair_off);
+    hipError_t e = tbn::launch_repack_bwd(codes, alpha, (int32_t)g.K, (int32_t)g.R, (int32_t)g.S, (int32_t)g.C,
+                                          codes_t, apair, stream);
+    if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_data (repack)");
+    // dx = conv(dy, flipped transposed filter) with padding R-1-pad, stride 1
+    tbn::ConvGemmArgs a = {};
+    a.x = dy;
+    a.codes = codes_t;
+    a.apair = apair;
+    a.colscale = nullptr;
+    a.y = dx;
+    a.N = (int32_t)g.N; a.H = (int32_t)g.P; a.W = (int32_t)g.Q; a.C = (int32_t)g.K; a.Kf = (int32_t)g.C;
+    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = 1; a.sw = 1;
+    a.ph = (int32_t)(g.R - 1 - g.ph); a.pw = (int32_t)(g.S - 1 - g.pw);
+    a.P = (int32_t)g.H; a.Q = (int32_t)g.W;
+    a.x_f32 = 0;
+    a.y_f32 = dxt == TBN_F32;
+    e = tbn::launch_conv_gemm(a, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_bwd_data");
+}
+
+tbn_status tbn_conv2d_bwd_weight(const tbn_conv_desc* desc, const void* x, const void* dy, float* dw,
+                                 int32_t accumulate, void* ws, size_t ws_bytes, hipStream_t stream) {
+    Geometry g;
+    tbn_status st = check_desc(desc, &g);
+    if (st != TBN_OK) return st;
+    if (!x || !dy || !dw) return fail(TBN_ERR_NULL, "x, dy and dw are required");
+    if (!aligned16(x) || !aligned16(dy) || !aligned16(dw)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    const int splits = wgrad_splits(g);
+    const int64_t count = g.K * g.R * g.S * g.C;
+    const bool direct = splits == 1;  // one split writes (or adds to) dw itself
+    if (!direct) {
+        const size_t need = (size_t)splits * (size_t)count * 4;
+        if (!ws || ws_bytes < need) return fail(TBN_ERR_WORKSPACE, "workspace too small");
+        if (!aligned16(ws)) return fail(TBN_ERR_ALIGN, "workspace must be 16-byte aligned");
+    }
+    tbn::WgradArgs a = {};
+    a.x = reinterpret_cast<const uint16_t*>(x);
+    a.dy = reinterpret_cast<const uint16_t*>(dy);
+    a.out = direct ? dw : reinterpret_cast<float*>(ws);
+    a.N = (int32_t)g.N; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.C = (int32_t)g.C; a.K = (int32_t)g.K;
+    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = (int32_t)g.sh; a.sw = (int32_t)g.sw;
+    a.ph = (int32_t)g.ph; a.pw = (int32_t)g.pw; a.P = (int32_t)g.P; a.Q = (int32_t)g.Q;
+    const int64_t chunks = (g.N * g.P * g.Q + 63) / 64;
+    a.splits = splits;
+    a.chunks_per_split = (int32_t)((chunks + splits - 1) / splits);
+    a.accumulate = direct && accumulate ? 1 : 0;
+    hipError_t e = tbn::launch_wgrad(a, stream);
+    if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_weight");
+    if (!direct) {
+        e = tbn::launch_split_reduce(reinterpret_cast<const float*>(ws), splits, count, dw, accumulate, stream);
+        if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_weight (reduce)");
+    }
+    return TBN_OK;
+}
+
+tbn_status tbn_sgd_step(float* w, float* v, const float* g, int64_t count, float lr, float momentum,
+                        float weight_decay, hipStream_t stream) {
+    if (!w || !v || !g) return fail(TBN_ERR_NULL, "w, v and g are required");
+    if (count <= 0) return fail(TBN_ERR_SHAPE, "count must be positive");
+    if (!aligned16(w) || !aligned16(v) || !aligned16(g)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    hipError_t e = tbn::launch_sgd(w, v, g, count, lr, momentum, weight_decay, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_sgd_step");
+}
+
+}  // extern "C"

@@ -1,0 +1,57 @@
+// tbn_kernels.h -- host-side launchers of the gfx950 kernels (internal to libtbn).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tbn {
+
+// Geometry + operands of the implicit GEMM that serves both the forward pass and the
+// backward-data pass.  Rows are output pixels (n, p, q) of an NHWC "input" x; columns
+// are the Kf "filters" whose packed codes hold n = R*S*C elements each.
+struct ConvGemmArgs {
+    const void* x;            // NHWC [N][H][W][C], bf16 (or fp32 when x_f32)
+    const uint32_t* codes;    // TBN2 codes of Kf filters of n elements
+    const uint32_t* apair;    // per element pair: bf16 scale pair (backward-data), or null
+    const float* colscale;    // per column fp32 scale (alpha in the forward pass), or null
+    const float* scale;       // epilogue: optional per-column multiplier
+    const float* bias;        // epilogue: optional per-column addend
+    const void* residual;     // epilogue: optional NHWC [N][P][Q][Kf] addend, y's dtype
+    void* y;                  // NHWC [N][P][Q][Kf]
+    int32_t N, H, W, C, Kf, R, S, sh, sw, ph, pw, P, Q;
+    int32_t relu;
+    int32_t x_f32;
+    int32_t y_f32;
+};
+
+hipError_t launch_quantize(const float* w, int64_t K, int64_t n, uint32_t* codes, float* alpha,
+                           int32_t* counts, hipStream_t stream);
+
+hipError_t launch_conv_gemm(const ConvGemmArgs& a, hipStream_t stream);
+
+// Re-pack the codes of K filters [K][R][S][C] into the codes of the C filters of the
+// transposed, spatially flipped layer [C][R][S][K] (backward-data operand), and build
+// the bf16 scale pairs of that layer's element pairs.
+hipError_t launch_repack_bwd(const uint32_t* codes, const float* alpha, int32_t K, int32_t R,
+                             int32_t S, int32_t C, uint32_t* codes_t, uint32_t* apair,
+                             hipStream_t stream);
+
+struct WgradArgs {
+    const uint16_t* x;        // NHWC [N][H][W][C] bf16
+    const uint16_t* dy;       // NHWC [N][P][Q][K] bf16
+    float* out;               // [splits][K][R*S*C] fp32 partials, or dw when splits == 1
+    int32_t N, H, W, C, K, R, S, sh, sw, ph, pw, P, Q;
+    int32_t splits;           // number of reduction splits (grid y)
+    int32_t chunks_per_split; // 64-pixel chunks per split
+    int32_t accumulate;       // splits == 1 only: add to `out` instead of overwriting
+};
+
+hipError_t launch_wgrad(const WgradArgs& a, hipStream_t stream);
+
+hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, float* dw,
+                               int32_t accumulate, hipStream_t stream);
+
+hipError_t launch_sgd(float* w, float* v, const float* g, int64_t count, float lr, float mu,
+                      float wd, hipStream_t stream);
+
+}  // namespace tbn

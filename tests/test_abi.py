@@ -1,0 +1,91 @@
+"""The C ABI on the CPU: the library loads, exports every function include/tbn.h declares,
+and its host-side shape arithmetic and argument checks behave as documented.  No call
+here reaches a kernel (every checked call fails validation before any launch)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+import paper_1701_00485_amd as tbn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "tbn.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\*?\s+\*?(tbn_[a-z_0-9]+)\(", text, re.M)))
+
+
+def test_library_exports_every_declared_function():
+    lib = tbn.load()
+    names = _declared()
+    assert "tbn_quantize" in names and "tbn_conv2d_bwd_weight" in names
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(tbn.exported_symbols()) == names
+
+
+def test_status_strings():
+    lib = tbn.load()
+    for s, name in enumerate(["TBN_OK", "TBN_ERR_NULL", "TBN_ERR_SHAPE", "TBN_ERR_UNSUPPORTED",
+                              "TBN_ERR_ALIGN", "TBN_ERR_WORKSPACE", "TBN_ERR_HIP"]):
+        assert lib.tbn_status_str(s).decode() == name
+    assert lib.tbn_status_str(99).decode() == "TBN_ERR_UNKNOWN"
+
+
+@pytest.mark.parametrize("g", [
+    (2, 7, 6, 1, 3, 5, 5, 1, 2), (1, 9, 9, 3, 5, 3, 3, 2, 1), (1, 224, 224, 3, 64, 7, 7, 2, 3),
+    (64, 56, 56, 64, 128, 1, 1, 2, 0), (128, 56, 56, 256, 256, 3, 3, 1, 1), (1, 4, 4, 6, 2, 4, 4, 1, 0)])
+def test_out_dims_match_oracle(g):
+    assert tbn.ConvDesc(*g).out_dims() == oracle.ConvDesc(*g).out_dims()
+
+
+@pytest.mark.parametrize("g", [(0, 4, 4, 1, 1, 1, 1, 1, 0), (1, 2, 2, 1, 1, 5, 5, 1, 0),
+                               (1, 4, 4, 1, 1, 1, 1, 0, 0), (1, 4, 4, 1, 1, 1, 1, 1, -1)])
+def test_bad_geometry(g):
+    with pytest.raises(tbn.TbnError) as e:
+        tbn.ConvDesc(*g).out_dims()
+    assert e.value.status == 2
+
+
+@pytest.mark.parametrize("K,n", [(1, 1), (32, 25), (64, 64), (65, 129), (512, 3136), (1000, 512)])
+def test_packed_words_match_oracle(K, n):
+    assert tbn.packed_words(K, n) == oracle.packed_words(K, n)
+    assert tbn.packed_words(0, n) == -1
+
+
+def test_argument_errors_before_launch():
+    lib = tbn.load()
+    vp = ctypes.c_void_p
+    # NULL pointers
+    assert lib.tbn_quantize(None, 4, 4, None, None, None, None) == 1
+    d = tbn.ConvDesc(1, 8, 8, 8, 8, 3, 3, 1, 1)
+    assert lib.tbn_conv2d_fwd(ctypes.byref(d), None, 0, None, None, None, None, 0, None, 0, None) == 1
+    # misaligned pointers (never dereferenced: validation fails first)
+    bad = vp(0x1002)
+    good = vp(0x100000)
+    assert lib.tbn_quantize(good, 4, 4, bad, good, None, None) == 4
+    assert lib.tbn_conv2d_fwd(ctypes.byref(d), bad, 0, good, good, None, good, 0, None, 0, None) == 4
+    # shape errors
+    assert lib.tbn_quantize(good, 0, 4, good, good, None, None) == 2
+    assert lib.tbn_sgd_step(good, good, good, 0, 0.1, 0.9, 0.0, None) == 2
+    # stride-2 backward-data is not implemented
+    d2 = tbn.ConvDesc(1, 8, 8, 8, 8, 3, 3, 2, 1)
+    assert lib.tbn_conv2d_bwd_data(ctypes.byref(d2), good, good, good, good, 0, good, 1 << 20, None) == 3
+    # workspace too small
+    ws = ctypes.c_size_t()
+    assert lib.tbn_workspace_size(tbn.OP_BWD_DATA, ctypes.byref(d), ctypes.byref(ws)) == 0
+    assert ws.value > 0
+    assert lib.tbn_conv2d_bwd_data(ctypes.byref(d), good, good, good, good, 0, good, ws.value - 1, None) == 5
+    assert lib.tbn_last_error().decode() == "workspace too small"
+
+
+def test_workspace_sizes():
+    d = tbn.ConvDesc(128, 56, 56, 256, 256, 3, 3, 1, 1)
+    assert tbn.workspace_size(tbn.OP_FWD, d) == 0
+    # transposed codes (4 column blocks x 36 element blocks x 1 KiB) + bf16 scale pairs
+    assert tbn.workspace_size(tbn.OP_BWD_DATA, d) == 4 * 36 * 1024 + 36 * 32 * 4
+    wb = tbn.workspace_size(tbn.OP_BWD_WEIGHT, d)
+    assert wb % (256 * 2304 * 4) == 0 and wb >= 256 * 2304 * 4

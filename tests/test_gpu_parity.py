@@ -1,0 +1,275 @@
+"""GPU parity: every call of the C ABI against the fp64 oracle on the same seeded inputs.
+
+Bars (from the method's arithmetic):
+  * codes, packed words and B1/B2 counts: bit-exact;
+  * alpha: within 1 fp32 ulp (both sides sum in fp64 and round once; only the order of
+    the fp64 sums differs);
+  * convolution outputs and gradients: normalised max error max|g - r| / max|r| <= 1e-2
+    (bf16 operands, fp32 accumulation; fwd with fp32 output is in fact ~1e-6);
+  * SGD: fp32 element-wise arithmetic, relative 1e-6 of the largest value.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def nerr(got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    scale = np.max(np.abs(ref)) if ref.size else 0.0
+    if scale == 0.0:
+        return float(np.max(np.abs(got))) if got.size else 0.0
+    return float(np.max(np.abs(got - ref)) / scale)
+
+
+def to_dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    return t if dtype is None else t.to(dtype)
+
+
+def bf16_dev(bits):
+    return to_dev(bits.view(np.int16)).view(torch.bfloat16)
+
+
+def words_np(codes_t):
+    return codes_t.cpu().numpy().view(np.uint32)
+
+
+def ulp_diff(a, b):
+    a = np.asarray(a, np.float32).view(np.int32).astype(np.int64)
+    b = np.asarray(b, np.float32).view(np.int32).astype(np.int64)
+    return np.abs(a - b)
+
+
+# ---------------------------------------------------------------------------------------
+# Quantiser (Sec. 2 Eq. 3-5)
+# ---------------------------------------------------------------------------------------
+def _boundary_weights(K, n, name):
+    g = synth.rng(0, name)
+    base = np.array([-1.0, 0.0, -0.0, 1.0, 2.0, -2.0, 1e-40, -1e-40, 3.4e38, -3.4e38], np.float32)
+    vals = base[g.integers(0, base.size, size=(K, n))]
+    steps = g.integers(-2, 3, size=(K, n))
+    out = vals.copy()
+    for s in (-2, -1, 1, 2):
+        m = steps == s
+        v = out[m]
+        for _ in range(abs(s)):
+            v = np.nextafter(v, np.float32(np.sign(s) * np.inf))
+        out[m] = v
+    return out.astype(np.float32)
+
+
+QCASES = [
+    # K, n, distribution
+    (1, 1, "n1"), (32, 25, "n0.05"), (64, 800, "n0.05"), (10, 512, "n1"), (130, 2304, "n1"),
+    (512, 3136, "n0.05"), (7, 4608, "n3"), (65, 129, "boundary"), (200, 64, "boundary"),
+    (3, 100, "zeros"), (1000, 512, "n1"),
+]
+
+
+@pytest.mark.parametrize("K,n,dist", QCASES)
+def test_quantize_parity(tbn, K, n, dist):
+    log("quantize K=%d n=%d %s" % (K, n, dist))
+    if dist == "boundary":
+        w = _boundary_weights(K, n, "qb%d_%d" % (K, n))
+    elif dist == "zeros":
+        w = np.zeros((K, n), np.float32)
+        w[1, :] = -0.0
+        w[2, 5] = 1e-45
+    else:
+        w = synth.normal(1, "q%d_%d_%s" % (K, n, dist), (K, n), float(dist[1:]))
+    q = oracle.quantize(w)
+    codes, alpha, counts = tbn.quantize(to_dev(w))
+    torch.cuda.synchronize()
+    assert np.array_equal(words_np(codes), oracle.pack(q.codes)), "packed codes differ"
+    assert np.array_equal(counts.cpu().numpy(), np.stack([q.b1_size, q.b2_size], 1)), "B1/B2 counts differ"
+    d = ulp_diff(alpha.cpu().numpy(), q.alpha)
+    assert d.max() <= 1, "alpha differs by %d ulp" % d.max()
+    log("  alpha ulp max %d, exact %d/%d" % (d.max(), int((d == 0).sum()), K))
+
+
+def test_quantize_bit_pattern_sweep(tbn):
+    # Every fp32 sign/exponent/top-7-fraction pattern with 16 low-fraction variants:
+    # 2^16 * 16 values, finite ones compared with the oracle; NaN -> code -1 by contract.
+    hi = np.arange(1 << 16, dtype=np.uint32) << 16
+    lo = np.array([0, 1, 2, 3, 0x7FFF, 0x8000, 0x8001, 0xFFFE, 0xFFFF, 0x1234, 0x4000, 0xC000,
+                   0x00FF, 0xFF00, 0x5555, 0xAAAA], np.uint32)
+    bits = (hi[:, None] | lo[None, :]).ravel()
+    w = bits.view(np.float32)
+    finite = np.isfinite(w)
+    wf = w[finite]
+    n = 4096
+    wf = wf[: wf.size // n * n].reshape(-1, n)
+    q = oracle.quantize(wf)
+    codes, _, _ = tbn.quantize(to_dev(wf))
+    torch.cuda.synchronize()
+    assert np.array_equal(words_np(codes), oracle.pack(q.codes))
+    # non-finite inputs: +-inf behave as |W| > 1; NaN takes code -1
+    special = np.array([[np.inf, -np.inf, np.nan, -np.nan, 0.5, -0.5, 2.0, -2.0]], np.float32)
+    codes, _, _ = tbn.quantize(to_dev(special))
+    torch.cuda.synchronize()
+    got = oracle.unpack(words_np(codes), 1, 8)[0].tolist()
+    assert got == [2, -2, -1, -1, 1, -1, 2, -2]
+
+
+# ---------------------------------------------------------------------------------------
+# Convolutions (Sec. 2 Eq. 1; Sec. 3)
+# ---------------------------------------------------------------------------------------
+CONV_CASES = [
+    # n, h, w, c, k, r, s, stride, pad
+    (16, 28, 28, 1, 32, 5, 5, 1, 2),        # single two-bit layer, MNIST-shaped
+    (4, 14, 14, 32, 64, 5, 5, 1, 2),        # LeNet conv2 shape, small batch
+    (2, 9, 9, 3, 5, 3, 3, 2, 1),            # tiny, ragged everything
+    (2, 16, 16, 64, 64, 3, 3, 1, 1),
+    (2, 15, 13, 64, 96, 3, 3, 1, 1),        # ragged pixels and filters
+    (3, 12, 12, 128, 130, 3, 3, 2, 1),      # stride 2, filters beyond two 64-blocks
+    (2, 14, 14, 256, 256, 3, 3, 1, 1),
+    (4, 1, 1, 512, 10, 1, 1, 1, 0),         # FC 512 -> 10 as a 1x1 conv
+    (8, 7, 7, 64, 512, 7, 7, 1, 0),         # FC 3136 -> 512 as a 7x7 "valid" conv
+    (2, 16, 16, 64, 128, 1, 1, 2, 0),       # 1x1 stride-2 projection
+    (1, 33, 31, 3, 64, 7, 7, 2, 3),         # stem-like, C = 3
+    (2, 10, 10, 40, 24, 3, 3, 1, 1),        # C = 40 (not a multiple of 64), K = 24
+]
+
+
+def _conv_inputs(g, stream, wstd=1.0):
+    n, h, w, c, k, r, s, st, pd = g
+    d = oracle.ConvDesc(*g)
+    P, Q = d.out_dims()
+    xb = synth.normal_bf16(stream, "x%s" % (g,), (n, h, w, c))
+    dyb = synth.normal_bf16(stream, "dy%s" % (g,), (n, P, Q, k))
+    wr = synth.normal(stream, "w%s" % (g,), (k, r * s * c), wstd)
+    return d, P, Q, xb, dyb, wr
+
+
+@pytest.mark.parametrize("g", CONV_CASES)
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_fwd_parity(tbn, g, out):
+    log("fwd %s out=%s" % (g, out))
+    d, P, Q, xb, _, wr = _conv_inputs(g, 2)
+    q = oracle.quantize(wr)
+    ref = oracle.conv_fwd(d, oracle.bf16_bits_to_f64(xb), q.codes, q.alpha.astype(np.float64))
+    codes, alpha, _ = tbn.quantize(to_dev(wr))
+    desc = tbn.ConvDesc(*g)
+    y = tbn.conv2d_fwd(desc, bf16_dev(xb), codes, alpha,
+                       out_dtype=torch.float32 if out == "f32" else torch.bfloat16)
+    torch.cuda.synchronize()
+    e = nerr(y.float().cpu().numpy(), ref)
+    log("  normalised max error %.3e" % e)
+    assert e <= (1e-4 if out == "f32" else TOL)
+
+
+def test_fwd_fp32_input_single_layer(tbn):
+    # 16 x 1 x 28 x 28 fp32 uniform[0,1) input, 32 filters 5x5, pad 2, N(0, 0.05) masters.
+    g = (16, 28, 28, 1, 32, 5, 5, 1, 2)
+    d = oracle.ConvDesc(*g)
+    x = synth.uniform(0, "x", (16, 28, 28, 1))
+    wr = synth.normal(0, "w", (32, 25), 0.05)
+    q = oracle.quantize(wr)
+    ref = oracle.conv_fwd(d, oracle.round_bf16(x), q.codes, q.alpha.astype(np.float64))
+    codes, alpha, _ = tbn.quantize(to_dev(wr))
+    y = tbn.conv2d_fwd(tbn.ConvDesc(*g), to_dev(x), codes, alpha, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert np.array_equal(words_np(codes), oracle.pack(q.codes))
+    e = nerr(y.cpu().numpy(), ref)
+    log("single layer fp32 input: normalised max error %.3e" % e)
+    assert e <= 1e-4
+
+
+@pytest.mark.parametrize("g", [(2, 16, 16, 64, 64, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1),
+                               (3, 12, 12, 128, 130, 3, 3, 2, 1), (2, 10, 10, 40, 24, 3, 3, 1, 1)])
+def test_fwd_epilogue(tbn, g):
+    log("fwd epilogue %s" % (g,))
+    d, P, Q, xb, _, wr = _conv_inputs(g, 3)
+    k = g[4]
+    q = oracle.quantize(wr)
+    scale = synth.uniform(3, "sc", (k,), 0.5, 1.5)
+    bias = synth.normal(3, "bi", (k,), 0.1)
+    resb = synth.normal_bf16(3, "res", (g[0], P, Q, k))
+    acc = oracle.conv_fwd(d, oracle.bf16_bits_to_f64(xb), q.codes, q.alpha.astype(np.float64))
+    ref = np.maximum(acc * scale.astype(np.float64) + bias + oracle.bf16_bits_to_f64(resb), 0.0)
+    codes, alpha, _ = tbn.quantize(to_dev(wr))
+    y = tbn.conv2d_fwd(tbn.ConvDesc(*g), bf16_dev(xb), codes, alpha, out_dtype=torch.bfloat16,
+                       scale=to_dev(scale), bias=to_dev(bias), residual=bf16_dev(resb), relu=True)
+    torch.cuda.synchronize()
+    e = nerr(y.float().cpu().numpy(), ref)
+    log("  normalised max error %.3e" % e)
+    assert e <= TOL
+
+
+BWD_CASES = [c for c in CONV_CASES if c[7] == 1] + [(2, 8, 8, 64, 64, 3, 3, 1, 0), (2, 6, 6, 64, 64, 5, 5, 1, 4)]
+
+
+@pytest.mark.parametrize("g", BWD_CASES)
+def test_bwd_data_parity(tbn, g):
+    log("bwd_data %s" % (g,))
+    d, P, Q, _, dyb, wr = _conv_inputs(g, 4)
+    q = oracle.quantize(wr)
+    ref = oracle.conv_bwd_data(d, oracle.bf16_bits_to_f64(dyb), q.codes, q.alpha.astype(np.float64))
+    codes, alpha, _ = tbn.quantize(to_dev(wr))
+    dx = tbn.conv2d_bwd_data(tbn.ConvDesc(*g), bf16_dev(dyb), codes, alpha, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    e = nerr(dx.cpu().numpy(), ref)
+    log("  normalised max error %.3e" % e)
+    assert e <= TOL
+
+
+@pytest.mark.parametrize("g", CONV_CASES)
+@pytest.mark.parametrize("accumulate", [False, True])
+def test_bwd_weight_parity(tbn, g, accumulate):
+    log("bwd_weight %s accumulate=%s" % (g, accumulate))
+    d, P, Q, xb, dyb, _ = _conv_inputs(g, 5)
+    ref = oracle.conv_bwd_weight(d, oracle.bf16_bits_to_f64(xb), oracle.bf16_bits_to_f64(dyb))
+    prior = synth.normal(5, "prior%s" % (g,), ref.shape, 1.0)
+    dw0 = to_dev(prior) if accumulate else None
+    dw = tbn.conv2d_bwd_weight(tbn.ConvDesc(*g), bf16_dev(xb), bf16_dev(dyb), dw=dw0, accumulate=accumulate)
+    torch.cuda.synchronize()
+    want = ref + prior if accumulate else ref
+    e = nerr(dw.cpu().numpy(), want)
+    log("  normalised max error %.3e" % e)
+    assert e <= 1e-4
+
+
+def test_sgd_parity(tbn):
+    n = 1_000_003
+    w = synth.normal(6, "w", (n,), 0.05)
+    v = synth.normal(6, "v", (n,), 0.01)
+    g = synth.normal(6, "g", (n,), 1.0)
+    wr, vr = oracle.sgd(w, v, g, 0.1, 0.9, 1e-4)
+    wt, vt = to_dev(w), to_dev(v)
+    tbn.sgd_step(wt, vt, to_dev(g), 0.1, 0.9, 1e-4)
+    torch.cuda.synchronize()
+    assert nerr(wt.cpu().numpy(), wr) <= 1e-6
+    assert nerr(vt.cpu().numpy(), vr) <= 1e-6
+
+
+def test_repeat_runs_are_bitwise_identical(tbn):
+    g = (2, 14, 14, 256, 256, 3, 3, 1, 1)
+    _, _, _, xb, dyb, wr = _conv_inputs(g, 7)
+    desc = tbn.ConvDesc(*g)
+    codes, alpha, _ = tbn.quantize(to_dev(wr))
+    x, dy = bf16_dev(xb), bf16_dev(dyb)
+    outs = []
+    for _ in range(3):
+        outs.append((tbn.conv2d_fwd(desc, x, codes, alpha).clone(),
+                     tbn.conv2d_bwd_data(desc, dy, codes, alpha).clone(),
+                     tbn.conv2d_bwd_weight(desc, x, dy).clone()))
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        for a, b in zip(o, outs[0]):
+            assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a.view(torch.int32),
+                               b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32))
