@@ -19,6 +19,8 @@
 //     filter (l % 32) of its 32-column group (one coalesced 16-byte load per lane, 512
 //     bytes per wave) and decodes at each 16-element MFMA step the 8 elements the MFMA
 //     B layout gives it (elements 8*(l/32)..+7 of the step) with 2 integer ops per pair.
+#include <cstdlib>
+
 #include "tbn_device.h"
 #include "tbn_kernels.h"
 
@@ -58,8 +60,11 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(const ConvGemmArgs a) {
     const int nchunks = (n + BK - 1) / BK;
     const int KB = (a.Kf + 63) / 64;
     const int tilesN = (a.Kf + BN - 1) / BN;
-    const int64_t tm = blockIdx.x / tilesN;
-    const int tn = blockIdx.x % tilesN;
+    // XCD-aware order: each XCD runs a contiguous range of tiles (column tiles of one row
+    // tile first), so the activation rows and halos a tile re-reads stay in one L2.
+    const int64_t tile = xcd_remap(blockIdx.x, gridDim.x);
+    const int64_t tm = tile / tilesN;
+    const int tn = (int)(tile % tilesN);
     const int64_t m0 = tm * BM;
     const int n0 = tn * BN;
     const int64_t HWC = (int64_t)a.H * a.W * C;
@@ -298,9 +303,16 @@ hipError_t launch_cfg(const ConvGemmArgs& a, hipStream_t stream) {
     return hipGetLastError();
 }
 
+// Tile-shape override for tuning and for the tests that cover every shape:
+// TBN_CONV_TILE=<index> (read at each launch; unset = the built-in choice).
+int tile_override() {
+    const char* e = getenv("TBN_CONV_TILE");
+    return e ? atoi(e) : -1;
+}
+
 template <int AM, bool BWD>
-hipError_t launch_mode(const ConvGemmArgs& a, hipStream_t stream) {
-    if (a.Kf <= 64) return launch_cfg<256, 64, 64, 64, AM, BWD>(a, stream);
+hipError_t launch_mode(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
+    if (cfg == 1 || (cfg < 0 && a.Kf <= 64)) return launch_cfg<256, 64, 64, 64, AM, BWD>(a, stream);
     return launch_cfg<128, 128, 64, 64, AM, BWD>(a, stream);
 }
 
@@ -359,10 +371,15 @@ __global__ __launch_bounds__(256) void repack_bwd_kernel(const uint32_t* __restr
 
 }  // namespace
 
-hipError_t launch_conv_gemm(const ConvGemmArgs& a, hipStream_t stream) {
+hipError_t launch_conv_gemm(const ConvGemmArgs& args, hipStream_t stream) {
+    ConvGemmArgs a = args;
+    a.div_q = make_fastdiv((uint32_t)a.Q);
+    a.div_pq = make_fastdiv((uint32_t)a.P * (uint32_t)a.Q);
+    const int cfg = tile_override();
+    if (conv_dma_eligible(a) && (cfg < 0 || cfg >= 10)) return launch_conv_dma(a, cfg, stream);
     const bool vec = (a.C % 8 == 0) && !a.x_f32;
-    if (a.apair) return vec ? launch_mode<A_VEC8, true>(a, stream) : launch_mode<A_SCALAR, true>(a, stream);
-    return vec ? launch_mode<A_VEC8, false>(a, stream) : launch_mode<A_SCALAR, false>(a, stream);
+    if (a.apair) return vec ? launch_mode<A_VEC8, true>(a, cfg, stream) : launch_mode<A_SCALAR, true>(a, cfg, stream);
+    return vec ? launch_mode<A_VEC8, false>(a, cfg, stream) : launch_mode<A_SCALAR, false>(a, cfg, stream);
 }
 
 hipError_t launch_repack_bwd(const uint32_t* codes, const float* alpha, int32_t K, int32_t R, int32_t S,

@@ -1,0 +1,492 @@
+// tbn_conv_dma.hip -- the main implicit-GEMM convolution kernel for bf16 NHWC activations
+// with C % 8 == 0 (every layer of the workloads except the C = 1 / C = 3 first layers).
+// It computes the same GEMM as tbn_conv.hip (the forward pass, Sec. 2 Eq. 1, and the
+// backward-data pass through the approximate filters, Sec. 3) at a much lower
+// instruction count per MFMA:
+//
+//   * every operand of a stage goes from memory straight into LDS with buffer loads in
+//     LDS-DMA mode: the activation tile (16 bytes per lane), the 1 KiB packed-code blocks
+//     of the tile's filters, and in the backward-data pass the stage's bf16 scale pairs.
+//     Zero padding costs nothing: an out-of-image tap gets an out-of-range buffer offset
+//     and the hardware returns zeros.  Which of a row's R*S taps fall inside the image is
+//     precomputed once per row as a 64-bit mask;
+//   * the DMAs run up to three stages deep (a ring of LDS buffers): the loads of stage
+//     c+2 are in flight while stage c is multiplied.  They are issued from inline
+//     assembly and waited for with explicit vmcnt counts, because the compiler treats
+//     any LDS-DMA as a write to all of LDS and would otherwise wait for every
+//     outstanding DMA before each LDS read;
+//   * LDS rows are 128 bytes (64 bf16) with the 16-byte segments XOR-swizzled by
+//     (row / 2) % 8, so the DMA writes and the 16-byte MFMA operand reads are free of
+//     bank conflicts without padding;
+//   * the two-bit filter operand is decoded in registers from the LDS copy of the codes
+//     (one AND and one shift-add per bf16 pair, per-lane masks precomputed);
+//   * the MFMA is issued with the decoded filters as its first operand, so the
+//     accumulators hold the transposed tile and each lane owns runs of four consecutive
+//     output channels of one pixel; the epilogue stages each tile row through LDS with
+//     16-byte writes and applies scale, bias, residual and ReLU to 8 consecutive
+//     channels per lane, written with 16-byte stores;
+//   * blocks are ordered XCD-aware (each XCD runs a contiguous range of tiles).
+//
+// M0 is written by the DMA helper; nothing else in these kernels uses M0.
+#include "tbn_device.h"
+#include "tbn_kernels.h"
+
+namespace tbn {
+
+namespace {
+
+constexpr int BK = 64;     // reduction elements per stage
+constexpr int ROWB = 128;  // LDS bytes per activation row of a stage
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// Buffer resource for raw (unstructured) buffer loads of `bytes` bytes at `base`.
+__device__ __forceinline__ v4i make_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    v4i r;
+    r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    r.y = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xFFFFu));
+    r.z = __builtin_amdgcn_readfirstlane((int)bytes);
+    r.w = 0x00020000;
+    return r;
+}
+
+// One LDS-DMA: lane i's 16 (or 4) bytes at byte `voff` of the buffer land at LDS
+// address lds + 16*i (4*i).  An offset beyond the buffer yields zeros.
+__device__ __forceinline__ void dma_b128(v4i rsrc, uint32_t lds, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(lds), "v"(voff), "s"(rsrc)
+                 : "memory");
+}
+__device__ __forceinline__ void dma_b32(v4i rsrc, uint32_t lds, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :
+                 : "s"(lds), "v"(voff), "s"(rsrc)
+                 : "memory");
+}
+
+// s_waitcnt vmcnt(n) (gfx9 encoding: vmcnt in bits 3:0 and 15:14; others left at max)
+__device__ __forceinline__ void wait_vmcnt(int n) {
+    switch (n) {
+        case 0: __builtin_amdgcn_s_waitcnt(0x0F70); break;
+        case 1: __builtin_amdgcn_s_waitcnt(0x0F71); break;
+        case 2: __builtin_amdgcn_s_waitcnt(0x0F72); break;
+        case 3: __builtin_amdgcn_s_waitcnt(0x0F73); break;
+        case 4: __builtin_amdgcn_s_waitcnt(0x0F74); break;
+        case 5: __builtin_amdgcn_s_waitcnt(0x0F75); break;
+        case 6: __builtin_amdgcn_s_waitcnt(0x0F76); break;
+        case 7: __builtin_amdgcn_s_waitcnt(0x0F77); break;
+        case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
+        case 9: __builtin_amdgcn_s_waitcnt(0x0F79); break;
+        case 10: __builtin_amdgcn_s_waitcnt(0x0F7A); break;
+        default: __builtin_amdgcn_s_waitcnt(0x0F70); break;
+    }
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+template <int BM, int BN>
+struct StageLayout {
+    static constexpr int A = 0;                  // BM rows x 128 B
+    static constexpr int B = BM * ROWB;          // BN filters x 16 B (BN/64 blocks of 1 KiB)
+    static constexpr int P = B + BN * 16;        // 256 B of bf16 scale pairs (backward-data)
+    static constexpr int BYTES = P + 256;
+};
+
+// UNI: C % 64 == 0, so all 64 elements of a stage share one tap (r, s) and the tap
+// bookkeeping is wave-uniform (scalar registers).
+template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool BWD, bool UNI>
+__global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) {
+    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+    constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr int AR = BM / 32;      // activation DMAs per wave per stage (8 rows each)
+    constexpr int NBLK = BN / 64;    // 1 KiB code blocks per stage
+    using L = StageLayout<BM, BN>;
+    static_assert(WAVES_M * WAVES_N == 4, "four waves per block");
+    static_assert(TM >= 1 && TN >= 1 && BM % 32 == 0 && BN % 64 == 0 && NBLK <= 4, "tile shape");
+    static_assert(STAGES * L::BYTES >= 4 * 32 * (WN + 4) * 4, "epilogue staging fits in the ring");
+
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * L::BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WAVES_N;
+    const int wn = wave % WAVES_N;
+    const int half = lane >> 5;
+    const int l32 = lane & 31;
+
+    const int64_t PQ = (int64_t)a.P * a.Q;
+    const int64_t M = (int64_t)a.N * PQ;
+    const int C = a.C;
+    const int n = a.R * a.S * C;
+    const int nchunks = (n + BK - 1) / BK;
+    const int KB = (a.Kf + 63) / 64;
+    const int tilesN = (a.Kf + BN - 1) / BN;
+    const int64_t tile = xcd_remap(blockIdx.x, gridDim.x);
+    const int64_t m0 = (tile / tilesN) * BM;
+    const int n0 = (int)(tile % tilesN) * BN;
+
+    const v4i rs_x = make_rsrc(a.x, (uint32_t)((int64_t)a.N * a.H * a.W * C * 2));
+    const v4i rs_c = make_rsrc(a.codes, (uint32_t)((int64_t)KB * nchunks * 1024));
+    v4i rs_p = rs_c;
+    if constexpr (BWD) rs_p = make_rsrc(a.apair, (uint32_t)nchunks * 128u);
+    const uint32_t smem_base = lds_addr(smem);
+
+    // ---- activation rows this lane fills: row = 8 * (wave + 4 j) + lane / 8 ----
+    int32_t rbase[AR];      // element offset of the row's (h0, w0) in x (may be negative)
+    uint32_t rmask[AR][2];  // bit r*S + s of the 64 set iff tap (r, s) lies inside the image
+#pragma unroll
+    for (int j = 0; j < AR; ++j) {
+        const int64_t m = m0 + 8 * (wave + 4 * j) + (lane >> 3);
+        uint64_t mask = 0;
+        rbase[j] = 0;
+        if (m < M) {
+            const uint32_t mm = (uint32_t)m;  // < 2^31, checked by the host
+            const uint32_t img = fdiv(mm, a.div_pq);
+            const uint32_t pq = mm - img * (uint32_t)PQ;
+            const uint32_t p = fdiv(pq, a.div_q);
+            const uint32_t q = pq - p * (uint32_t)a.Q;
+            const int h0 = (int)p * a.sh - a.ph, w0 = (int)q * a.sw - a.pw;
+            rbase[j] = ((int32_t)img * a.H + h0) * a.W * C + w0 * C;
+            uint64_t wbits = 0;
+            for (int s = 0; s < a.S; ++s)
+                if ((unsigned)(w0 + s) < (unsigned)a.W) wbits |= 1ull << s;
+            for (int r = 0; r < a.R; ++r)
+                if ((unsigned)(h0 + r) < (unsigned)a.H) mask |= wbits << (r * a.S);
+        }
+        rmask[j][0] = (uint32_t)mask;
+        rmask[j][1] = (uint32_t)(mask >> 32);
+    }
+    // logical 16-byte segment this lane loads (its LDS slot is lane % 8 of the row)
+    const int lseg = (lane & 7) ^ ((4 * (wave & 1)) | ((lane >> 4) & 3));
+    // general path: (r, s, c) of element 8 * lseg of the next stage to issue (per lane)
+    int er = 0, es = 0, ec = 0;
+    // uniform path: (r, s) and first channel of the next stage (the same for every lane)
+    int ur = 0, us = 0, uc = 0;
+    int32_t rb2[AR];        // uniform path: row offset plus this lane's channel offset
+    uint32_t nmask[AR][2];  // uniform path: complement of rmask (bit set = tap outside)
+    if constexpr (UNI) {
+#pragma unroll
+        for (int j = 0; j < AR; ++j) {
+            rb2[j] = rbase[j] + 8 * lseg;
+            nmask[j][0] = ~rmask[j][0];
+            nmask[j][1] = ~rmask[j][1];
+        }
+    } else {
+        const int e0 = lseg * 8;
+        const int rs = e0 / C;
+        ec = e0 - rs * C;
+        er = rs / a.S;
+        es = rs - er * a.S;
+    }
+    // code block of this wave (waves < NBLK copy one 1 KiB block per stage)
+    const int fb = n0 / 64 + wave;
+    const bool copies_codes = wave < NBLK;
+    const bool codes_valid = fb < KB;
+    const bool copies_pairs = BWD && wave == 0;
+    const int dmas = AR + (copies_codes ? 1 : 0) + (copies_pairs ? 1 : 0);  // per stage, this wave
+
+    auto issue = [&](int chunk) {
+        const uint32_t st = smem_base + (uint32_t)((chunk % STAGES) * L::BYTES);
+        if constexpr (UNI) {
+            // out-of-image taps (and the padding stage past the filter, tap clamped to
+            // bit 63, which is clear in rmask because R*S <= 63) get offset bit 31 set,
+            // beyond the buffer, so the hardware returns zeros
+            const int tap = min(ur * a.S + us, 63);
+            const int32_t toff = (ur * a.W + us) * C + uc;
+            if (tap < 32) {
+#pragma unroll
+                for (int j = 0; j < AR; ++j) {
+                    const uint32_t out = (nmask[j][0] >> tap) & 1u;
+                    dma_b128(rs_x, st + L::A + (uint32_t)(8 * (wave + 4 * j) * ROWB),
+                             ((uint32_t)(rb2[j] + toff) << 1) | (out << 31));
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < AR; ++j) {
+                    const uint32_t out = (nmask[j][1] >> (tap - 32)) & 1u;
+                    dma_b128(rs_x, st + L::A + (uint32_t)(8 * (wave + 4 * j) * ROWB),
+                             ((uint32_t)(rb2[j] + toff) << 1) | (out << 31));
+                }
+            }
+            uc += BK;
+            if (uc == C) {
+                uc = 0;
+                if (++us == a.S) {
+                    us = 0;
+                    ++ur;
+                }
+            }
+        } else {
+            // taps past the filter (padding elements of the last stage) clamp to bit 63,
+            // which is clear because R*S <= 63
+            const int tap = min(er * a.S + es, 63);
+            const int tword = tap >> 5, tbit = tap & 31;
+            const int32_t toff = (er * a.W + es) * C + ec;
+#pragma unroll
+            for (int j = 0; j < AR; ++j) {
+                const bool ok = ((tword ? rmask[j][1] : rmask[j][0]) >> tbit) & 1u;
+                const uint32_t off = ok ? (uint32_t)(rbase[j] + toff) << 1 : 0x80000000u;
+                dma_b128(rs_x, st + L::A + (uint32_t)(8 * (wave + 4 * j) * ROWB), off);
+            }
+            ec += BK;
+            while (ec >= C) {
+                ec -= C;
+                if (++es == a.S) {
+                    es = 0;
+                    ++er;
+                }
+            }
+        }
+        if (copies_codes) {
+            const uint32_t off = codes_valid ? (uint32_t)(((int64_t)fb * nchunks + chunk) * 1024 + lane * 16)
+                                             : 0x80000000u;
+            dma_b128(rs_c, st + L::B + (uint32_t)(wave * 1024), off);
+        }
+        if constexpr (BWD) {
+            if (copies_pairs) {
+                const uint32_t off = lane < 32 ? (uint32_t)(chunk * 128 + lane * 4) : 0x80000000u;
+                dma_b32(rs_p, st + L::P, off);
+            }
+        }
+    };
+
+    // ---- operand addressing inside a stage ----
+    const int sw = (l32 >> 1) & 7;  // row swizzle of this lane's MFMA rows
+    int seg_off[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) seg_off[u] = 16 * ((2 * u + half) ^ sw);
+    const int arow = (wm * WM + l32) * ROWB;
+    const int bcol = (wn * WN + l32) * 16;
+    uint32_t mk[4], shl[4];
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+        mk[jj] = 0x01010101u << (4 * half + jj);
+        shl[jj] = 7 - 4 * half - jj;
+    }
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][t][v] = 0.0f;
+
+    // prologue: the first STAGES-1 stages in flight
+#pragma unroll
+    for (int c = 0; c < STAGES - 1; ++c)
+        if (c < nchunks) issue(c);
+    for (int chunk = 0; chunk < nchunks; ++chunk) {
+        // this wave's DMAs of stage `chunk` landed (later stages may still be in flight)
+        const int later = min(nchunks - 1 - chunk, STAGES - 2);
+        wait_vmcnt(later * dmas);
+        __syncthreads();  // ... and every other wave's; all reads of stage chunk-1 are done
+        if (chunk + STAGES - 1 < nchunks) issue(chunk + STAGES - 1);  // into stage chunk-1's buffer
+        const uint8_t* st = smem + (chunk % STAGES) * L::BYTES;
+        u32x4 braw[TN];
+#pragma unroll
+        for (int t = 0; t < TN; ++t) braw[t] = *reinterpret_cast<const u32x4*>(st + L::B + bcol + 32 * 16 * t);
+        u32x4 base[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if constexpr (BWD)
+                base[u] = *reinterpret_cast<const u32x4*>(st + L::P + 32 * u + 16 * half);
+            else
+                base[u] = u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
+        }
+        auto decode_b = [&](int u, bf16x8* bfr) {
+#pragma unroll
+            for (int t = 0; t < TN; ++t) {
+                const uint32_t w = braw[t][u];
+                u32x4 d;
+                d.x = ((w & mk[0]) << shl[0]) + base[u].x;
+                d.y = ((w & mk[1]) << shl[1]) + base[u].y;
+                d.z = ((w & mk[2]) << shl[2]) + base[u].z;
+                d.w = ((w & mk[3]) << shl[3]) + base[u].w;
+                bfr[t] = as_bf16x8(d);
+            }
+        };
+        auto read_a = [&](int u, bf16x8* af) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                af[i] = *reinterpret_cast<const bf16x8*>(st + L::A + arow + 32 * i * ROWB + seg_off[u]);
+        };
+        if constexpr (TM <= 4) {
+            // all of the stage's A operands are read up front so that LDS latency
+            // overlaps the decode and the first MFMAs
+            bf16x8 afs[4][TM];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) read_a(u, afs[u]);
+            __builtin_amdgcn_sched_barrier(0);  // keep the LDS reads ahead of the MFMAs
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                bf16x8 bfr[TN];
+                decode_b(u, bfr);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(bfr[t], afs[u][i], acc[i][t]);
+            }
+        } else {
+            // tall wave tiles: A operands one 16-element step ahead
+            bf16x8 afc[TM], afn[TM];
+            read_a(0, afc);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (u < 3) read_a(u + 1, afn);
+                bf16x8 bfr[TN];
+                decode_b(u, bfr);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(bfr[t], afc[i], acc[i][t]);
+                if (u < 3) {
+#pragma unroll
+                    for (int i = 0; i < TM; ++i) afc[i] = afn[i];
+                }
+            }
+        }
+    }
+
+    // ---- epilogue.  The MFMA computed the transposed tile (filters x pixels): lane l of
+    //      32x32 tile (i, t) holds pixel 32 i + l % 32 and, for each v / 4, four
+    //      consecutive filters 32 t + 8 (v / 4) + 4 (l / 32) + 0..3.  Each 32-pixel tile row
+    //      is staged through LDS with one 16-byte write per four filters, then every lane
+    //      takes 8 consecutive channels of one pixel, applies y = act(acc * colscale *
+    //      scale + bias + residual) and writes them with 16-byte stores. ----
+    __syncthreads();  // every wave is done reading the ring
+    constexpr int PITCH = WN + 4;  // floats per staged pixel row
+    float* stage = reinterpret_cast<float*>(smem) + wave * 32 * PITCH;
+    const int Kf = a.Kf;
+    constexpr int CG = WN / 8;    // 8-channel groups per pixel row of the wave tile
+    constexpr int RPP = 64 / CG;  // pixel rows per pass
+    const int gcol = lane % CG;
+    const int grow = lane / CG;
+    const int col0 = n0 + wn * WN + 8 * gcol;
+    float cs[8], bi[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int col = col0 + e;
+        const bool ok = col < Kf;
+        float sc = ok && a.colscale ? a.colscale[col] : 1.0f;
+        if (ok && a.scale) sc *= a.scale[col];
+        cs[e] = sc;
+        bi[e] = ok && a.bias ? a.bias[col] : 0.0f;
+    }
+    const bool vec_store = (Kf % 8) == 0;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<f32x4*>(&stage[l32 * PITCH + 32 * t + 8 * g + 4 * half]) =
+                    f32x4{acc[i][t][4 * g], acc[i][t][4 * g + 1], acc[i][t][4 * g + 2], acc[i][t][4 * g + 3]};
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS writes are visible to it
+#pragma unroll
+        for (int pass = 0; pass < 32 / RPP; ++pass) {
+            const int r = pass * RPP + grow;
+            const int64_t row = m0 + wm * WM + 32 * i + r;
+            if (row >= M) continue;
+            const f32x4 lo = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol]);
+            const f32x4 hi = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol + 4]);
+            float v8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+            const int64_t o = row * Kf + col0;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v8[e] = v8[e] * cs[e] + bi[e];
+            if (a.residual) {
+                if (a.y_f32) {
+                    const float* rp = reinterpret_cast<const float*>(a.residual) + o;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (col0 + e < Kf) v8[e] += rp[e];
+                } else {
+                    const uint16_t* rp = reinterpret_cast<const uint16_t*>(a.residual) + o;
+                    if (vec_store && col0 < Kf) {
+                        const u32x4 r8 = *reinterpret_cast<const u32x4*>(rp);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            v8[2 * e] += bf16_bits_to_f32(r8[e] & 0xFFFFu);
+                            v8[2 * e + 1] += bf16_bits_to_f32(r8[e] >> 16);
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (col0 + e < Kf) v8[e] += bf16_bits_to_f32(rp[e]);
+                    }
+                }
+            }
+            if (a.relu) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v8[e] = fmaxf(v8[e], 0.0f);
+            }
+            if (a.y_f32) {
+                float* yp = reinterpret_cast<float*>(a.y) + o;
+                if (vec_store && col0 < Kf) {
+                    *reinterpret_cast<f32x4*>(yp) = f32x4{v8[0], v8[1], v8[2], v8[3]};
+                    *reinterpret_cast<f32x4*>(yp + 4) = f32x4{v8[4], v8[5], v8[6], v8[7]};
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (col0 + e < Kf) yp[e] = v8[e];
+                }
+            } else {
+                uint16_t* yp = reinterpret_cast<uint16_t*>(a.y) + o;
+                if (vec_store && col0 < Kf) {
+                    *reinterpret_cast<u32x4*>(yp) = u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]),
+                                                          pack_bf16x2(v8[4], v8[5]), pack_bf16x2(v8[6], v8[7])};
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (col0 + e < Kf) yp[e] = (uint16_t)f32_to_bf16_bits(v8[e]);
+                }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // reads of this tile row done before it is overwritten
+    }
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool BWD>
+hipError_t launch_dma_cfg(const ConvGemmArgs& a, hipStream_t stream) {
+    const int64_t M = (int64_t)a.N * a.P * a.Q;
+    const int64_t tiles = ((M + BM - 1) / BM) * ((a.Kf + BN - 1) / BN);
+    if (a.C % 64 == 0)
+        hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, true>), dim3((unsigned)tiles),
+                           dim3(256), 0, stream, a);
+    else
+        hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, false>), dim3((unsigned)tiles),
+                           dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+template <bool BWD>
+hipError_t launch_dma_mode(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
+    if (cfg < 10) cfg = a.Kf > 128 ? 10 : (a.Kf > 64 ? 12 : 14);
+    switch (cfg) {
+        case 11: return launch_dma_cfg<128, 128, 1, 4, 3, BWD>(a, stream);
+        case 12: return launch_dma_cfg<128, 128, 2, 2, 3, BWD>(a, stream);
+        case 14: return launch_dma_cfg<128, 64, 2, 2, 3, BWD>(a, stream);
+        case 16: return launch_dma_cfg<256, 128, 1, 4, 2, BWD>(a, stream);
+        default: return launch_dma_cfg<128, 256, 1, 4, 3, BWD>(a, stream);
+    }
+}
+
+}  // namespace
+
+bool conv_dma_eligible(const ConvGemmArgs& a) {
+    const int64_t xbytes = (int64_t)a.N * a.H * a.W * a.C * 2;
+    const int64_t nchunks = ((int64_t)a.R * a.S * a.C + BK - 1) / BK;
+    const int64_t cbytes = (int64_t)((a.Kf + 63) / 64) * nchunks * 1024;
+    return !a.x_f32 && a.C % 8 == 0 && a.R * a.S <= 63 && xbytes < 0x7FFFFFF0ll && cbytes < 0x7FFFFFF0ll;
+}
+
+hipError_t launch_conv_dma(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
+    return a.apair ? launch_dma_mode<true>(a, cfg, stream) : launch_dma_mode<false>(a, cfg, stream);
+}
+
+}  // namespace tbn

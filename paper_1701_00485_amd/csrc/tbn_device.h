@@ -15,19 +15,20 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
-// fp32 -> bf16 bits, round to nearest even (NaN kept quiet).
+// fp32 -> bf16 bits, round to nearest even (the gfx950 conversion instruction).
 __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (u >> 16) | 0x40u;
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return u >> 16;
+    return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
-// Two bf16 values packed low/high into one 32-bit word.
+// Two bf16 values packed low/high into one 32-bit word (one v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    bf16x2 v;
+    v.x = (__bf16)lo;
+    v.y = (__bf16)hi;
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 // Decode four bf16 pairs (8 consecutive elements) from one packed word.
@@ -49,6 +50,16 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own L2).  This
+// maps dispatch index b of nblocks to a work index such that every XCD receives one
+// contiguous range of work indices, keeping neighbouring tiles in one L2.
+__device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t nblocks) {
+    constexpr int64_t kXcd = 8;
+    const int64_t per = nblocks / kXcd, rem = nblocks % kXcd;
+    const int64_t xcd = b % kXcd, local = b / kXcd;
+    return xcd * per + (xcd < rem ? xcd : rem) + local;
 }
 
 }  // namespace tbn

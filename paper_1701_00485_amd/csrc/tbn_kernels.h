@@ -6,6 +6,26 @@
 
 namespace tbn {
 
+// Unsigned division by a runtime constant d >= 1 for numerators below 2^31
+// (round-up multiplier: q = (mulhi(n, mul) + n) >> shift).
+struct FastDiv {
+    uint32_t d, mul, shift;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+    FastDiv f;
+    f.d = d;
+    uint32_t s = 0;
+    while ((1ull << s) < d) ++s;
+    f.shift = s;
+    f.mul = (uint32_t)(((1ull << 32) * ((1ull << s) - d)) / d + 1);
+    return f;
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
+    return (__umulhi(n, f.mul) + n) >> f.shift;
+}
+
 // Geometry + operands of the implicit GEMM that serves both the forward pass and the
 // backward-data pass.  Rows are output pixels (n, p, q) of an NHWC "input" x; columns
 // are the Kf "filters" whose packed codes hold n = R*S*C elements each.
@@ -22,12 +42,17 @@ struct ConvGemmArgs {
     int32_t relu;
     int32_t x_f32;
     int32_t y_f32;
+    FastDiv div_q, div_pq;    // division by Q and by P*Q (output pixel -> (n, p, q))
 };
 
 hipError_t launch_quantize(const float* w, int64_t K, int64_t n, uint32_t* codes, float* alpha,
                            int32_t* counts, hipStream_t stream);
 
 hipError_t launch_conv_gemm(const ConvGemmArgs& a, hipStream_t stream);
+
+// LDS-DMA variant (bf16 x, C % 8 == 0, R*S <= 63, x < 2 GiB); cfg selects the tile shape.
+bool conv_dma_eligible(const ConvGemmArgs& a);
+hipError_t launch_conv_dma(const ConvGemmArgs& a, int cfg, hipStream_t stream);
 
 // Re-pack the codes of K filters [K][R][S][C] into the codes of the C filters of the
 // transposed, spatially flipped layer [C][R][S][K] (backward-data operand), and build

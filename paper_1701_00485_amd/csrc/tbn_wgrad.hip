@@ -23,26 +23,6 @@ namespace {
 constexpr int BK = 64;
 constexpr int LDA = BK + 8;
 
-// Unsigned division by a runtime constant d >= 1 for numerators below 2^31
-// (round-up multiplier: q = (mulhi(n, mul) + n) >> shift).
-struct FastDiv {
-    uint32_t d, mul, shift;
-};
-
-inline FastDiv make_fastdiv(uint32_t d) {
-    FastDiv f;
-    f.d = d;
-    uint32_t s = 0;
-    while ((1ull << s) < d) ++s;
-    f.shift = s;
-    f.mul = (uint32_t)(((1ull << 32) * ((1ull << s) - d)) / d + 1);
-    return f;
-}
-
-__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
-    return (__umulhi(n, f.mul) + n) >> f.shift;
-}
-
 struct WgradKernelArgs {
     WgradArgs a;
     FastDiv div_q, div_pq;
@@ -100,17 +80,23 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradKernelArgs ka) {
     const int64_t M = (int64_t)a.N * PQ;
     const int64_t nchunks = (M + BK - 1) / BK;
     const int tilesJ = (J + BN - 1) / BN;
-    const int tk = blockIdx.x / tilesJ;
-    const int tj = blockIdx.x % tilesJ;
+    const int tiles = tilesJ * ((K + BM - 1) / BM);
+    // XCD-aware order: the blocks one XCD runs are consecutive in (split, tile) order, so
+    // the tiles sharing a split's pixel range share that XCD's L2.
+    const int t = (int)xcd_remap(blockIdx.x, gridDim.x);
+    const int split = t / tiles;
+    const int tk = (t % tiles) / tilesJ;
+    const int tj = (t % tiles) % tilesJ;
     const int k0 = tk * BM;
     const int j0 = tj * BN;
-    const int64_t c_begin = (int64_t)blockIdx.y * a.chunks_per_split;
+    const int64_t c_begin = (int64_t)split * a.chunks_per_split;
     int64_t c_end = c_begin + a.chunks_per_split;
     if (c_end > nchunks) c_end = nchunks;
 
-    // staging map: thread -> 8 columns (cg) x 4 pixels (pg)
-    const int cg = tid & 15;
-    const int pg = tid >> 4;  // 0..15: pixels 4*pg .. 4*pg+3 of the chunk
+    // staging map: thread -> 4 pixels (pg) x 8 columns (cg).  Pixel groups vary fastest
+    // so that the 16 lanes sharing a column write one contiguous 128-byte LDS row segment.
+    const int pg = tid & 15;  // pixels 4*pg .. 4*pg+3 of the chunk
+    const int cg = tid >> 4;  // columns 8*cg .. 8*cg+7 of the tile
     // dy columns
     const int kcol = k0 + 8 * cg;
     const bool k_ok = kcol < K;
@@ -217,7 +203,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradKernelArgs ka) {
         }
     }
 
-    float* out = a.out + (int64_t)blockIdx.y * K * J;
+    float* out = a.out + (int64_t)split * K * J;
 #pragma unroll
     for (int t = 0; t < TN; ++t) {
         const int col = j0 + wn * WN + 32 * t + l32;
@@ -254,7 +240,7 @@ hipError_t launch_wgrad(const WgradArgs& a, hipStream_t stream) {
     ka.a = a;
     ka.div_q = make_fastdiv((uint32_t)a.Q);
     ka.div_pq = make_fastdiv((uint32_t)a.P * (uint32_t)a.Q);
-    const dim3 grid((unsigned)tiles, (unsigned)a.splits);
+    const dim3 grid((unsigned)(tiles * a.splits));
     if (a.K % 8 == 0 && a.C % 8 == 0)
         hipLaunchKernelGGL((wgrad_kernel<128, 128, 64, 64, true>), grid, dim3(256), 0, stream, ka);
     else

@@ -273,3 +273,29 @@ def test_repeat_runs_are_bitwise_identical(tbn):
         for a, b in zip(o, outs[0]):
             assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a.view(torch.int32),
                                b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32))
+
+
+TILE_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1), (2, 10, 10, 40, 24, 3, 3, 1, 1),
+              (3, 12, 12, 128, 130, 3, 3, 2, 1)]
+
+
+@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 14, 16])
+def test_every_tile_shape(tbn, tile, monkeypatch):
+    # each tile shape of the convolution kernels against the oracle (fwd and bwd_data)
+    monkeypatch.setenv("TBN_CONV_TILE", str(tile))
+    for g in TILE_CASES:
+        log("tile %d %s" % (tile, g))
+        d, P, Q, xb, dyb, wr = _conv_inputs(g, 8)
+        q = oracle.quantize(wr)
+        a64 = q.alpha.astype(np.float64)
+        codes, alpha, _ = tbn.quantize(to_dev(wr))
+        desc = tbn.ConvDesc(*g)
+        y = tbn.conv2d_fwd(desc, bf16_dev(xb), codes, alpha, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        e = nerr(y.cpu().numpy(), oracle.conv_fwd(d, oracle.bf16_bits_to_f64(xb), q.codes, a64))
+        assert e <= 1e-4, "fwd tile %d %s: %.3e" % (tile, g, e)
+        if g[7] == 1:
+            dx = tbn.conv2d_bwd_data(desc, bf16_dev(dyb), codes, alpha, out_dtype=torch.float32)
+            torch.cuda.synchronize()
+            e = nerr(dx.cpu().numpy(), oracle.conv_bwd_data(d, oracle.bf16_bits_to_f64(dyb), q.codes, a64))
+            assert e <= TOL, "bwd_data tile %d %s: %.3e" % (tile, g, e)
