@@ -54,12 +54,23 @@ tbn_status check_desc(const tbn_conv_desc* d, Geometry* g) {
     return TBN_OK;
 }
 
-// bwd_weight: number of reduction splits for a geometry (shared by sizing and launch)
+tbn::WgradArgs wgrad_args(const Geometry& g) {
+    tbn::WgradArgs a = {};
+    a.N = (int32_t)g.N; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.C = (int32_t)g.C; a.K = (int32_t)g.K;
+    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = (int32_t)g.sh; a.sw = (int32_t)g.sw;
+    a.ph = (int32_t)g.ph; a.pw = (int32_t)g.pw; a.P = (int32_t)g.P; a.Q = (int32_t)g.Q;
+    return a;
+}
+
+// bwd_weight: number of reduction splits for a geometry (shared by sizing and launch).
+// The LDS-DMA kernel runs one 512-thread block per CU; the fallback four per CU.
 int wgrad_splits(const Geometry& g) {
     const int64_t J = g.R * g.S * g.C;
-    const int64_t tiles = ((g.K + 127) / 128) * ((J + 127) / 128);
+    const bool dma = tbn::wgrad_dma_eligible(wgrad_args(g));
+    const int64_t tiles = dma ? tbn::wgrad_dma_tiles((int)g.K, (int)J) : ((g.K + 127) / 128) * ((J + 127) / 128);
     const int64_t chunks = (g.N * g.P * g.Q + 63) / 64;
-    int64_t splits = (1024 + tiles - 1) / tiles;
+    const int64_t target = dma ? 256 : 1024;
+    int64_t splits = target / tiles;
     const int64_t max_by_len = chunks / 16 > 0 ? chunks / 16 : 1;  // >= 16 chunks per split
     if (splits > max_by_len) splits = max_by_len;
     if (splits > 256) splits = 256;
@@ -231,13 +242,10 @@ tbn_status tbn_conv2d_bwd_weight(const tbn_conv_desc* desc, const void* x, const
         if (!ws || ws_bytes < need) return fail(TBN_ERR_WORKSPACE, "workspace too small");
         if (!aligned16(ws)) return fail(TBN_ERR_ALIGN, "workspace must be 16-byte aligned");
     }
-    tbn::WgradArgs a = {};
+    tbn::WgradArgs a = wgrad_args(g);
     a.x = reinterpret_cast<const uint16_t*>(x);
     a.dy = reinterpret_cast<const uint16_t*>(dy);
     a.out = direct ? dw : reinterpret_cast<float*>(ws);
-    a.N = (int32_t)g.N; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.C = (int32_t)g.C; a.K = (int32_t)g.K;
-    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = (int32_t)g.sh; a.sw = (int32_t)g.sw;
-    a.ph = (int32_t)g.ph; a.pw = (int32_t)g.pw; a.P = (int32_t)g.P; a.Q = (int32_t)g.Q;
     const int64_t chunks = (g.N * g.P * g.Q + 63) / 64;
     a.splits = splits;
     a.chunks_per_split = (int32_t)((chunks + splits - 1) / splits);

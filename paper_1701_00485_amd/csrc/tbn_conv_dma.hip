@@ -29,6 +29,7 @@
 //
 // M0 is written by the DMA helper; nothing else in these kernels uses M0.
 #include "tbn_device.h"
+#include "tbn_dma.h"
 #include "tbn_kernels.h"
 
 namespace tbn {
@@ -37,56 +38,6 @@ namespace {
 
 constexpr int BK = 64;     // reduction elements per stage
 constexpr int ROWB = 128;  // LDS bytes per activation row of a stage
-
-typedef int v4i __attribute__((ext_vector_type(4)));
-
-// Buffer resource for raw (unstructured) buffer loads of `bytes` bytes at `base`.
-__device__ __forceinline__ v4i make_rsrc(const void* base, uint32_t bytes) {
-    const uint64_t a = reinterpret_cast<uint64_t>(base);
-    v4i r;
-    r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
-    r.y = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xFFFFu));
-    r.z = __builtin_amdgcn_readfirstlane((int)bytes);
-    r.w = 0x00020000;
-    return r;
-}
-
-// One LDS-DMA: lane i's 16 (or 4) bytes at byte `voff` of the buffer land at LDS
-// address lds + 16*i (4*i).  An offset beyond the buffer yields zeros.
-__device__ __forceinline__ void dma_b128(v4i rsrc, uint32_t lds, uint32_t voff) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                 :
-                 : "s"(lds), "v"(voff), "s"(rsrc)
-                 : "memory");
-}
-__device__ __forceinline__ void dma_b32(v4i rsrc, uint32_t lds, uint32_t voff) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
-                 :
-                 : "s"(lds), "v"(voff), "s"(rsrc)
-                 : "memory");
-}
-
-// s_waitcnt vmcnt(n) (gfx9 encoding: vmcnt in bits 3:0 and 15:14; others left at max)
-__device__ __forceinline__ void wait_vmcnt(int n) {
-    switch (n) {
-        case 0: __builtin_amdgcn_s_waitcnt(0x0F70); break;
-        case 1: __builtin_amdgcn_s_waitcnt(0x0F71); break;
-        case 2: __builtin_amdgcn_s_waitcnt(0x0F72); break;
-        case 3: __builtin_amdgcn_s_waitcnt(0x0F73); break;
-        case 4: __builtin_amdgcn_s_waitcnt(0x0F74); break;
-        case 5: __builtin_amdgcn_s_waitcnt(0x0F75); break;
-        case 6: __builtin_amdgcn_s_waitcnt(0x0F76); break;
-        case 7: __builtin_amdgcn_s_waitcnt(0x0F77); break;
-        case 8: __builtin_amdgcn_s_waitcnt(0x0F78); break;
-        case 9: __builtin_amdgcn_s_waitcnt(0x0F79); break;
-        case 10: __builtin_amdgcn_s_waitcnt(0x0F7A); break;
-        default: __builtin_amdgcn_s_waitcnt(0x0F70); break;
-    }
-}
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
 
 template <int BM, int BN>
 struct StageLayout {

@@ -73,6 +73,12 @@ struct WgradArgs {
 
 hipError_t launch_wgrad(const WgradArgs& a, hipStream_t stream);
 
+// LDS-DMA + transposing-read variant (C % 8 == 0, K % 8 == 0, tensors < 2 GiB),
+// 256 x 256 output tiles of 512 threads; launch_wgrad uses it when eligible.
+bool wgrad_dma_eligible(const WgradArgs& a);
+int wgrad_dma_tiles(int K, int J);
+hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream);
+
 hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, float* dw,
                                int32_t accumulate, hipStream_t stream);
 

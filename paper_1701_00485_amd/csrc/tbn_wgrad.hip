@@ -234,6 +234,7 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
 }  // namespace
 
 hipError_t launch_wgrad(const WgradArgs& a, hipStream_t stream) {
+    if (wgrad_dma_eligible(a)) return launch_wgrad_dma(a, stream);
     const int J = a.R * a.S * a.C;
     const int tiles = ((a.K + 127) / 128) * ((J + 127) / 128);
     WgradKernelArgs ka;
