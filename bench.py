@@ -55,6 +55,33 @@ def layer_flops():
     return 2.0 * M * L["k"] * kred, P, Q
 
 
+# Which kernel carries each timed call, and the sources its HBM counters were taken on.
+KERNEL_OF_OP = {
+    "fwd": ("conv_dma_kernel<128, 256, 1, 4, 3, false, true>", ["tbn_conv_dma.hip", "tbn_dma.h", "tbn_device.h"]),
+    "bwd_data": ("conv_dma_kernel<128, 256, 1, 4, 3, true, true>", ["tbn_conv_dma.hip", "tbn_dma.h", "tbn_device.h"]),
+    "bwd_weight": ("wgrad_dma_kernel", ["tbn_wgrad_dma.hip", "tbn_dma.h", "tbn_device.h"]),
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv3x3_256x256_56x56_b128_train_step_traffic.json")
+
+
+def measured_traffic(op):
+    """Calibrated HBM bytes per launch from the committed counter run, or None when the
+    kernel source changed since the counters were taken."""
+    import hashlib
+    try:
+        data = json.load(open(TRAFFIC_FILE))
+    except OSError:
+        return None
+    key, files = KERNEL_OF_OP[op]
+    m = hashlib.sha256()
+    for f in files:
+        m.update(open(os.path.join(ROOT, "paper_1701_00485_amd", "csrc", f), "rb").read())
+    for name, rec in data["kernels"].items():
+        if key in name and rec["source_sha"] == m.hexdigest()[:16]:
+            return rec["bytes"]
+    return None
+
+
 def cpu_baseline(budget_s: float):
     """The fp64 oracle on a bounded slice of the same step: the three convolutions on one
     image of the batch (the work is linear in the batch, scaled by 128), plus quantise and
@@ -207,7 +234,7 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(dom),
         },
     }
     if not args.no_cpu_baseline:
