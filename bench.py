@@ -39,6 +39,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-resnet", action="store_true", help="skip the ResNet-18 forward figures")
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle sample")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain device copy of known size (HBM counter calibration)")
@@ -123,6 +124,85 @@ def cpu_baseline(budget_s: float):
                   "on 1 of 128 images (scaled x128); measured %.1f s, extrapolated %.0f s per step" %
                   (t5 - t0, step_s),
     }
+
+
+def resnet18_fwd(dev, steps=10, warmup=3):
+    """ResNet-18 forward (all convolutions and the classifier two-bit) at batch 64 and 1:
+    images/s, and the achieved TFLOP/s of the nine stride-1 3x3 layers with C = K >= 128."""
+    import torch
+
+    import synth
+    from paper_1701_00485_amd.networks import ResNet18
+
+    net = ResNet18(device=dev)
+    out = {"model": "ResNet-18, two-bit convolutions and classifier, BN folded, 224x224 bf16 N(0,1)"}
+    stream = torch.cuda.current_stream()
+    for batch in (64, 1):
+        x = torch.from_numpy(synth.normal_bf16(4, "bench_x%d" % batch, (batch, 224, 224, 3)).view(np.int16))
+        x = x.to(dev).view(torch.bfloat16)
+        for _ in range(warmup):
+            net.forward(x)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            net.forward(x)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / steps
+        rec = {"ms_per_batch": round(ms, 4), "images_per_s": round(batch / (ms * 1e-3), 1),
+               "effective_tflops": round(ResNet18.flops(batch) / (ms * 1e-3) / 1e12, 2)}
+        if batch == 1:
+            # the whole forward captured once as a HIP graph and replayed
+            g = torch.cuda.CUDAGraph()
+            side = torch.cuda.Stream()
+            side.wait_stream(stream)
+            with torch.cuda.stream(side):
+                net.forward(x)
+                torch.cuda.synchronize()
+                with torch.cuda.graph(g, stream=side):
+                    logits_g = net.forward(x)
+            torch.cuda.synchronize()
+            for _ in range(warmup):
+                g.replay()
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(steps * 10):
+                g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            gms = e0.elapsed_time(e1) / (steps * 10)
+            rec["graph_ms_per_batch"] = round(gms, 4)
+            rec["graph_images_per_s"] = round(1.0 / (gms * 1e-3), 1)
+            del logits_g
+        out["batch%d" % batch] = rec
+    # the nine large stride-1 3x3 layers at batch 64, each timed alone
+    x = torch.from_numpy(synth.normal_bf16(4, "bench_x64", (64, 224, 224, 3)).view(np.int16)).to(dev)
+    trace = []
+    net.forward(x.view(torch.bfloat16), trace)
+    torch.cuda.synchronize()
+    layers = []
+    for kind, layer, inp, outp, res in trace:
+        if kind != "conv" or layer.k != 3 or layer.stride != 1 or layer.cin < 128:
+            continue
+        relu = True
+        for _ in range(2):
+            layer(inp, relu=relu, residual=res)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(steps):
+            layer(inp, relu=relu, residual=res)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / steps * 1e3
+        n, h, w, c = inp.shape
+        fl = 2.0 * n * h * w * layer.cout * 9 * c
+        layers.append({"layer": layer.name, "us": round(us, 1), "tflops": round(fl / (us * 1e-6) / 1e12, 1)})
+    fr = [l["tflops"] / PEAK_BF16_TFLOPS for l in layers]
+    out["large_3x3_layers_batch64"] = layers
+    out["large_3x3_frac_of_bf16_peak"] = {"min": round(min(fr), 4), "mean": round(float(np.mean(fr)), 4)}
+    return out
 
 
 def main():
@@ -237,6 +317,8 @@ def main():
             "traffic": measured_traffic(dom),
         },
     }
+    if not args.no_resnet:
+        result["resnet18_fwd"] = resnet18_fwd(dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(result), flush=True)

@@ -137,7 +137,7 @@ tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt
  *   dy     NHWC [N][P][Q][K] bf16.   dx  NHWC [N][H][W][C], dtype dxt (overwritten).
  *   ws     tbn_workspace_size(TBN_OP_BWD_DATA) bytes: the codes re-packed for the
  *          transposed, flipped filter and the bf16 scales.
- * Requires stride 1 in both directions (TBN_ERR_UNSUPPORTED otherwise) and K even.
+ * Requires stride 1 in both directions (TBN_ERR_UNSUPPORTED otherwise).
  */
 tbn_status tbn_conv2d_bwd_data(const tbn_conv_desc* desc, const void* dy, const uint32_t* codes,
                                const float* alpha, void* dx, tbn_dtype dxt, void* ws,
@@ -164,6 +164,59 @@ tbn_status tbn_conv2d_bwd_weight(const tbn_conv_desc* desc, const void* x, const
  */
 tbn_status tbn_sgd_step(float* w, float* v, const float* g, int64_t count, float lr,
                         float momentum, float weight_decay, hipStream_t stream);
+
+/* ------------------------------------------------------------------------------------ */
+/* Layers around the two-bit convolutions in the workloads (Sec. 4 names ResNet-18 with   */
+/* batch normalisation; the smaller workloads add max pooling, ReLU and a softmax         */
+/* cross-entropy loss).  Activations are NHWC bf16 unless stated; same conventions as    */
+/* above (device pointers, 16-byte alignment, asynchronous on `stream`).                  */
+/* ------------------------------------------------------------------------------------ */
+
+/* Pooling geometry: input N x H x W x C, square window k, stride, zero-size padding
+ * (padded positions never win a maximum).  P = (H + 2*pad - k)/stride + 1 (floor). */
+typedef struct tbn_pool_desc {
+    int32_t n, h, w, c, k, stride, pad;
+} tbn_pool_desc;
+
+tbn_status tbn_pool_out_dims(const tbn_pool_desc* desc, int32_t* p, int32_t* q);
+
+/* y[n,p,q,c] = max over the window; argmax (optional, int32 [N][P][Q][C]) receives the
+ * input position h*W + w of the maximum, ties going to the first in row-major window
+ * order (-1 for an empty window, whose output is 0). */
+tbn_status tbn_maxpool2d_fwd(const tbn_pool_desc* desc, const void* x, void* y, int32_t* argmax,
+                             hipStream_t stream);
+
+/* dx[n,h,w,c] = sum of dy[n,p,q,c] over the windows whose argmax is (h, w).  dx has dtype
+ * dxt and is overwritten (deterministic gather, no atomics). */
+tbn_status tbn_maxpool2d_bwd(const tbn_pool_desc* desc, const void* dy, const int32_t* argmax, void* dx,
+                             tbn_dtype dxt, hipStream_t stream);
+
+/* y[n][c] = mean over (h, w) of x[n][h][w][c] (fp32 sum); y has dtype yt. */
+tbn_status tbn_avgpool_global(int32_t n, int32_t h, int32_t w, int32_t c, const void* x, void* y, tbn_dtype yt,
+                              hipStream_t stream);
+
+/* Batch normalisation with batch statistics over rows = N*H*W positions per channel:
+ * y = act(gamma (x - mean) inv_std + beta), inv_std = 1/sqrt(biased var + eps);
+ * relu != 0 fuses max(., 0).  mean and inv_std [c] are written for the backward pass. */
+tbn_status tbn_batchnorm_train_fwd(const void* x, int64_t rows, int32_t c, const float* gamma, const float* beta,
+                                   float eps, int32_t relu, void* y, float* mean, float* inv_std,
+                                   hipStream_t stream);
+
+/* Backward of the above (through the batch statistics; with relu, g = dy * [y > 0]):
+ * dx = gamma inv_std (g - mean(g) - xhat mean(g xhat)), dgamma = sum g xhat,
+ * dbeta = sum g.  Sums are taken in a fixed order. */
+tbn_status tbn_batchnorm_train_bwd(const void* x, const void* y, const void* dy, int64_t rows, int32_t c,
+                                   int32_t relu, const float* mean, const float* inv_std, const float* gamma,
+                                   float* dgamma, float* dbeta, void* dx, hipStream_t stream);
+
+/* dx = dy where y > 0, else 0 (ReLU'(0) = 0). */
+tbn_status tbn_relu_bwd(const void* y, const void* dy, int64_t count, void* dx, hipStream_t stream);
+
+/* Softmax cross-entropy over fp32 logits [n][classes] with int32 labels: loss[0] = mean
+ * over the batch of logsumexp(z) - z[label]; dlogits (bf16) = (softmax(z) - onehot)/n.
+ * loss_per_sample is caller workspace of n floats. */
+tbn_status tbn_softmax_xent(const float* logits, const int32_t* labels, int32_t n, int32_t classes, float* loss,
+                            float* loss_per_sample, void* dlogits, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -70,6 +70,21 @@ def _load():
     lib.orc_conv_bwd_weight_sampled_bf16.restype = ctypes.c_int
     lib.orc_sgd.argtypes = [p, p, p, i64, ctypes.c_double, ctypes.c_double, ctypes.c_double]
     lib.orc_sgd.restype = None
+    lib.orc_maxpool_fwd.argtypes = [p, p, p, p]
+    lib.orc_maxpool_fwd.restype = ctypes.c_int
+    lib.orc_maxpool_bwd.argtypes = [p, p, p, p]
+    lib.orc_maxpool_bwd.restype = ctypes.c_int
+    lib.orc_avgpool_global.argtypes = [p, p, p]
+    lib.orc_avgpool_global.restype = None
+    d = ctypes.c_double
+    lib.orc_bn_infer.argtypes = [p, i64, i64, p, p, p, p, d, p]
+    lib.orc_bn_infer.restype = None
+    lib.orc_bn_train_fwd.argtypes = [p, i64, i64, p, p, d, p, p, p]
+    lib.orc_bn_train_fwd.restype = None
+    lib.orc_bn_train_bwd.argtypes = [p, p, i64, i64, p, d, p, p, p]
+    lib.orc_bn_train_bwd.restype = None
+    lib.orc_softmax_xent.argtypes = [p, p, i64, i64, p]
+    lib.orc_softmax_xent.restype = ctypes.c_double
     _lib = lib
     return lib
 
@@ -275,3 +290,80 @@ def sgd(w, v, g, eta, mu=0.9, lam=1e-4):
     g = _c(g, np.float64).ravel()
     _load().orc_sgd(_ptr(w), _ptr(v), _ptr(g), w.size, float(eta), float(mu), float(lam))
     return w, v
+
+
+# --------------------------------------------------------------------------------------
+# Layers around the two-bit convolutions (Sec. 4: ResNet-18 with batch normalisation)
+# --------------------------------------------------------------------------------------
+def maxpool_fwd(x, k, s, p):
+    """x NHWC fp64 -> (y, argmax flat input index; ties to the first in window order)."""
+    x = _c(x, np.float64)
+    N, H, W, C = x.shape
+    dims = np.array([N, H, W, C, k, s, p], np.int32)
+    P, Q = (H + 2 * p - k) // s + 1, (W + 2 * p - k) // s + 1
+    y = np.zeros((N, P, Q, C))
+    arg = np.zeros((N, P, Q, C), np.int64)
+    if _load().orc_maxpool_fwd(_ptr(dims), _ptr(x), _ptr(y), _ptr(arg)) != 0:
+        raise OracleError("maxpool_fwd: bad geometry")
+    return y, arg
+
+
+def maxpool_bwd(dy, arg, x_shape, k, s, p):
+    dy = _c(dy, np.float64)
+    arg = _c(arg, np.int64)
+    N, H, W, C = x_shape
+    dims = np.array([N, H, W, C, k, s, p], np.int32)
+    dx = np.zeros(x_shape)
+    _load().orc_maxpool_bwd(_ptr(dims), _ptr(dy), _ptr(arg), _ptr(dx))
+    return dx
+
+
+def avgpool_global(x):
+    x = _c(x, np.float64)
+    N, H, W, C = x.shape
+    dims = np.array([N, H, W, C], np.int32)
+    y = np.zeros((N, C))
+    _load().orc_avgpool_global(_ptr(dims), _ptr(x), _ptr(y))
+    return y
+
+
+def bn_infer(x, gamma, beta, mean, var, eps=1e-5):
+    x = _c(x, np.float64)
+    C = x.shape[-1]
+    y = np.zeros_like(x)
+    _load().orc_bn_infer(_ptr(x), x.size // C, C, _ptr(_c(gamma, np.float64)), _ptr(_c(beta, np.float64)),
+                         _ptr(_c(mean, np.float64)), _ptr(_c(var, np.float64)), float(eps), _ptr(y))
+    return y
+
+
+def bn_train_fwd(x, gamma, beta, eps=1e-5):
+    x = _c(x, np.float64)
+    C = x.shape[-1]
+    y = np.zeros_like(x)
+    mean = np.zeros(C)
+    var = np.zeros(C)
+    _load().orc_bn_train_fwd(_ptr(x), x.size // C, C, _ptr(_c(gamma, np.float64)), _ptr(_c(beta, np.float64)),
+                             float(eps), _ptr(y), _ptr(mean), _ptr(var))
+    return y, mean, var
+
+
+def bn_train_bwd(x, dy, gamma, eps=1e-5):
+    x = _c(x, np.float64)
+    dy = _c(dy, np.float64)
+    C = x.shape[-1]
+    dx = np.zeros_like(x)
+    dg = np.zeros(C)
+    db = np.zeros(C)
+    _load().orc_bn_train_bwd(_ptr(x), _ptr(dy), x.size // C, C, _ptr(_c(gamma, np.float64)), float(eps),
+                             _ptr(dx), _ptr(dg), _ptr(db))
+    return dx, dg, db
+
+
+def softmax_xent(z, labels):
+    """Mean softmax cross-entropy and its gradient with respect to the logits."""
+    z = _c(z, np.float64)
+    labels = _c(labels, np.int64)
+    N, K = z.shape
+    dz = np.zeros_like(z)
+    loss = _load().orc_softmax_xent(_ptr(z), _ptr(labels), N, K, _ptr(dz))
+    return loss, dz

@@ -428,3 +428,140 @@ void orc_sgd(double* w, double* v, const double* g, int64_t count, double eta, d
         w[i] = w[i] - eta * v[i];
     }
 }
+
+/* ------------------------------------------------------------------------------------ */
+/* Layers the workloads put around the two-bit convolutions (Sec. 4 uses ResNet-18 with  */
+/* batch normalisation).  Textbook definitions, NHWC, fp64.                               */
+/* ------------------------------------------------------------------------------------ */
+
+/* Max pooling, window k x k, stride s, padding p (padded positions never win).  The
+ * index of the maximum is the flat NHWC input index; ties go to the first maximum in
+ * row-major window order.  Windows with no valid input produce 0 and index -1. */
+int orc_maxpool_fwd(const int32_t* dims /* N,H,W,C,k,s,p */, const double* x, double* y,
+                    int64_t* arg) {
+    const int64_t N = dims[0], H = dims[1], W = dims[2], C = dims[3], k = dims[4], s = dims[5],
+                  p = dims[6];
+    if (N <= 0 || H <= 0 || W <= 0 || C <= 0 || k <= 0 || s <= 0 || p < 0 || H + 2 * p < k ||
+        W + 2 * p < k)
+        return ORC_ERR_SHAPE;
+    const int64_t P = (H + 2 * p - k) / s + 1, Q = (W + 2 * p - k) / s + 1;
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t pp = 0; pp < P; ++pp)
+            for (int64_t qq = 0; qq < Q; ++qq)
+                for (int64_t c = 0; c < C; ++c) {
+                    double best = 0.0;
+                    int64_t bi = -1;
+                    for (int64_t r = 0; r < k; ++r)
+                        for (int64_t t = 0; t < k; ++t) {
+                            const int64_t h = pp * s - p + r, w = qq * s - p + t;
+                            if (h < 0 || h >= H || w < 0 || w >= W) continue;
+                            const int64_t idx = ((n * H + h) * W + w) * C + c;
+                            if (bi < 0 || x[idx] > best) {
+                                best = x[idx];
+                                bi = idx;
+                            }
+                        }
+                    const int64_t o = ((n * P + pp) * Q + qq) * C + c;
+                    y[o] = bi < 0 ? 0.0 : best;
+                    if (arg) arg[o] = bi;
+                }
+    return ORC_OK;
+}
+
+/* Gradient of max pooling: each output gradient goes to the input its window selected. */
+int orc_maxpool_bwd(const int32_t* dims, const double* dy, const int64_t* arg, double* dx) {
+    const int64_t N = dims[0], H = dims[1], W = dims[2], C = dims[3], k = dims[4], s = dims[5],
+                  p = dims[6];
+    const int64_t P = (H + 2 * p - k) / s + 1, Q = (W + 2 * p - k) / s + 1;
+    for (int64_t i = 0; i < N * H * W * C; ++i) dx[i] = 0.0;
+    for (int64_t o = 0; o < N * P * Q * C; ++o)
+        if (arg[o] >= 0) dx[arg[o]] += dy[o];
+    return ORC_OK;
+}
+
+/* Global average pooling: y[n][c] = mean over (h, w) of x[n][h][w][c]. */
+void orc_avgpool_global(const int32_t* dims /* N,H,W,C */, const double* x, double* y) {
+    const int64_t N = dims[0], HW = (int64_t)dims[1] * dims[2], C = dims[3];
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t c = 0; c < C; ++c) {
+            double acc = 0.0;
+            for (int64_t i = 0; i < HW; ++i) acc += x[(n * HW + i) * C + c];
+            y[n * C + c] = acc / (double)HW;
+        }
+}
+
+/* Batch normalisation, inference form: y = gamma (x - mean) / sqrt(var + eps) + beta. */
+void orc_bn_infer(const double* x, int64_t rows, int64_t C, const double* gamma, const double* beta,
+                  const double* mean, const double* var, double eps, double* y) {
+    for (int64_t i = 0; i < rows; ++i)
+        for (int64_t c = 0; c < C; ++c)
+            y[i * C + c] = gamma[c] * (x[i * C + c] - mean[c]) / sqrt(var[c] + eps) + beta[c];
+}
+
+/* Batch normalisation, training form: per-channel mean and biased variance over the
+ * `rows` = N*H*W positions, y = gamma * (x - mean) / sqrt(var + eps) + beta. */
+void orc_bn_train_fwd(const double* x, int64_t rows, int64_t C, const double* gamma,
+                      const double* beta, double eps, double* y, double* mean_out,
+                      double* var_out) {
+    for (int64_t c = 0; c < C; ++c) {
+        double m = 0.0;
+        for (int64_t i = 0; i < rows; ++i) m += x[i * C + c];
+        m /= (double)rows;
+        double v = 0.0;
+        for (int64_t i = 0; i < rows; ++i) v += (x[i * C + c] - m) * (x[i * C + c] - m);
+        v /= (double)rows;
+        const double inv = 1.0 / sqrt(v + eps);
+        for (int64_t i = 0; i < rows; ++i) y[i * C + c] = gamma[c] * (x[i * C + c] - m) * inv + beta[c];
+        if (mean_out) mean_out[c] = m;
+        if (var_out) var_out[c] = v;
+    }
+}
+
+/* Gradient of the training form of batch normalisation (chain rule through the batch
+ * mean and variance):  dx = gamma / sqrt(var + eps) * (dy - mean(dy) - xhat mean(dy xhat)),
+ * dgamma = sum dy xhat, dbeta = sum dy. */
+void orc_bn_train_bwd(const double* x, const double* dy, int64_t rows, int64_t C,
+                      const double* gamma, double eps, double* dx, double* dgamma, double* dbeta) {
+    for (int64_t c = 0; c < C; ++c) {
+        double m = 0.0;
+        for (int64_t i = 0; i < rows; ++i) m += x[i * C + c];
+        m /= (double)rows;
+        double v = 0.0;
+        for (int64_t i = 0; i < rows; ++i) v += (x[i * C + c] - m) * (x[i * C + c] - m);
+        v /= (double)rows;
+        const double inv = 1.0 / sqrt(v + eps);
+        double sdy = 0.0, sdyx = 0.0;
+        for (int64_t i = 0; i < rows; ++i) {
+            const double xh = (x[i * C + c] - m) * inv;
+            sdy += dy[i * C + c];
+            sdyx += dy[i * C + c] * xh;
+        }
+        for (int64_t i = 0; i < rows; ++i) {
+            const double xh = (x[i * C + c] - m) * inv;
+            dx[i * C + c] = gamma[c] * inv * (dy[i * C + c] - sdy / rows - xh * sdyx / rows);
+        }
+        if (dgamma) dgamma[c] = sdyx;
+        if (dbeta) dbeta[c] = sdy;
+    }
+}
+
+/* Softmax cross-entropy, mean over the batch: loss = mean_n (logsumexp(z_n) - z_n[y_n]);
+ * dz[n][j] = (softmax(z_n)[j] - [j == y_n]) / N. */
+double orc_softmax_xent(const double* z, const int64_t* labels, int64_t N, int64_t classes,
+                        double* dz) {
+    double loss = 0.0;
+    for (int64_t n = 0; n < N; ++n) {
+        const double* zn = z + n * classes;
+        double mx = zn[0];
+        for (int64_t j = 1; j < classes; ++j)
+            if (zn[j] > mx) mx = zn[j];
+        double se = 0.0;
+        for (int64_t j = 0; j < classes; ++j) se += exp(zn[j] - mx);
+        const double lse = mx + log(se);
+        loss += lse - zn[labels[n]];
+        if (dz)
+            for (int64_t j = 0; j < classes; ++j)
+                dz[n * classes + j] = (exp(zn[j] - lse) - (j == labels[n] ? 1.0 : 0.0)) / (double)N;
+    }
+    return loss / (double)N;
+}

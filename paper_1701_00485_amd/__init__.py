@@ -80,6 +80,14 @@ def load():
         "tbn_conv2d_bwd_data": ([vp, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_conv2d_bwd_weight": ([vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_sgd_step": ([vp, vp, vp, i64, f32, f32, f32, vp], i32),
+        "tbn_pool_out_dims": ([vp, vp, vp], i32),
+        "tbn_maxpool2d_fwd": ([vp, vp, vp, vp, vp], i32),
+        "tbn_maxpool2d_bwd": ([vp, vp, vp, vp, i32, vp], i32),
+        "tbn_avgpool_global": ([i32, i32, i32, i32, vp, vp, i32, vp], i32),
+        "tbn_batchnorm_train_fwd": ([vp, i64, i32, vp, vp, f32, i32, vp, vp, vp, vp], i32),
+        "tbn_batchnorm_train_bwd": ([vp, vp, vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp], i32),
+        "tbn_relu_bwd": ([vp, vp, i64, vp, vp], i32),
+        "tbn_softmax_xent": ([vp, vp, i32, i32, vp, vp, vp, vp], i32),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(lib, name)
@@ -90,9 +98,11 @@ def load():
 
 
 def exported_symbols():
-    return ["tbn_status_str", "tbn_last_error", "tbn_conv_out_dims", "tbn_packed_words",
-            "tbn_workspace_size", "tbn_quantize", "tbn_conv2d_fwd", "tbn_conv2d_bwd_data",
-            "tbn_conv2d_bwd_weight", "tbn_sgd_step"]
+    return sorted(["tbn_status_str", "tbn_last_error", "tbn_conv_out_dims", "tbn_packed_words",
+                   "tbn_workspace_size", "tbn_quantize", "tbn_conv2d_fwd", "tbn_conv2d_bwd_data",
+                   "tbn_conv2d_bwd_weight", "tbn_sgd_step", "tbn_pool_out_dims", "tbn_maxpool2d_fwd",
+                   "tbn_maxpool2d_bwd", "tbn_avgpool_global", "tbn_batchnorm_train_fwd",
+                   "tbn_batchnorm_train_bwd", "tbn_relu_bwd", "tbn_softmax_xent"])
 
 
 def _status_name(s: int) -> str:
@@ -171,8 +181,9 @@ def quantize(w: torch.Tensor, codes=None, alpha=None, counts=None, want_counts=T
 
 
 def conv2d_fwd(desc: ConvDesc, x, codes, alpha, y=None, out_dtype=torch.bfloat16, scale=None, bias=None,
-               residual=None, relu=False):
-    """y = act(alpha_k * scale_k * (x conv W~) + bias_k + residual), NHWC."""
+               residual=None, relu=False, ws=None):
+    """y = act(alpha_k * scale_k * (x conv W~) + bias_k + residual), NHWC.  `ws`: workspace
+    of workspace_size(OP_FWD, desc) bytes (allocated here when None and needed)."""
     P, Q = desc.out_dims()
     _numel(x, desc.n * desc.h * desc.w * desc.c, "x")
     _numel(codes, packed_words(desc.k, desc.r * desc.s * desc.c), "codes")
@@ -190,10 +201,14 @@ def conv2d_fwd(desc: ConvDesc, x, codes, alpha, y=None, out_dtype=torch.bfloat16
                       _dev(bias, "bias", (torch.float32,)).value if bias is not None else None,
                       _dev(residual, "residual").value if residual is not None else None,
                       1 if relu else 0)
+    if ws is None:
+        need = workspace_size(OP_FWD, desc)
+        ws = torch.empty(need, dtype=torch.uint8, device=x.device) if need else None
     _call("tbn_conv2d_fwd", ctypes.byref(desc), _dev(x, "x", (torch.bfloat16, torch.float32)),
           _dtype_code(x.dtype), _dev(codes, "codes", (torch.int32,)), _dev(alpha, "alpha", (torch.float32,)),
           ctypes.byref(ep) if ep is not None else None, _dev(y, "y", (torch.bfloat16, torch.float32)),
-          _dtype_code(y.dtype), None, 0, _stream())
+          _dtype_code(y.dtype), _dev(ws, "ws") if ws is not None else None,
+          ws.numel() * ws.element_size() if ws is not None else 0, _stream())
     return y
 
 
@@ -236,3 +251,85 @@ def sgd_step(w, v, g, lr, momentum=0.9, weight_decay=1e-4):
     _call("tbn_sgd_step", _dev(w, "w", (torch.float32,)), _dev(v, "v", (torch.float32,)),
           _dev(g, "g", (torch.float32,)), n, float(lr), float(momentum), float(weight_decay), _stream())
     return w, v
+
+
+# --------------------------------------------------------------------------------------
+# Layers around the two-bit convolutions
+# --------------------------------------------------------------------------------------
+class PoolDesc(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_int32) for f in ("n", "h", "w", "c", "k", "stride", "pad")]
+
+    def out_dims(self):
+        p, q = ctypes.c_int32(), ctypes.c_int32()
+        _call("tbn_pool_out_dims", ctypes.byref(self), ctypes.byref(p), ctypes.byref(q))
+        return p.value, q.value
+
+
+def maxpool2d_fwd(x, k, stride, pad, want_argmax=False):
+    """x NHWC bf16 -> (y, argmax int32 or None)."""
+    n, h, w, c = x.shape
+    d = PoolDesc(n, h, w, c, k, stride, pad)
+    P, Q = d.out_dims()
+    y = torch.empty((n, P, Q, c), dtype=torch.bfloat16, device=x.device)
+    arg = torch.empty((n, P, Q, c), dtype=torch.int32, device=x.device) if want_argmax else None
+    _call("tbn_maxpool2d_fwd", ctypes.byref(d), _dev(x, "x", (torch.bfloat16,)), _dev(y, "y"),
+          _dev(arg, "argmax", (torch.int32,)) if arg is not None else None, _stream())
+    return y, arg
+
+
+def maxpool2d_bwd(dy, argmax, x_shape, k, stride, pad, out_dtype=torch.bfloat16):
+    n, h, w, c = x_shape
+    d = PoolDesc(n, h, w, c, k, stride, pad)
+    dx = torch.empty(tuple(x_shape), dtype=out_dtype, device=dy.device)
+    _call("tbn_maxpool2d_bwd", ctypes.byref(d), _dev(dy, "dy", (torch.bfloat16,)),
+          _dev(argmax, "argmax", (torch.int32,)), _dev(dx, "dx"), _dtype_code(out_dtype), _stream())
+    return dx
+
+
+def avgpool_global(x, out_dtype=torch.bfloat16):
+    n, h, w, c = x.shape
+    y = torch.empty((n, c), dtype=out_dtype, device=x.device)
+    _call("tbn_avgpool_global", n, h, w, c, _dev(x, "x", (torch.bfloat16,)), _dev(y, "y"),
+          _dtype_code(out_dtype), _stream())
+    return y
+
+
+def batchnorm_train_fwd(x, gamma, beta, eps=1e-5, relu=False):
+    c = x.shape[-1]
+    y = torch.empty_like(x)
+    mean = torch.empty(c, dtype=torch.float32, device=x.device)
+    inv_std = torch.empty(c, dtype=torch.float32, device=x.device)
+    _call("tbn_batchnorm_train_fwd", _dev(x, "x", (torch.bfloat16,)), x.numel() // c, c,
+          _dev(gamma, "gamma", (torch.float32,)), _dev(beta, "beta", (torch.float32,)), float(eps),
+          1 if relu else 0, _dev(y, "y"), _dev(mean, "mean"), _dev(inv_std, "inv_std"), _stream())
+    return y, mean, inv_std
+
+
+def batchnorm_train_bwd(x, y, dy, mean, inv_std, gamma, relu=False):
+    c = x.shape[-1]
+    dx = torch.empty_like(x)
+    dgamma = torch.empty(c, dtype=torch.float32, device=x.device)
+    dbeta = torch.empty(c, dtype=torch.float32, device=x.device)
+    _call("tbn_batchnorm_train_bwd", _dev(x, "x", (torch.bfloat16,)), _dev(y, "y", (torch.bfloat16,)),
+          _dev(dy, "dy", (torch.bfloat16,)), x.numel() // c, c, 1 if relu else 0, _dev(mean, "mean"),
+          _dev(inv_std, "inv_std"), _dev(gamma, "gamma"), _dev(dgamma, "dgamma"), _dev(dbeta, "dbeta"),
+          _dev(dx, "dx"), _stream())
+    return dx, dgamma, dbeta
+
+
+def relu_bwd(y, dy):
+    dx = torch.empty_like(dy)
+    _call("tbn_relu_bwd", _dev(y, "y", (torch.bfloat16,)), _dev(dy, "dy", (torch.bfloat16,)), dy.numel(),
+          _dev(dx, "dx"), _stream())
+    return dx
+
+
+def softmax_xent(logits, labels):
+    """logits fp32 [n][classes], labels int32 [n] -> (loss fp32 [1], dlogits bf16)."""
+    n, k = logits.shape
+    loss = torch.empty(1, dtype=torch.float32, device=logits.device)
+    per = torch.empty(n, dtype=torch.float32, device=logits.device)
+    dz = torch.empty((n, k), dtype=torch.bfloat16, device=logits.device)
+    _call("tbn_softmax_xent", _dev(logits, "logits", (torch.float32,)), _dev(labels, "labels", (torch.int32,)),
+          n, k, _dev(loss, "loss"), _dev(per, "per"), _dev(dz, "dz"), _stream())
+    return loss, dz

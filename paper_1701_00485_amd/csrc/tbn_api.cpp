@@ -79,8 +79,10 @@ int wgrad_splits(const Geometry& g) {
 }
 
 struct BwdDataWs {
-    int64_t codes_bytes, apair_off, apair_bytes, total;
+    int64_t codes_bytes, apair_off, apair_bytes, partial_off, partial_bytes, total;
 };
+
+tbn::ConvGemmArgs bwd_data_args(const Geometry& g, tbn_dtype dxt);
 
 BwdDataWs bwd_data_ws(const Geometry& g) {
     BwdDataWs w;
@@ -89,8 +91,35 @@ BwdDataWs bwd_data_ws(const Geometry& g) {
     w.codes_bytes = ((g.C + 63) / 64) * nbt * 256 * 4;
     w.apair_off = round_up(w.codes_bytes, 256);
     w.apair_bytes = nbt * 32 * 4;
-    w.total = w.apair_off + round_up(w.apair_bytes, 256);
+    w.partial_off = w.apair_off + round_up(w.apair_bytes, 256);
+    // the split-K partials of the GEMM do not depend on the output dtype
+    w.partial_bytes = (int64_t)tbn::conv_gemm_partial_bytes(bwd_data_args(g, TBN_BF16));
+    w.total = w.partial_off + w.partial_bytes;
     return w;
+}
+
+// Forward GEMM arguments of a geometry (pointers filled in by the caller).
+tbn::ConvGemmArgs fwd_args(const Geometry& g, tbn_dtype xt, tbn_dtype yt) {
+    tbn::ConvGemmArgs a = {};
+    a.N = (int32_t)g.N; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.C = (int32_t)g.C; a.Kf = (int32_t)g.K;
+    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = (int32_t)g.sh; a.sw = (int32_t)g.sw;
+    a.ph = (int32_t)g.ph; a.pw = (int32_t)g.pw; a.P = (int32_t)g.P; a.Q = (int32_t)g.Q;
+    a.x_f32 = xt == TBN_F32;
+    a.y_f32 = yt == TBN_F32;
+    return a;
+}
+
+// Backward-data as a forward convolution: dx = conv(dy, flipped transposed filter), padding
+// R-1-pad, stride 1.
+tbn::ConvGemmArgs bwd_data_args(const Geometry& g, tbn_dtype dxt) {
+    tbn::ConvGemmArgs a = {};
+    a.N = (int32_t)g.N; a.H = (int32_t)g.P; a.W = (int32_t)g.Q; a.C = (int32_t)g.K; a.Kf = (int32_t)g.C;
+    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = 1; a.sw = 1;
+    a.ph = (int32_t)(g.R - 1 - g.ph); a.pw = (int32_t)(g.S - 1 - g.pw);
+    a.P = (int32_t)g.H; a.Q = (int32_t)g.W;
+    a.x_f32 = 0;
+    a.y_f32 = dxt == TBN_F32;
+    return a;
 }
 
 }  // namespace
@@ -133,7 +162,7 @@ tbn_status tbn_workspace_size(tbn_op op, const tbn_conv_desc* desc, size_t* byte
     if (st != TBN_OK) return st;
     if (!bytes) return fail(TBN_ERR_NULL, "bytes is NULL");
     switch (op) {
-        case TBN_OP_FWD: *bytes = 0; return TBN_OK;
+        case TBN_OP_FWD: *bytes = tbn::conv_gemm_partial_bytes(fwd_args(g, TBN_BF16, TBN_BF16)); return TBN_OK;
         case TBN_OP_BWD_DATA: *bytes = (size_t)bwd_data_ws(g).total; return TBN_OK;
         case TBN_OP_BWD_WEIGHT: {
             const int splits = wgrad_splits(g);
@@ -158,8 +187,6 @@ tbn_status tbn_quantize(const float* w, int64_t k, int64_t n, uint32_t* codes, f
 tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt, const uint32_t* codes,
                           const float* alpha, const tbn_epilogue* ep, void* y, tbn_dtype yt, void* ws,
                           size_t ws_bytes, hipStream_t stream) {
-    (void)ws;
-    (void)ws_bytes;
     Geometry g;
     tbn_status st = check_desc(desc, &g);
     if (st != TBN_OK) return st;
@@ -168,7 +195,13 @@ tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt
         return fail(TBN_ERR_UNSUPPORTED, "unknown dtype");
     if (!aligned16(x) || !aligned16(codes) || !aligned16(y) || !aligned4(alpha))
         return fail(TBN_ERR_ALIGN, "x, codes and y must be 16-byte aligned");
-    tbn::ConvGemmArgs a = {};
+    tbn::ConvGemmArgs a = fwd_args(g, xt, yt);
+    const size_t need = tbn::conv_gemm_partial_bytes(a);
+    if (need) {
+        if (!ws || ws_bytes < need) return fail(TBN_ERR_WORKSPACE, "workspace too small");
+        if (!aligned16(ws)) return fail(TBN_ERR_ALIGN, "workspace must be 16-byte aligned");
+        a.partial = reinterpret_cast<float*>(ws);
+    }
     a.x = x;
     a.codes = codes;
     a.apair = nullptr;
@@ -183,11 +216,6 @@ tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt
         a.relu = ep->relu ? 1 : 0;
     }
     a.y = y;
-    a.N = (int32_t)g.N; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.C = (int32_t)g.C; a.Kf = (int32_t)g.K;
-    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = (int32_t)g.sh; a.sw = (int32_t)g.sw;
-    a.ph = (int32_t)g.ph; a.pw = (int32_t)g.pw; a.P = (int32_t)g.P; a.Q = (int32_t)g.Q;
-    a.x_f32 = xt == TBN_F32;
-    a.y_f32 = yt == TBN_F32;
     hipError_t e = tbn::launch_conv_gemm(a, stream);
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_fwd");
 }
@@ -210,19 +238,13 @@ tbn_status tbn_conv2d_bwd_data(const tbn_conv_desc* desc, const void* dy, const 
     hipError_t e = tbn::launch_repack_bwd(codes, alpha, (int32_t)g.K, (int32_t)g.R, (int32_t)g.S, (int32_t)g.C,
                                           codes_t, apair, stream);
     if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_data (repack)");
-    // dx = conv(dy, flipped transposed filter) with padding R-1-pad, stride 1
-    tbn::ConvGemmArgs a = {};
+    tbn::ConvGemmArgs a = bwd_data_args(g, dxt);
     a.x = dy;
     a.codes = codes_t;
     a.apair = apair;
     a.colscale = nullptr;
     a.y = dx;
-    a.N = (int32_t)g.N; a.H = (int32_t)g.P; a.W = (int32_t)g.Q; a.C = (int32_t)g.K; a.Kf = (int32_t)g.C;
-    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = 1; a.sw = 1;
-    a.ph = (int32_t)(g.R - 1 - g.ph); a.pw = (int32_t)(g.S - 1 - g.pw);
-    a.P = (int32_t)g.H; a.Q = (int32_t)g.W;
-    a.x_f32 = 0;
-    a.y_f32 = dxt == TBN_F32;
+    if (w.partial_bytes) a.partial = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + w.partial_off);
     e = tbn::launch_conv_gemm(a, stream);
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_bwd_data");
 }
@@ -266,6 +288,106 @@ tbn_status tbn_sgd_step(float* w, float* v, const float* g, int64_t count, float
     if (!aligned16(w) || !aligned16(v) || !aligned16(g)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
     hipError_t e = tbn::launch_sgd(w, v, g, count, lr, momentum, weight_decay, stream);
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_sgd_step");
+}
+
+namespace {
+
+tbn_status check_pool(const tbn_pool_desc* d, tbn::PoolArgs* a) {
+    if (!d) return fail(TBN_ERR_NULL, "desc is NULL");
+    if (d->n <= 0 || d->h <= 0 || d->w <= 0 || d->c <= 0 || d->k <= 0 || d->stride <= 0 || d->pad < 0)
+        return fail(TBN_ERR_SHAPE, "invalid pooling geometry");
+    if (d->h + 2 * (int64_t)d->pad < d->k || d->w + 2 * (int64_t)d->pad < d->k)
+        return fail(TBN_ERR_SHAPE, "window larger than the padded input");
+    if ((int64_t)d->n * d->h * d->w * d->c > ((int64_t)1 << 40)) return fail(TBN_ERR_SHAPE, "tensor too large");
+    a->N = d->n; a->H = d->h; a->W = d->w; a->C = d->c; a->k = d->k; a->s = d->stride; a->pad = d->pad;
+    a->P = (d->h + 2 * d->pad - d->k) / d->stride + 1;
+    a->Q = (d->w + 2 * d->pad - d->k) / d->stride + 1;
+    return TBN_OK;
+}
+
+}  // namespace
+
+tbn_status tbn_pool_out_dims(const tbn_pool_desc* desc, int32_t* p, int32_t* q) {
+    tbn::PoolArgs a;
+    tbn_status st = check_pool(desc, &a);
+    if (st != TBN_OK) return st;
+    if (!p || !q) return fail(TBN_ERR_NULL, "output pointer is NULL");
+    *p = a.P;
+    *q = a.Q;
+    return TBN_OK;
+}
+
+tbn_status tbn_maxpool2d_fwd(const tbn_pool_desc* desc, const void* x, void* y, int32_t* argmax, hipStream_t stream) {
+    tbn::PoolArgs a;
+    tbn_status st = check_pool(desc, &a);
+    if (st != TBN_OK) return st;
+    if (!x || !y) return fail(TBN_ERR_NULL, "x and y are required");
+    if (!aligned16(x) || !aligned16(y) || (argmax && !aligned4(argmax))) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    hipError_t e = tbn::launch_maxpool_fwd(a, reinterpret_cast<const uint16_t*>(x), reinterpret_cast<uint16_t*>(y),
+                                           argmax, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_maxpool2d_fwd");
+}
+
+tbn_status tbn_maxpool2d_bwd(const tbn_pool_desc* desc, const void* dy, const int32_t* argmax, void* dx, tbn_dtype dxt,
+                             hipStream_t stream) {
+    tbn::PoolArgs a;
+    tbn_status st = check_pool(desc, &a);
+    if (st != TBN_OK) return st;
+    if (!dy || !argmax || !dx) return fail(TBN_ERR_NULL, "dy, argmax and dx are required");
+    if (dxt != TBN_BF16 && dxt != TBN_F32) return fail(TBN_ERR_UNSUPPORTED, "unknown dtype");
+    if (!aligned16(dy) || !aligned16(dx) || !aligned4(argmax)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    hipError_t e = tbn::launch_maxpool_bwd(a, reinterpret_cast<const uint16_t*>(dy), argmax, dx, dxt == TBN_F32, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_maxpool2d_bwd");
+}
+
+tbn_status tbn_avgpool_global(int32_t n, int32_t h, int32_t w, int32_t c, const void* x, void* y, tbn_dtype yt,
+                              hipStream_t stream) {
+    if (!x || !y) return fail(TBN_ERR_NULL, "x and y are required");
+    if (n <= 0 || h <= 0 || w <= 0 || c <= 0) return fail(TBN_ERR_SHAPE, "sizes must be positive");
+    if (yt != TBN_BF16 && yt != TBN_F32) return fail(TBN_ERR_UNSUPPORTED, "unknown dtype");
+    if (!aligned16(x) || !aligned16(y)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    hipError_t e = tbn::launch_avgpool(n, h * w, c, reinterpret_cast<const uint16_t*>(x), y, yt == TBN_F32, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_avgpool_global");
+}
+
+tbn_status tbn_batchnorm_train_fwd(const void* x, int64_t rows, int32_t c, const float* gamma, const float* beta,
+                                   float eps, int32_t relu, void* y, float* mean, float* inv_std, hipStream_t stream) {
+    if (!x || !gamma || !beta || !y || !mean || !inv_std) return fail(TBN_ERR_NULL, "missing pointer");
+    if (rows <= 0 || c <= 0) return fail(TBN_ERR_SHAPE, "sizes must be positive");
+    if (!aligned16(x) || !aligned16(y)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    hipError_t e = tbn::launch_bn_train_fwd(reinterpret_cast<const uint16_t*>(x), rows, c, gamma, beta, eps, relu ? 1 : 0,
+                                            reinterpret_cast<uint16_t*>(y), mean, inv_std, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_batchnorm_train_fwd");
+}
+
+tbn_status tbn_batchnorm_train_bwd(const void* x, const void* y, const void* dy, int64_t rows, int32_t c, int32_t relu,
+                                   const float* mean, const float* inv_std, const float* gamma, float* dgamma,
+                                   float* dbeta, void* dx, hipStream_t stream) {
+    if (!x || !y || !dy || !mean || !inv_std || !gamma || !dgamma || !dbeta || !dx)
+        return fail(TBN_ERR_NULL, "missing pointer");
+    if (rows <= 0 || c <= 0) return fail(TBN_ERR_SHAPE, "sizes must be positive");
+    if (!aligned16(x) || !aligned16(y) || !aligned16(dy) || !aligned16(dx)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    hipError_t e = tbn::launch_bn_train_bwd(reinterpret_cast<const uint16_t*>(x), reinterpret_cast<const uint16_t*>(y),
+                                            reinterpret_cast<const uint16_t*>(dy), rows, c, relu ? 1 : 0, mean, inv_std,
+                                            gamma, dgamma, dbeta, reinterpret_cast<uint16_t*>(dx), stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_batchnorm_train_bwd");
+}
+
+tbn_status tbn_relu_bwd(const void* y, const void* dy, int64_t count, void* dx, hipStream_t stream) {
+    if (!y || !dy || !dx) return fail(TBN_ERR_NULL, "missing pointer");
+    if (count <= 0) return fail(TBN_ERR_SHAPE, "count must be positive");
+    hipError_t e = tbn::launch_relu_bwd(reinterpret_cast<const uint16_t*>(y), reinterpret_cast<const uint16_t*>(dy), count,
+                                        reinterpret_cast<uint16_t*>(dx), stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_relu_bwd");
+}
+
+tbn_status tbn_softmax_xent(const float* logits, const int32_t* labels, int32_t n, int32_t classes, float* loss,
+                            float* loss_per_sample, void* dlogits, hipStream_t stream) {
+    if (!logits || !labels || !loss || !loss_per_sample || !dlogits) return fail(TBN_ERR_NULL, "missing pointer");
+    if (n <= 0 || classes <= 0) return fail(TBN_ERR_SHAPE, "sizes must be positive");
+    hipError_t e = tbn::launch_softmax_xent(logits, labels, n, classes, loss, loss_per_sample,
+                                            reinterpret_cast<uint16_t*>(dlogits), stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_softmax_xent");
 }
 
 }  // extern "C"

@@ -303,12 +303,6 @@ hipError_t launch_cfg(const ConvGemmArgs& a, hipStream_t stream) {
     return hipGetLastError();
 }
 
-// Tile-shape override for tuning and for the tests that cover every shape:
-// TBN_CONV_TILE=<index> (read at each launch; unset = the built-in choice).
-int tile_override() {
-    const char* e = getenv("TBN_CONV_TILE");
-    return e ? atoi(e) : -1;
-}
 
 template <int AM, bool BWD>
 hipError_t launch_mode(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
@@ -371,12 +365,33 @@ __global__ __launch_bounds__(256) void repack_bwd_kernel(const uint32_t* __restr
 
 }  // namespace
 
+// Tile-shape override for tuning and for the tests that cover every shape:
+// TBN_CONV_TILE=<index> (read at each launch; unset = the built-in choice).
+int conv_tile_override() {
+    const char* e = getenv("TBN_CONV_TILE");
+    return e ? atoi(e) : -1;
+}
+
+int conv_splits_override() {
+    const char* e = getenv("TBN_CONV_SPLITS");
+    return e ? atoi(e) : -1;
+}
+
+static bool use_dma(const ConvGemmArgs& a, int cfg) { return conv_dma_eligible(a) && (cfg < 0 || cfg >= 10); }
+
+size_t conv_gemm_partial_bytes(const ConvGemmArgs& a) {
+    const int cfg = conv_tile_override();
+    return use_dma(a, cfg) ? plan_conv_dma(a, cfg).partial_bytes : 0;
+}
+
 hipError_t launch_conv_gemm(const ConvGemmArgs& args, hipStream_t stream) {
     ConvGemmArgs a = args;
     a.div_q = make_fastdiv((uint32_t)a.Q);
     a.div_pq = make_fastdiv((uint32_t)a.P * (uint32_t)a.Q);
-    const int cfg = tile_override();
-    if (conv_dma_eligible(a) && (cfg < 0 || cfg >= 10)) return launch_conv_dma(a, cfg, stream);
+    a.splits = 1;
+    a.chunks_per_split = 1 << 30;
+    const int cfg = conv_tile_override();
+    if (use_dma(a, cfg)) return launch_conv_dma(a, plan_conv_dma(a, cfg), stream);
     const bool vec = (a.C % 8 == 0) && !a.x_f32;
     if (a.apair) return vec ? launch_mode<A_VEC8, true>(a, cfg, stream) : launch_mode<A_SCALAR, true>(a, cfg, stream);
     return vec ? launch_mode<A_VEC8, false>(a, cfg, stream) : launch_mode<A_SCALAR, false>(a, cfg, stream);

@@ -77,9 +77,16 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
     const int nchunks = (n + BK - 1) / BK;
     const int KB = (a.Kf + 63) / 64;
     const int tilesN = (a.Kf + BN - 1) / BN;
-    const int64_t tile = xcd_remap(blockIdx.x, gridDim.x);
+    const int64_t tiles = ((M + BM - 1) / BM) * tilesN;
+    // XCD-aware order over (split, tile); each split reduces a contiguous range of stages
+    const int64_t work = xcd_remap(blockIdx.x, gridDim.x);
+    const int split = (int)(work / tiles);
+    const int64_t tile = work % tiles;
     const int64_t m0 = (tile / tilesN) * BM;
     const int n0 = (int)(tile % tilesN) * BN;
+    const int c_begin = split * a.chunks_per_split;
+    const int c_end = min(c_begin + a.chunks_per_split, nchunks);
+    const int nloc = c_end - c_begin;
 
     const v4i rs_x = make_rsrc(a.x, (uint32_t)((int64_t)a.N * a.H * a.W * C * 2));
     const v4i rs_c = make_rsrc(a.codes, (uint32_t)((int64_t)KB * nchunks * 1024));
@@ -127,8 +134,13 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
             nmask[j][0] = ~rmask[j][0];
             nmask[j][1] = ~rmask[j][1];
         }
+        const int e0 = c_begin * BK;
+        const int rs = e0 / C;
+        uc = e0 - rs * C;
+        ur = rs / a.S;
+        us = rs - ur * a.S;
     } else {
-        const int e0 = lseg * 8;
+        const int e0 = c_begin * BK + lseg * 8;
         const int rs = e0 / C;
         ec = e0 - rs * C;
         er = rs / a.S;
@@ -142,7 +154,7 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
     const int dmas = AR + (copies_codes ? 1 : 0) + (copies_pairs ? 1 : 0);  // per stage, this wave
 
     auto issue = [&](int chunk) {
-        const uint32_t st = smem_base + (uint32_t)((chunk % STAGES) * L::BYTES);
+        const uint32_t st = smem_base + (uint32_t)(((chunk - c_begin) % STAGES) * L::BYTES);
         if constexpr (UNI) {
             // out-of-image taps (and the padding stage past the filter, tap clamped to
             // bit 63, which is clear in rmask because R*S <= 63) get offset bit 31 set,
@@ -231,14 +243,14 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
     // prologue: the first STAGES-1 stages in flight
 #pragma unroll
     for (int c = 0; c < STAGES - 1; ++c)
-        if (c < nchunks) issue(c);
-    for (int chunk = 0; chunk < nchunks; ++chunk) {
-        // this wave's DMAs of stage `chunk` landed (later stages may still be in flight)
-        const int later = min(nchunks - 1 - chunk, STAGES - 2);
+        if (c < nloc) issue(c_begin + c);
+    for (int il = 0; il < nloc; ++il) {
+        // this wave's DMAs of stage il landed (later stages may still be in flight)
+        const int later = min(nloc - 1 - il, STAGES - 2);
         wait_vmcnt(later * dmas);
-        __syncthreads();  // ... and every other wave's; all reads of stage chunk-1 are done
-        if (chunk + STAGES - 1 < nchunks) issue(chunk + STAGES - 1);  // into stage chunk-1's buffer
-        const uint8_t* st = smem + (chunk % STAGES) * L::BYTES;
+        __syncthreads();  // ... and every other wave's; all reads of stage il-1 are done
+        if (il + STAGES - 1 < nloc) issue(c_begin + il + STAGES - 1);  // into stage il-1's buffer
+        const uint8_t* st = smem + (il % STAGES) * L::BYTES;
         u32x4 braw[TN];
 #pragma unroll
         for (int t = 0; t < TN; ++t) braw[t] = *reinterpret_cast<const u32x4*>(st + L::B + bcol + 32 * 16 * t);
@@ -330,6 +342,8 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
         bi[e] = ok && a.bias ? a.bias[col] : 0.0f;
     }
     const bool vec_store = (Kf % 8) == 0;
+    const bool partial_out = a.splits > 1;  // raw fp32 sums of this split (Kf % 8 == 0)
+    float* part = partial_out ? a.partial + (int64_t)split * M * Kf : nullptr;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -348,6 +362,13 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
             const f32x4 hi = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol + 4]);
             float v8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
             const int64_t o = row * Kf + col0;
+            if (partial_out) {
+                if (col0 < Kf) {
+                    *reinterpret_cast<f32x4*>(part + o) = lo;
+                    *reinterpret_cast<f32x4*>(part + o + 4) = hi;
+                }
+                continue;
+            }
 #pragma unroll
             for (int e = 0; e < 8; ++e) v8[e] = v8[e] * cs[e] + bi[e];
             if (a.residual) {
@@ -402,28 +423,88 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
     }
 }
 
+// Sum of the split-K partials in split order, then the epilogue; one thread per 8 outputs.
+__global__ __launch_bounds__(256) void conv_split_epilogue_kernel(const ConvGemmArgs a) {
+    const int64_t M = (int64_t)a.N * a.P * a.Q;
+    const int Kf = a.Kf;
+    const int64_t groups = M * (Kf / 8);
+    const int64_t gi = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (gi >= groups) return;
+    const int64_t o = gi * 8;
+    const int col0 = (int)(o % Kf);
+    float v8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int z = 0; z < a.splits; ++z) {
+        const float* pp = a.partial + (int64_t)z * M * Kf + o;
+        const f32x4 lo = *reinterpret_cast<const f32x4*>(pp);
+        const f32x4 hi = *reinterpret_cast<const f32x4*>(pp + 4);
+        v8[0] += lo.x; v8[1] += lo.y; v8[2] += lo.z; v8[3] += lo.w;
+        v8[4] += hi.x; v8[5] += hi.y; v8[6] += hi.z; v8[7] += hi.w;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int col = col0 + e;
+        float sc = a.colscale ? a.colscale[col] : 1.0f;
+        if (a.scale) sc *= a.scale[col];
+        v8[e] = v8[e] * sc + (a.bias ? a.bias[col] : 0.0f);
+    }
+    if (a.residual) {
+        if (a.y_f32) {
+            const float* rp = reinterpret_cast<const float*>(a.residual) + o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v8[e] += rp[e];
+        } else {
+            const u32x4 r8 = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.residual) + o);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                v8[2 * e] += bf16_bits_to_f32(r8[e] & 0xFFFFu);
+                v8[2 * e + 1] += bf16_bits_to_f32(r8[e] >> 16);
+            }
+        }
+    }
+    if (a.relu) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v8[e] = fmaxf(v8[e], 0.0f);
+    }
+    if (a.y_f32) {
+        float* yp = reinterpret_cast<float*>(a.y) + o;
+        *reinterpret_cast<f32x4*>(yp) = f32x4{v8[0], v8[1], v8[2], v8[3]};
+        *reinterpret_cast<f32x4*>(yp + 4) = f32x4{v8[4], v8[5], v8[6], v8[7]};
+    } else {
+        *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(a.y) + o) =
+            u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]), pack_bf16x2(v8[4], v8[5]),
+                  pack_bf16x2(v8[6], v8[7])};
+    }
+}
+
 template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool BWD>
 hipError_t launch_dma_cfg(const ConvGemmArgs& a, hipStream_t stream) {
     const int64_t M = (int64_t)a.N * a.P * a.Q;
     const int64_t tiles = ((M + BM - 1) / BM) * ((a.Kf + BN - 1) / BN);
+    const dim3 grid((unsigned)(tiles * a.splits));
     if (a.C % 64 == 0)
-        hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, true>), dim3((unsigned)tiles),
-                           dim3(256), 0, stream, a);
+        hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, true>), grid, dim3(256), 0, stream, a);
     else
-        hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, false>), dim3((unsigned)tiles),
-                           dim3(256), 0, stream, a);
+        hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, false>), grid, dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 
 template <bool BWD>
 hipError_t launch_dma_mode(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
-    if (cfg < 10) cfg = a.Kf > 128 ? 10 : (a.Kf > 64 ? 12 : 14);
     switch (cfg) {
         case 11: return launch_dma_cfg<128, 128, 1, 4, 3, BWD>(a, stream);
         case 12: return launch_dma_cfg<128, 128, 2, 2, 3, BWD>(a, stream);
         case 14: return launch_dma_cfg<128, 64, 2, 2, 3, BWD>(a, stream);
         case 16: return launch_dma_cfg<256, 128, 1, 4, 2, BWD>(a, stream);
         default: return launch_dma_cfg<128, 256, 1, 4, 3, BWD>(a, stream);
+    }
+}
+
+void cfg_tile(int cfg, int* bm, int* bn) {
+    switch (cfg) {
+        case 11: case 12: *bm = 128; *bn = 128; return;
+        case 14: *bm = 128; *bn = 64; return;
+        case 16: *bm = 256; *bn = 128; return;
+        default: *bm = 128; *bn = 256; return;
     }
 }
 
@@ -436,8 +517,49 @@ bool conv_dma_eligible(const ConvGemmArgs& a) {
     return !a.x_f32 && a.C % 8 == 0 && a.R * a.S <= 63 && xbytes < 0x7FFFFFF0ll && cbytes < 0x7FFFFFF0ll;
 }
 
-hipError_t launch_conv_dma(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
-    return a.apair ? launch_dma_mode<true>(a, cfg, stream) : launch_dma_mode<false>(a, cfg, stream);
+ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
+    const int64_t M = (int64_t)a.N * a.P * a.Q;
+    const int nchunks = (int)(((int64_t)a.R * a.S * a.C + BK - 1) / BK);
+    ConvPlan p;
+    p.cfg = cfg;
+    int bm, bn;
+    if (p.cfg < 10) {
+        p.cfg = a.Kf > 128 ? 10 : (a.Kf > 64 ? 12 : 14);
+        cfg_tile(p.cfg, &bm, &bn);
+        // too few tiles for one wave of blocks: narrower tiles, then split the reduction
+        if (((M + bm - 1) / bm) * ((a.Kf + bn - 1) / bn) < 384) p.cfg = 14;
+    }
+    cfg_tile(p.cfg, &bm, &bn);
+    const int64_t tiles = ((M + bm - 1) / bm) * ((a.Kf + bn - 1) / bn);
+    int64_t splits = 1;
+    if (a.Kf % 8 == 0) {
+        const int forced = conv_splits_override();
+        if (forced > 0) {
+            splits = forced;
+        } else if (tiles < 384) {
+            splits = (640 + tiles - 1) / tiles;
+            const int64_t max_splits = nchunks / 3 > 0 ? nchunks / 3 : 1;  // >= 3 stages per split
+            if (splits > max_splits) splits = max_splits;
+        }
+        if (splits > nchunks) splits = nchunks;
+        if (splits < 1) splits = 1;
+    }
+    p.chunks_per_split = (int)((nchunks + splits - 1) / splits);
+    p.splits = (int)((nchunks + p.chunks_per_split - 1) / p.chunks_per_split);
+    p.partial_bytes = p.splits > 1 ? (size_t)p.splits * (size_t)M * (size_t)a.Kf * 4 : 0;
+    return p;
+}
+
+hipError_t launch_conv_dma(const ConvGemmArgs& args, const ConvPlan& plan, hipStream_t stream) {
+    ConvGemmArgs a = args;
+    a.splits = plan.splits;
+    a.chunks_per_split = plan.chunks_per_split;
+    if (a.splits > 1 && !a.partial) return hipErrorInvalidValue;
+    hipError_t e = a.apair ? launch_dma_mode<true>(a, plan.cfg, stream) : launch_dma_mode<false>(a, plan.cfg, stream);
+    if (e != hipSuccess || a.splits <= 1) return e;
+    const int64_t groups = (int64_t)a.N * a.P * a.Q * (a.Kf / 8);
+    hipLaunchKernelGGL(conv_split_epilogue_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, stream, a);
+    return hipGetLastError();
 }
 
 }  // namespace tbn

@@ -43,6 +43,9 @@ struct ConvGemmArgs {
     int32_t x_f32;
     int32_t y_f32;
     FastDiv div_q, div_pq;    // division by Q and by P*Q (output pixel -> (n, p, q))
+    float* partial;           // split-K: fp32 partial sums [splits][M][Kf] (workspace)
+    int32_t splits;           // split-K: number of reduction ranges (1 = none)
+    int32_t chunks_per_split; // split-K: 64-element stages per range
 };
 
 hipError_t launch_quantize(const float* w, int64_t K, int64_t n, uint32_t* codes, float* alpha,
@@ -50,9 +53,24 @@ hipError_t launch_quantize(const float* w, int64_t K, int64_t n, uint32_t* codes
 
 hipError_t launch_conv_gemm(const ConvGemmArgs& a, hipStream_t stream);
 
-// LDS-DMA variant (bf16 x, C % 8 == 0, R*S <= 63, x < 2 GiB); cfg selects the tile shape.
+// LDS-DMA variant (bf16 x, C % 8 == 0, R*S <= 63, x < 2 GiB).  Its plan picks the tile
+// shape and, for layers with too few output tiles to fill the GPU, a split of the reduction
+// whose fp32 partials live in caller workspace; cfg >= 10 forces a tile shape.
+struct ConvPlan {
+    int cfg;
+    int splits;
+    int chunks_per_split;
+    size_t partial_bytes;
+};
 bool conv_dma_eligible(const ConvGemmArgs& a);
-hipError_t launch_conv_dma(const ConvGemmArgs& a, int cfg, hipStream_t stream);
+ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg);
+hipError_t launch_conv_dma(const ConvGemmArgs& a, const ConvPlan& plan, hipStream_t stream);
+// Tile-shape and reduction-split overrides for tuning and tests (TBN_CONV_TILE and
+// TBN_CONV_SPLITS environment variables, read at every call; -1 when unset).
+int conv_tile_override();
+int conv_splits_override();
+// Bytes of split-K partials the forward / backward-data GEMM of these arguments needs.
+size_t conv_gemm_partial_bytes(const ConvGemmArgs& a);
 
 // Re-pack the codes of K filters [K][R][S][C] into the codes of the C filters of the
 // transposed, spatially flipped layer [C][R][S][K] (backward-data operand), and build
@@ -81,6 +99,23 @@ hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream);
 
 hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, float* dw,
                                int32_t accumulate, hipStream_t stream);
+
+struct PoolArgs {
+    int32_t N, H, W, C, k, s, pad, P, Q;
+};
+
+hipError_t launch_maxpool_fwd(const PoolArgs& a, const uint16_t* x, uint16_t* y, int32_t* arg, hipStream_t s);
+hipError_t launch_maxpool_bwd(const PoolArgs& a, const uint16_t* dy, const int32_t* arg, void* dx, int dx_f32,
+                              hipStream_t s);
+hipError_t launch_avgpool(int32_t N, int32_t HW, int32_t C, const uint16_t* x, void* y, int y_f32, hipStream_t s);
+hipError_t launch_bn_train_fwd(const uint16_t* x, int64_t rows, int32_t C, const float* gamma, const float* beta,
+                               float eps, int relu, uint16_t* y, float* mean, float* inv_std, hipStream_t s);
+hipError_t launch_bn_train_bwd(const uint16_t* x, const uint16_t* y, const uint16_t* dy, int64_t rows, int32_t C,
+                               int relu, const float* mean, const float* inv_std, const float* gamma, float* dgamma,
+                               float* dbeta, uint16_t* dx, hipStream_t s);
+hipError_t launch_relu_bwd(const uint16_t* y, const uint16_t* dy, int64_t total, uint16_t* dx, hipStream_t s);
+hipError_t launch_softmax_xent(const float* z, const int32_t* labels, int32_t N, int32_t K, float* loss,
+                               float* loss_per_sample, uint16_t* dz, hipStream_t s);
 
 hipError_t launch_sgd(float* w, float* v, const float* g, int64_t count, float lr, float mu,
                       float wd, hipStream_t stream);

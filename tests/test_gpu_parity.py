@@ -275,6 +275,44 @@ def test_repeat_runs_are_bitwise_identical(tbn):
                                b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32))
 
 
+SPLIT_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1), (3, 12, 12, 128, 136, 3, 3, 2, 1),
+               (2, 7, 7, 512, 512, 3, 3, 1, 1)]
+
+
+@pytest.mark.parametrize("splits", [1, 2, 7, 1000])
+def test_reduction_splits(tbn, splits, monkeypatch):
+    # the reduction split into ranges summed by the epilogue kernel: fused epilogue (scale,
+    # bias, bf16 residual, ReLU) and fp32 output of fwd, and bwd_data, against the oracle;
+    # 1000 clamps to one 64-element stage per range
+    monkeypatch.setenv("TBN_CONV_SPLITS", str(splits))
+    for g in SPLIT_CASES:
+        log("splits %d %s" % (splits, g))
+        d, P, Q, xb, dyb, wr = _conv_inputs(g, 9)
+        k = g[4]
+        q = oracle.quantize(wr)
+        a64 = q.alpha.astype(np.float64)
+        scale = synth.uniform(9, "sc", (k,), 0.5, 1.5)
+        bias = synth.normal(9, "bi", (k,), 0.1)
+        resb = synth.normal_bf16(9, "res", (g[0], P, Q, k))
+        acc = oracle.conv_fwd(d, oracle.bf16_bits_to_f64(xb), q.codes, a64)
+        ref = np.maximum(acc * scale.astype(np.float64) + bias + oracle.bf16_bits_to_f64(resb), 0.0)
+        codes, alpha, _ = tbn.quantize(to_dev(wr))
+        desc = tbn.ConvDesc(*g)
+        y = tbn.conv2d_fwd(desc, bf16_dev(xb), codes, alpha, out_dtype=torch.bfloat16, scale=to_dev(scale),
+                           bias=to_dev(bias), residual=bf16_dev(resb), relu=True)
+        y32 = tbn.conv2d_fwd(desc, bf16_dev(xb), codes, alpha, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        e = nerr(y.float().cpu().numpy(), ref)
+        assert e <= TOL, "fwd epilogue splits %d %s: %.3e" % (splits, g, e)
+        e = nerr(y32.cpu().numpy(), acc)
+        assert e <= 1e-4, "fwd splits %d %s: %.3e" % (splits, g, e)
+        if g[7] == 1:
+            dx = tbn.conv2d_bwd_data(desc, bf16_dev(dyb), codes, alpha, out_dtype=torch.float32)
+            torch.cuda.synchronize()
+            e = nerr(dx.cpu().numpy(), oracle.conv_bwd_data(d, oracle.bf16_bits_to_f64(dyb), q.codes, a64))
+            assert e <= TOL, "bwd_data splits %d %s: %.3e" % (splits, g, e)
+
+
 TILE_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1), (2, 10, 10, 40, 24, 3, 3, 1, 1),
               (3, 12, 12, 128, 130, 3, 3, 2, 1)]
 
