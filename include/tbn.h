@@ -121,11 +121,25 @@ tbn_status tbn_quantize(const float* w, int64_t k, int64_t n, uint32_t* codes, f
  *   codes  TBN2 packed codes of the K filters (n = R*S*C); alpha [K] fp32.
  *   ep     optional epilogue (NULL = none).
  *   y      NHWC [N][P][Q][K], dtype yt.
- *   ws     workspace of tbn_workspace_size(TBN_OP_FWD) bytes (currently 0: may be NULL).
+ *   ws     workspace of tbn_workspace_size(TBN_OP_FWD) bytes: fp32 partial sums when
+ *          the layer has too few output tiles to fill the GPU and its reduction is split
+ *          (may be NULL when that size is 0).  TBN_ERR_WORKSPACE if smaller.
  */
 tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt,
                           const uint32_t* codes, const float* alpha, const tbn_epilogue* ep,
                           void* y, tbn_dtype yt, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Forward pass of a layer kept in full precision (Eq. 1 with the real filters; the first
+ * convolution of the CIFAR-shaped network stays unquantised):
+ *   y[n,p,q,k] = sum_{r,s,c} x[n, p*sh-ph+r, q*sw-pw+s, c] * bf16(w[k,r,s,c]),
+ * then the optional epilogue.  Filters are rounded to bf16 (nearest even) on load, as are
+ * TBN_F32 activations; products and sums are fp32.  Meant for thin layers (few input
+ * channels): it runs on the vector ALUs, not the matrix cores.
+ *   x   NHWC [N][H][W][C], dtype xt.   w  [K][R][S][C] fp32.   y  NHWC [N][P][Q][K], dtype yt.
+ */
+tbn_status tbn_conv2d_fwd_dense(const tbn_conv_desc* desc, const void* x, tbn_dtype xt, const float* w,
+                                const tbn_epilogue* ep, void* y, tbn_dtype yt, hipStream_t stream);
 
 /*
  * Backward pass to the layer input through the approximate filters W^ = alpha W~

@@ -59,6 +59,8 @@ def _load():
     lib.orc_out_dims.restype = ctypes.c_int
     lib.orc_conv_fwd.argtypes = [p, p, p, p, ctypes.c_int, p]
     lib.orc_conv_fwd.restype = ctypes.c_int
+    lib.orc_conv_fwd_dense.argtypes = [p, p, p, p]
+    lib.orc_conv_fwd_dense.restype = ctypes.c_int
     lib.orc_conv_bwd_data.argtypes = [p, p, p, p, p]
     lib.orc_conv_bwd_data.restype = ctypes.c_int
     lib.orc_conv_bwd_weight.argtypes = [p, p, p, p]
@@ -212,6 +214,19 @@ def conv_fwd(desc: ConvDesc, x: np.ndarray, codes: np.ndarray, alpha: np.ndarray
     d = desc.as_array()
     if _load().orc_conv_fwd(_ptr(d), _ptr(x), _ptr(codes), _ptr(alpha), form, _ptr(y)) != 0:
         raise OracleError("conv_fwd failed")
+    return y
+
+
+def conv_fwd_dense(desc: ConvDesc, x: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """Eq. (1) with real-valued filters w [K][R][S][C] (a full-precision layer)."""
+    P, Q = desc.out_dims()
+    x = _c(x, np.float64)
+    w = _c(w, np.float64)
+    if x.size != desc.n * desc.h * desc.w * desc.c or w.size != desc.k * desc.r * desc.s * desc.c:
+        raise OracleError("conv_fwd_dense: operand sizes do not match the geometry")
+    y = np.zeros((desc.n, P, Q, desc.k), np.float64)
+    if _load().orc_conv_fwd_dense(_ptr(desc.as_array()), _ptr(x), _ptr(w), _ptr(y)) != 0:
+        raise OracleError("conv_fwd_dense failed")
     return y
 
 

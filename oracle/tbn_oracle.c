@@ -240,6 +240,41 @@ int orc_conv_fwd(const int32_t* d, const double* x, const int8_t* codes, const d
 }
 
 /*
+ * Forward convolution with real-valued filters (Eq. 1 with full-precision weights): the
+ * layer that stays in full precision (the first convolution of the CIFAR-shaped network)
+ * uses it.  w is [K][R][S][C].
+ */
+int orc_conv_fwd_dense(const int32_t* d, const double* x, const double* wts, double* y) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t N = d[DN], H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t nn = 0; nn < N; ++nn) {
+        for (int64_t p = 0; p < P; ++p) {
+            for (int64_t q = 0; q < Q; ++q) {
+                for (int64_t k = 0; k < K; ++k) {
+                    double acc = 0.0;
+                    for (int64_t r = 0; r < R; ++r) {
+                        int64_t h = p * sh - ph + r;
+                        if (h < 0 || h >= H) continue;
+                        for (int64_t s = 0; s < S; ++s) {
+                            int64_t w = q * sw - pw + s;
+                            if (w < 0 || w >= W) continue;
+                            const double* xp = x + ((nn * H + h) * W + w) * C;
+                            const double* wp = wts + ((k * R + r) * S + s) * C;
+                            for (int64_t c = 0; c < C; ++c) acc += xp[c] * wp[c];
+                        }
+                    }
+                    y[((nn * P + p) * Q + q) * K + k] = acc;
+                }
+            }
+        }
+    }
+    return ORC_OK;
+}
+
+/*
  * Backward pass to the layer input through the approximate filters W^ = alpha W~
  * (Sec. 3: both passes use the approximate filters; Algorithm 1, backward step).
  * By the chain rule through y[n,p,q,k] = sum x[n, p*sh-ph+r, q*sw-pw+s, c] W^[k,r,s,c]:

@@ -77,6 +77,7 @@ def load():
         "tbn_workspace_size": ([i32, vp, vp], i32),
         "tbn_quantize": ([vp, i64, i64, vp, vp, vp, vp], i32),
         "tbn_conv2d_fwd": ([vp, vp, i32, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
+        "tbn_conv2d_fwd_dense": ([vp, vp, i32, vp, vp, vp, i32, vp], i32),
         "tbn_conv2d_bwd_data": ([vp, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_conv2d_bwd_weight": ([vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_sgd_step": ([vp, vp, vp, i64, f32, f32, f32, vp], i32),
@@ -99,7 +100,8 @@ def load():
 
 def exported_symbols():
     return sorted(["tbn_status_str", "tbn_last_error", "tbn_conv_out_dims", "tbn_packed_words",
-                   "tbn_workspace_size", "tbn_quantize", "tbn_conv2d_fwd", "tbn_conv2d_bwd_data",
+                   "tbn_workspace_size", "tbn_quantize", "tbn_conv2d_fwd", "tbn_conv2d_fwd_dense",
+                   "tbn_conv2d_bwd_data",
                    "tbn_conv2d_bwd_weight", "tbn_sgd_step", "tbn_pool_out_dims", "tbn_maxpool2d_fwd",
                    "tbn_maxpool2d_bwd", "tbn_avgpool_global", "tbn_batchnorm_train_fwd",
                    "tbn_batchnorm_train_bwd", "tbn_relu_bwd", "tbn_softmax_xent"])
@@ -209,6 +211,32 @@ def conv2d_fwd(desc: ConvDesc, x, codes, alpha, y=None, out_dtype=torch.bfloat16
           ctypes.byref(ep) if ep is not None else None, _dev(y, "y", (torch.bfloat16, torch.float32)),
           _dtype_code(y.dtype), _dev(ws, "ws") if ws is not None else None,
           ws.numel() * ws.element_size() if ws is not None else 0, _stream())
+    return y
+
+
+def conv2d_fwd_dense(desc: ConvDesc, x, w, y=None, out_dtype=torch.bfloat16, scale=None, bias=None,
+                     residual=None, relu=False):
+    """Full-precision layer: y = act(scale_k * (x conv bf16(w)) + bias_k + residual), NHWC;
+    w fp32 [K][R][S][C]."""
+    P, Q = desc.out_dims()
+    _numel(x, desc.n * desc.h * desc.w * desc.c, "x")
+    _numel(w, desc.k * desc.r * desc.s * desc.c, "w")
+    if y is None:
+        y = torch.empty((desc.n, P, Q, desc.k), dtype=out_dtype, device=x.device)
+    _numel(y, desc.n * P * Q * desc.k, "y")
+    ep = None
+    if scale is not None or bias is not None or residual is not None or relu:
+        if residual is not None:
+            _numel(residual, y.numel(), "residual")
+            if residual.dtype != y.dtype:
+                raise TypeError("residual must have y's dtype")
+        ep = Epilogue(_dev(scale, "scale", (torch.float32,)).value if scale is not None else None,
+                      _dev(bias, "bias", (torch.float32,)).value if bias is not None else None,
+                      _dev(residual, "residual").value if residual is not None else None,
+                      1 if relu else 0)
+    _call("tbn_conv2d_fwd_dense", ctypes.byref(desc), _dev(x, "x", (torch.bfloat16, torch.float32)),
+          _dtype_code(x.dtype), _dev(w, "w", (torch.float32,)), ctypes.byref(ep) if ep is not None else None,
+          _dev(y, "y", (torch.bfloat16, torch.float32)), _dtype_code(y.dtype), _stream())
     return y
 
 

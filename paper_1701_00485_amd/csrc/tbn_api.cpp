@@ -220,6 +220,38 @@ tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_fwd");
 }
 
+tbn_status tbn_conv2d_fwd_dense(const tbn_conv_desc* desc, const void* x, tbn_dtype xt, const float* w,
+                                const tbn_epilogue* ep, void* y, tbn_dtype yt, hipStream_t stream) {
+    Geometry g;
+    tbn_status st = check_desc(desc, &g);
+    if (st != TBN_OK) return st;
+    if (!x || !w || !y) return fail(TBN_ERR_NULL, "x, w and y are required");
+    if ((xt != TBN_BF16 && xt != TBN_F32) || (yt != TBN_BF16 && yt != TBN_F32))
+        return fail(TBN_ERR_UNSUPPORTED, "unknown dtype");
+    if (!aligned16(x) || !aligned16(y) || !aligned4(w)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    if (g.K > 65535 * 16) return fail(TBN_ERR_SHAPE, "too many filters");
+    tbn::DenseConvArgs a = {};
+    if (ep) {
+        if ((ep->scale && !aligned4(ep->scale)) || (ep->bias && !aligned4(ep->bias)) ||
+            (ep->residual && !aligned16(ep->residual)))
+            return fail(TBN_ERR_ALIGN, "misaligned epilogue pointer");
+        a.scale = ep->scale;
+        a.bias = ep->bias;
+        a.residual = ep->residual;
+        a.relu = ep->relu ? 1 : 0;
+    }
+    a.x = x;
+    a.w = w;
+    a.y = y;
+    a.N = (int32_t)g.N; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.C = (int32_t)g.C; a.K = (int32_t)g.K;
+    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = (int32_t)g.sh; a.sw = (int32_t)g.sw;
+    a.ph = (int32_t)g.ph; a.pw = (int32_t)g.pw; a.P = (int32_t)g.P; a.Q = (int32_t)g.Q;
+    a.x_f32 = xt == TBN_F32;
+    a.y_f32 = yt == TBN_F32;
+    hipError_t e = tbn::launch_conv_dense(a, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_fwd_dense");
+}
+
 tbn_status tbn_conv2d_bwd_data(const tbn_conv_desc* desc, const void* dy, const uint32_t* codes, const float* alpha,
                                void* dx, tbn_dtype dxt, void* ws, size_t ws_bytes, hipStream_t stream) {
     Geometry g;

@@ -100,6 +100,19 @@ hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream);
 hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, float* dw,
                                int32_t accumulate, hipStream_t stream);
 
+struct DenseConvArgs {
+    const void* x;
+    const float* w;          // [K][R][S][C] fp32, rounded to bf16 on load
+    const float* scale;
+    const float* bias;
+    const void* residual;
+    void* y;
+    int32_t N, H, W, C, K, R, S, sh, sw, ph, pw, P, Q;
+    int32_t relu, x_f32, y_f32;
+};
+
+hipError_t launch_conv_dense(const DenseConvArgs& a, hipStream_t stream);
+
 struct PoolArgs {
     int32_t N, H, W, C, k, s, pad, P, Q;
 };

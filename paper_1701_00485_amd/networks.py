@@ -140,3 +140,250 @@ class ResNet18:
                 h, cin = h2, cout
         total += 2 * batch * 512 * 1000
         return total
+
+
+# --------------------------------------------------------------------------------------
+# Training (Algorithm 1): quantise every layer, forward, softmax cross-entropy, backward
+# through the approximate filters, straight-through gradient to the real filters, SGD.
+# --------------------------------------------------------------------------------------
+LR, MOMENTUM, WEIGHT_DECAY = 0.1, 0.9, 1e-4
+
+
+def _seeded(stream, name):
+    import zlib
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([1701_00485 + stream, zlib.crc32(name.encode())])))
+
+
+class TwoBitLayer:
+    """A trainable two-bit convolution (or fully-connected layer as an R x S "valid"
+    convolution over the whole map): fp32 real filters [K][R*S*C], momentum buffer, and the
+    codes / scales of the current quantisation."""
+
+    def __init__(self, name, cin, cout, k, stride, pad, device, stream, std=0.05):
+        self.name, self.cin, self.cout, self.k, self.stride, self.pad = name, cin, cout, k, stride, pad
+        g = _seeded(stream, name)
+        n = k * k * cin
+        self.w = torch.from_numpy((g.standard_normal((cout, n), dtype=np.float32) * np.float32(std))).to(device)
+        self.v = torch.zeros_like(self.w)
+        self.codes = self.alpha = None
+
+    def desc(self, x):
+        n, h, w, _ = x.shape
+        return tbn.ConvDesc(n, h, w, self.cin, self.cout, self.k, self.k, self.stride, self.pad)
+
+    def quantize(self):
+        self.codes, self.alpha, _ = tbn.quantize(self.w, codes=self.codes, alpha=self.alpha, want_counts=False)
+
+    def forward(self, x, relu=False, out_dtype=torch.bfloat16):
+        return tbn.conv2d_fwd(self.desc(x), x, self.codes, self.alpha, out_dtype=out_dtype, relu=relu)
+
+    def backward(self, x, dy, need_dx=True):
+        d = self.desc(x)
+        dx = tbn.conv2d_bwd_data(d, dy, self.codes, self.alpha) if need_dx else None
+        dw = tbn.conv2d_bwd_weight(d, x, dy)
+        return dx, dw
+
+
+class DenseLayer:
+    """A trainable full-precision convolution (filters rounded to bf16 at use)."""
+
+    def __init__(self, name, cin, cout, k, stride, pad, device, stream, std=0.05):
+        self.name, self.cin, self.cout, self.k, self.stride, self.pad = name, cin, cout, k, stride, pad
+        g = _seeded(stream, name)
+        self.w = torch.from_numpy((g.standard_normal((cout, k * k * cin), dtype=np.float32) * np.float32(std))).to(device)
+        self.v = torch.zeros_like(self.w)
+
+    def desc(self, x):
+        n, h, w, _ = x.shape
+        return tbn.ConvDesc(n, h, w, self.cin, self.cout, self.k, self.k, self.stride, self.pad)
+
+    def forward(self, x, relu=False, out_dtype=torch.bfloat16):
+        return tbn.conv2d_fwd_dense(self.desc(x), x, self.w, out_dtype=out_dtype, relu=relu)
+
+    def backward(self, x, dy, need_dx=False):
+        if need_dx:
+            raise NotImplementedError("the full-precision layer is the first layer: no input gradient")
+        return None, tbn.conv2d_bwd_weight(self.desc(x), x, dy)
+
+
+class BatchNorm:
+    """Batch normalisation in training form (batch statistics), gamma ~ U(0.5, 1.5),
+    beta ~ N(0, 0.1); trained without weight decay."""
+
+    def __init__(self, name, c, device, stream):
+        g = _seeded(stream, name + ".bn")
+        self.name = name + ".bn"
+        self.gamma = torch.from_numpy(g.uniform(0.5, 1.5, c).astype(np.float32)).to(device)
+        self.beta = torch.from_numpy(g.normal(0.0, 0.1, c).astype(np.float32)).to(device)
+        self.vg = torch.zeros_like(self.gamma)
+        self.vb = torch.zeros_like(self.beta)
+
+
+class _Trainer:
+    """Shared step logic: `rec` (when given a list) receives (kind, info, tensors) for every
+    operation, with copies of whatever the step later overwrites."""
+
+    def _rec(self, trace, kind, info, **t):
+        if trace is not None:
+            trace.append((kind, info, t))
+
+    def _sgd(self, trace, name, w, v, g, wd):
+        if trace is not None:
+            w0, v0 = w.clone(), v.clone()
+        tbn.sgd_step(w, v, g, self.lr, MOMENTUM, wd)
+        if trace is not None:
+            self._rec(trace, "sgd", (name, wd), w=w0, v=v0, g=g, w_new=w, v_new=v)
+
+    def _quantize(self, trace):
+        for l in self.two_bit_layers():
+            l.quantize()
+            self._rec(trace, "quantize", l, w=l.w.clone(), codes=l.codes.clone(), alpha=l.alpha.clone())
+
+
+class LeNet(_Trainer):
+    """MNIST-shaped LeNet, every layer two-bit: conv 5x5 1->32 pad 2, ReLU, max pool 2,
+    conv 5x5 32->64 pad 2, ReLU, max pool 2, FC 3136->512 (7x7 "valid" convolution), ReLU,
+    FC 512->10; softmax cross-entropy, mean over the batch."""
+
+    def __init__(self, device="cuda", stream=2, lr=LR):
+        self.lr = lr
+        self.conv1 = TwoBitLayer("conv1", 1, 32, 5, 1, 2, device, stream)
+        self.conv2 = TwoBitLayer("conv2", 32, 64, 5, 1, 2, device, stream)
+        self.fc1 = TwoBitLayer("fc1", 64, 512, 7, 1, 0, device, stream)
+        self.fc2 = TwoBitLayer("fc2", 512, 10, 1, 1, 0, device, stream)
+
+    def two_bit_layers(self):
+        return [self.conv1, self.conv2, self.fc1, self.fc2]
+
+    @staticmethod
+    def flops(batch):
+        f = 0
+        for (h, c, k, r, hout) in [(28, 1, 32, 5, 28), (14, 32, 64, 5, 14), (7, 64, 512, 7, 1), (1, 512, 10, 1, 1)]:
+            f += 2 * batch * hout * hout * k * r * r * c
+        return f
+
+    def step(self, x, labels, trace=None):
+        """x [N][28][28][1] bf16, labels [N] int32 -> loss (fp32 [1]); updates the weights."""
+        rec = self._rec
+        N = x.shape[0]
+        self._quantize(trace)
+        a1 = self.conv1.forward(x, relu=True)
+        rec(trace, "conv_fwd", (self.conv1, True), x=x, y=a1)
+        p1, arg1 = tbn.maxpool2d_fwd(a1, 2, 2, 0, want_argmax=True)
+        rec(trace, "maxpool", (2, 2, 0), x=a1, y=p1, arg=arg1)
+        a2 = self.conv2.forward(p1, relu=True)
+        rec(trace, "conv_fwd", (self.conv2, True), x=p1, y=a2)
+        p2, arg2 = tbn.maxpool2d_fwd(a2, 2, 2, 0, want_argmax=True)
+        rec(trace, "maxpool", (2, 2, 0), x=a2, y=p2, arg=arg2)
+        h3 = self.fc1.forward(p2, relu=True)
+        rec(trace, "conv_fwd", (self.fc1, True), x=p2, y=h3)
+        z = self.fc2.forward(h3, out_dtype=torch.float32)
+        rec(trace, "conv_fwd", (self.fc2, False), x=h3, y=z)
+        loss, dz = tbn.softmax_xent(z.view(N, 10), labels)
+        rec(trace, "xent", None, z=z.view(N, 10), labels=labels, loss=loss, dz=dz)
+        dz = dz.view(N, 1, 1, 10)
+        dh3, dw4 = self.fc2.backward(h3, dz)
+        rec(trace, "conv_bwd", self.fc2, x=h3, dy=dz, dx=dh3, dw=dw4)
+        dz3 = tbn.relu_bwd(h3, dh3)
+        rec(trace, "relu_bwd", None, y=h3, dy=dh3, dx=dz3)
+        dp2, dw3 = self.fc1.backward(p2, dz3)
+        rec(trace, "conv_bwd", self.fc1, x=p2, dy=dz3, dx=dp2, dw=dw3)
+        da2 = tbn.maxpool2d_bwd(dp2, arg2, a2.shape, 2, 2, 0)
+        rec(trace, "maxpool_bwd", (2, 2, 0), dy=dp2, arg=arg2, dx=da2)
+        dz2 = tbn.relu_bwd(a2, da2)
+        rec(trace, "relu_bwd", None, y=a2, dy=da2, dx=dz2)
+        dp1, dw2 = self.conv2.backward(p1, dz2)
+        rec(trace, "conv_bwd", self.conv2, x=p1, dy=dz2, dx=dp1, dw=dw2)
+        da1 = tbn.maxpool2d_bwd(dp1, arg1, a1.shape, 2, 2, 0)
+        rec(trace, "maxpool_bwd", (2, 2, 0), dy=dp1, arg=arg1, dx=da1)
+        dz1 = tbn.relu_bwd(a1, da1)
+        rec(trace, "relu_bwd", None, y=a1, dy=da1, dx=dz1)
+        _, dw1 = self.conv1.backward(x, dz1, need_dx=False)
+        rec(trace, "conv_bwd", self.conv1, x=x, dy=dz1, dx=None, dw=dw1)
+        for l, g in zip(self.two_bit_layers(), (dw1, dw2, dw3, dw4)):
+            self._sgd(trace, l.name, l.w, l.v, g.view(l.w.shape), WEIGHT_DECAY)
+        return loss
+
+
+class VGGSmall(_Trainer):
+    """CIFAR-shaped VGG: conv 3x3 3->128 in full precision (bf16 filters), then two-bit
+    conv 3x3 128->128, pool, 128->256, 256->256, pool, 256->512, 512->512, pool, FC 8192->10
+    (4x4 "valid" convolution); training-form batch normalisation and ReLU after every
+    convolution; softmax cross-entropy, mean over the batch."""
+
+    PLAN = [(3, 128, False), (128, 128, True), (128, 256, False), (256, 256, True), (256, 512, False),
+            (512, 512, True)]  # (cin, cout, max pool after)
+
+    def __init__(self, device="cuda", stream=3, lr=LR):
+        self.lr = lr
+        self.convs, self.bns = [], []
+        for i, (cin, cout, _) in enumerate(self.PLAN):
+            name = "conv%d" % (i + 1)
+            layer = DenseLayer if i == 0 else TwoBitLayer
+            self.convs.append(layer(name, cin, cout, 3, 1, 1, device, stream))
+            self.bns.append(BatchNorm(name, cout, device, stream))
+        self.fc = TwoBitLayer("fc", 512, 10, 4, 1, 0, device, stream)
+
+    def two_bit_layers(self):
+        return self.convs[1:] + [self.fc]
+
+    @staticmethod
+    def flops(batch):
+        f, h = 0, 32
+        for cin, cout, pool in VGGSmall.PLAN:
+            f += 2 * batch * h * h * cout * 9 * cin
+            if pool:
+                h //= 2
+        return f + 2 * batch * 10 * 8192
+
+    def step(self, x, labels, trace=None):
+        """x [N][32][32][3] bf16, labels [N] int32 -> loss (fp32 [1]); updates the weights."""
+        rec = self._rec
+        N = x.shape[0]
+        self._quantize(trace)
+        saved = []  # per conv: (input, pre-BN output, post-BN-ReLU output, mean, inv_std, pool argmax)
+        h = x
+        for conv, bn, (_, _, pool) in zip(self.convs, self.bns, self.PLAN):
+            z = conv.forward(h)
+            extra = {"w": conv.w.clone()} if trace is not None and isinstance(conv, DenseLayer) else {}
+            rec(trace, "conv_fwd", (conv, False), x=h, y=z, **extra)
+            a, mean, inv_std = tbn.batchnorm_train_fwd(z, bn.gamma, bn.beta, relu=True)
+            if trace is not None:  # gamma and beta are updated in place at the end of the step
+                rec(trace, "bn_fwd", bn, x=z, y=a, mean=mean, inv_std=inv_std, gamma=bn.gamma.clone(),
+                    beta=bn.beta.clone())
+            arg = None
+            out = a
+            if pool:
+                out, arg = tbn.maxpool2d_fwd(a, 2, 2, 0, want_argmax=True)
+                rec(trace, "maxpool", (2, 2, 0), x=a, y=out, arg=arg)
+            saved.append((h, z, a, mean, inv_std, arg))
+            h = out
+        logits = self.fc.forward(h, out_dtype=torch.float32)
+        rec(trace, "conv_fwd", (self.fc, False), x=h, y=logits)
+        loss, dz = tbn.softmax_xent(logits.view(N, 10), labels)
+        rec(trace, "xent", None, z=logits.view(N, 10), labels=labels, loss=loss, dz=dz)
+        dh, dwfc = self.fc.backward(h, dz.view(N, 1, 1, 10))
+        rec(trace, "conv_bwd", self.fc, x=h, dy=dz.view(N, 1, 1, 10), dx=dh, dw=dwfc)
+        grads = [None] * len(self.convs)
+        bn_grads = [None] * len(self.convs)
+        for i in reversed(range(len(self.convs))):
+            conv, bn = self.convs[i], self.bns[i]
+            hin, z, a, mean, inv_std, arg = saved[i]
+            if arg is not None:
+                da = tbn.maxpool2d_bwd(dh, arg, a.shape, 2, 2, 0)
+                rec(trace, "maxpool_bwd", (2, 2, 0), dy=dh, arg=arg, dx=da)
+            else:
+                da = dh
+            dzi, dg, db = tbn.batchnorm_train_bwd(z, a, da, mean, inv_std, bn.gamma, relu=True)
+            if trace is not None:
+                rec(trace, "bn_bwd", bn, x=z, y=a, dy=da, gamma=bn.gamma.clone(), dx=dzi, dgamma=dg, dbeta=db)
+            dh, dw = conv.backward(hin, dzi, need_dx=i > 0)
+            rec(trace, "conv_bwd", conv, x=hin, dy=dzi, dx=dh, dw=dw)
+            grads[i], bn_grads[i] = dw, (dg, db)
+        for conv, g in zip(self.convs, grads):
+            self._sgd(trace, conv.name, conv.w, conv.v, g.view(conv.w.shape), WEIGHT_DECAY)
+        self._sgd(trace, self.fc.name, self.fc.w, self.fc.v, dwfc.view(self.fc.w.shape), WEIGHT_DECAY)
+        for bn, (dg, db) in zip(self.bns, bn_grads):
+            self._sgd(trace, bn.name + ".gamma", bn.gamma, bn.vg, dg, 0.0)
+            self._sgd(trace, bn.name + ".beta", bn.beta, bn.vb, db, 0.0)
+        return loss

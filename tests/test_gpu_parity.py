@@ -211,6 +211,34 @@ def test_fwd_epilogue(tbn, g):
     assert e <= TOL
 
 
+DENSE_CASES = [(4, 32, 32, 3, 128, 3, 3, 1, 1), (2, 9, 9, 3, 5, 3, 3, 2, 1), (2, 12, 11, 40, 24, 3, 3, 1, 1),
+               (1, 20, 20, 70, 16, 3, 3, 1, 1)]  # the last reduces over 630 > one LDS fill of 512
+
+
+@pytest.mark.parametrize("g", DENSE_CASES)
+def test_fwd_dense_parity(tbn, g):
+    # the full-precision layer: filters rounded to bf16, fp32 accumulation, fused epilogue
+    log("fwd dense %s" % (g,))
+    d, P, Q, xb, _, _ = _conv_inputs(g, 5)
+    k = g[4]
+    w = synth.normal(5, "wd%s" % (g,), (k, g[5] * g[6] * g[3]), 0.3)
+    scale = synth.uniform(5, "sc", (k,), 0.5, 1.5)
+    bias = synth.normal(5, "bi", (k,), 0.1)
+    resb = synth.normal_bf16(5, "res", (g[0], P, Q, k))
+    acc = oracle.conv_fwd_dense(d, oracle.bf16_bits_to_f64(xb), oracle.round_bf16(w))
+    desc = tbn.ConvDesc(*g)
+    y32 = tbn.conv2d_fwd_dense(desc, bf16_dev(xb), to_dev(w), out_dtype=torch.float32)
+    y = tbn.conv2d_fwd_dense(desc, bf16_dev(xb), to_dev(w), scale=to_dev(scale), bias=to_dev(bias),
+                             residual=bf16_dev(resb), relu=True)
+    xf = oracle.bf16_bits_to_f64(xb).astype(np.float32)  # fp32 input holding bf16 values
+    yf = tbn.conv2d_fwd_dense(desc, to_dev(xf), to_dev(w), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert nerr(y32.cpu().numpy(), acc) <= 1e-5
+    assert nerr(yf.cpu().numpy(), acc) <= 1e-5
+    ref = np.maximum(acc * scale.astype(np.float64) + bias + oracle.bf16_bits_to_f64(resb), 0.0)
+    assert nerr(y.float().cpu().numpy(), ref) <= TOL
+
+
 BWD_CASES = [c for c in CONV_CASES if c[7] == 1] + [(2, 8, 8, 64, 64, 3, 3, 1, 0), (2, 6, 6, 64, 64, 5, 5, 1, 4)]
 
 

@@ -196,3 +196,26 @@ def test_sgd_hand_step():
     # v = 0.45 + 2.01 = 2.46; w = 1 - 0.246 = 0.754
     w, v = oracle.sgd([1.0], [0.5], [2.0], 0.1, 0.9, 0.01)
     assert v[0] == pytest.approx(2.46, abs=1e-15) and w[0] == pytest.approx(0.754, abs=1e-15)
+
+
+@pytest.mark.parametrize("g", GEOMS)
+def test_dense_fwd_matches_torch_conv2d(g):
+    # the full-precision layer: Eq. (1) with real filters, pinned to torch's fp64 conv2d
+    n, h, w, c, k, r, s, st, pd = g
+    desc = oracle.ConvDesc(*g)
+    x = synth.normal(0, "dx%s" % (g,), (n, h, w, c)).astype(np.float64)
+    wr = synth.normal(0, "dw%s" % (g,), (k, r, s, c)).astype(np.float64)
+    y = oracle.conv_fwd_dense(desc, x, wr)
+    xt = torch.from_numpy(np.ascontiguousarray(x.transpose(0, 3, 1, 2)))
+    wt = torch.from_numpy(np.ascontiguousarray(wr.transpose(0, 3, 1, 2)))
+    ref = F.conv2d(xt, wt, stride=st, padding=pd).numpy().transpose(0, 2, 3, 1)
+    assert np.allclose(y, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_dense_fwd_with_approximate_filters_equals_two_bit_fwd():
+    # real filters alpha W~ give exactly the two-bit layer (dense form of Eq. 1)
+    g = (2, 9, 8, 5, 6, 3, 3, 1, 1)
+    desc, x, q, _ = _problem(g, "dense2bit")
+    wd = q.alpha64[:, None] * q.codes.astype(np.float64)
+    y = oracle.conv_fwd_dense(desc, x, wd)
+    assert np.allclose(y, oracle.conv_fwd(desc, x, q.codes, q.alpha64, form=2), rtol=0, atol=1e-13)
