@@ -40,6 +40,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-resnet", action="store_true", help="skip the ResNet-18 forward figures")
+    ap.add_argument("--no-small", action="store_true", help="skip the single-layer, LeNet and VGG figures")
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle sample")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain device copy of known size (HBM counter calibration)")
@@ -205,6 +206,57 @@ def resnet18_fwd(dev, steps=10, warmup=3):
     return out
 
 
+def small_configs(dev, steps=20, warmup=3):
+    """The smaller workloads: one two-bit layer on MNIST-shaped fp32 input (forward only,
+    latency-bound), and full training iterations of the MNIST-shaped LeNet (batch 256) and
+    the CIFAR-shaped VGG (batch 128)."""
+    import torch
+
+    import paper_1701_00485_amd as tbn
+    import synth
+    from paper_1701_00485_amd.networks import LeNet, VGGSmall
+
+    stream = torch.cuda.current_stream()
+    out = {}
+
+    def timed(fn, n):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    # single layer: 16 x 28 x 28 x 1 fp32 U[0,1) -> 32 filters 5x5 pad 2, fp32 output
+    d = tbn.ConvDesc(16, 28, 28, 1, 32, 5, 5, 1, 2)
+    x = torch.from_numpy(synth.uniform(1, "x", (16, 28, 28, 1))).to(dev)
+    w = torch.from_numpy(synth.normal(1, "w", (32, 25), 0.05)).to(dev)
+    codes, alpha, _ = tbn.quantize(w, want_counts=False)
+    y = torch.empty((16, 28, 28, 32), dtype=torch.float32, device=dev)
+    ms = timed(lambda: tbn.conv2d_fwd(d, x, codes, alpha, y=y), 200)
+    fl = 2.0 * 16 * 28 * 28 * 32 * 25
+    byts = 16 * 28 * 28 * 4 + y.numel() * 4 + codes.numel() * 4 + 32 * 4
+    out["single_layer_fwd"] = {"shape": "16x28x28x1 fp32 -> 32 filters 5x5 pad 2, fp32 out", "us_per_call": round(ms * 1e3, 2),
+                               "effective_tflops": round(fl / (ms * 1e-3) / 1e12, 3),
+                               "hbm_frac": round(byts / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+
+    for name, cls, batch, mk in (
+            ("lenet_train", LeNet, 256,
+             lambda: synth.bf16_bits(synth.uniform(2, "bench_x", (256, 28, 28, 1)))),
+            ("vgg_small_train", VGGSmall, 128, lambda: synth.normal_bf16(3, "bench_x", (128, 32, 32, 3)))):
+        net = cls(device=dev)
+        xb = torch.from_numpy(mk().view(np.int16)).to(dev).view(torch.bfloat16)
+        lab = torch.from_numpy(synth.labels(2, "bench_lab", batch, 10).astype(np.int32)).to(dev)
+        ms = timed(lambda: net.step(xb, lab), steps)
+        out[name] = {"batch": batch, "ms_per_iteration": round(ms, 4), "images_per_s": round(batch / (ms * 1e-3), 1),
+                     "effective_tflops": round(cls.train_flops(batch) / (ms * 1e-3) / 1e12, 2)}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -319,6 +371,8 @@ def main():
     }
     if not args.no_resnet:
         result["resnet18_fwd"] = resnet18_fwd(dev)
+    if not args.no_small:
+        result["small_workloads"] = small_configs(dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(result), flush=True)

@@ -377,7 +377,9 @@ int conv_splits_override() {
     return e ? atoi(e) : -1;
 }
 
-static bool use_dma(const ConvGemmArgs& a, int cfg) { return conv_dma_eligible(a) && (cfg < 0 || cfg >= 10); }
+static bool use_dma(const ConvGemmArgs& a, int cfg) {
+    return conv_dma_eligible(a) && (cfg < 0 || (cfg >= 10 && cfg < 20));
+}
 
 size_t conv_gemm_partial_bytes(const ConvGemmArgs& a) {
     const int cfg = conv_tile_override();
@@ -392,6 +394,8 @@ hipError_t launch_conv_gemm(const ConvGemmArgs& args, hipStream_t stream) {
     a.chunks_per_split = 1 << 30;
     const int cfg = conv_tile_override();
     if (use_dma(a, cfg)) return launch_conv_dma(a, plan_conv_dma(a, cfg), stream);
+    ThinGeom tg;
+    if ((cfg < 0 || cfg == 20) && conv_thin_plan(a, &tg)) return launch_conv_thin(a, tg, stream);
     const bool vec = (a.C % 8 == 0) && !a.x_f32;
     if (a.apair) return vec ? launch_mode<A_VEC8, true>(a, cfg, stream) : launch_mode<A_SCALAR, true>(a, cfg, stream);
     return vec ? launch_mode<A_VEC8, false>(a, cfg, stream) : launch_mode<A_SCALAR, false>(a, cfg, stream);

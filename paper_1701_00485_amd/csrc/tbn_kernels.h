@@ -72,6 +72,20 @@ int conv_splits_override();
 // Bytes of split-K partials the forward / backward-data GEMM of these arguments needs.
 size_t conv_gemm_partial_bytes(const ConvGemmArgs& a);
 
+// Forward pass for inputs with few channels (C < 8 bf16, or fp32 with C <= 8): input patch
+// and decoded filters staged in LDS with the channels padded to a power of two.
+struct ThinGeom {
+    int32_t CP, T, logT, RT, WPITCH, PH, PW;
+    int32_t tiles_p, tiles_q;
+    int64_t ntiles;
+    int32_t w_off, p_off, s_off, lds_bytes;
+    int32_t pbuf;  // bf16 elements per patch buffer (two buffers)
+    int32_t rowlen, nelem, ept;  // input elements per patch row, per patch, per thread
+    FastDiv div_rowlen, div_c;
+};
+bool conv_thin_plan(const ConvGemmArgs& a, ThinGeom* g);
+hipError_t launch_conv_thin(const ConvGemmArgs& a, const ThinGeom& g, hipStream_t stream);
+
 // Re-pack the codes of K filters [K][R][S][C] into the codes of the C filters of the
 // transposed, spatially flipped layer [C][R][S][K] (backward-data operand), and build
 // the bf16 scale pairs of that layer's element pairs.

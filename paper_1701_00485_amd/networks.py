@@ -257,10 +257,16 @@ class LeNet(_Trainer):
 
     @staticmethod
     def flops(batch):
+        """Dense FLOP of one forward pass."""
         f = 0
         for (h, c, k, r, hout) in [(28, 1, 32, 5, 28), (14, 32, 64, 5, 14), (7, 64, 512, 7, 1), (1, 512, 10, 1, 1)]:
             f += 2 * batch * hout * hout * k * r * r * c
         return f
+
+    @staticmethod
+    def train_flops(batch):
+        """Forward, backward-data (not for the first layer) and backward-weight."""
+        return 3 * LeNet.flops(batch) - 2 * batch * 28 * 28 * 32 * 25
 
     def step(self, x, labels, trace=None):
         """x [N][28][28][1] bf16, labels [N] int32 -> loss (fp32 [1]); updates the weights."""
@@ -335,6 +341,11 @@ class VGGSmall(_Trainer):
             if pool:
                 h //= 2
         return f + 2 * batch * 10 * 8192
+
+    @staticmethod
+    def train_flops(batch):
+        """Forward, backward-data (not for the first layer) and backward-weight."""
+        return 3 * VGGSmall.flops(batch) - 2 * batch * 32 * 32 * 128 * 27
 
     def step(self, x, labels, trace=None):
         """x [N][32][32][3] bf16, labels [N] int32 -> loss (fp32 [1]); updates the weights."""

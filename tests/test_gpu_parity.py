@@ -143,6 +143,10 @@ CONV_CASES = [
     (2, 16, 16, 64, 128, 1, 1, 2, 0),       # 1x1 stride-2 projection
     (1, 33, 31, 3, 64, 7, 7, 2, 3),         # stem-like, C = 3
     (2, 10, 10, 40, 24, 3, 3, 1, 1),        # C = 40 (not a multiple of 64), K = 24
+    (3, 40, 70, 3, 64, 7, 7, 2, 3),         # stem 7x7/2 over RGB: several row and column tiles
+    (2, 11, 13, 7, 72, 3, 3, 1, 1),         # 7 channels (padded to 8), two filter blocks
+    (1, 19, 23, 4, 64, 5, 5, 2, 2),         # 4 channels, stride 2
+    (2, 9, 9, 2, 16, 3, 3, 1, 0),           # 2 channels, no padding
 ]
 
 
@@ -342,10 +346,10 @@ def test_reduction_splits(tbn, splits, monkeypatch):
 
 
 TILE_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1), (2, 10, 10, 40, 24, 3, 3, 1, 1),
-              (3, 12, 12, 128, 130, 3, 3, 2, 1)]
+              (3, 12, 12, 128, 130, 3, 3, 2, 1), (2, 19, 17, 3, 40, 7, 7, 2, 3)]
 
 
-@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 14, 16])
+@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 14, 16, 20])
 def test_every_tile_shape(tbn, tile, monkeypatch):
     # each tile shape of the convolution kernels against the oracle (fwd and bwd_data)
     monkeypatch.setenv("TBN_CONV_TILE", str(tile))
