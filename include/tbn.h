@@ -209,19 +209,25 @@ tbn_status tbn_maxpool2d_bwd(const tbn_pool_desc* desc, const void* dy, const in
 tbn_status tbn_avgpool_global(int32_t n, int32_t h, int32_t w, int32_t c, const void* x, void* y, tbn_dtype yt,
                               hipStream_t stream);
 
+/* Bytes of fp32 workspace the two batch-normalisation calls need for rows x c (per-chunk
+ * partial sums of the per-channel reductions). */
+tbn_status tbn_batchnorm_workspace_size(int64_t rows, int32_t c, size_t* bytes);
+
 /* Batch normalisation with batch statistics over rows = N*H*W positions per channel:
  * y = act(gamma (x - mean) inv_std + beta), inv_std = 1/sqrt(biased var + eps);
- * relu != 0 fuses max(., 0).  mean and inv_std [c] are written for the backward pass. */
+ * relu != 0 fuses max(., 0).  mean and inv_std [c] are written for the backward pass.
+ * The mean and the centred sum of squares are two passes of fixed-order fp32 sums
+ * (deterministic).  ws: tbn_batchnorm_workspace_size bytes (TBN_ERR_WORKSPACE if less). */
 tbn_status tbn_batchnorm_train_fwd(const void* x, int64_t rows, int32_t c, const float* gamma, const float* beta,
-                                   float eps, int32_t relu, void* y, float* mean, float* inv_std,
-                                   hipStream_t stream);
+                                   float eps, int32_t relu, void* y, float* mean, float* inv_std, void* ws,
+                                   size_t ws_bytes, hipStream_t stream);
 
 /* Backward of the above (through the batch statistics; with relu, g = dy * [y > 0]):
  * dx = gamma inv_std (g - mean(g) - xhat mean(g xhat)), dgamma = sum g xhat,
- * dbeta = sum g.  Sums are taken in a fixed order. */
+ * dbeta = sum g.  Sums are taken in a fixed order.  ws as for the forward call. */
 tbn_status tbn_batchnorm_train_bwd(const void* x, const void* y, const void* dy, int64_t rows, int32_t c,
                                    int32_t relu, const float* mean, const float* inv_std, const float* gamma,
-                                   float* dgamma, float* dbeta, void* dx, hipStream_t stream);
+                                   float* dgamma, float* dbeta, void* dx, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* dx = dy where y > 0, else 0 (ReLU'(0) = 0). */
 tbn_status tbn_relu_bwd(const void* y, const void* dy, int64_t count, void* dx, hipStream_t stream);

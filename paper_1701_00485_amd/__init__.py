@@ -85,8 +85,10 @@ def load():
         "tbn_maxpool2d_fwd": ([vp, vp, vp, vp, vp], i32),
         "tbn_maxpool2d_bwd": ([vp, vp, vp, vp, i32, vp], i32),
         "tbn_avgpool_global": ([i32, i32, i32, i32, vp, vp, i32, vp], i32),
-        "tbn_batchnorm_train_fwd": ([vp, i64, i32, vp, vp, f32, i32, vp, vp, vp, vp], i32),
-        "tbn_batchnorm_train_bwd": ([vp, vp, vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp], i32),
+        "tbn_batchnorm_workspace_size": ([i64, i32, vp], i32),
+        "tbn_batchnorm_train_fwd": ([vp, i64, i32, vp, vp, f32, i32, vp, vp, vp, vp, ctypes.c_size_t, vp], i32),
+        "tbn_batchnorm_train_bwd": ([vp, vp, vp, i64, i32, i32, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp],
+                                    i32),
         "tbn_relu_bwd": ([vp, vp, i64, vp, vp], i32),
         "tbn_softmax_xent": ([vp, vp, i32, i32, vp, vp, vp, vp], i32),
     }
@@ -103,8 +105,8 @@ def exported_symbols():
                    "tbn_workspace_size", "tbn_quantize", "tbn_conv2d_fwd", "tbn_conv2d_fwd_dense",
                    "tbn_conv2d_bwd_data",
                    "tbn_conv2d_bwd_weight", "tbn_sgd_step", "tbn_pool_out_dims", "tbn_maxpool2d_fwd",
-                   "tbn_maxpool2d_bwd", "tbn_avgpool_global", "tbn_batchnorm_train_fwd",
-                   "tbn_batchnorm_train_bwd", "tbn_relu_bwd", "tbn_softmax_xent"])
+                   "tbn_maxpool2d_bwd", "tbn_avgpool_global", "tbn_batchnorm_workspace_size",
+                   "tbn_batchnorm_train_fwd", "tbn_batchnorm_train_bwd", "tbn_relu_bwd", "tbn_softmax_xent"])
 
 
 def _status_name(s: int) -> str:
@@ -322,26 +324,44 @@ def avgpool_global(x, out_dtype=torch.bfloat16):
     return y
 
 
-def batchnorm_train_fwd(x, gamma, beta, eps=1e-5, relu=False):
+def batchnorm_workspace_size(rows: int, c: int) -> int:
+    b = ctypes.c_size_t()
+    _call("tbn_batchnorm_workspace_size", int(rows), int(c), ctypes.byref(b))
+    return b.value
+
+
+def _bn_ws(rows, c, ws, device):
+    need = batchnorm_workspace_size(rows, c)
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=device)
+    return ws
+
+
+def batchnorm_train_fwd(x, gamma, beta, eps=1e-5, relu=False, ws=None):
     c = x.shape[-1]
+    rows = x.numel() // c
     y = torch.empty_like(x)
     mean = torch.empty(c, dtype=torch.float32, device=x.device)
     inv_std = torch.empty(c, dtype=torch.float32, device=x.device)
-    _call("tbn_batchnorm_train_fwd", _dev(x, "x", (torch.bfloat16,)), x.numel() // c, c,
+    ws = _bn_ws(rows, c, ws, x.device)
+    _call("tbn_batchnorm_train_fwd", _dev(x, "x", (torch.bfloat16,)), rows, c,
           _dev(gamma, "gamma", (torch.float32,)), _dev(beta, "beta", (torch.float32,)), float(eps),
-          1 if relu else 0, _dev(y, "y"), _dev(mean, "mean"), _dev(inv_std, "inv_std"), _stream())
+          1 if relu else 0, _dev(y, "y"), _dev(mean, "mean"), _dev(inv_std, "inv_std"), _dev(ws, "ws"),
+          ws.numel() * ws.element_size(), _stream())
     return y, mean, inv_std
 
 
-def batchnorm_train_bwd(x, y, dy, mean, inv_std, gamma, relu=False):
+def batchnorm_train_bwd(x, y, dy, mean, inv_std, gamma, relu=False, ws=None):
     c = x.shape[-1]
+    rows = x.numel() // c
     dx = torch.empty_like(x)
     dgamma = torch.empty(c, dtype=torch.float32, device=x.device)
     dbeta = torch.empty(c, dtype=torch.float32, device=x.device)
+    ws = _bn_ws(rows, c, ws, x.device)
     _call("tbn_batchnorm_train_bwd", _dev(x, "x", (torch.bfloat16,)), _dev(y, "y", (torch.bfloat16,)),
-          _dev(dy, "dy", (torch.bfloat16,)), x.numel() // c, c, 1 if relu else 0, _dev(mean, "mean"),
+          _dev(dy, "dy", (torch.bfloat16,)), rows, c, 1 if relu else 0, _dev(mean, "mean"),
           _dev(inv_std, "inv_std"), _dev(gamma, "gamma"), _dev(dgamma, "dgamma"), _dev(dbeta, "dbeta"),
-          _dev(dx, "dx"), _stream())
+          _dev(dx, "dx"), _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream())
     return dx, dgamma, dbeta
 
 

@@ -382,26 +382,47 @@ tbn_status tbn_avgpool_global(int32_t n, int32_t h, int32_t w, int32_t c, const 
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_avgpool_global");
 }
 
+tbn_status tbn_batchnorm_workspace_size(int64_t rows, int32_t c, size_t* bytes) {
+    if (!bytes) return fail(TBN_ERR_NULL, "bytes is NULL");
+    if (rows <= 0 || c <= 0) return fail(TBN_ERR_SHAPE, "sizes must be positive");
+    if (rows > kI32Max * (int64_t)64 || (int64_t)c > kI32Max / 64) return fail(TBN_ERR_SHAPE, "too large");
+    *bytes = tbn::plan_bn(rows, c).ws_bytes;
+    return TBN_OK;
+}
+
+static tbn_status check_bn_ws(int64_t rows, int32_t c, const void* ws, size_t ws_bytes) {
+    if (!ws || ws_bytes < tbn::plan_bn(rows, c).ws_bytes) return fail(TBN_ERR_WORKSPACE, "workspace too small");
+    if (!aligned16(ws)) return fail(TBN_ERR_ALIGN, "workspace must be 16-byte aligned");
+    return TBN_OK;
+}
+
 tbn_status tbn_batchnorm_train_fwd(const void* x, int64_t rows, int32_t c, const float* gamma, const float* beta,
-                                   float eps, int32_t relu, void* y, float* mean, float* inv_std, hipStream_t stream) {
+                                   float eps, int32_t relu, void* y, float* mean, float* inv_std, void* ws,
+                                   size_t ws_bytes, hipStream_t stream) {
     if (!x || !gamma || !beta || !y || !mean || !inv_std) return fail(TBN_ERR_NULL, "missing pointer");
     if (rows <= 0 || c <= 0) return fail(TBN_ERR_SHAPE, "sizes must be positive");
     if (!aligned16(x) || !aligned16(y)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    tbn_status st = check_bn_ws(rows, c, ws, ws_bytes);
+    if (st != TBN_OK) return st;
     hipError_t e = tbn::launch_bn_train_fwd(reinterpret_cast<const uint16_t*>(x), rows, c, gamma, beta, eps, relu ? 1 : 0,
-                                            reinterpret_cast<uint16_t*>(y), mean, inv_std, stream);
+                                            reinterpret_cast<uint16_t*>(y), mean, inv_std,
+                                            reinterpret_cast<float*>(ws), stream);
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_batchnorm_train_fwd");
 }
 
 tbn_status tbn_batchnorm_train_bwd(const void* x, const void* y, const void* dy, int64_t rows, int32_t c, int32_t relu,
                                    const float* mean, const float* inv_std, const float* gamma, float* dgamma,
-                                   float* dbeta, void* dx, hipStream_t stream) {
+                                   float* dbeta, void* dx, void* ws, size_t ws_bytes, hipStream_t stream) {
     if (!x || !y || !dy || !mean || !inv_std || !gamma || !dgamma || !dbeta || !dx)
         return fail(TBN_ERR_NULL, "missing pointer");
     if (rows <= 0 || c <= 0) return fail(TBN_ERR_SHAPE, "sizes must be positive");
     if (!aligned16(x) || !aligned16(y) || !aligned16(dy) || !aligned16(dx)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    tbn_status st = check_bn_ws(rows, c, ws, ws_bytes);
+    if (st != TBN_OK) return st;
     hipError_t e = tbn::launch_bn_train_bwd(reinterpret_cast<const uint16_t*>(x), reinterpret_cast<const uint16_t*>(y),
                                             reinterpret_cast<const uint16_t*>(dy), rows, c, relu ? 1 : 0, mean, inv_std,
-                                            gamma, dgamma, dbeta, reinterpret_cast<uint16_t*>(dx), stream);
+                                            gamma, dgamma, dbeta, reinterpret_cast<uint16_t*>(dx),
+                                            reinterpret_cast<float*>(ws), stream);
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_batchnorm_train_bwd");
 }
 

@@ -86,91 +86,188 @@ __global__ __launch_bounds__(256) void avgpool_kernel(int32_t N, int32_t HW, int
 }
 
 // ---- batch normalisation, training form ----
-// Per-channel statistics over rows = N*H*W: a block of 256 threads owns 8 channels
-// (one 16-byte column strip), 32 row groups accumulate in fp32 and combine in LDS; the
-// result is written as (mean, inv_std).  Deterministic (fixed reduction order).
-__global__ __launch_bounds__(256) void bn_stats_kernel(const uint16_t* __restrict__ x, int64_t rows, int32_t C,
-                                                       float eps, float* __restrict__ mean,
-                                                       float* __restrict__ inv_std) {
-    __shared__ float s1[32][8], s2[32][8];
-    const int cl = threadIdx.x & 7, rg = threadIdx.x >> 3;
-    const int c = blockIdx.x * 8 + cl;
-    float a1 = 0.0f;
-    if (c < C)
-        for (int64_t r = rg; r < rows; r += 32) a1 += bf16_bits_to_f32(x[r * C + c]);
-    s1[rg][cl] = a1;
-    __syncthreads();
-    if (rg == 0) {
-        float t = 0.0f;
-        for (int g = 0; g < 32; ++g) t += s1[g][cl];
-        s1[0][cl] = t / (float)rows;
+// Per-channel sums over rows = N*H*W in two deterministic levels:
+//   * partial: block (b, slice) sums rows [b*rpc, (b+1)*rpc) for up to 256 channel groups
+//     (8 channels = one 16-byte load per row when C % 8 == 0, else 1); the 256 threads
+//     cover tpr = 256 / groups rows at a time, then combine their row lanes through LDS in
+//     a fixed order and write partial[b][c];
+//   * finalize: one thread per channel adds partial[0..chunks)[c] in order.
+// Modes: BN_SUM sums x; BN_SQDEV sums (x - mean)^2 (two-pass variance); BN_BWD sums
+// g and g * xhat, with g = dy masked by y > 0 when ReLU followed the normalisation.
+enum { BN_SUM = 0, BN_SQDEV = 1, BN_BWD = 2 };
+
+template <int MODE, bool VEC>
+__global__ __launch_bounds__(256) void bn_partial_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ y,
+                                                         const uint16_t* __restrict__ dy, int64_t rows, int32_t C,
+                                                         int64_t rpc, int relu, const float* __restrict__ mean,
+                                                         const float* __restrict__ inv_std, float* __restrict__ p1,
+                                                         float* __restrict__ p2) {
+    constexpr int NV = VEC ? 8 : 1;
+    __shared__ float s1[256 * NV], s2[MODE == BN_BWD ? 256 * NV : 1];
+    const int G = VEC ? C / 8 : C;
+    const int gbase = blockIdx.y * 256;
+    const int Gs = min(256, G - gbase);
+    const int tpr = 256 / Gs;
+    const int t = threadIdx.x;
+    const int g = t % Gs, r0 = t / Gs;
+    const bool active = r0 < tpr;
+    const int c0 = (gbase + g) * NV;
+    const int64_t rbeg = (int64_t)blockIdx.x * rpc;
+    const int64_t rend = min(rows, rbeg + rpc);
+    float a1[NV], a2[NV], m[NV], is[NV];
+#pragma unroll
+    for (int e = 0; e < NV; ++e) {
+        a1[e] = a2[e] = 0.0f;
+        m[e] = MODE != BN_SUM ? mean[c0 + e] : 0.0f;
+        is[e] = MODE == BN_BWD ? inv_std[c0 + e] : 0.0f;
+    }
+    if (active) {
+        for (int64_t r = rbeg + r0; r < rend; r += tpr) {
+            const int64_t i = r * C + c0;
+            float xv[NV], dv[NV], yv[NV];
+            if constexpr (VEC) {
+                const u32x4 xw = *reinterpret_cast<const u32x4*>(x + i);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    xv[2 * e] = bf16_bits_to_f32(xw[e] & 0xFFFFu);
+                    xv[2 * e + 1] = bf16_bits_to_f32(xw[e] >> 16);
+                }
+                if constexpr (MODE == BN_BWD) {
+                    const u32x4 dw = *reinterpret_cast<const u32x4*>(dy + i);
+                    const u32x4 yw = *reinterpret_cast<const u32x4*>(y + i);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        dv[2 * e] = bf16_bits_to_f32(dw[e] & 0xFFFFu);
+                        dv[2 * e + 1] = bf16_bits_to_f32(dw[e] >> 16);
+                        yv[2 * e] = bf16_bits_to_f32(yw[e] & 0xFFFFu);
+                        yv[2 * e + 1] = bf16_bits_to_f32(yw[e] >> 16);
+                    }
+                }
+            } else {
+                xv[0] = bf16_bits_to_f32(x[i]);
+                if constexpr (MODE == BN_BWD) {
+                    dv[0] = bf16_bits_to_f32(dy[i]);
+                    yv[0] = bf16_bits_to_f32(y[i]);
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < NV; ++e) {
+                if constexpr (MODE == BN_SUM) {
+                    a1[e] += xv[e];
+                } else if constexpr (MODE == BN_SQDEV) {
+                    const float d = xv[e] - m[e];
+                    a1[e] += d * d;
+                } else {
+                    const float gv = (relu && !(yv[e] > 0.0f)) ? 0.0f : dv[e];
+                    a1[e] += gv;
+                    a2[e] += gv * (xv[e] - m[e]) * is[e];
+                }
+            }
+        }
+    }
+    const int W = Gs * NV;  // channels of this slice
+    if (active) {
+#pragma unroll
+        for (int e = 0; e < NV; ++e) {
+            s1[r0 * W + g * NV + e] = a1[e];
+            if constexpr (MODE == BN_BWD) s2[r0 * W + g * NV + e] = a2[e];
+        }
     }
     __syncthreads();
-    const float m = s1[0][cl];
-    float a2 = 0.0f;
-    if (c < C)
-        for (int64_t r = rg; r < rows; r += 32) {
-            const float d = bf16_bits_to_f32(x[r * C + c]) - m;
-            a2 += d * d;
+    for (int c = t; c < W; c += 256) {
+        float u1 = 0.0f, u2 = 0.0f;
+        for (int rr = 0; rr < tpr; ++rr) {
+            u1 += s1[rr * W + c];
+            if constexpr (MODE == BN_BWD) u2 += s2[rr * W + c];
         }
-    s2[rg][cl] = a2;
-    __syncthreads();
-    if (rg == 0 && c < C) {
-        float t = 0.0f;
-        for (int g = 0; g < 32; ++g) t += s2[g][cl];
-        mean[c] = m;
-        inv_std[c] = 1.0f / sqrtf(t / (float)rows + eps);
+        const int64_t o = (int64_t)blockIdx.x * C + gbase * NV + c;
+        p1[o] = u1;
+        if constexpr (MODE == BN_BWD) p2[o] = u2;
     }
 }
 
-// y = act(gamma * (x - mean) * inv_std + beta)
+// 16 channels x 16 chunk lanes per block: lane j sums chunks j, j + 16, ... in order, then
+// the 16 lane sums are added in lane order.
+template <int MODE>
+__global__ __launch_bounds__(256) void bn_finalize_kernel(const float* __restrict__ p1, const float* __restrict__ p2,
+                                                          int64_t chunks, int32_t C, int64_t rows, float eps,
+                                                          float* __restrict__ out1, float* __restrict__ out2) {
+    __shared__ float s1[16][17], s2[16][17];
+    const int cl = threadIdx.x & 15, part = threadIdx.x >> 4;
+    const int c = blockIdx.x * 16 + cl;
+    float u1 = 0.0f, u2 = 0.0f;
+    if (c < C) {
+        int64_t b = part;
+        for (; b + 48 < chunks; b += 64) {  // four loads in flight, added in chunk order
+            const float v0 = p1[b * C + c], v1 = p1[(b + 16) * C + c];
+            const float v2 = p1[(b + 32) * C + c], v3 = p1[(b + 48) * C + c];
+            u1 += v0;
+            u1 += v1;
+            u1 += v2;
+            u1 += v3;
+            if constexpr (MODE == BN_BWD) {
+                const float w0 = p2[b * C + c], w1 = p2[(b + 16) * C + c];
+                const float w2 = p2[(b + 32) * C + c], w3 = p2[(b + 48) * C + c];
+                u2 += w0;
+                u2 += w1;
+                u2 += w2;
+                u2 += w3;
+            }
+        }
+        for (; b < chunks; b += 16) {
+            u1 += p1[b * C + c];
+            if constexpr (MODE == BN_BWD) u2 += p2[b * C + c];
+        }
+    }
+    s1[part][cl] = u1;
+    s2[part][cl] = u2;
+    __syncthreads();
+    if (part != 0 || c >= C) return;
+    float t1 = 0.0f, t2 = 0.0f;
+    for (int j = 0; j < 16; ++j) {
+        t1 += s1[j][cl];
+        t2 += s2[j][cl];
+    }
+    if constexpr (MODE == BN_SUM) {
+        out1[c] = t1 / (float)rows;  // mean
+    } else if constexpr (MODE == BN_SQDEV) {
+        out1[c] = 1.0f / sqrtf(t1 / (float)rows + eps);  // inv_std (biased variance)
+    } else {
+        out1[c] = t1;  // dbeta
+        out2[c] = t2;  // dgamma
+    }
+}
+
+// y = act(gamma * (x - mean) * inv_std + beta); VEC: 8 channels (16 bytes) per thread
+template <bool VEC>
 __global__ __launch_bounds__(256) void bn_apply_kernel(const uint16_t* __restrict__ x, int64_t total, int32_t C,
                                                        const float* __restrict__ mean, const float* __restrict__ inv_std,
                                                        const float* __restrict__ gamma, const float* __restrict__ beta,
                                                        int relu, uint16_t* __restrict__ y) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    constexpr int NV = VEC ? 8 : 1;
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * NV;
     if (i >= total) return;
-    const int c = (int)(i % C);
-    float v = gamma[c] * (bf16_bits_to_f32(x[i]) - mean[c]) * inv_std[c] + beta[c];
-    if (relu) v = fmaxf(v, 0.0f);
-    y[i] = (uint16_t)f32_to_bf16_bits(v);
-}
-
-// Backward: g = dy * [y > 0] (when relu), then per channel sums of g and g * xhat.
-__global__ __launch_bounds__(256) void bn_bwd_stats_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ y,
-                                                           const uint16_t* __restrict__ dy, int64_t rows, int32_t C,
-                                                           int relu, const float* __restrict__ mean,
-                                                           const float* __restrict__ inv_std, float* __restrict__ dgamma,
-                                                           float* __restrict__ dbeta) {
-    __shared__ float s1[32][8], s2[32][8];
-    const int cl = threadIdx.x & 7, rg = threadIdx.x >> 3;
-    const int c = blockIdx.x * 8 + cl;
-    float a1 = 0.0f, a2 = 0.0f;
-    if (c < C) {
-        const float m = mean[c], is = inv_std[c];
-        for (int64_t r = rg; r < rows; r += 32) {
-            const int64_t i = r * C + c;
-            float g = bf16_bits_to_f32(dy[i]);
-            if (relu && !(bf16_bits_to_f32(y[i]) > 0.0f)) g = 0.0f;
-            a1 += g;
-            a2 += g * (bf16_bits_to_f32(x[i]) - m) * is;
+    const int c0 = (int)(i % C);
+    if constexpr (VEC) {
+        const u32x4 xw = *reinterpret_cast<const u32x4*>(x + i);
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const uint32_t b = (e & 1) ? (xw[e / 2] >> 16) : (xw[e / 2] & 0xFFFFu);
+            v[e] = gamma[c0 + e] * (bf16_bits_to_f32(b) - mean[c0 + e]) * inv_std[c0 + e] + beta[c0 + e];
+            if (relu) v[e] = fmaxf(v[e], 0.0f);
         }
-    }
-    s1[rg][cl] = a1;
-    s2[rg][cl] = a2;
-    __syncthreads();
-    if (rg == 0 && c < C) {
-        float t1 = 0.0f, t2 = 0.0f;
-        for (int g = 0; g < 32; ++g) {
-            t1 += s1[g][cl];
-            t2 += s2[g][cl];
-        }
-        dbeta[c] = t1;
-        dgamma[c] = t2;
+        *reinterpret_cast<u32x4*>(y + i) = u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                                  pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+    } else {
+        float v = gamma[c0] * (bf16_bits_to_f32(x[i]) - mean[c0]) * inv_std[c0] + beta[c0];
+        if (relu) v = fmaxf(v, 0.0f);
+        y[i] = (uint16_t)f32_to_bf16_bits(v);
     }
 }
 
 // dx = gamma * inv_std * (g - dbeta / rows - xhat * dgamma / rows)
+template <bool VEC>
 __global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ y,
                                                            const uint16_t* __restrict__ dy, int64_t total, int64_t rows,
                                                            int32_t C, int relu, const float* __restrict__ mean,
@@ -178,15 +275,43 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const uint16_t* __res
                                                            const float* __restrict__ gamma,
                                                            const float* __restrict__ dgamma,
                                                            const float* __restrict__ dbeta, uint16_t* __restrict__ dx) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    constexpr int NV = VEC ? 8 : 1;
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * NV;
     if (i >= total) return;
-    const int c = (int)(i % C);
-    float g = bf16_bits_to_f32(dy[i]);
-    if (relu && !(bf16_bits_to_f32(y[i]) > 0.0f)) g = 0.0f;
-    const float xh = (bf16_bits_to_f32(x[i]) - mean[c]) * inv_std[c];
+    const int c0 = (int)(i % C);
     const float inv_rows = 1.0f / (float)rows;
-    const float v = gamma[c] * inv_std[c] * (g - dbeta[c] * inv_rows - xh * dgamma[c] * inv_rows);
-    dx[i] = (uint16_t)f32_to_bf16_bits(v);
+    uint32_t xb[NV], yb[NV], db[NV];
+    if constexpr (VEC) {
+        const u32x4 xw = *reinterpret_cast<const u32x4*>(x + i);
+        const u32x4 yw = *reinterpret_cast<const u32x4*>(y + i);
+        const u32x4 dw = *reinterpret_cast<const u32x4*>(dy + i);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int sh = (e & 1) * 16;
+            xb[e] = (xw[e / 2] >> sh) & 0xFFFFu;
+            yb[e] = (yw[e / 2] >> sh) & 0xFFFFu;
+            db[e] = (dw[e / 2] >> sh) & 0xFFFFu;
+        }
+    } else {
+        xb[0] = x[i];
+        yb[0] = y[i];
+        db[0] = dy[i];
+    }
+    float v[NV];
+#pragma unroll
+    for (int e = 0; e < NV; ++e) {
+        const int c = c0 + e;
+        float g = bf16_bits_to_f32(db[e]);
+        if (relu && !(bf16_bits_to_f32(yb[e]) > 0.0f)) g = 0.0f;
+        const float xh = (bf16_bits_to_f32(xb[e]) - mean[c]) * inv_std[c];
+        v[e] = gamma[c] * inv_std[c] * (g - dbeta[c] * inv_rows - xh * dgamma[c] * inv_rows);
+    }
+    if constexpr (VEC) {
+        *reinterpret_cast<u32x4*>(dx + i) = u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                                   pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+    } else {
+        dx[i] = (uint16_t)f32_to_bf16_bits(v[0]);
+    }
 }
 
 // gradient of ReLU applied after the fact: g = dy * [y > 0]
@@ -249,21 +374,75 @@ hipError_t launch_avgpool(int32_t N, int32_t HW, int32_t C, const uint16_t* x, v
     return hipGetLastError();
 }
 
+BnPlan plan_bn(int64_t rows, int32_t C) {
+    BnPlan p;
+    p.vec = C % 8 == 0;
+    const int G = p.vec ? C / 8 : C;
+    const int gs = G < 256 ? G : 256;
+    const int tpr = 256 / gs;
+    int64_t rpc = (rows + 511) / 512;             // about 512 row chunks
+    if (rpc < 8 * (int64_t)tpr) rpc = 8 * (int64_t)tpr;  // at least 8 rows per thread
+    p.rpc = rpc;
+    p.chunks = (rows + rpc - 1) / rpc;
+    p.slices = (G + 255) / 256;
+    p.ws_bytes = (size_t)2 * p.chunks * C * 4;
+    return p;
+}
+
+namespace {
+
+template <int MODE>
+void bn_partial(const BnPlan& p, const uint16_t* x, const uint16_t* y, const uint16_t* dy, int64_t rows, int32_t C,
+                int relu, const float* mean, const float* inv_std, float* p1, float* p2, hipStream_t s) {
+    const dim3 grid((unsigned)p.chunks, (unsigned)p.slices);
+    if (p.vec)
+        hipLaunchKernelGGL((bn_partial_kernel<MODE, true>), grid, dim3(256), 0, s, x, y, dy, rows, C, p.rpc, relu, mean,
+                           inv_std, p1, p2);
+    else
+        hipLaunchKernelGGL((bn_partial_kernel<MODE, false>), grid, dim3(256), 0, s, x, y, dy, rows, C, p.rpc, relu,
+                           mean, inv_std, p1, p2);
+}
+
+}  // namespace
+
 hipError_t launch_bn_train_fwd(const uint16_t* x, int64_t rows, int32_t C, const float* gamma, const float* beta,
-                               float eps, int relu, uint16_t* y, float* mean, float* inv_std, hipStream_t s) {
-    hipLaunchKernelGGL(bn_stats_kernel, dim3((unsigned)((C + 7) / 8)), dim3(256), 0, s, x, rows, C, eps, mean, inv_std);
-    hipLaunchKernelGGL(bn_apply_kernel, dim3(blocks_for(rows * C)), dim3(256), 0, s, x, rows * C, C, mean, inv_std,
-                       gamma, beta, relu, y);
+                               float eps, int relu, uint16_t* y, float* mean, float* inv_std, float* ws,
+                               hipStream_t s) {
+    const BnPlan p = plan_bn(rows, C);
+    float* p1 = ws;
+    const unsigned cb = (unsigned)((C + 15) / 16);
+    bn_partial<BN_SUM>(p, x, nullptr, nullptr, rows, C, 0, nullptr, nullptr, p1, nullptr, s);
+    hipLaunchKernelGGL(bn_finalize_kernel<BN_SUM>, dim3(cb), dim3(256), 0, s, p1, nullptr, p.chunks, C, rows, eps,
+                       mean, nullptr);
+    bn_partial<BN_SQDEV>(p, x, nullptr, nullptr, rows, C, 0, mean, nullptr, p1, nullptr, s);
+    hipLaunchKernelGGL(bn_finalize_kernel<BN_SQDEV>, dim3(cb), dim3(256), 0, s, p1, nullptr, p.chunks, C, rows, eps,
+                       inv_std, nullptr);
+    const int64_t total = rows * C;
+    if (p.vec)
+        hipLaunchKernelGGL(bn_apply_kernel<true>, dim3(blocks_for(total / 8)), dim3(256), 0, s, x, total, C, mean,
+                           inv_std, gamma, beta, relu, y);
+    else
+        hipLaunchKernelGGL(bn_apply_kernel<false>, dim3(blocks_for(total)), dim3(256), 0, s, x, total, C, mean, inv_std,
+                           gamma, beta, relu, y);
     return hipGetLastError();
 }
 
 hipError_t launch_bn_train_bwd(const uint16_t* x, const uint16_t* y, const uint16_t* dy, int64_t rows, int32_t C,
                                int relu, const float* mean, const float* inv_std, const float* gamma, float* dgamma,
-                               float* dbeta, uint16_t* dx, hipStream_t s) {
-    hipLaunchKernelGGL(bn_bwd_stats_kernel, dim3((unsigned)((C + 7) / 8)), dim3(256), 0, s, x, y, dy, rows, C, relu,
-                       mean, inv_std, dgamma, dbeta);
-    hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(blocks_for(rows * C)), dim3(256), 0, s, x, y, dy, rows * C, rows, C,
-                       relu, mean, inv_std, gamma, dgamma, dbeta, dx);
+                               float* dbeta, uint16_t* dx, float* ws, hipStream_t s) {
+    const BnPlan p = plan_bn(rows, C);
+    float* p1 = ws;
+    float* p2 = ws + p.chunks * C;
+    bn_partial<BN_BWD>(p, x, y, dy, rows, C, relu, mean, inv_std, p1, p2, s);
+    hipLaunchKernelGGL(bn_finalize_kernel<BN_BWD>, dim3((unsigned)((C + 15) / 16)), dim3(256), 0, s, p1, p2,
+                       p.chunks, C, rows, 0.0f, dbeta, dgamma);
+    const int64_t total = rows * C;
+    if (p.vec)
+        hipLaunchKernelGGL(bn_bwd_apply_kernel<true>, dim3(blocks_for(total / 8)), dim3(256), 0, s, x, y, dy, total, rows,
+                           C, relu, mean, inv_std, gamma, dgamma, dbeta, dx);
+    else
+        hipLaunchKernelGGL(bn_bwd_apply_kernel<false>, dim3(blocks_for(total)), dim3(256), 0, s, x, y, dy, total, rows,
+                           C, relu, mean, inv_std, gamma, dgamma, dbeta, dx);
     return hipGetLastError();
 }
 

@@ -135,11 +135,20 @@ hipError_t launch_maxpool_fwd(const PoolArgs& a, const uint16_t* x, uint16_t* y,
 hipError_t launch_maxpool_bwd(const PoolArgs& a, const uint16_t* dy, const int32_t* arg, void* dx, int dx_f32,
                               hipStream_t s);
 hipError_t launch_avgpool(int32_t N, int32_t HW, int32_t C, const uint16_t* x, void* y, int y_f32, hipStream_t s);
+// Batch normalisation statistics: per-chunk partial sums in workspace, then per channel.
+struct BnPlan {
+    int64_t rpc, chunks;  // rows per chunk, chunks
+    int32_t slices;       // groups of 256 channel groups
+    int32_t vec;          // C % 8 == 0: 8 channels per 16-byte access
+    size_t ws_bytes;      // two fp32 partial arrays [chunks][C]
+};
+BnPlan plan_bn(int64_t rows, int32_t C);
 hipError_t launch_bn_train_fwd(const uint16_t* x, int64_t rows, int32_t C, const float* gamma, const float* beta,
-                               float eps, int relu, uint16_t* y, float* mean, float* inv_std, hipStream_t s);
+                               float eps, int relu, uint16_t* y, float* mean, float* inv_std, float* ws,
+                               hipStream_t s);
 hipError_t launch_bn_train_bwd(const uint16_t* x, const uint16_t* y, const uint16_t* dy, int64_t rows, int32_t C,
                                int relu, const float* mean, const float* inv_std, const float* gamma, float* dgamma,
-                               float* dbeta, uint16_t* dx, hipStream_t s);
+                               float* dbeta, uint16_t* dx, float* ws, hipStream_t s);
 hipError_t launch_relu_bwd(const uint16_t* y, const uint16_t* dy, int64_t total, uint16_t* dx, hipStream_t s);
 hipError_t launch_softmax_xent(const float* z, const int32_t* labels, int32_t N, int32_t K, float* loss,
                                float* loss_per_sample, uint16_t* dz, hipStream_t s);

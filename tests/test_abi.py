@@ -107,3 +107,14 @@ def test_forward_workspace_checked():
     assert lib.tbn_conv2d_fwd(*args, good, need - 1, None) == 5
     assert lib.tbn_last_error().decode() == "workspace too small"
     assert lib.tbn_conv2d_fwd(*args, ctypes.c_void_p(0x100004), need, None) == 4
+
+
+def test_batchnorm_workspace_checked():
+    lib = tbn.load()
+    good = ctypes.c_void_p(0x100000)
+    need = tbn.batchnorm_workspace_size(131072, 128)
+    assert need > 0 and need % (128 * 4) == 0
+    args = (good, 131072, 128, good, good, ctypes.c_float(1e-5), 1, good, good, good)
+    assert lib.tbn_batchnorm_train_fwd(*args, None, 0, None) == 5
+    assert lib.tbn_batchnorm_train_fwd(*args, good, need - 4, None) == 5
+    assert lib.tbn_last_error().decode() == "workspace too small"
