@@ -354,7 +354,7 @@ tbn_status tbn_maxpool2d_fwd(const tbn_pool_desc* desc, const void* x, void* y, 
     tbn_status st = check_pool(desc, &a);
     if (st != TBN_OK) return st;
     if (!x || !y) return fail(TBN_ERR_NULL, "x and y are required");
-    if (!aligned16(x) || !aligned16(y) || (argmax && !aligned4(argmax))) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    if (!aligned16(x) || !aligned16(y) || (argmax && !aligned16(argmax))) return fail(TBN_ERR_ALIGN, "misaligned pointer");
     hipError_t e = tbn::launch_maxpool_fwd(a, reinterpret_cast<const uint16_t*>(x), reinterpret_cast<uint16_t*>(y),
                                            argmax, stream);
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_maxpool2d_fwd");
@@ -367,7 +367,7 @@ tbn_status tbn_maxpool2d_bwd(const tbn_pool_desc* desc, const void* dy, const in
     if (st != TBN_OK) return st;
     if (!dy || !argmax || !dx) return fail(TBN_ERR_NULL, "dy, argmax and dx are required");
     if (dxt != TBN_BF16 && dxt != TBN_F32) return fail(TBN_ERR_UNSUPPORTED, "unknown dtype");
-    if (!aligned16(dy) || !aligned16(dx) || !aligned4(argmax)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    if (!aligned16(dy) || !aligned16(dx) || !aligned16(argmax)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
     hipError_t e = tbn::launch_maxpool_bwd(a, reinterpret_cast<const uint16_t*>(dy), argmax, dx, dxt == TBN_F32, stream);
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_maxpool2d_bwd");
 }

@@ -21,40 +21,72 @@ __device__ __forceinline__ void st_act(void* p, int64_t i, float v, int f32) {
         reinterpret_cast<uint16_t*>(p)[i] = (uint16_t)f32_to_bf16_bits(v);
 }
 
+// NV channels per thread (8 = one 16-byte access when C % 8 == 0).  bf16 values compare
+// as their fp32 widening; ties keep the first window position in row-major order.
+template <int NV>
 __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const PoolArgs a, const uint16_t* __restrict__ x,
                                                           uint16_t* __restrict__ y, int32_t* __restrict__ arg) {
     const int64_t total = (int64_t)a.N * a.P * a.Q * a.C;
-    const int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t o = ((int64_t)blockIdx.x * 256 + threadIdx.x) * NV;
     if (o >= total) return;
     const int c = (int)(o % a.C);
     const int64_t pix = o / a.C;
     const int q = (int)(pix % a.Q), p = (int)((pix / a.Q) % a.P);
     const int64_t n = pix / ((int64_t)a.P * a.Q);
-    float best = 0.0f;
-    int bi = -1;
+    float best[NV];
+    int bi[NV];
+#pragma unroll
+    for (int e = 0; e < NV; ++e) {
+        best[e] = 0.0f;
+        bi[e] = -1;
+    }
     for (int r = 0; r < a.k; ++r) {
         const int h = p * a.s - a.pad + r;
         if ((unsigned)h >= (unsigned)a.H) continue;
         for (int t = 0; t < a.k; ++t) {
             const int w = q * a.s - a.pad + t;
             if ((unsigned)w >= (unsigned)a.W) continue;
-            const float v = bf16_bits_to_f32(x[((n * a.H + h) * a.W + w) * a.C + c]);
-            if (bi < 0 || v > best) {
-                best = v;
-                bi = h * a.W + w;
+            const int64_t xi = ((n * a.H + h) * a.W + w) * a.C + c;
+            uint32_t b[NV];
+            if constexpr (NV == 8) {
+                const u32x4 v = *reinterpret_cast<const u32x4*>(x + xi);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) b[e] = (e & 1) ? (v[e / 2] >> 16) : (v[e / 2] & 0xFFFFu);
+            } else {
+                b[0] = x[xi];
+            }
+#pragma unroll
+            for (int e = 0; e < NV; ++e) {
+                const float v = bf16_bits_to_f32(b[e]);
+                if (bi[e] < 0 || v > best[e]) {
+                    best[e] = v;
+                    bi[e] = h * a.W + w;
+                }
             }
         }
     }
-    y[o] = (uint16_t)f32_to_bf16_bits(best);  // exact: the maximum is a bf16 value
-    if (arg) arg[o] = bi;
+    // exact: each maximum is a bf16 value
+    if constexpr (NV == 8) {
+        *reinterpret_cast<u32x4*>(y + o) = u32x4{pack_bf16x2(best[0], best[1]), pack_bf16x2(best[2], best[3]),
+                                                  pack_bf16x2(best[4], best[5]), pack_bf16x2(best[6], best[7])};
+        if (arg) {
+            *reinterpret_cast<u32x4*>(arg + o) = u32x4{(uint32_t)bi[0], (uint32_t)bi[1], (uint32_t)bi[2], (uint32_t)bi[3]};
+            *reinterpret_cast<u32x4*>(arg + o + 4) =
+                u32x4{(uint32_t)bi[4], (uint32_t)bi[5], (uint32_t)bi[6], (uint32_t)bi[7]};
+        }
+    } else {
+        y[o] = (uint16_t)f32_to_bf16_bits(best[0]);
+        if (arg) arg[o] = bi[0];
+    }
 }
 
-// dx[n,h,w,c] = sum of dy over the windows that chose (h, w)
+// dx[n,h,w,c] = sum of dy over the windows that chose (h, w); NV channels per thread
+template <int NV>
 __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const PoolArgs a, const uint16_t* __restrict__ dy,
                                                           const int32_t* __restrict__ arg, void* __restrict__ dx,
                                                           int dx_f32) {
     const int64_t total = (int64_t)a.N * a.H * a.W * a.C;
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * NV;
     if (i >= total) return;
     const int c = (int)(i % a.C);
     const int64_t pix = i / a.C;
@@ -64,13 +96,39 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const PoolArgs a, cons
     // windows p with p*s - pad <= h <= p*s - pad + k - 1
     const int p_lo = max(0, (h + a.pad - a.k + a.s) / a.s), p_hi = min(a.P - 1, (h + a.pad) / a.s);
     const int q_lo = max(0, (w + a.pad - a.k + a.s) / a.s), q_hi = min(a.Q - 1, (w + a.pad) / a.s);
-    float acc = 0.0f;
+    float acc[NV];
+#pragma unroll
+    for (int e = 0; e < NV; ++e) acc[e] = 0.0f;
     for (int p = p_lo; p <= p_hi; ++p)
         for (int q = q_lo; q <= q_hi; ++q) {
             const int64_t o = ((n * a.P + p) * a.Q + q) * a.C + c;
-            if (arg[o] == me) acc += bf16_bits_to_f32(dy[o]);
+            if constexpr (NV == 8) {
+                const u32x4 a0 = *reinterpret_cast<const u32x4*>(arg + o);
+                const u32x4 a1 = *reinterpret_cast<const u32x4*>(arg + o + 4);
+                const u32x4 d = *reinterpret_cast<const u32x4*>(dy + o);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t ae = e < 4 ? a0[e] : a1[e - 4];
+                    const uint32_t db = (e & 1) ? (d[e / 2] >> 16) : (d[e / 2] & 0xFFFFu);
+                    if ((int)ae == me) acc[e] += bf16_bits_to_f32(db);
+                }
+            } else {
+                if (arg[o] == me) acc[0] += bf16_bits_to_f32(dy[o]);
+            }
         }
-    st_act(dx, i, acc, dx_f32);
+    if constexpr (NV == 8) {
+        if (dx_f32) {
+            float* dp = reinterpret_cast<float*>(dx) + i;
+            *reinterpret_cast<f32x4*>(dp) = f32x4{acc[0], acc[1], acc[2], acc[3]};
+            *reinterpret_cast<f32x4*>(dp + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
+        } else {
+            *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(dx) + i) =
+                u32x4{pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]), pack_bf16x2(acc[4], acc[5]),
+                      pack_bf16x2(acc[6], acc[7])};
+        }
+    } else {
+        st_act(dx, i, acc[0], dx_f32);
+    }
 }
 
 // y[n][c] = mean over h, w of x[n][h][w][c]; one thread per (n, c)
@@ -357,15 +415,21 @@ unsigned blocks_for(int64_t total) { return (unsigned)((total + 255) / 256); }
 }  // namespace
 
 hipError_t launch_maxpool_fwd(const PoolArgs& a, const uint16_t* x, uint16_t* y, int32_t* arg, hipStream_t s) {
-    hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(blocks_for((int64_t)a.N * a.P * a.Q * a.C)), dim3(256), 0, s, a, x, y,
-                       arg);
+    const int64_t total = (int64_t)a.N * a.P * a.Q * a.C;
+    if (a.C % 8 == 0)
+        hipLaunchKernelGGL(maxpool_fwd_kernel<8>, dim3(blocks_for(total / 8)), dim3(256), 0, s, a, x, y, arg);
+    else
+        hipLaunchKernelGGL(maxpool_fwd_kernel<1>, dim3(blocks_for(total)), dim3(256), 0, s, a, x, y, arg);
     return hipGetLastError();
 }
 
 hipError_t launch_maxpool_bwd(const PoolArgs& a, const uint16_t* dy, const int32_t* arg, void* dx, int dx_f32,
                               hipStream_t s) {
-    hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(blocks_for((int64_t)a.N * a.H * a.W * a.C)), dim3(256), 0, s, a, dy,
-                       arg, dx, dx_f32);
+    const int64_t total = (int64_t)a.N * a.H * a.W * a.C;
+    if (a.C % 8 == 0)
+        hipLaunchKernelGGL(maxpool_bwd_kernel<8>, dim3(blocks_for(total / 8)), dim3(256), 0, s, a, dy, arg, dx, dx_f32);
+    else
+        hipLaunchKernelGGL(maxpool_bwd_kernel<1>, dim3(blocks_for(total)), dim3(256), 0, s, a, dy, arg, dx, dx_f32);
     return hipGetLastError();
 }
 

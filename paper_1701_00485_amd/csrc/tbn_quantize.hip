@@ -1,14 +1,15 @@
 // tbn_quantize.hip -- per-filter discretisation (Sec. 2, Eq. 3) and optimal scale
 // (Sec. 2, Eq. 4-5) as a wavefront reduction, writing the TBN2 packed codes directly.
 //
-// One wave per filter.  The wave walks the filter in chunks of 64 elements; lane l
-// reads element 64c + l (one coalesced 256-byte row segment per chunk), takes the two
+// A block per filter; each of its waves walks chunks of 64 elements; lane l reads element
+// 64c + l (one coalesced 256-byte row segment per chunk), takes the two
 // predicates of Eq. (3) -- magnitude (|W| > 1) and sign (!(W > 0), which puts both zeros
 // and -1 <= W <= 0 on the negative side) -- and the wave turns them into two 64-bit
 // ballots.  Lanes 0..3 then assemble the four packed words of the chunk from the
 // ballots (even elements to bytes 0/1, odd elements to bytes 2/3) and store them as one
-// 16-byte segment.  The B1/B2 sums of Eq. (4)-(5) accumulate per lane in fp64 and are
-// reduced across the wave at the end; |B2| is the popcount of the magnitude ballots.
+// 16-byte segment.  The B1/B2 sums of Eq. (4)-(5) accumulate per lane in fp64, are
+// reduced across each wave and then over the waves in order; |B2| is the popcount of the
+// magnitude ballots.
 #include "tbn_device.h"
 #include "tbn_kernels.h"
 
@@ -29,57 +30,83 @@ __device__ __forceinline__ double wave_sum(double v) {
     return v;
 }
 
+// One block of four waves per filter: wave v takes the chunks c = v, v + 4, ... (four at a
+// time, loads issued together), and the per-wave fp64 sums and counts are combined in wave
+// order through LDS.
 __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__ w, int64_t K,
                                                        int64_t n, uint32_t* __restrict__ codes,
                                                        float* __restrict__ alpha,
                                                        int32_t* __restrict__ counts) {
+    __shared__ double sh1[4], sh2[4];
+    __shared__ int64_t shn[4];
     const int lane = threadIdx.x & 63;
-    const int64_t k = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // filter of this wave
+    const int wave = threadIdx.x >> 6;
+    const int64_t k = blockIdx.x;  // filter of this block
     const int64_t nb = (n + 63) / 64;
-    const int64_t kpad = (K + 63) / 64 * 64;
-    if (k >= kpad) return;
     uint32_t* out = codes + ((k / 64) * nb * 64 + (k % 64)) * 4;  // + chunk*256 per chunk
     if (k >= K) {  // padding filter of the last 64-filter block: all bits zero
-        for (int64_t c = lane; c < nb * 4; c += 64) out[(c / 4) * 256 + (c % 4)] = 0u;
+        for (int64_t c = threadIdx.x; c < nb * 4; c += 256) out[(c / 4) * 256 + (c % 4)] = 0u;
         return;
     }
     const float* wk = w + k * n;
     double s1 = 0.0, s2 = 0.0;
     int64_t n2 = 0;
-    for (int64_t c = 0; c < nb; ++c) {
-        const int64_t i = c * 64 + lane;
-        bool mag = false, neg = false;
-        if (i < n) {
+    for (int64_t c0 = wave; c0 < nb; c0 += 16) {
+        uint32_t u[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {  // branch-free loads: out-of-range lanes read w[k][0]
+            const int64_t i = (c0 + 4 * j) * 64 + lane;
+            u[j] = __float_as_uint(wk[i < n ? i : 0]);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t c = c0 + 4 * j;
+            if (c >= nb) break;
+            const bool in = c * 64 + lane < n;
             // The predicates of Eq. (3) on the bit pattern, so that they are exact in any
             // denormal mode: |W| > 1, and W > 0 (false for both zeros and for NaN).
-            const uint32_t u = __float_as_uint(wk[i]);
-            const uint32_t abits = u & 0x7FFFFFFFu;
+            const uint32_t abits = u[j] & 0x7FFFFFFFu;
             const bool nan = abits > 0x7F800000u;
-            mag = !nan && abits > 0x3F800000u;
-            neg = !(!nan && !(u >> 31) && abits != 0u);
-            const double a = (double)__uint_as_float(abits);
-            if (mag) s2 += a; else s1 += a;  // a NaN weight makes alpha NaN
-        }
-        const uint64_t M = __ballot(mag);
-        const uint64_t S = __ballot(neg);
-        n2 += __popcll(M);
-        if (lane < 4) {
-            const uint32_t m16 = (uint32_t)(M >> (16 * lane)) & 0xFFFFu;
-            const uint32_t s16 = (uint32_t)(S >> (16 * lane)) & 0xFFFFu;
-            const uint32_t word = even_bits16(m16) | (even_bits16(s16) << 8) |
-                                  (even_bits16(m16 >> 1) << 16) | (even_bits16(s16 >> 1) << 24);
-            out[c * 256 + lane] = word;
+            const bool mag = in && !nan && abits > 0x3F800000u;
+            const bool neg = in && !(!nan && !(u[j] >> 31) && abits != 0u);
+            if (in) {
+                const double a = (double)__uint_as_float(abits);
+                if (mag) s2 += a; else s1 += a;  // a NaN weight makes alpha NaN
+            }
+            const uint64_t M = __ballot(mag);
+            const uint64_t S = __ballot(neg);
+            n2 += __popcll(M);
+            if (lane < 4) {
+                const uint32_t m16 = (uint32_t)(M >> (16 * lane)) & 0xFFFFu;
+                const uint32_t s16 = (uint32_t)(S >> (16 * lane)) & 0xFFFFu;
+                const uint32_t word = even_bits16(m16) | (even_bits16(s16) << 8) |
+                                      (even_bits16(m16 >> 1) << 16) | (even_bits16(s16 >> 1) << 24);
+                out[c * 256 + lane] = word;
+            }
         }
     }
     s1 = wave_sum(s1);
     s2 = wave_sum(s2);
     if (lane == 0) {
-        const int64_t n1 = n - n2;
-        const double a = (s1 + 2.0 * s2) / (double)(n1 + 4 * n2);
+        sh1[wave] = s1;
+        sh2[wave] = s2;
+        shn[wave] = n2;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double t1 = 0.0, t2 = 0.0;
+        int64_t tn2 = 0;
+        for (int v = 0; v < 4; ++v) {
+            t1 += sh1[v];
+            t2 += sh2[v];
+            tn2 += shn[v];
+        }
+        const int64_t n1 = n - tn2;
+        const double a = (t1 + 2.0 * t2) / (double)(n1 + 4 * tn2);
         alpha[k] = (float)a;
         if (counts) {
             counts[2 * k] = (int32_t)n1;
-            counts[2 * k + 1] = (int32_t)n2;
+            counts[2 * k + 1] = (int32_t)tn2;
         }
     }
 }
@@ -87,8 +114,7 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
 hipError_t launch_quantize(const float* w, int64_t K, int64_t n, uint32_t* codes, float* alpha,
                            int32_t* counts, hipStream_t stream) {
     const int64_t kpad = (K + 63) / 64 * 64;
-    const dim3 grid((unsigned)((kpad + 3) / 4));
-    hipLaunchKernelGGL(quantize_kernel, grid, dim3(256), 0, stream, w, K, n, codes, alpha, counts);
+    hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)kpad), dim3(256), 0, stream, w, K, n, codes, alpha, counts);
     return hipGetLastError();
 }
 
