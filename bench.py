@@ -61,7 +61,7 @@ def layer_flops():
 KERNEL_OF_OP = {
     "fwd": ("conv_dma_kernel<128, 256, 1, 4, 3, false, true>", ["tbn_conv_dma.hip", "tbn_dma.h", "tbn_device.h"]),
     "bwd_data": ("conv_dma_kernel<128, 256, 1, 4, 3, true, true>", ["tbn_conv_dma.hip", "tbn_dma.h", "tbn_device.h"]),
-    "bwd_weight": ("wgrad_dma_kernel", ["tbn_wgrad_dma.hip", "tbn_dma.h", "tbn_device.h"]),
+    "bwd_weight": ("wgrad_rows_kernel", ["tbn_wgrad_dma.hip", "tbn_dma.h", "tbn_device.h"]),
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv3x3_256x256_56x56_b128_train_step_traffic.json")
 

@@ -67,9 +67,10 @@ tbn::WgradArgs wgrad_args(const Geometry& g) {
 int wgrad_splits(const Geometry& g) {
     const int64_t J = g.R * g.S * g.C;
     const bool dma = tbn::wgrad_dma_eligible(wgrad_args(g));
-    const int64_t tiles = dma ? tbn::wgrad_dma_tiles((int)g.K, (int)J) : ((g.K + 127) / 128) * ((J + 127) / 128);
+    const tbn::WgradDmaPlan plan = tbn::wgrad_dma_plan((int)g.K, (int)J);
+    const int64_t tiles = dma ? plan.tiles : ((g.K + 127) / 128) * ((J + 127) / 128);
     const int64_t chunks = (g.N * g.P * g.Q + 63) / 64;
-    const int64_t target = dma ? 256 : 1024;
+    const int64_t target = dma ? plan.resident_blocks : 1024;
     int64_t splits = target / tiles;
     const int64_t max_by_len = chunks / 16 > 0 ? chunks / 16 : 1;  // >= 16 chunks per split
     if (splits > max_by_len) splits = max_by_len;

@@ -26,11 +26,12 @@ __device__ __forceinline__ v4i make_rsrc(const void* base, uint32_t bytes) {
 }
 
 // One LDS-DMA: lane i's 16 (or 4) bytes at byte `voff` of the buffer land at LDS
-// address lds + 16*i (4*i).  An offset beyond the buffer yields zeros.
+// address lds + 16*i (4*i).  An offset beyond the buffer yields zeros.  `lds` must be the
+// same in every active lane (it is read from the first one into M0).
 __device__ __forceinline__ void dma_b128(v4i rsrc, uint32_t lds, uint32_t voff) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                  :
-                 : "s"(lds), "v"(voff), "s"(rsrc)
+                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(rsrc)
                  : "memory");
 }
 __device__ __forceinline__ void dma_b32(v4i rsrc, uint32_t lds, uint32_t voff) {

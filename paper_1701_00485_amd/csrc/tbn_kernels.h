@@ -108,7 +108,13 @@ hipError_t launch_wgrad(const WgradArgs& a, hipStream_t stream);
 // LDS-DMA + transposing-read variant (C % 8 == 0, K % 8 == 0, tensors < 2 GiB),
 // 256 x 256 output tiles of 512 threads; launch_wgrad uses it when eligible.
 bool wgrad_dma_eligible(const WgradArgs& a);
-int wgrad_dma_tiles(int K, int J);
+// Stage layout of the LDS-DMA weight-gradient kernel (1 = pixel-major rows for K >= 128,
+// 0 = segment-major; TBN_WGRAD_CFG forces one for tests), its output tiles and how many
+// blocks are resident at once.
+struct WgradDmaPlan {
+    int cfg, tiles, resident_blocks;
+};
+WgradDmaPlan wgrad_dma_plan(int K, int J);
 hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream);
 
 hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, float* dw,

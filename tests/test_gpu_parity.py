@@ -276,6 +276,21 @@ def test_bwd_weight_parity(tbn, g, accumulate):
     assert e <= 1e-4
 
 
+@pytest.mark.parametrize("cfg", [0, 1])
+def test_bwd_weight_tile_shapes(tbn, cfg, monkeypatch):
+    # every tile / stage geometry of the transposing-read weight-gradient kernel
+    monkeypatch.setenv("TBN_WGRAD_CFG", str(cfg))
+    for g in [(2, 14, 14, 256, 256, 3, 3, 1, 1), (3, 12, 12, 128, 136, 3, 3, 2, 1), (5, 9, 7, 64, 96, 3, 3, 1, 1),
+              (2, 16, 16, 64, 128, 1, 1, 2, 0)]:
+        d, P, Q, xb, dyb, _ = _conv_inputs(g, 5)
+        ref = oracle.conv_bwd_weight(d, oracle.bf16_bits_to_f64(xb), oracle.bf16_bits_to_f64(dyb))
+        dw = tbn.conv2d_bwd_weight(tbn.ConvDesc(*g), bf16_dev(xb), bf16_dev(dyb))
+        torch.cuda.synchronize()
+        e = nerr(dw.cpu().numpy(), ref)
+        log("bwd_weight cfg %d %s: %.3e" % (cfg, g, e))
+        assert e <= 1e-4
+
+
 def test_sgd_parity(tbn):
     n = 1_000_003
     w = synth.normal(6, "w", (n,), 0.05)
