@@ -257,6 +257,45 @@ def small_configs(dev, steps=20, warmup=3):
     return out
 
 
+def weight_streaming(dev, sets=8, reps=20):
+    """Batch-1 fully-connected layer 8192 -> 32768 (67 MB of packed codes) cycled over 8
+    filter sets (537 MB, more than the 256 MB last-level cache), so every call streams its
+    codes from HBM: achieved GB/s of the algorithmic bytes (codes, scales, input, output)."""
+    import torch
+
+    import paper_1701_00485_amd as tbn
+
+    C, K = 8192, 32768
+    d = tbn.ConvDesc(1, 1, 1, C, K, 1, 1, 1, 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(1701_00485)
+    filters = []
+    for _ in range(sets):
+        w = torch.randn(K, C, device=dev, generator=g) * 0.05  # real filters N(0, 0.05^2)
+        codes, alpha, _ = tbn.quantize(w, want_counts=False)
+        del w
+        filters.append((codes, alpha))
+    x = (torch.randn(1, 1, 1, C, device=dev, generator=g)).to(torch.bfloat16)
+    y = torch.empty(1, 1, 1, K, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        for c, a in filters:
+            tbn.conv2d_fwd(d, x, c, a, y=y, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        for c, a in filters:
+            tbn.conv2d_fwd(d, x, c, a, y=y, out_dtype=torch.float32)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / (reps * sets) * 1e3
+    byts = filters[0][0].numel() * 4 + K * 4 + C * 2 + K * 4
+    gbs = byts / (us * 1e-6) / 1e9
+    return {"shape": "batch 1, 8192 -> 32768, 8 filter sets (537 MB of codes)", "us_per_call": round(us, 2),
+            "bytes_per_call": byts, "achieved_GBs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -373,6 +412,7 @@ def main():
         result["resnet18_fwd"] = resnet18_fwd(dev)
     if not args.no_small:
         result["small_workloads"] = small_configs(dev)
+        result["weight_streaming"] = weight_streaming(dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(result), flush=True)

@@ -377,13 +377,24 @@ int conv_splits_override() {
     return e ? atoi(e) : -1;
 }
 
-static bool use_dma(const ConvGemmArgs& a, int cfg) {
-    return conv_dma_eligible(a) && (cfg < 0 || (cfg >= 10 && cfg < 20));
+// Which kernel runs a forward / backward-data GEMM: the weight-streaming kernel for a
+// fully-connected layer of at most 16 rows, the LDS-DMA implicit GEMM for C % 8 == 0, the
+// thin-input kernel for few channels, else the general one.  cfg (TBN_CONV_TILE) forces a
+// family: 0-1 general, 10-16 LDS-DMA tile shapes, 20 thin, 30 weight streaming.
+enum ConvPath { PATH_FC, PATH_DMA, PATH_THIN, PATH_GENERIC };
+
+static ConvPath choose_path(const ConvGemmArgs& a, int cfg, FcStreamPlan* fp, ThinGeom* tg) {
+    if ((cfg < 0 || cfg == 30) && fc_stream_plan(a, fp)) return PATH_FC;
+    if (conv_dma_eligible(a) && (cfg < 0 || (cfg >= 10 && cfg < 20))) return PATH_DMA;
+    if ((cfg < 0 || cfg == 20) && conv_thin_plan(a, tg)) return PATH_THIN;
+    return PATH_GENERIC;
 }
 
 size_t conv_gemm_partial_bytes(const ConvGemmArgs& a) {
     const int cfg = conv_tile_override();
-    return use_dma(a, cfg) ? plan_conv_dma(a, cfg).partial_bytes : 0;
+    FcStreamPlan fp;
+    ThinGeom tg;
+    return choose_path(a, cfg, &fp, &tg) == PATH_DMA ? plan_conv_dma(a, cfg).partial_bytes : 0;
 }
 
 hipError_t launch_conv_gemm(const ConvGemmArgs& args, hipStream_t stream) {
@@ -393,9 +404,14 @@ hipError_t launch_conv_gemm(const ConvGemmArgs& args, hipStream_t stream) {
     a.splits = 1;
     a.chunks_per_split = 1 << 30;
     const int cfg = conv_tile_override();
-    if (use_dma(a, cfg)) return launch_conv_dma(a, plan_conv_dma(a, cfg), stream);
+    FcStreamPlan fp;
     ThinGeom tg;
-    if ((cfg < 0 || cfg == 20) && conv_thin_plan(a, &tg)) return launch_conv_thin(a, tg, stream);
+    switch (choose_path(a, cfg, &fp, &tg)) {
+        case PATH_FC: return launch_fc_stream(a, fp, stream);
+        case PATH_DMA: return launch_conv_dma(a, plan_conv_dma(a, cfg), stream);
+        case PATH_THIN: return launch_conv_thin(a, tg, stream);
+        default: break;
+    }
     const bool vec = (a.C % 8 == 0) && !a.x_f32;
     if (a.apair) return vec ? launch_mode<A_VEC8, true>(a, cfg, stream) : launch_mode<A_SCALAR, true>(a, cfg, stream);
     return vec ? launch_mode<A_VEC8, false>(a, cfg, stream) : launch_mode<A_SCALAR, false>(a, cfg, stream);

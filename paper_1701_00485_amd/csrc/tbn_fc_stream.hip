@@ -1,0 +1,197 @@
+// tbn_fc_stream.hip -- forward pass of a two-bit fully-connected layer (Sec. 2 Eq. 1 with
+// the whole input as one filter window) for a small batch (N <= 16): the weight-streaming
+// regime, where the packed codes (0.25 byte per weight) are the only large operand and HBM
+// bandwidth, not arithmetic, sets the speed.
+//
+//   * a block of 4 waves owns the 64 filters of one 1 KiB-per-64-elements code block row;
+//     wave w takes filters 16 w .. 16 w + 15 as the 16 rows of v_mfma_f32_16x16x32_bf16,
+//     the batch is its 16 columns (columns >= N unused);
+//   * lane (f = lane % 16, g = lane / 16) loads, per step, the four code words of filter f
+//     in element block ib + g (16 bytes; the 64 lanes read four 256-byte runs);
+//   * the reduction order is permuted so that each lane feeds the MFMA only from its own
+//     words: MFMA s (s = 0..7) of a step takes, from lane group g, elements 8 s .. 8 s + 7
+//     of block ib + g, and the activation operand reads the same elements from LDS;
+//   * codes are decoded in registers to exact bf16 +-0.5/+-1 (half the code: the pair
+//     comes from one shift and one and-or, against three ops for +-1/+-2), and 2 alpha
+//     scales the fp32 sum (exact); the loads of the next steps are issued before the
+//     MFMAs of the current ones, and four accumulators keep four MFMA chains in flight;
+//   * the activations of the batch (N x n bf16) sit in LDS, zero-padded to whole steps,
+//     plus one zero row that the unused batch columns read (no branch per read; those
+//     output columns are never stored);
+//   * alpha, the optional scale / bias / residual / ReLU are applied to the fp32 sums.
+#include "tbn_device.h"
+#include "tbn_kernels.h"
+
+namespace tbn {
+
+namespace {
+
+constexpr int kU = 4;  // code loads (16 bytes per lane) in flight per wave and buffer
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4_t mfma16(bf16x8 a, bf16x8 b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// (t << SH) | base in one v_lshl_or_b32 (the compiler splits it into two VOP2 ops to keep
+// its literal operands; with base in an SGPR the VOP3 form needs none).
+template <int SH>
+__device__ __forceinline__ uint32_t lshl_or(uint32_t t, uint32_t base) {
+    uint32_t r;
+    asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(t), "n"(SH), "s"(base));
+    return r;
+}
+
+// Elements 8 h .. 8 h + 7 of a packed word as bf16 code / 2: pair j moves the magnitude
+// bits (bit j of bytes 0 and 2) to bit 7 of each half and the sign bits (bytes 1 and 3)
+// to bit 15, over 0.5 = 0x3F00 (bit 7 clear, so the magnitude bit makes 1.0 by an or):
+// one and and one shift-or per pair.
+template <int H>
+__device__ __forceinline__ bf16x8 decode8_half(uint32_t w, uint32_t base) {
+    u32x4 r;
+    r[0] = lshl_or<7 - 4 * H>(w & (0x01010101u << (4 * H)), base);
+    r[1] = lshl_or<6 - 4 * H>(w & (0x01010101u << (4 * H + 1)), base);
+    r[2] = lshl_or<5 - 4 * H>(w & (0x01010101u << (4 * H + 2)), base);
+    r[3] = lshl_or<4 - 4 * H>(w & (0x01010101u << (4 * H + 3)), base);
+    return as_bf16x8(r);
+}
+
+__global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, int32_t n, int32_t nsteps,
+                                                        int32_t xpitch) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t xl[];  // [N + 1][xpitch] bf16
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int N = a.N;
+    const int K = a.Kf;
+    const int NB = (n + 63) / 64;  // element blocks of a filter row
+
+
+    const int f = lane & 15, g = lane >> 4;
+    const int kb = blockIdx.x;              // 64-filter block
+    const int fr = 16 * wave + f;           // filter row inside the block
+    const u32x4* codes = reinterpret_cast<const u32x4*>(a.codes) + ((int64_t)kb * NB * 64 + fr);
+    // activation operand: batch column f of lane group g (the zero row for columns >= N)
+    const uint16_t* xrow = xl + (f < N ? f : N) * xpitch;
+
+    // four accumulators in rotation keep four independent MFMA chains in flight
+    f32x4_t acc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    u32x4 wa[kU], wb[kU];
+    auto load = [&](u32x4 (&w)[kU], int step0) {
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            int ib = 4 * (step0 + u) + g;
+            ib = ib < NB ? ib : NB - 1;  // in bounds; its activations are zero past n
+            w[u] = codes[(int64_t)ib * 64];
+        }
+    };
+    const uint32_t half_one = __builtin_amdgcn_readfirstlane(0x3F003F00u);  // bf16 (0.5, 0.5)
+    auto compute = [&](const u32x4 (&w)[kU], int step0) {
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const uint16_t* xb = xrow + (4 * (step0 + u) + g) * 64;
+            bf16x8 bx[8];  // the step's activation operands, read before its MFMAs
+#pragma unroll
+            for (int s = 0; s < 8; ++s) bx[s] = *reinterpret_cast<const bf16x8*>(xb + 8 * s);
+#pragma unroll
+            for (int s = 0; s < 8; s += 2) {
+                acc[s & 3] = mfma16(decode8_half<0>(w[u][s >> 1], half_one), bx[s], acc[s & 3]);
+                acc[(s + 1) & 3] = mfma16(decode8_half<1>(w[u][s >> 1], half_one), bx[s + 1], acc[(s + 1) & 3]);
+            }
+        }
+    };
+    // nsteps is a multiple of 2 kU (the host pads the activations in LDS to match); the
+    // first code loads are in flight while the activations are staged
+    load(wa, 0);
+    load(wb, kU);
+    // ---- the batch's activations into LDS (zero beyond n, and the zero row) ----
+    if (!a.x_f32 && n % 8 == 0) {
+        // 16-byte pieces, the loads of a thread issued together
+        const int pieces = (N + 1) * xpitch / 8;
+        const int ppr = xpitch / 8;  // pieces per row
+        for (int i0 = tid; i0 < pieces; i0 += 256 * 8) {
+            u32x4 v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int i = i0 + 256 * u;
+                const int r = i / ppr, e = (i - r * ppr) * 8;
+                const bool ok = i < pieces && r < N && e < n;
+                v[u] = ok ? *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.x) + (int64_t)r * n + e)
+                          : u32x4{0u, 0u, 0u, 0u};
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (i0 + 256 * u < pieces) reinterpret_cast<u32x4*>(xl)[i0 + 256 * u] = v[u];
+        }
+    } else {
+        for (int i = tid; i < (N + 1) * xpitch; i += 256) {
+            const int r = i / xpitch, e = i - (i / xpitch) * xpitch;
+            uint16_t v = 0;
+            if (e < n && r < N)
+                v = a.x_f32 ? (uint16_t)f32_to_bf16_bits(reinterpret_cast<const float*>(a.x)[(int64_t)r * n + e])
+                            : reinterpret_cast<const uint16_t*>(a.x)[(int64_t)r * n + e];
+            xl[i] = v;
+        }
+    }
+    __syncthreads();
+    for (int st = 0; st < nsteps; st += 2 * kU) {
+        compute(wa, st);
+        if (st + 2 * kU < nsteps) load(wa, st + 2 * kU);
+        compute(wb, st + kU);
+        if (st + 3 * kU < nsteps) load(wb, st + 3 * kU);
+    }
+
+    // ---- epilogue: lane holds batch column f, filters 4 g .. 4 g + 3 of the wave's 16 ----
+    if (f >= N) return;
+    const int k0 = kb * 64 + 16 * wave + 4 * g;
+    const f32x4_t t = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    float v4[4] = {t.x, t.y, t.z, t.w};
+    const int64_t o = (int64_t)f * K + k0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int k = k0 + e;
+        if (k >= K) break;
+        float sc = 2.0f * (a.colscale ? a.colscale[k] : 1.0f);  // the codes were decoded halved
+        if (a.scale) sc *= a.scale[k];
+        float v = v4[e] * sc + (a.bias ? a.bias[k] : 0.0f);
+        if (a.residual)
+            v += a.y_f32 ? reinterpret_cast<const float*>(a.residual)[o + e]
+                         : bf16_bits_to_f32(reinterpret_cast<const uint16_t*>(a.residual)[o + e]);
+        if (a.relu) v = fmaxf(v, 0.0f);
+        if (a.y_f32)
+            reinterpret_cast<float*>(a.y)[o + e] = v;
+        else
+            reinterpret_cast<uint16_t*>(a.y)[o + e] = (uint16_t)f32_to_bf16_bits(v);
+    }
+}
+
+}  // namespace
+
+bool fc_stream_plan(const ConvGemmArgs& a, FcStreamPlan* p) {
+    // a fully-connected layer: the filter window covers the whole (unpadded) input map
+    if (a.apair || a.N > 16 || a.P != 1 || a.Q != 1 || a.R != a.H || a.S != a.W || a.ph != 0 || a.pw != 0)
+        return false;
+    const int64_t n = (int64_t)a.R * a.S * a.C;
+    const int64_t nb = (n + 63) / 64;
+    const int64_t per = 4 * 2 * kU;  // element blocks consumed per loop iteration
+    const int64_t steps_blocks = (nb + per - 1) / per * per;
+    const int64_t xpitch = steps_blocks * 64;
+    const int64_t lds = (int64_t)(a.N + 1) * xpitch * 2;  // + the zero row
+    if (lds > 64 * 1024 || n > (1 << 24)) return false;
+    p->n = (int32_t)n;
+    p->nsteps = (int32_t)(steps_blocks / 4);
+    p->xpitch = (int32_t)xpitch;
+    p->lds_bytes = (int32_t)lds;
+    return true;
+}
+
+hipError_t launch_fc_stream(const ConvGemmArgs& a, const FcStreamPlan& p, hipStream_t stream) {
+    const dim3 grid((unsigned)((a.Kf + 63) / 64));
+    hipLaunchKernelGGL(fc_stream_kernel, grid, dim3(256), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch);
+    return hipGetLastError();
+}
+
+}  // namespace tbn

@@ -86,6 +86,14 @@ struct ThinGeom {
 bool conv_thin_plan(const ConvGemmArgs& a, ThinGeom* g);
 hipError_t launch_conv_thin(const ConvGemmArgs& a, const ThinGeom& g, hipStream_t stream);
 
+// Forward pass of a fully-connected layer (the filter window covers the whole input map)
+// for a batch of at most 16: codes streamed from HBM into 16x16x32 MFMAs.
+struct FcStreamPlan {
+    int32_t n, nsteps, xpitch, lds_bytes;
+};
+bool fc_stream_plan(const ConvGemmArgs& a, FcStreamPlan* p);
+hipError_t launch_fc_stream(const ConvGemmArgs& a, const FcStreamPlan& p, hipStream_t stream);
+
 // Re-pack the codes of K filters [K][R][S][C] into the codes of the C filters of the
 // transposed, spatially flipped layer [C][R][S][K] (backward-data operand), and build
 // the bf16 scale pairs of that layer's element pairs.

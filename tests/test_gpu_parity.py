@@ -243,6 +243,61 @@ def test_fwd_dense_parity(tbn, g):
     assert nerr(y.float().cpu().numpy(), ref) <= TOL
 
 
+FC_CASES = [
+    # n, h, w, c, k, r, s, stride, pad: the filter window covers the whole input map
+    (1, 1, 1, 8192, 4096, 1, 1, 1, 0),      # weight streaming at batch 1
+    (3, 1, 1, 100, 70, 1, 1, 1, 0),         # ragged reduction and filter count
+    (16, 1, 1, 512, 1000, 1, 1, 1, 0),      # the ResNet classifier at the widest batch
+    (2, 4, 4, 512, 10, 4, 4, 1, 0),         # the CIFAR classifier, 4x4 map
+    (1, 7, 7, 64, 512, 7, 7, 1, 0),         # the MNIST fc1, 7x7 map
+]
+
+
+@pytest.mark.parametrize("g", FC_CASES)
+def test_fc_stream_parity(tbn, g):
+    # fully-connected layers at small batch (codes streamed into 16x16x32 MFMAs), with the
+    # fused epilogue and with fp32 input
+    log("fc %s" % (g,))
+    d, P, Q, xb, _, wr = _conv_inputs(g, 10)
+    k = g[4]
+    q = oracle.quantize(wr)
+    a64 = q.alpha.astype(np.float64)
+    acc = oracle.conv_fwd(d, oracle.bf16_bits_to_f64(xb), q.codes, a64)
+    codes, alpha, _ = tbn.quantize(to_dev(wr))
+    desc = tbn.ConvDesc(*g)
+    y32 = tbn.conv2d_fwd(desc, bf16_dev(xb), codes, alpha, out_dtype=torch.float32)
+    scale = synth.uniform(10, "sc", (k,), 0.5, 1.5)
+    bias = synth.normal(10, "bi", (k,), 0.1)
+    resb = synth.normal_bf16(10, "res", (g[0], 1, 1, k))
+    y = tbn.conv2d_fwd(desc, bf16_dev(xb), codes, alpha, scale=to_dev(scale), bias=to_dev(bias),
+                       residual=bf16_dev(resb), relu=True)
+    xf = oracle.bf16_bits_to_f64(xb).astype(np.float32)
+    yf = tbn.conv2d_fwd(desc, to_dev(xf), codes, alpha, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert nerr(y32.cpu().numpy(), acc) <= 1e-4
+    assert nerr(yf.cpu().numpy(), acc) <= 1e-4
+    ref = np.maximum(acc * scale.astype(np.float64) + bias + oracle.bf16_bits_to_f64(resb), 0.0)
+    assert nerr(y.float().cpu().numpy(), ref) <= TOL
+
+
+def test_fc_stream_weight_streaming_size(tbn):
+    # 8192 -> 16384 at batch 1 (32 MiB of codes): sampled outputs against the oracle
+    g = (1, 1, 1, 8192, 16384, 1, 1, 1, 0)
+    d = oracle.ConvDesc(*g)
+    xb = synth.normal_bf16(10, "wsx", (1, 1, 1, 8192))
+    wr = synth.normal(10, "wsw", (16384, 8192), 1.0)
+    codes, alpha, _ = tbn.quantize(to_dev(wr))
+    y = tbn.conv2d_fwd(tbn.ConvDesc(*g), bf16_dev(xb), codes, alpha, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    idx = synth.sample_indices(10, "wsidx", 16384, 512)
+    q = oracle.quantize(wr[idx])  # quantisation is per filter: the sampled filters alone
+    sub = oracle.ConvDesc(1, 1, 1, 8192, len(idx), 1, 1, 1, 0)
+    ref = oracle.conv_fwd(sub, oracle.bf16_bits_to_f64(xb), q.codes, q.alpha.astype(np.float64))
+    e = nerr(y.cpu().numpy().reshape(-1)[idx], ref.reshape(-1))
+    log("weight streaming 8192x16384, 512 sampled filters: %.3e" % e)
+    assert e <= 1e-4
+
+
 BWD_CASES = [c for c in CONV_CASES if c[7] == 1] + [(2, 8, 8, 64, 64, 3, 3, 1, 0), (2, 6, 6, 64, 64, 5, 5, 1, 4)]
 
 
@@ -361,10 +416,11 @@ def test_reduction_splits(tbn, splits, monkeypatch):
 
 
 TILE_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1), (2, 10, 10, 40, 24, 3, 3, 1, 1),
-              (3, 12, 12, 128, 130, 3, 3, 2, 1), (2, 19, 17, 3, 40, 7, 7, 2, 3)]
+              (3, 12, 12, 128, 130, 3, 3, 2, 1), (2, 19, 17, 3, 40, 7, 7, 2, 3), (4, 1, 1, 512, 72, 1, 1, 1, 0),
+              (3, 5, 5, 64, 80, 5, 5, 1, 0)]
 
 
-@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 14, 16, 20])
+@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 14, 16, 20, 30])
 def test_every_tile_shape(tbn, tile, monkeypatch):
     # each tile shape of the convolution kernels against the oracle (fwd and bwd_data)
     monkeypatch.setenv("TBN_CONV_TILE", str(tile))
