@@ -223,18 +223,19 @@ __global__ __launch_bounds__(512, 1) void wgrad_seg_kernel(const WgradDmaArgs ka
 // DMA instruction copies one pixel's 512 contiguous bytes (lanes 0..31, 16 bytes each),
 // so every request covers whole 128-byte lines; the per-pixel address arithmetic is
 // wave-uniform and each lane's channel / tap offset is fixed for the whole kernel.
-constexpr int PIXR = 64;
 constexpr int PPITCH = 576;
-constexpr int PR_OP = PIXR * PPITCH;       // one operand tile of a stage
-constexpr int PR_STAGE = 2 * PR_OP;
 
+// PIXR pixels per stage, STAGES-deep ring.
+template <int PIXR, int STAGES>
 __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs ka) {
     const WgradArgs& a = ka.a;
     constexpr int WNW = 4;          // waves along j (2 x 4 waves)
     constexpr int TM = 4, TN = 2;   // wave tile 128 x 64 of the 256 x 256 block tile
     constexpr int PPW = PIXR / 8;   // pixels each wave copies per stage
+    constexpr int PR_OP = PIXR * PPITCH;  // one operand tile of a stage
+    constexpr int PR_STAGE = 2 * PR_OP;
 
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * PR_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * PR_STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -253,8 +254,9 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
     const int split = t_ / tiles;
     const int k0 = ((t_ % tiles) / tilesJ) * 256;
     const int j0 = ((t_ % tiles) % tilesJ) * 256;
-    const int64_t c_begin = (int64_t)split * a.chunks_per_split;  // 64-pixel chunks
-    const int64_t c_end = min(c_begin + (int64_t)a.chunks_per_split, nchunks);
+    // the split ranges are given in 64-pixel chunks
+    const int64_t c_begin = (int64_t)split * a.chunks_per_split * (64 / PIXR);
+    const int64_t c_end = min(c_begin + (int64_t)a.chunks_per_split * (64 / PIXR), nchunks);
 
     const v4i rs_dy = make_rsrc(a.dy, (uint32_t)(M * K * 2));
     const v4i rs_x = make_rsrc(a.x, (uint32_t)((int64_t)a.N * a.H * a.W * C * 2));
@@ -272,7 +274,7 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
     const int64_t HWC = (int64_t)a.H * a.W * C;
 
     auto issue = [&](int64_t chunk) {
-        const uint32_t st = smem_base + (uint32_t)((chunk & 1) * PR_STAGE);
+        const uint32_t st = smem_base + (uint32_t)((chunk % STAGES) * PR_STAGE);
         if (lane < 32) {
 #pragma unroll
             for (int pp = 0; pp < PPW; ++pp) {
@@ -317,12 +319,16 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][t][v] = 0.0f;
 
-    if (c_begin < c_end) issue(c_begin);
+#pragma unroll
+    for (int c = 0; c < STAGES - 1; ++c)
+        if (c_begin + c < c_end) issue(c_begin + c);
     for (int64_t chunk = c_begin; chunk < c_end; ++chunk) {
-        wait_vmcnt(0);    // this wave's DMAs of stage `chunk` landed
-        __syncthreads();  // ... and every other wave's; all reads of the other buffer are done
-        if (chunk + 1 < c_end) issue(chunk + 1);
-        const uint32_t st = smem_base + (uint32_t)((chunk & 1) * PR_STAGE);
+        // this wave's DMAs of stage `chunk` landed (later stages may still be in flight)
+        const int later = (int)min(c_end - 1 - chunk, (int64_t)(STAGES - 2));
+        wait_vmcnt(later * kDmas);
+        __syncthreads();  // ... and every other wave's; all reads of stage chunk-1 are done
+        if (chunk + STAGES - 1 < c_end) issue(chunk + STAGES - 1);  // into stage chunk-1's buffer
+        const uint32_t st = smem_base + (uint32_t)((chunk % STAGES) * PR_STAGE);
         bf16x8 af[2][TM], bf[2][TN];
         auto load = [&](int u, int b) {
 #pragma unroll
@@ -340,7 +346,6 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
                 for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(af[u & 1][i], bf[u & 1][t], acc[i][t]);
         }
     }
-    (void)kDmas;
 
     float* out = a.out + (int64_t)split * K * J;
     const int l32 = lane & 31, half = lane >> 5;
@@ -389,7 +394,7 @@ hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream) {
     const WgradDmaPlan p = wgrad_dma_plan(a.K, a.R * a.S * a.C);
     const dim3 grid((unsigned)(p.tiles * a.splits));
     if (p.cfg == 1)
-        hipLaunchKernelGGL(wgrad_rows_kernel, grid, dim3(512), 0, stream, ka);
+        hipLaunchKernelGGL((wgrad_rows_kernel<64, 2>), grid, dim3(512), 0, stream, ka);
     else
         hipLaunchKernelGGL(wgrad_seg_kernel, grid, dim3(512), 0, stream, ka);
     return hipGetLastError();

@@ -118,3 +118,28 @@ def test_batchnorm_workspace_checked():
     assert lib.tbn_batchnorm_train_fwd(*args, None, 0, None) == 5
     assert lib.tbn_batchnorm_train_fwd(*args, good, need - 4, None) == 5
     assert lib.tbn_last_error().decode() == "workspace too small"
+
+
+@pytest.mark.parametrize("g,why", [
+    ((1 << 16, 200, 200, 8, 8, 1, 1, 1, 0), "more than 2^31 - 1 pixels"),
+    ((1, 8, 8, 1 << 26, 8, 5, 5, 1, 2), "filter has more than 2^30 elements"),
+])
+def test_index_range_limits(g, why):
+    # sizes whose pixel or filter indices would overflow the kernels' 32-bit arithmetic are
+    # rejected before any launch (pointers are never dereferenced)
+    lib = tbn.load()
+    good = ctypes.c_void_p(0x100000)
+    d = tbn.ConvDesc(*g)
+    assert lib.tbn_conv2d_fwd(ctypes.byref(d), good, 0, good, good, None, good, 0, good, 1 << 40, None) == 2
+    assert lib.tbn_last_error().decode() == why
+    assert lib.tbn_conv2d_bwd_weight(ctypes.byref(d), good, good, good, 0, good, 1 << 40, None) == 2
+
+
+def test_unknown_dtype_and_pool_geometry():
+    lib = tbn.load()
+    good = ctypes.c_void_p(0x100000)
+    d = tbn.ConvDesc(1, 8, 8, 8, 8, 3, 3, 1, 1)
+    assert lib.tbn_conv2d_fwd(ctypes.byref(d), good, 7, good, good, None, good, 0, None, 0, None) == 3
+    pd = tbn.PoolDesc(1, 2, 2, 8, 3, 1, 0)  # window larger than the input
+    p, q = ctypes.c_int32(), ctypes.c_int32()
+    assert lib.tbn_pool_out_dims(ctypes.byref(pd), ctypes.byref(p), ctypes.byref(q)) == 2

@@ -147,6 +147,8 @@ CONV_CASES = [
     (2, 11, 13, 7, 72, 3, 3, 1, 1),         # 7 channels (padded to 8), two filter blocks
     (1, 19, 23, 4, 64, 5, 5, 2, 2),         # 4 channels, stride 2
     (2, 9, 9, 2, 16, 3, 3, 1, 0),           # 2 channels, no padding
+    (1, 1, 1, 16, 8, 3, 3, 1, 1),           # 1x1 image under a 3x3 window: only the centre tap
+    (2, 5, 5, 8, 1, 3, 3, 1, 1),            # a single filter
 ]
 
 
