@@ -187,16 +187,28 @@ def resnet18_fwd(dev, steps=10, warmup=3):
         if kind != "conv" or layer.k != 3 or layer.stride != 1 or layer.cin < 128:
             continue
         relu = True
-        for _ in range(2):
-            layer(inp, relu=relu, residual=res)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        # the calls are captured as a HIP graph and replayed, so the time is the device's
+        # (a layer of ~15 GFLOP is shorter than the host's per-call work)
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            for _ in range(2):
+                layer(inp, relu=relu, residual=res)
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=side):
+                for _ in range(steps):
+                    layer(inp, relu=relu, residual=res)
         torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
-        for _ in range(steps):
-            layer(inp, relu=relu, residual=res)
+        graph.replay()
         e1.record(stream)
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / steps * 1e3
+        del graph
         n, h, w, c = inp.shape
         fl = 2.0 * n * h * w * layer.cout * 9 * c
         layers.append({"layer": layer.name, "us": round(us, 1), "tflops": round(fl / (us * 1e-6) / 1e12, 1)})
