@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup-seconds", type=float, default=0.3,
+                    help="keep running untimed steps until at least this much time has passed "
+                         "(the GPU clocks rise over the first tens of milliseconds of load)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-resnet", action="store_true", help="skip the ResNet-18 forward figures")
     ap.add_argument("--no-small", action="store_true", help="skip the single-layer, LeNet and VGG figures")
@@ -363,9 +366,13 @@ def main():
         tbn.sgd_step(w, v, dw, LR, MOMENTUM, WD)
         mark(5)
 
-    for _ in range(args.warmup):
+    # untimed: at least W steps and at least --warmup-seconds of steady load
+    warm_run = 0
+    t_warm = time.perf_counter()
+    while warm_run < args.warmup or time.perf_counter() - t_warm < args.warmup_seconds:
         step()
-    torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        warm_run += 1
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -396,6 +403,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_steps_run": warm_run,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True,
         "scaling": "weak",

@@ -380,7 +380,7 @@ int conv_splits_override() {
 // Which kernel runs a forward / backward-data GEMM: the weight-streaming kernel for a
 // fully-connected layer of at most 16 rows, the LDS-DMA implicit GEMM for C % 8 == 0, the
 // thin-input kernel for few channels, else the general one.  cfg (TBN_CONV_TILE) forces a
-// family: 0-1 general, 10-16 LDS-DMA tile shapes, 20 thin, 30 weight streaming.
+// family: 0-1 general, 10-18 LDS-DMA tile shapes, 20 thin, 30 weight streaming.
 enum ConvPath { PATH_FC, PATH_DMA, PATH_THIN, PATH_GENERIC };
 
 static ConvPath choose_path(const ConvGemmArgs& a, int cfg, FcStreamPlan* fp, ThinGeom* tg) {

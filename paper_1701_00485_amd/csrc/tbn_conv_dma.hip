@@ -495,6 +495,7 @@ hipError_t launch_dma_mode(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
         case 12: return launch_dma_cfg<128, 128, 2, 2, 3, BWD>(a, stream);
         case 14: return launch_dma_cfg<128, 64, 2, 2, 3, BWD>(a, stream);
         case 16: return launch_dma_cfg<256, 128, 1, 4, 2, BWD>(a, stream);
+        case 18: return launch_dma_cfg<64, 128, 1, 4, 4, BWD>(a, stream);
         default: return launch_dma_cfg<128, 256, 1, 4, 3, BWD>(a, stream);
     }
 }
@@ -503,6 +504,7 @@ void cfg_tile(int cfg, int* bm, int* bn) {
     switch (cfg) {
         case 11: case 12: *bm = 128; *bn = 128; return;
         case 14: *bm = 128; *bn = 64; return;
+        case 18: *bm = 64; *bn = 128; return;
         case 16: *bm = 256; *bn = 128; return;
         default: *bm = 128; *bn = 256; return;
     }
@@ -526,8 +528,10 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
     if (p.cfg < 10) {
         p.cfg = a.Kf > 128 ? 10 : (a.Kf > 64 ? 12 : 14);
         cfg_tile(p.cfg, &bm, &bn);
-        // too few tiles for one wave of blocks: narrower tiles, then split the reduction
-        if (((M + bm - 1) / bm) * ((a.Kf + bn - 1) / bn) < 384) p.cfg = 14;
+        // too few tiles for one wave of blocks: shorter tiles (64 pixels x 128 filters, a
+        // four-deep ring) when there are at least 128 filters, else 128 x 64; then split
+        // the reduction
+        if (((M + bm - 1) / bm) * ((a.Kf + bn - 1) / bn) < 384) p.cfg = a.Kf >= 128 ? 18 : 14;
     }
     cfg_tile(p.cfg, &bm, &bn);
     const int64_t tiles = ((M + bm - 1) / bm) * ((a.Kf + bn - 1) / bn);
@@ -537,8 +541,12 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
         if (forced > 0) {
             splits = forced;
         } else if (tiles < 384) {
-            splits = (640 + tiles - 1) / tiles;
-            const int64_t max_splits = nchunks / 3 > 0 ? nchunks / 3 : 1;  // >= 3 stages per split
+            // measured: about 384 blocks of the 64 x 128 tile with >= 6 stages each, or
+            // 640 blocks of the 128 x 64 tile with >= 3 stages each
+            const bool shortt = p.cfg == 18;
+            const int64_t target = shortt ? 384 : 640, min_stages = shortt ? 6 : 3;
+            splits = (target + tiles - 1) / tiles;
+            const int64_t max_splits = nchunks / min_stages > 0 ? nchunks / min_stages : 1;
             if (splits > max_splits) splits = max_splits;
         }
         if (splits > nchunks) splits = nchunks;

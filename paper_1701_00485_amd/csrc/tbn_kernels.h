@@ -121,6 +121,7 @@ bool wgrad_dma_eligible(const WgradArgs& a);
 // blocks are resident at once.
 struct WgradDmaPlan {
     int cfg, tiles, resident_blocks;
+    int pix;  // pixel-major kernel: pixels per stage (32, 48 or 64)
 };
 WgradDmaPlan wgrad_dma_plan(int K, int J);
 hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream);

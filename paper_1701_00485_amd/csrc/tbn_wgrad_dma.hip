@@ -11,17 +11,19 @@
 // loop spends no vector ALU work on data movement:
 //   * a block of 8 waves owns a 256 (k) x 256 (j) output tile; each wave 128 x 64 made of
 //     32x32 v_mfma_f32_32x32x16_bf16 tiles with fp32 accumulators;
-//   * a stage is 64 pixels, two stages in LDS: the DMAs of stage c+1 overlap the MFMAs of
-//     stage c, and the operands of each 16-pixel step are read during the previous one;
+//   * stages of pixels in a ring of LDS buffers: the DMAs of later stages overlap the
+//     MFMAs of the current one, and the operands of each 16-pixel step are read during the
+//     previous one;
 //   * the pixel range is split over the grid (split-K): each split writes fp32 partials
 //     that a second kernel adds in a fixed order (deterministic result).
 // Two stage layouts:
 //   * pixel-major (wide layers): each pixel's 256 dy channels / 256 x columns form one
-//     row of the stage, padded to 576 bytes; one DMA instruction copies one pixel's 512
-//     contiguous bytes, so the requests cover whole cache lines;
-//   * segment-major (K < 128): for every 8-channel segment the 64 pixels' 16-byte pieces
-//     are contiguous (one DMA instruction, lane = pixel), segments 1088 bytes apart; with
-//     few valid dy channels this issues fewer copies.
+//     512-byte row of the stage, two pixels per 1088-byte slot, so that one 64-lane DMA
+//     instruction copies two pixels' contiguous bytes and the requests cover whole cache
+//     lines; 48-pixel stages, three deep, with an L2 prefetch of a later stage;
+//   * segment-major (K < 128): 64-pixel stages, two deep; for every 8-channel segment the
+//     64 pixels' 16-byte pieces are contiguous (one DMA instruction, lane = pixel),
+//     segments 1088 bytes apart; with few valid dy channels this issues fewer copies.
 #include <cstdlib>
 
 #include "tbn_device.h"
@@ -49,6 +51,7 @@ struct WgStage {
 struct WgradDmaArgs {
     WgradArgs a;
     FastDiv div_q, div_pq;
+    int32_t pf_dist;  // pixel-major kernel: stages between a copy and the L2 prefetch issued with it
 };
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -218,24 +221,35 @@ __global__ __launch_bounds__(512, 1) void wgrad_seg_kernel(const WgradDmaArgs ka
 }
 
 // Pixel-major variant: a stage holds PIXR pixels of the dy tile (256 channels, 512 bytes)
-// then the same pixels of the x tile (256 columns), each pixel row padded to 576 bytes
-// (with that pitch the transposing reads below use every LDS bank exactly twice).  One
-// DMA instruction copies one pixel's 512 contiguous bytes (lanes 0..31, 16 bytes each),
-// so every request covers whole 128-byte lines; the per-pixel address arithmetic is
-// wave-uniform and each lane's channel / tap offset is fixed for the whole kernel.
-constexpr int PPITCH = 576;
+// then the same pixels of the x tile (256 columns).  Pixel rows are stored in pairs:
+// pixels i and i + PIXR/2 of the stage share a 1088-byte slot (512 + 512 + 64 bytes of
+// padding), so one DMA instruction with all 64 lanes active copies two pixels (each lane
+// 16 bytes; the vector memory pipe issues a 32-lane copy at the cost of a full one) and
+// every request covers whole 128-byte lines.  A transposing read touches four
+// consecutive stage pixels and the four 8 further on (then the next four of each); in
+// consecutive slots those rows start 64 bytes apart modulo 256, so every LDS bank is used
+// at most twice.  The order in which the pixels enter the reduction follows this layout
+// (a permutation within the stage).
+constexpr int PP = 1088;  // bytes per pair of pixel rows
 
-// PIXR pixels per stage, STAGES-deep ring.
+// PIXR pixels per stage (a multiple of 16), STAGES-deep ring; 2 x 4 waves of 128 x 64,
+// two waves per SIMD.  (One wave per SIMD with 128 x 128 wave tiles reads a third less
+// from LDS per MFMA but measured slower: the stage boundaries are no longer covered.)
 template <int PIXR, int STAGES>
 __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs ka) {
     const WgradArgs& a = ka.a;
-    constexpr int WNW = 4;          // waves along j (2 x 4 waves)
-    constexpr int TM = 4, TN = 2;   // wave tile 128 x 64 of the 256 x 256 block tile
-    constexpr int PPW = PIXR / 8;   // pixels each wave copies per stage
-    constexpr int PR_OP = PIXR * PPITCH;  // one operand tile of a stage
+    constexpr int WAVES = 8;
+    constexpr int WNW = 4;              // waves along j
+    constexpr int TM = 4, TN = 2;       // wave tile 128 x 64 of the 256 x 256 block tile
+    constexpr int NPAIR = PIXR / 2;     // pixel pairs per stage
+    constexpr int PAIRS = NPAIR / WAVES;  // pairs each wave copies per stage
+    constexpr int PR_OP = NPAIR * PP;   // one operand tile of a stage
     constexpr int PR_STAGE = 2 * PR_OP;
+    constexpr int DUMP = STAGES * PR_STAGE;  // 256 bytes that the L2 prefetches land in
+    static_assert(PIXR % 16 == 0 && NPAIR % WAVES == 0, "stage size");
+    static_assert(DUMP + 256 <= 160 * 1024, "LDS");
 
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * PR_STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[DUMP + 256];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -247,65 +261,121 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
     const int J = a.R * a.S * C;
     const uint32_t PQ = (uint32_t)a.P * a.Q;
     const int64_t M = (int64_t)a.N * PQ;
-    const int64_t nchunks = (M + PIXR - 1) / PIXR;
     const int tilesJ = (J + 255) / 256;
     const int tiles = tilesJ * ((K + 255) / 256);
     const int t_ = (int)xcd_remap(blockIdx.x, gridDim.x);
     const int split = t_ / tiles;
     const int k0 = ((t_ % tiles) / tilesJ) * 256;
     const int j0 = ((t_ % tiles) % tilesJ) * 256;
-    // the split ranges are given in 64-pixel chunks
-    const int64_t c_begin = (int64_t)split * a.chunks_per_split * (64 / PIXR);
-    const int64_t c_end = min(c_begin + (int64_t)a.chunks_per_split * (64 / PIXR), nchunks);
+    // this split's pixels (the ranges are given in 64-pixel chunks) and its stages
+    const int64_t m_begin = (int64_t)split * a.chunks_per_split * 64;
+    const int64_t m_end = min(m_begin + (int64_t)a.chunks_per_split * 64, M);
+    const int nst = m_end > m_begin ? (int)((m_end - m_begin + PIXR - 1) / PIXR) : 0;
 
     const v4i rs_dy = make_rsrc(a.dy, (uint32_t)(M * K * 2));
     const v4i rs_x = make_rsrc(a.x, (uint32_t)((int64_t)a.N * a.H * a.W * C * 2));
     const uint32_t smem_base = lds_addr(smem);
 
-    // this lane's 8-channel segment of the dy row and of the x column tile
+    // this lane's 8-channel segment of the dy row and of the x column tile, and which
+    // pixel of a pair it copies
     const int seg = lane & 31;
+    const int half = lane >> 5;
     const bool dy_ok = k0 + 8 * seg < K;
     const uint32_t dy_col = (uint32_t)(k0 + 8 * seg) * 2u;
+    const uint32_t dy_bad = dy_ok ? 0u : 0x80000000u;
     const int jx = j0 + 8 * seg;
     const bool x_ok = jx < J;
     const int rsx = x_ok ? jx / C : 0;
     const int xc = x_ok ? jx - rsx * C : 0;
     const int xr = rsx / a.S, xs = rsx - (rsx / a.S) * a.S;
-    const int64_t HWC = (int64_t)a.H * a.W * C;
+    const uint32_t HWC = (uint32_t)((int64_t)a.H * a.W * C);
 
-    auto issue = [&](int64_t chunk) {
-        const uint32_t st = smem_base + (uint32_t)((chunk % STAGES) * PR_STAGE);
-        if (lane < 32) {
+    // (image, h, w) of output pixel m, for the x tap (r, s)
+    auto locate = [&](uint32_t mm, int r, int s_, uint32_t* img, int* h, int* w) {
+        *img = fdiv(mm, ka.div_pq);
+        const uint32_t pq = mm - *img * PQ;
+        const uint32_t p = fdiv(pq, ka.div_q);
+        const uint32_t q_ = pq - p * (uint32_t)a.Q;
+        *h = (int)p * a.sh - a.ph + r;
+        *w = (int)q_ * a.sw - a.pw + s_;
+    };
+
+    // Byte offsets of this lane's copies of a stage (bit 31 set: outside the image or past
+    // the split's last pixel, the hardware returns zeros): pair jj of the wave holds stage
+    // pixels PAIRS wave + jj and that + NPAIR.  Computed for the next stage while the
+    // MFMAs of the current one run.
+    uint32_t o_dy[PAIRS], o_x[PAIRS];
+    auto table = [&](int st_i) {
 #pragma unroll
-            for (int pp = 0; pp < PPW; ++pp) {
-                const int pl = PPW * wave + pp;  // pixel of the stage (wave-uniform)
-                const int64_t m = chunk * PIXR + pl;
-                const bool mok = m < M;
-                const uint32_t mm = mok ? (uint32_t)m : 0u;
-                const uint32_t img = fdiv(mm, ka.div_pq);
-                const uint32_t pq = mm - img * PQ;
-                const uint32_t p = fdiv(pq, ka.div_q);
-                const uint32_t q_ = pq - p * (uint32_t)a.Q;
-                const int h = (int)p * a.sh - a.ph + xr, w = (int)q_ * a.sw - a.pw + xs;
-                const uint32_t offd = (mok && dy_ok) ? mm * (uint32_t)K * 2u + dy_col : 0x80000000u;
-                dma_b128(rs_dy, st + (uint32_t)(pl * PPITCH), offd);
-                const bool ok = mok && x_ok && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
-                const uint32_t offx = ok ? ((uint32_t)(img * HWC) + (uint32_t)((h * a.W + w) * C + xc)) * 2u : 0x80000000u;
-                dma_b128(rs_x, st + (uint32_t)(PR_OP + pl * PPITCH), offx);
-            }
+        for (int jj = 0; jj < PAIRS; ++jj) {
+            const int64_t m = m_begin + (int64_t)st_i * PIXR + PAIRS * wave + jj + NPAIR * half;
+            const bool mok = m < m_end;
+            const uint32_t mm = mok ? (uint32_t)m : 0u;
+            uint32_t img;
+            int h, w;
+            locate(mm, xr, xs, &img, &h, &w);
+            o_dy[jj] = mok ? (mm * (uint32_t)K * 2u + dy_col) | dy_bad : 0x80000000u;
+            const bool ok = mok && x_ok && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+            o_x[jj] = ok ? (img * HWC + (uint32_t)((h * a.W + w) * C + xc)) * 2u : 0x80000000u;
         }
     };
-    constexpr int kDmas = 2 * PPW;
+    auto issue = [&](int st_i) {
+        const uint32_t st = smem_base + (uint32_t)((st_i % STAGES) * PR_STAGE);
+#pragma unroll
+        for (int jj = 0; jj < PAIRS; ++jj) {
+            const int j = PAIRS * wave + jj;  // pair slot (wave-uniform)
+            dma_b128(rs_dy, st + (uint32_t)(j * PP), o_dy[jj]);
+            dma_b128(rs_x, st + (uint32_t)(PR_OP + j * PP), o_x[jj]);
+        }
+    };
+    constexpr int kDmas = 2 * PAIRS;
+
+    // L2 prefetch of a later stage: one 4-byte copy per thread into a dump area touches one
+    // 128-byte line (waves 0-3: the dy rows, stage pixel (tid % 256) / 4, line tid % 4 of
+    // its 512 bytes; waves 4-7: the same for the x rows), so that the copies of that stage
+    // find their lines in L2.
+    const int pf_line = tid & 3;
+    const int pf_pix = (tid & 255) >> 2;
+    const bool pf_is_x = wave >= 4;  // wave-uniform
+    const int pf_k = k0 + 64 * pf_line;
+    const int pf_j = j0 + 64 * pf_line;
+    const bool pf_jok = pf_j < J;
+    const int pf_rs = pf_jok ? pf_j / C : 0;
+    const int pf_c = pf_jok ? pf_j - pf_rs * C : 0;
+    const int pf_r = pf_rs / a.S, pf_s = pf_rs - (pf_rs / a.S) * a.S;
+    auto prefetch = [&](int st_i) {
+        const int64_t m = m_begin + (int64_t)st_i * PIXR + pf_pix;
+        const bool mok = pf_pix < PIXR && m < m_end;
+        const uint32_t mm = mok ? (uint32_t)m : 0u;
+        if (pf_is_x) {
+            uint32_t img;
+            int h, w;
+            locate(mm, pf_r, pf_s, &img, &h, &w);
+            const bool ok = mok && pf_jok && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+            dma_b32(rs_x, smem_base + DUMP,
+                    ok ? (img * HWC + (uint32_t)((h * a.W + w) * C + pf_c)) * 2u : 0x80000000u);
+        } else {
+            dma_b32(rs_dy, smem_base + DUMP,
+                    mok && pf_k < K ? (mm * (uint32_t)K + (uint32_t)pf_k) * 2u : 0x80000000u);
+        }
+    };
+    const int pf_dist = ka.pf_dist;
 
     // transposing reads: lane (g = lane / 16, i = lane % 16) reads the 8 bytes of channels
-    // 16 (g % 2) + 4 (i % 4) .. + 3 of pixel 8 (g / 2) + i / 4 (+ 4 for the second read)
+    // 16 (g % 2) + 4 (i % 4) .. + 3 of stage pixel 16 u + 8 (g / 2) + i / 4 (+ 4 for the
+    // second read) in step u; stage pixel r sits at (r % NPAIR) * PP + (r / NPAIR) * 512
     const int g = lane >> 4, i16 = lane & 15;
-    const uint32_t lane_off = (uint32_t)((8 * (g >> 1) + (i16 >> 2)) * PPITCH + (16 * (g & 1) + 4 * (i16 & 3)) * 2);
-    const uint32_t a_base = lane_off + (uint32_t)(wm * 128 * 2);
-    const uint32_t b_base = (uint32_t)PR_OP + lane_off + (uint32_t)(wn * 32 * TN * 2);
+    const int rho = 8 * (g >> 1) + (i16 >> 2);
+    const uint32_t col_off = (uint32_t)((16 * (g & 1) + 4 * (i16 & 3)) * 2);
+    auto row_off = [&](int u) {
+        const int r = 16 * u + rho;
+        return (uint32_t)((r % NPAIR) * PP + (r / NPAIR) * 512) + col_off;
+    };
+    const uint32_t a_base = (uint32_t)(wm * 128 * 2);
+    const uint32_t b_base = (uint32_t)PR_OP + (uint32_t)(wn * 32 * TN * 2);
     auto operand = [&](uint32_t addr) {
         const v4i16 lo = read_tr(addr);
-        const v4i16 hi = read_tr(addr + 4 * PPITCH);
+        const v4i16 hi = read_tr(addr + 4 * PP);
         typedef short v8i16 __attribute__((ext_vector_type(8)));
         const v8i16 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
         return __builtin_bit_cast(bf16x8, v);
@@ -319,22 +389,35 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][t][v] = 0.0f;
 
+    // every issue() is followed by one prefetch; a stage's copies are complete once at most
+    // the copies and prefetches issued after them are outstanding
 #pragma unroll
-    for (int c = 0; c < STAGES - 1; ++c)
-        if (c_begin + c < c_end) issue(c_begin + c);
-    for (int64_t chunk = c_begin; chunk < c_end; ++chunk) {
-        // this wave's DMAs of stage `chunk` landed (later stages may still be in flight)
-        const int later = (int)min(c_end - 1 - chunk, (int64_t)(STAGES - 2));
-        wait_vmcnt(later * kDmas);
-        __syncthreads();  // ... and every other wave's; all reads of stage chunk-1 are done
-        if (chunk + STAGES - 1 < c_end) issue(chunk + STAGES - 1);  // into stage chunk-1's buffer
-        const uint32_t st = smem_base + (uint32_t)((chunk % STAGES) * PR_STAGE);
+    for (int c = 0; c < STAGES - 1; ++c) {
+        table(c);
+        if (c < nst) {
+            issue(c);
+            prefetch(c + pf_dist);
+        }
+    }
+    table(STAGES - 1);
+    for (int it = 0; it < nst; ++it) {
+        // this wave's DMAs of stage `it` landed (later stages may still be in flight)
+        const int later = min(nst - 1 - it, STAGES - 2);
+        wait_vmcnt(later * (kDmas + 1) + 1);
+        __syncthreads();  // ... and every other wave's; all reads of stage it-1 are done
+        if (it + STAGES - 1 < nst) {
+            issue(it + STAGES - 1);  // into stage it-1's buffer
+            prefetch(it + STAGES - 1 + pf_dist);
+            table(it + STAGES);      // the offsets of the next copy, during the MFMAs
+        }
+        const uint32_t st = smem_base + (uint32_t)((it % STAGES) * PR_STAGE);
         bf16x8 af[2][TM], bf[2][TN];
         auto load = [&](int u, int b) {
+            const uint32_t ro = row_off(u);
 #pragma unroll
-            for (int i = 0; i < TM; ++i) af[b][i] = operand(st + a_base + (uint32_t)(64 * i + u * 16 * PPITCH));
+            for (int i = 0; i < TM; ++i) af[b][i] = operand(st + a_base + (uint32_t)(64 * i) + ro);
 #pragma unroll
-            for (int t = 0; t < TN; ++t) bf[b][t] = operand(st + b_base + (uint32_t)(64 * t + u * 16 * PPITCH));
+            for (int t = 0; t < TN; ++t) bf[b][t] = operand(st + b_base + (uint32_t)(64 * t) + ro);
         };
         load(0, 0);
 #pragma unroll
@@ -348,7 +431,7 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
     }
 
     float* out = a.out + (int64_t)split * K * J;
-    const int l32 = lane & 31, half = lane >> 5;
+    const int l32 = lane & 31;
 #pragma unroll
     for (int t = 0; t < TN; ++t) {
         const int col = j0 + wn * 32 * TN + 32 * t + l32;
@@ -383,6 +466,10 @@ WgradDmaPlan wgrad_dma_plan(int K, int J) {
     if (e && (atoi(e) == 0 || atoi(e) == 1)) p.cfg = atoi(e);
     p.tiles = ((K + TILE_K - 1) / TILE_K) * ((J + 255) / 256);
     p.resident_blocks = 256;  // one block per CU
+    // pixel-major kernel: 48-pixel stages in a three-deep ring (measured best of 32 / 48 / 64)
+    p.pix = 48;
+    const char* px = getenv("TBN_WGRAD_PIX");
+    if (px && (atoi(px) == 32 || atoi(px) == 64)) p.pix = atoi(px);
     return p;
 }
 
@@ -391,12 +478,19 @@ hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream) {
     ka.a = a;
     ka.div_q = make_fastdiv((uint32_t)a.Q);
     ka.div_pq = make_fastdiv((uint32_t)a.P * (uint32_t)a.Q);
+    const char* pf = getenv("TBN_WGRAD_PF");
+    ka.pf_dist = pf ? atoi(pf) : 3;  // stages ahead (measured: 3 with 48-pixel stages)
     const WgradDmaPlan p = wgrad_dma_plan(a.K, a.R * a.S * a.C);
     const dim3 grid((unsigned)(p.tiles * a.splits));
-    if (p.cfg == 1)
-        hipLaunchKernelGGL((wgrad_rows_kernel<64, 2>), grid, dim3(512), 0, stream, ka);
-    else
+    if (p.cfg == 1) {
+        switch (p.pix) {
+            case 32: hipLaunchKernelGGL((wgrad_rows_kernel<32, 4>), grid, dim3(512), 0, stream, ka); break;
+            case 64: hipLaunchKernelGGL((wgrad_rows_kernel<64, 2>), grid, dim3(512), 0, stream, ka); break;
+            default: hipLaunchKernelGGL((wgrad_rows_kernel<48, 3>), grid, dim3(512), 0, stream, ka); break;
+        }
+    } else {
         hipLaunchKernelGGL(wgrad_seg_kernel, grid, dim3(512), 0, stream, ka);
+    }
     return hipGetLastError();
 }
 

@@ -333,10 +333,13 @@ def test_bwd_weight_parity(tbn, g, accumulate):
     assert e <= 1e-4
 
 
-@pytest.mark.parametrize("cfg", [0, 1])
-def test_bwd_weight_tile_shapes(tbn, cfg, monkeypatch):
-    # every tile / stage geometry of the transposing-read weight-gradient kernel
+@pytest.mark.parametrize("cfg,pix", [(0, 48), (1, 32), (1, 48), (1, 64)])
+def test_bwd_weight_tile_shapes(tbn, cfg, pix, monkeypatch):
+    # every tile / stage geometry of the transposing-read weight-gradient kernels (the
+    # 48-pixel stages do not divide the 64-pixel split ranges: the last stage of a range is
+    # partial)
     monkeypatch.setenv("TBN_WGRAD_CFG", str(cfg))
+    monkeypatch.setenv("TBN_WGRAD_PIX", str(pix))
     for g in [(2, 14, 14, 256, 256, 3, 3, 1, 1), (3, 12, 12, 128, 136, 3, 3, 2, 1), (5, 9, 7, 64, 96, 3, 3, 1, 1),
               (2, 16, 16, 64, 128, 1, 1, 2, 0)]:
         d, P, Q, xb, dyb, _ = _conv_inputs(g, 5)
@@ -344,7 +347,7 @@ def test_bwd_weight_tile_shapes(tbn, cfg, monkeypatch):
         dw = tbn.conv2d_bwd_weight(tbn.ConvDesc(*g), bf16_dev(xb), bf16_dev(dyb))
         torch.cuda.synchronize()
         e = nerr(dw.cpu().numpy(), ref)
-        log("bwd_weight cfg %d %s: %.3e" % (cfg, g, e))
+        log("bwd_weight cfg %d pix %d %s: %.3e" % (cfg, pix, g, e))
         assert e <= 1e-4
 
 
@@ -422,7 +425,7 @@ TILE_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1)
               (3, 5, 5, 64, 80, 5, 5, 1, 0)]
 
 
-@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 14, 16, 20, 30])
+@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 14, 16, 18, 20, 30])
 def test_every_tile_shape(tbn, tile, monkeypatch):
     # each tile shape of the convolution kernels against the oracle (fwd and bwd_data)
     monkeypatch.setenv("TBN_CONV_TILE", str(tile))
