@@ -541,10 +541,11 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
         if (forced > 0) {
             splits = forced;
         } else if (tiles < 384) {
-            // measured: about 384 blocks of the 64 x 128 tile with >= 6 stages each, or
-            // 640 blocks of the 128 x 64 tile with >= 3 stages each
+            // measured: the 64 x 128 tile split only below ~192 tiles (then to about 192
+            // blocks with >= 6 stages each: a split costs a partial-sum pass), the 128 x 64
+            // tile to about 640 blocks with >= 3 stages each
             const bool shortt = p.cfg == 18;
-            const int64_t target = shortt ? 384 : 640, min_stages = shortt ? 6 : 3;
+            const int64_t target = shortt ? 192 : 640, min_stages = shortt ? 6 : 3;
             splits = (target + tiles - 1) / tiles;
             const int64_t max_splits = nchunks / min_stages > 0 ? nchunks / min_stages : 1;
             if (splits > max_splits) splits = max_splits;

@@ -143,6 +143,49 @@ __global__ __launch_bounds__(256) void avgpool_kernel(int32_t N, int32_t HW, int
     st_act(y, o, acc / (float)HW, y_f32);
 }
 
+// C % 8 == 0: eight lanes per group of 8 channels of one image; lane j sums positions
+// j, j + 8, ... with 16-byte loads, then the eight partial sums are combined by a fixed
+// butterfly (the result does not depend on scheduling).
+__global__ __launch_bounds__(256) void avgpool8_kernel(int32_t N, int32_t HW, int32_t C, const uint16_t* __restrict__ x,
+                                                       void* __restrict__ y, int y_f32) {
+    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t grp = t >> 3;  // (n, channel group), N * C / 8 of them
+    const int j = (int)(t & 7);
+    const int G = C / 8;
+    const bool ok = grp < (int64_t)N * G;
+    const int64_t n = ok ? grp / G : 0;
+    const int c0 = ok ? (int)(grp - n * G) * 8 : 0;
+    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (ok) {
+        for (int i = j; i < HW; i += 8) {
+            const u32x4 v = *reinterpret_cast<const u32x4*>(x + (n * HW + i) * C + c0);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                acc[2 * e] += bf16_bits_to_f32(v[e] & 0xFFFFu);
+                acc[2 * e + 1] += bf16_bits_to_f32(v[e] >> 16);
+            }
+        }
+    }
+    // every lane of the wave takes part in the shuffles (groups of 8 lanes never straddle
+    // a wave; lanes past the end carry zeros)
+#pragma unroll
+    for (int m = 1; m < 8; m <<= 1)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], m, 8);
+    if (!ok || j != 0) return;
+    const float inv = 1.0f / (float)HW;
+    const int64_t o = n * C + c0;
+    if (y_f32) {
+        float* yp = reinterpret_cast<float*>(y) + o;
+        *reinterpret_cast<f32x4*>(yp) = f32x4{acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv};
+        *reinterpret_cast<f32x4*>(yp + 4) = f32x4{acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv};
+    } else {
+        *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(y) + o) =
+            u32x4{pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv),
+                  pack_bf16x2(acc[4] * inv, acc[5] * inv), pack_bf16x2(acc[6] * inv, acc[7] * inv)};
+    }
+}
+
 // ---- batch normalisation, training form ----
 // Per-channel sums over rows = N*H*W in two deterministic levels:
 //   * partial: block (b, slice) sums rows [b*rpc, (b+1)*rpc) for up to 256 channel groups
@@ -434,7 +477,10 @@ hipError_t launch_maxpool_bwd(const PoolArgs& a, const uint16_t* dy, const int32
 }
 
 hipError_t launch_avgpool(int32_t N, int32_t HW, int32_t C, const uint16_t* x, void* y, int y_f32, hipStream_t s) {
-    hipLaunchKernelGGL(avgpool_kernel, dim3(blocks_for((int64_t)N * C)), dim3(256), 0, s, N, HW, C, x, y, y_f32);
+    if (C % 8 == 0)  // 16-byte rows (the caller guarantees 16-byte aligned buffers)
+        hipLaunchKernelGGL(avgpool8_kernel, dim3(blocks_for((int64_t)N * C)), dim3(256), 0, s, N, HW, C, x, y, y_f32);
+    else
+        hipLaunchKernelGGL(avgpool_kernel, dim3(blocks_for((int64_t)N * C)), dim3(256), 0, s, N, HW, C, x, y, y_f32);
     return hipGetLastError();
 }
 

@@ -39,12 +39,18 @@ def test_maxpool(tbn, shape, k, s, p):
     assert nerr(dx.cpu().numpy(), dx_ref) <= 1e-6
 
 
-def test_avgpool(tbn):
-    xb = synth.normal_bf16(10, "ap", (64, 7, 7, 512))
+@pytest.mark.parametrize("shape", [(64, 7, 7, 512), (3, 1, 1, 16), (2, 3, 5, 24), (5, 4, 4, 13), (1, 9, 11, 3)])
+def test_avgpool(tbn, shape):
+    # 16-byte channel groups (C % 8 == 0, fewer or more positions than the 8 lanes that
+    # share a group) and the per-channel path (C % 8 != 0)
+    xb = synth.normal_bf16(10, "ap%s" % (shape,), shape)
     ref = oracle.avgpool_global(oracle.bf16_bits_to_f64(xb))
     y = tbn.avgpool_global(bf16_dev(xb), out_dtype=torch.float32)
     torch.cuda.synchronize()
     assert nerr(y.cpu().numpy(), ref) <= 1e-5
+    yb = tbn.avgpool_global(bf16_dev(xb))
+    torch.cuda.synchronize()
+    assert nerr(oracle.bf16_bits_to_f64(yb.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)), ref) <= 1e-2
 
 
 @pytest.mark.parametrize("shape,relu", [((8, 16, 16, 128), True), ((4, 8, 8, 24), False), ((2, 5, 5, 13), True),
