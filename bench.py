@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-resnet", action="store_true", help="skip the ResNet-18 forward figures")
     ap.add_argument("--no-small", action="store_true", help="skip the single-layer, LeNet and VGG figures")
-    ap.add_argument("--cpu-seconds", type=float, default=20.0, help="budget of the oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain device copy of known size (HBM counter calibration)")
     return ap.parse_args()
@@ -88,9 +88,10 @@ def measured_traffic(op):
 
 
 def cpu_baseline(budget_s: float):
-    """The fp64 oracle on a bounded slice of the same step: the three convolutions on one
-    image of the batch (the work is linear in the batch, scaled by 128), plus quantise and
-    SGD over the whole layer."""
+    """The fp64 oracle on a bounded slice of the same step: quantise and SGD over the whole
+    layer, and the three convolutions on as many images of the batch as fit in `budget_s`
+    seconds (at least one; the work is linear in the batch, so the mean per-image time is
+    scaled by 128)."""
     import oracle
     import synth
 
@@ -100,24 +101,26 @@ def cpu_baseline(budget_s: float):
     d = oracle.ConvDesc(1, L["h"], L["w"], L["c"], L["k"], L["r"], L["s"], L["stride"], L["pad"])
     P, Q = d.out_dims()
     n = L["r"] * L["s"] * L["c"]
-    x = oracle.bf16_bits_to_f64(synth.normal_bf16(5, "x1", (1, L["h"], L["w"], L["c"])))
-    dy = oracle.bf16_bits_to_f64(synth.normal_bf16(5, "dy1", (1, P, Q, L["k"])))
     w = synth.normal(5, "w", (L["k"], n), 0.05)
     v = np.zeros_like(w)
     t0 = time.perf_counter()
     q = oracle.quantize(w)
     a64 = q.alpha.astype(np.float64)
-    t1 = time.perf_counter()
-    oracle.conv_fwd(d, x, q.codes, a64)
+    t_quant = time.perf_counter() - t0
+    conv_s, images, g = 0.0, 0, None
+    while images < L["n"] and (images == 0 or conv_s < budget_s):
+        x = oracle.bf16_bits_to_f64(synth.normal_bf16(5, "x1_%d" % images, (1, L["h"], L["w"], L["c"])))
+        dy = oracle.bf16_bits_to_f64(synth.normal_bf16(5, "dy1_%d" % images, (1, P, Q, L["k"])))
+        t1 = time.perf_counter()
+        oracle.conv_fwd(d, x, q.codes, a64)
+        oracle.conv_bwd_data(d, dy, q.codes, a64)
+        g = oracle.conv_bwd_weight(d, x, dy).reshape(L["k"], n)
+        conv_s += time.perf_counter() - t1
+        images += 1
     t2 = time.perf_counter()
-    oracle.conv_bwd_data(d, dy, q.codes, a64)
-    t3 = time.perf_counter()
-    g = oracle.conv_bwd_weight(d, x, dy).reshape(L["k"], n)
-    t4 = time.perf_counter()
     oracle.sgd(w, v, g, LR, MOMENTUM, WD)
-    t5 = time.perf_counter()
-    per_image = (t2 - t1) + (t3 - t2) + (t4 - t3)
-    step_s = (t1 - t0) + (t5 - t4) + per_image * L["n"]
+    t_sgd = time.perf_counter() - t2
+    step_s = t_quant + t_sgd + conv_s / images * L["n"]
     conv_flops, _, _ = layer_flops()
     return {
         "value": round(3 * conv_flops / step_s / 1e12, 6),
@@ -125,8 +128,8 @@ def cpu_baseline(budget_s: float):
         "cores": int(os.environ.get("OMP_NUM_THREADS", threads)),
         "kind": "oracle",
         "sample": "fp64 oracle: quantise + SGD over the full 256x3x3x256 layer, fwd/bwd_data/bwd_weight "
-                  "on 1 of 128 images (scaled x128); measured %.1f s, extrapolated %.0f s per step" %
-                  (t5 - t0, step_s),
+                  "on %d of 128 images (mean per image scaled x128); measured %.1f s, extrapolated %.0f s "
+                  "per step" % (images, t_quant + t_sgd + conv_s, step_s),
     }
 
 
@@ -311,6 +314,50 @@ def weight_streaming(dev, sets=8, reps=20):
             "bytes_per_call": byts, "achieved_GBs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
+def fused_update(dev, reps=20):
+    """The update step fused with the next quantisation (one pass over the real weights:
+    12 B read + 8.25 B written per weight) against SGD followed by a separate quantisation
+    (16 B read + 8.25 B written), on the training layer and on a 4096 x 4608 filter set
+    (18.9 M weights, larger than the last-level cache)."""
+    import torch
+
+    import paper_1701_00485_amd as tbn
+
+    stream = torch.cuda.current_stream()
+    out = {}
+    for name, K, n in (("train_layer_256x2304", 256, 2304), ("filters_4096x4608", 4096, 4608)):
+        g = torch.Generator(device=dev)
+        g.manual_seed(1701_00485)
+        w = torch.randn(K, n, device=dev, generator=g) * 0.05
+        v = torch.zeros_like(w)
+        gr = torch.randn(K, n, device=dev, generator=g)
+        codes, alpha, _ = tbn.quantize(w, want_counts=False)
+
+        def fused():
+            tbn.sgd_step_quantize(w, v, gr, 1e-6, 0.9, 1e-4, codes=codes, alpha=alpha, want_counts=False)
+
+        def separate():
+            tbn.sgd_step(w, v, gr, 1e-6, 0.9, 1e-4)
+            tbn.quantize(w, codes, alpha, want_counts=False)
+
+        rec = {}
+        for label, fn, byts in (("fused", fused, 20.25), ("separate", separate, 24.25)):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) / reps * 1e3
+            gbs = byts * K * n / (us * 1e-6) / 1e9
+            rec[label] = {"us": round(us, 2), "achieved_GBs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+        out[name] = rec
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -433,6 +480,7 @@ def main():
     if not args.no_small:
         result["small_workloads"] = small_configs(dev)
         result["weight_streaming"] = weight_streaming(dev)
+        result["fused_update_quantize"] = fused_update(dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(result), flush=True)

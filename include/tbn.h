@@ -179,6 +179,21 @@ tbn_status tbn_conv2d_bwd_weight(const tbn_conv_desc* desc, const void* x, const
 tbn_status tbn_sgd_step(float* w, float* v, const float* g, int64_t count, float lr,
                         float momentum, float weight_decay, hipStream_t stream);
 
+/*
+ * The update step of Algorithm 1 fused with the quantisation that opens the next
+ * iteration (Sec. 2 Eq. 3 and Eq. 5 applied to the updated filters), in one pass over
+ * the real weights:
+ *   v = momentum * v + (g + weight_decay * w);   w = w - lr * v   (fp32, in place, the same
+ *   rounding as tbn_sgd_step), then codes / alpha / counts of the updated w exactly as
+ *   tbn_quantize would produce them.
+ *   w, v, g  [K][n] fp32, one filter per row.   codes, alpha, counts: as tbn_quantize.
+ * Reads 12 bytes and writes 8.25 bytes per weight, against 16 + 8.25 for tbn_sgd_step
+ * followed by tbn_quantize.
+ */
+tbn_status tbn_sgd_step_quantize(float* w, float* v, const float* g, int64_t k, int64_t n, float lr,
+                                 float momentum, float weight_decay, uint32_t* codes, float* alpha,
+                                 int32_t* counts, hipStream_t stream);
+
 /* ------------------------------------------------------------------------------------ */
 /* Layers around the two-bit convolutions in the workloads (Sec. 4 names ResNet-18 with   */
 /* batch normalisation; the smaller workloads add max pooling, ReLU and a softmax         */

@@ -72,6 +72,8 @@ def _load():
     lib.orc_conv_bwd_weight_sampled_bf16.restype = ctypes.c_int
     lib.orc_sgd.argtypes = [p, p, p, i64, ctypes.c_double, ctypes.c_double, ctypes.c_double]
     lib.orc_sgd.restype = None
+    lib.orc_sgd_f32.argtypes = [p, p, p, i64, ctypes.c_float, ctypes.c_float, ctypes.c_float]
+    lib.orc_sgd_f32.restype = None
     lib.orc_maxpool_fwd.argtypes = [p, p, p, p]
     lib.orc_maxpool_fwd.restype = ctypes.c_int
     lib.orc_maxpool_bwd.argtypes = [p, p, p, p]
@@ -304,6 +306,16 @@ def sgd(w, v, g, eta, mu=0.9, lam=1e-4):
     v = np.array(v, dtype=np.float64, copy=True).ravel()
     g = _c(g, np.float64).ravel()
     _load().orc_sgd(_ptr(w), _ptr(v), _ptr(g), w.size, float(eta), float(mu), float(lam))
+    return w, v
+
+
+def sgd_f32(w, v, g, eta, mu=0.9, lam=1e-4):
+    """The SGD step in fp32 with fused multiply-adds (the rounding that decides the next
+    codes).  Returns (w_new, v_new) fp32; inputs are not modified."""
+    w = np.array(w, dtype=np.float32, copy=True).ravel()
+    v = np.array(v, dtype=np.float32, copy=True).ravel()
+    g = _c(g, np.float32).ravel()
+    _load().orc_sgd_f32(_ptr(w), _ptr(v), _ptr(g), w.size, float(eta), float(mu), float(lam))
     return w, v
 
 

@@ -464,6 +464,18 @@ void orc_sgd(double* w, double* v, const double* g, int64_t count, double eta, d
     }
 }
 
+/* The same two update lines in fp32, each multiply-add fused and rounded once (C99 fmaf).
+ * The updated weight decides the next iteration's codes (Eq. 3), an integer result, so
+ * the fused update-and-quantise step is checked against this form, which reproduces the
+ * fp32 rounding of the update exactly; orc_sgd above is the same step in fp64. */
+void orc_sgd_f32(float* w, float* v, const float* g, int64_t count, float eta, float mu,
+                 float lambda) {
+    for (int64_t i = 0; i < count; ++i) {
+        v[i] = fmaf(mu, v[i], fmaf(lambda, w[i], g[i]));
+        w[i] = fmaf(-eta, v[i], w[i]);
+    }
+}
+
 /* ------------------------------------------------------------------------------------ */
 /* Layers the workloads put around the two-bit convolutions (Sec. 4 uses ResNet-18 with  */
 /* batch normalisation).  Textbook definitions, NHWC, fp64.                               */

@@ -11,6 +11,7 @@ Calls (same names as the C ABI, without the ``tbn_`` prefix):
   conv2d_bwd_data(desc, dy, codes, alpha)  Sec. 3        -> dx
   conv2d_bwd_weight(desc, x, dy)    Sec. 3 (straight-through) -> dW
   sgd_step(w, v, g, lr, momentum, weight_decay)  Sec. 4 optimiser
+  sgd_step_quantize(w, v, g, lr, ...)  the update fused with the next quantisation
 """
 from __future__ import annotations
 
@@ -81,6 +82,7 @@ def load():
         "tbn_conv2d_bwd_data": ([vp, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_conv2d_bwd_weight": ([vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_sgd_step": ([vp, vp, vp, i64, f32, f32, f32, vp], i32),
+        "tbn_sgd_step_quantize": ([vp, vp, vp, i64, i64, f32, f32, f32, vp, vp, vp, vp], i32),
         "tbn_pool_out_dims": ([vp, vp, vp], i32),
         "tbn_maxpool2d_fwd": ([vp, vp, vp, vp, vp], i32),
         "tbn_maxpool2d_bwd": ([vp, vp, vp, vp, i32, vp], i32),
@@ -104,7 +106,7 @@ def exported_symbols():
     return sorted(["tbn_status_str", "tbn_last_error", "tbn_conv_out_dims", "tbn_packed_words",
                    "tbn_workspace_size", "tbn_quantize", "tbn_conv2d_fwd", "tbn_conv2d_fwd_dense",
                    "tbn_conv2d_bwd_data",
-                   "tbn_conv2d_bwd_weight", "tbn_sgd_step", "tbn_pool_out_dims", "tbn_maxpool2d_fwd",
+                   "tbn_conv2d_bwd_weight", "tbn_sgd_step", "tbn_sgd_step_quantize", "tbn_pool_out_dims", "tbn_maxpool2d_fwd",
                    "tbn_maxpool2d_bwd", "tbn_avgpool_global", "tbn_batchnorm_workspace_size",
                    "tbn_batchnorm_train_fwd", "tbn_batchnorm_train_bwd", "tbn_relu_bwd", "tbn_softmax_xent"])
 
@@ -281,6 +283,29 @@ def sgd_step(w, v, g, lr, momentum=0.9, weight_decay=1e-4):
     _call("tbn_sgd_step", _dev(w, "w", (torch.float32,)), _dev(v, "v", (torch.float32,)),
           _dev(g, "g", (torch.float32,)), n, float(lr), float(momentum), float(weight_decay), _stream())
     return w, v
+
+
+def sgd_step_quantize(w, v, g, lr, momentum=0.9, weight_decay=1e-4, codes=None, alpha=None, counts=None,
+                      want_counts=True):
+    """SGD update of w [K][n] (in place, with momentum v) fused with the quantisation of
+    the updated filters.  Returns (codes, alpha, counts) as quantize() does."""
+    K = w.shape[0]
+    n = w.numel() // K
+    _numel(v, K * n, "v")
+    _numel(g, K * n, "g")
+    if codes is None:
+        codes = torch.empty(packed_words(K, n), dtype=torch.int32, device=w.device)
+    if alpha is None:
+        alpha = torch.empty(K, dtype=torch.float32, device=w.device)
+    if counts is None and want_counts:
+        counts = torch.empty((K, 2), dtype=torch.int32, device=w.device)
+    _numel(codes, packed_words(K, n), "codes")
+    _numel(alpha, K, "alpha")
+    pc = _dev(counts, "counts", (torch.int32,)) if counts is not None else None
+    _call("tbn_sgd_step_quantize", _dev(w, "w", (torch.float32,)), _dev(v, "v", (torch.float32,)),
+          _dev(g, "g", (torch.float32,)), K, n, float(lr), float(momentum), float(weight_decay),
+          _dev(codes, "codes", (torch.int32,)), _dev(alpha, "alpha", (torch.float32,)), pc, _stream())
+    return codes, alpha, counts
 
 
 # --------------------------------------------------------------------------------------

@@ -323,6 +323,20 @@ tbn_status tbn_sgd_step(float* w, float* v, const float* g, int64_t count, float
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_sgd_step");
 }
 
+tbn_status tbn_sgd_step_quantize(float* w, float* v, const float* g, int64_t k, int64_t n, float lr,
+                                 float momentum, float weight_decay, uint32_t* codes, float* alpha,
+                                 int32_t* counts, hipStream_t stream) {
+    if (!w || !v || !g || !codes || !alpha) return fail(TBN_ERR_NULL, "w, v, g, codes and alpha are required");
+    if (k <= 0 || n <= 0) return fail(TBN_ERR_SHAPE, "k and n must be positive");
+    if (n > kI32Max || k > kI32Max / 2) return fail(TBN_ERR_SHAPE, "k or n too large");
+    if (!aligned4(w) || !aligned4(v) || !aligned4(g) || !aligned16(codes) || !aligned4(alpha) ||
+        (counts && !aligned4(counts)))
+        return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    const tbn::SgdArgs sgd = {w, v, g, lr, momentum, weight_decay};
+    hipError_t e = tbn::launch_sgd_quantize(sgd, k, n, codes, alpha, counts, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_sgd_step_quantize");
+}
+
 namespace {
 
 tbn_status check_pool(const tbn_pool_desc* d, tbn::PoolArgs* a) {

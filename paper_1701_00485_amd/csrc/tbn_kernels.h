@@ -51,6 +51,16 @@ struct ConvGemmArgs {
 hipError_t launch_quantize(const float* w, int64_t K, int64_t n, uint32_t* codes, float* alpha,
                            int32_t* counts, hipStream_t stream);
 
+// Momentum-SGD operands of the fused update-and-quantise step ([K][n] fp32 each).
+struct SgdArgs {
+    float* w;
+    float* v;
+    const float* g;
+    float lr, mu, wd;
+};
+hipError_t launch_sgd_quantize(const SgdArgs& sgd, int64_t K, int64_t n, uint32_t* codes, float* alpha,
+                               int32_t* counts, hipStream_t stream);
+
 hipError_t launch_conv_gemm(const ConvGemmArgs& a, hipStream_t stream);
 
 // LDS-DMA variant (bf16 x, C % 8 == 0, R*S <= 63, x < 2 GiB).  Its plan picks the tile

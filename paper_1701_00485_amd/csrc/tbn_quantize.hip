@@ -9,7 +9,8 @@
 // ballots (even elements to bytes 0/1, odd elements to bytes 2/3) and store them as one
 // 16-byte segment.  The B1/B2 sums of Eq. (4)-(5) accumulate per lane in fp64, are
 // reduced across each wave and then over the waves in order; |B2| is the popcount of the
-// magnitude ballots.
+// magnitude ballots.  The same kernel can first apply the SGD update to each weight (the
+// update step of Algorithm 1 fused with the next iteration's quantisation).
 #include "tbn_device.h"
 #include "tbn_kernels.h"
 
@@ -30,13 +31,24 @@ __device__ __forceinline__ double wave_sum(double v) {
     return v;
 }
 
+// Momentum-SGD update of one weight (Sec. 4 optimiser), written with explicit fused
+// multiply-adds so that the standalone update and the fused update-and-quantise step give
+// bit-identical weights: v = momentum v + (g + decay w), w = w - lr v.
+__device__ __forceinline__ void sgd_update(float& w, float& v, float g, float lr, float mu, float wd) {
+    v = __builtin_fmaf(mu, v, __builtin_fmaf(wd, w, g));
+    w = __builtin_fmaf(-lr, v, w);
+}
+
 // One block of four waves per filter: wave v takes the chunks c = v, v + 4, ... (four at a
 // time, loads issued together), and the per-wave fp64 sums and counts are combined in wave
-// order through LDS.
+// order through LDS.  With SGD, each element is first updated in place (w, v from their
+// gradient g) and the updated weight is what Eq. (3)-(5) see: the next iteration's
+// quantisation fused into this iteration's update, one pass over the filter.
+template <bool SGD>
 __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__ w, int64_t K,
                                                        int64_t n, uint32_t* __restrict__ codes,
                                                        float* __restrict__ alpha,
-                                                       int32_t* __restrict__ counts) {
+                                                       int32_t* __restrict__ counts, SgdArgs sgd) {
     __shared__ double sh1[4], sh2[4];
     __shared__ int64_t shn[4];
     const int lane = threadIdx.x & 63;
@@ -57,6 +69,26 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
         for (int j = 0; j < 4; ++j) {  // branch-free loads: out-of-range lanes read w[k][0]
             const int64_t i = (c0 + 4 * j) * 64 + lane;
             u[j] = __float_as_uint(wk[i < n ? i : 0]);
+        }
+        if constexpr (SGD) {
+            float vv[4], gg[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t i = (c0 + 4 * j) * 64 + lane;
+                vv[j] = sgd.v[k * n + (i < n ? i : 0)];
+                gg[j] = sgd.g[k * n + (i < n ? i : 0)];
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t i = (c0 + 4 * j) * 64 + lane;
+                float wf = __uint_as_float(u[j]);
+                sgd_update(wf, vv[j], gg[j], sgd.lr, sgd.mu, sgd.wd);
+                u[j] = __float_as_uint(wf);
+                if (c0 + 4 * j < nb && i < n) {
+                    sgd.w[k * n + i] = wf;
+                    sgd.v[k * n + i] = vv[j];
+                }
+            }
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -114,7 +146,16 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
 hipError_t launch_quantize(const float* w, int64_t K, int64_t n, uint32_t* codes, float* alpha,
                            int32_t* counts, hipStream_t stream) {
     const int64_t kpad = (K + 63) / 64 * 64;
-    hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)kpad), dim3(256), 0, stream, w, K, n, codes, alpha, counts);
+    hipLaunchKernelGGL(quantize_kernel<false>, dim3((unsigned)kpad), dim3(256), 0, stream, w, K, n, codes, alpha,
+                       counts, SgdArgs{});
+    return hipGetLastError();
+}
+
+hipError_t launch_sgd_quantize(const SgdArgs& sgd, int64_t K, int64_t n, uint32_t* codes, float* alpha,
+                               int32_t* counts, hipStream_t stream) {
+    const int64_t kpad = (K + 63) / 64 * 64;
+    hipLaunchKernelGGL(quantize_kernel<true>, dim3((unsigned)kpad), dim3(256), 0, stream, sgd.w, K, n, codes,
+                       alpha, counts, sgd);
     return hipGetLastError();
 }
 

@@ -8,9 +8,10 @@ namespace tbn {
 
 namespace {
 
+// Explicit fused multiply-adds: the same rounding as the fused update-and-quantise kernel.
 __device__ __forceinline__ void sgd_one(float& w, float& v, float g, float lr, float mu, float wd) {
-    v = mu * v + (g + wd * w);
-    w = w - lr * v;
+    v = __builtin_fmaf(mu, v, __builtin_fmaf(wd, w, g));
+    w = __builtin_fmaf(-lr, v, w);
 }
 
 __global__ __launch_bounds__(256) void sgd_kernel(float* __restrict__ w, float* __restrict__ v,

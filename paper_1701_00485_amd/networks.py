@@ -147,6 +147,14 @@ class ResNet18:
 # through the approximate filters, straight-through gradient to the real filters, SGD.
 # --------------------------------------------------------------------------------------
 LR, MOMENTUM, WEIGHT_DECAY = 0.1, 0.9, 1e-4
+# Sec. 4 schedule: the learning rate starts at 0.1 and is divided by 10 at epochs 30, 40
+# and 50 (Algorithm 1 ends each iteration with a learning-rate update).
+LR_MILESTONES = (30, 40, 50)
+
+
+def lr_at(epoch, base=LR, milestones=LR_MILESTONES, factor=0.1):
+    """Learning rate of an epoch under the step schedule of Sec. 4."""
+    return base * factor ** sum(1 for m in milestones if epoch >= m)
 
 
 def _seeded(stream, name):
@@ -235,9 +243,36 @@ class _Trainer:
             self._rec(trace, "sgd", (name, wd), w=w0, v=v0, g=g, w_new=w, v_new=v)
 
     def _quantize(self, trace):
+        if getattr(self, "_codes_current", False):
+            return  # the previous step's fused update already quantised the new weights
         for l in self.two_bit_layers():
             l.quantize()
             self._rec(trace, "quantize", l, w=l.w.clone(), codes=l.codes.clone(), alpha=l.alpha.clone())
+
+    def _update_two_bit(self, trace, layer, g, fused):
+        """SGD on a two-bit layer's real filters; with `fused`, the same pass also
+        quantises the updated filters for the next iteration."""
+        if not fused:
+            self._sgd(trace, layer.name, layer.w, layer.v, g, WEIGHT_DECAY)
+            return
+        if trace is not None:
+            w0, v0 = layer.w.clone(), layer.v.clone()
+        layer.codes, layer.alpha, _ = tbn.sgd_step_quantize(layer.w, layer.v, g, self.lr, MOMENTUM, WEIGHT_DECAY,
+                                                            codes=layer.codes, alpha=layer.alpha,
+                                                            want_counts=False)
+        if trace is not None:
+            self._rec(trace, "sgd_quantize", (layer.name, WEIGHT_DECAY), w=w0, v=v0, g=g, w_new=layer.w,
+                      v_new=layer.v, codes=layer.codes.clone(), alpha=layer.alpha.clone())
+
+    def train(self, x, labels, iterations, iters_per_epoch=None, fused=True):
+        """Algorithm 1 run for `iterations` iterations on one batch, the learning rate set
+        by the Sec. 4 schedule (epochs of `iters_per_epoch` iterations, default: one
+        epoch per iteration).  Returns the loss of every iteration (fp32 tensor)."""
+        losses = []
+        for it in range(iterations):
+            self.lr = lr_at(it // (iters_per_epoch or 1))
+            losses.append(self.step(x, labels, fused=fused))
+        return torch.cat([l.view(1) for l in losses])
 
 
 class LeNet(_Trainer):
@@ -268,8 +303,10 @@ class LeNet(_Trainer):
         """Forward, backward-data (not for the first layer) and backward-weight."""
         return 3 * LeNet.flops(batch) - 2 * batch * 28 * 28 * 32 * 25
 
-    def step(self, x, labels, trace=None):
-        """x [N][28][28][1] bf16, labels [N] int32 -> loss (fp32 [1]); updates the weights."""
+    def step(self, x, labels, trace=None, fused=False):
+        """x [N][28][28][1] bf16, labels [N] int32 -> loss (fp32 [1]); updates the weights.
+        `fused`: update and re-quantise each two-bit layer in one pass (the next step then
+        skips its quantisation)."""
         rec = self._rec
         N = x.shape[0]
         self._quantize(trace)
@@ -307,7 +344,8 @@ class LeNet(_Trainer):
         _, dw1 = self.conv1.backward(x, dz1, need_dx=False)
         rec(trace, "conv_bwd", self.conv1, x=x, dy=dz1, dx=None, dw=dw1)
         for l, g in zip(self.two_bit_layers(), (dw1, dw2, dw3, dw4)):
-            self._sgd(trace, l.name, l.w, l.v, g.view(l.w.shape), WEIGHT_DECAY)
+            self._update_two_bit(trace, l, g.view(l.w.shape), fused)
+        self._codes_current = fused
         return loss
 
 
@@ -347,8 +385,9 @@ class VGGSmall(_Trainer):
         """Forward, backward-data (not for the first layer) and backward-weight."""
         return 3 * VGGSmall.flops(batch) - 2 * batch * 32 * 32 * 128 * 27
 
-    def step(self, x, labels, trace=None):
-        """x [N][32][32][3] bf16, labels [N] int32 -> loss (fp32 [1]); updates the weights."""
+    def step(self, x, labels, trace=None, fused=False):
+        """x [N][32][32][3] bf16, labels [N] int32 -> loss (fp32 [1]); updates the weights.
+        `fused`: update and re-quantise each two-bit layer in one pass."""
         rec = self._rec
         N = x.shape[0]
         self._quantize(trace)
@@ -392,8 +431,12 @@ class VGGSmall(_Trainer):
             rec(trace, "conv_bwd", conv, x=hin, dy=dzi, dx=dh, dw=dw)
             grads[i], bn_grads[i] = dw, (dg, db)
         for conv, g in zip(self.convs, grads):
-            self._sgd(trace, conv.name, conv.w, conv.v, g.view(conv.w.shape), WEIGHT_DECAY)
-        self._sgd(trace, self.fc.name, self.fc.w, self.fc.v, dwfc.view(self.fc.w.shape), WEIGHT_DECAY)
+            if isinstance(conv, TwoBitLayer):
+                self._update_two_bit(trace, conv, g.view(conv.w.shape), fused)
+            else:
+                self._sgd(trace, conv.name, conv.w, conv.v, g.view(conv.w.shape), WEIGHT_DECAY)
+        self._update_two_bit(trace, self.fc, dwfc.view(self.fc.w.shape), fused)
+        self._codes_current = fused
         for bn, (dg, db) in zip(self.bns, bn_grads):
             self._sgd(trace, bn.name + ".gamma", bn.gamma, bn.vg, dg, 0.0)
             self._sgd(trace, bn.name + ".beta", bn.beta, bn.vb, db, 0.0)

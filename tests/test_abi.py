@@ -71,6 +71,9 @@ def test_argument_errors_before_launch():
     # shape errors
     assert lib.tbn_quantize(good, 0, 4, good, good, None, None) == 2
     assert lib.tbn_sgd_step(good, good, good, 0, 0.1, 0.9, 0.0, None) == 2
+    assert lib.tbn_sgd_step_quantize(good, good, good, 0, 4, 0.1, 0.9, 0.0, good, good, None, None) == 2
+    assert lib.tbn_sgd_step_quantize(good, good, good, 4, 4, 0.1, 0.9, 0.0, bad, good, None, None) == 4
+    assert lib.tbn_sgd_step_quantize(good, None, good, 4, 4, 0.1, 0.9, 0.0, good, good, None, None) == 1
     # stride-2 backward-data is not implemented
     d2 = tbn.ConvDesc(1, 8, 8, 8, 8, 3, 3, 2, 1)
     assert lib.tbn_conv2d_bwd_data(ctypes.byref(d2), good, good, good, good, 0, good, 1 << 20, None) == 3

@@ -102,6 +102,51 @@ def test_quantize_parity(tbn, K, n, dist):
     log("  alpha ulp max %d, exact %d/%d" % (d.max(), int((d == 0).sum()), K))
 
 
+SQCASES = [(1, 1), (3, 5), (70, 2341), (256, 2304), (512, 3136)]
+
+
+@pytest.mark.parametrize("K,n", SQCASES)
+def test_sgd_step_quantize_parity(tbn, K, n):
+    """Update fused with the next quantisation: the weights and momentum equal the
+    standalone SGD call and the fp32 oracle bit for bit; codes, counts and alpha equal the
+    standalone quantiser and the oracle's quantisation of the updated weights."""
+    log("sgd_step_quantize K=%d n=%d" % (K, n))
+    w = synth.normal(1, "sq_w%d_%d" % (K, n), (K, n), 1.0)
+    v = synth.normal(1, "sq_v%d_%d" % (K, n), (K, n), 0.5)
+    g = synth.normal(1, "sq_g%d_%d" % (K, n), (K, n), 1.0)
+    lr, mu, wd = 0.5, 0.5, 0.25
+    if K * n >= 4:
+        # elements whose exact update lands on the thresholds of Eq. (3): w_new = 1, 0, -1
+        w.flat[:3] = [1.5, 0.5, -0.5]
+        v.flat[:3] = [0.25, 0.25, 0.25]
+        g.flat[:3] = [0.5, 0.75, 1.0]
+    wf, vf = to_dev(w), to_dev(v)
+    gd = to_dev(g)
+    codes_f, alpha_f, counts_f = tbn.sgd_step_quantize(wf, vf, gd, lr, mu, wd)
+    ws, vs = to_dev(w), to_dev(v)
+    tbn.sgd_step(ws, vs, gd, lr, mu, wd)
+    codes_s, alpha_s, counts_s = tbn.quantize(ws)
+    torch.cuda.synchronize()
+    w_new, v_new = wf.cpu().numpy(), vf.cpu().numpy()
+    assert np.array_equal(w_new.view(np.int32), ws.cpu().numpy().view(np.int32)), "w differs from sgd_step"
+    assert np.array_equal(v_new.view(np.int32), vs.cpu().numpy().view(np.int32)), "v differs from sgd_step"
+    assert np.array_equal(words_np(codes_f), words_np(codes_s))
+    assert np.array_equal(alpha_f.cpu().numpy().view(np.int32), alpha_s.cpu().numpy().view(np.int32))
+    assert np.array_equal(counts_f.cpu().numpy(), counts_s.cpu().numpy())
+    w_o, v_o = oracle.sgd_f32(w, v, g, lr, mu, wd)
+    assert np.array_equal(w_new.ravel().view(np.int32), w_o.view(np.int32)), "w differs from the fp32 oracle"
+    assert np.array_equal(v_new.ravel().view(np.int32), v_o.view(np.int32)), "v differs from the fp32 oracle"
+    if K * n >= 4:
+        assert list(w_o[:3]) == [1.0, 0.0, -1.0]
+    q = oracle.quantize(w_o.reshape(K, n))
+    assert np.array_equal(words_np(codes_f), oracle.pack(q.codes)), "packed codes differ"
+    assert np.array_equal(counts_f.cpu().numpy(), np.stack([q.b1_size, q.b2_size], 1))
+    d = ulp_diff(alpha_f.cpu().numpy(), q.alpha)
+    assert d.max() <= 1, "alpha differs by %d ulp" % d.max()
+    w64, _ = oracle.sgd(w, v, g, lr, mu, wd)
+    assert nerr(w_new.ravel(), w64) <= 1e-6
+
+
 def test_quantize_bit_pattern_sweep(tbn):
     # Every fp32 sign/exponent/top-7-fraction pattern with 16 low-fraction variants:
     # 2^16 * 16 values, finite ones compared with the oracle; NaN -> code -1 by contract.

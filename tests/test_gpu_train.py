@@ -37,10 +37,11 @@ def _odesc(layer, x, n=None):
 
 
 class Checker:
-    def __init__(self, imgs, dw_samples):
+    def __init__(self, imgs, dw_samples, lr=0.1, q=None):
         self.imgs = imgs
         self.dw_samples = dw_samples
-        self.q = {}       # layer name -> oracle quantisation used by this step
+        self.lr = lr
+        self.q = dict(q or {})  # layer name -> oracle quantisation used by this step
         self.worst = {}
 
     def note(self, kind, e):
@@ -154,6 +155,21 @@ class Checker:
         assert nerr(t["v_new"].cpu().numpy().ravel(), np.ravel(v_ref)) <= 1e-6, name
 
 
+    def sgd_quantize(self, info, t):
+        # the update fused with the next quantisation: weights and momentum to the fp32
+        # oracle bit for bit, codes of the updated weights bit-exact, alpha within 1 ulp
+        name, wd = info
+        w_ref, v_ref = oracle.sgd_f32(t["w"].cpu().numpy(), t["v"].cpu().numpy(), t["g"].cpu().numpy(),
+                                      self.lr, 0.9, wd)
+        w_new = t["w_new"].cpu().numpy()
+        assert np.array_equal(w_new.ravel().view(np.int32), w_ref.view(np.int32)), name
+        assert np.array_equal(t["v_new"].cpu().numpy().ravel().view(np.int32), v_ref.view(np.int32)), name
+        q = oracle.quantize(w_new.reshape(w_new.shape[0], -1))
+        assert np.array_equal(t["codes"].cpu().numpy().view(np.uint32), oracle.pack(q.codes)), name
+        assert ulp_diff(t["alpha"].cpu().numpy(), q.alpha).max() <= 1, name
+        self.q[name] = q  # the codes the next iteration runs on
+
+
 def _run(net, x, labels, imgs, dw_samples):
     trace = []
     loss = net.step(x, labels, trace)
@@ -202,3 +218,59 @@ def test_vgg_small_step_batch128_sampled(tbn):
     imgs = [int(i) for i in synth.sample_indices(3, "imgs", 128, 2)[:2]]
     loss, worst, n = _run(net, x, lab, imgs, 1024)
     log("vgg-small batch 128 images %s: %d ops checked, loss %.4f, worst %s" % (imgs, n, loss, worst))
+
+
+def test_lenet_fused_update_steps_checked(tbn):
+    """Two iterations with the update fused into the next quantisation: every operation is
+    checked as above, and the second iteration runs on the codes the first one's fused
+    update produced (there is no separate quantisation)."""
+    from paper_1701_00485_amd.networks import LeNet
+    net = LeNet()
+    x, lab = _lenet_batch(256, "256")
+    imgs = [int(i) for i in synth.sample_indices(2, "imgs", 256, 4)[:2]]
+    q = None
+    for it in range(2):
+        trace = []
+        loss = net.step(x, lab, trace, fused=True)
+        torch.cuda.synchronize()
+        kinds = [k for k, _, _ in trace]
+        assert kinds.count("quantize") == (4 if it == 0 else 0)
+        assert kinds.count("sgd_quantize") == 4
+        chk = Checker(imgs, 1024, lr=net.lr, q=q)
+        chk.run(trace)
+        q = chk.q
+        log("lenet fused step %d: loss %.4f, worst %s" % (it, float(loss.item()), chk.worst))
+
+
+def test_lenet_fused_and_separate_updates_agree(tbn):
+    """The fused update-and-quantise pass gives bit-identical training to SGD followed by a
+    separate quantisation: same losses, weights and codes after three iterations."""
+    from paper_1701_00485_amd.networks import LeNet
+    x, lab = _lenet_batch(256, "256")
+    a, b = LeNet(), LeNet()
+    la = [float(a.step(x, lab, fused=False).item()) for _ in range(3)]
+    lb = [float(b.step(x, lab, fused=True).item()) for _ in range(3)]
+    a._quantize(None)  # b's codes are already those of its updated weights
+    torch.cuda.synchronize()
+    assert la == lb, (la, lb)
+    for la_, lb_ in zip(a.two_bit_layers(), b.two_bit_layers()):
+        assert torch.equal(la_.w, lb_.w) and torch.equal(la_.v, lb_.v), la_.name
+        assert torch.equal(la_.codes, lb_.codes) and torch.equal(la_.alpha, lb_.alpha), la_.name
+
+
+def test_lenet_training_loss_curve(tbn):
+    """Algorithm 1 for 60 iterations on one synthetic batch with the Sec. 4 step schedule
+    (one iteration per epoch: the rate drops tenfold at 30, 40 and 50).  The loss curve is
+    reported; the loss must fall steadily and stay finite.
+    Beyond the per-operation checks this is parity unpinned: no reference curve exists."""
+    from paper_1701_00485_amd.networks import LeNet, lr_at
+    net = LeNet()
+    x, lab = _lenet_batch(256, "curve")
+    losses = net.train(x, lab, 60).cpu().numpy()
+    log("lenet loss curve (every 5th): %s" % np.array2string(losses[::5], precision=3))
+    assert np.all(np.isfinite(losses))
+    assert net.lr == pytest.approx(lr_at(59))
+    # the loss falls: every 10-iteration mean below the previous one, 0.1 below the start
+    means = losses.reshape(6, 10).mean(axis=1)
+    assert np.all(np.diff(means) < 0), means
+    assert losses[-5:].mean() < losses[0] - 0.1, losses

@@ -219,3 +219,33 @@ def test_dense_fwd_with_approximate_filters_equals_two_bit_fwd():
     wd = q.alpha64[:, None] * q.codes.astype(np.float64)
     y = oracle.conv_fwd_dense(desc, x, wd)
     assert np.allclose(y, oracle.conv_fwd(desc, x, q.codes, q.alpha64, form=2), rtol=0, atol=1e-13)
+
+
+def test_sgd_f32_hand_step_exact():
+    # every product and sum below is exact in fp32, so the fused form must land on it:
+    # v = 0.5 * 0.25 + (0.5 + 0.25 * 1.5) = 1.0;  w = 1.5 - 0.5 * 1.0 = 1.0
+    w, v = oracle.sgd_f32([1.5], [0.25], [0.5], 0.5, 0.5, 0.25)
+    assert v[0] == 1.0 and w[0] == 1.0
+    assert w.dtype == np.float32
+
+
+def test_sgd_f32_single_rounding_per_fused_op():
+    # Each update line is one fused multiply-add: round(a * b + c) once.  Extended
+    # precision holds a fp32 product exactly (48 bits) and the sum to 64 bits, so rounding
+    # that to fp32 reproduces the single rounding for these inputs.
+    n = 20000
+    w0 = synth.normal(0, "sgdf32w", (n,), 1.0)
+    v0 = synth.normal(0, "sgdf32v", (n,), 0.3)
+    g0 = synth.normal(0, "sgdf32g", (n,), 1.0)
+    lr, mu, wd = np.float32(0.1), np.float32(0.9), np.float32(1e-4)
+    w, v = oracle.sgd_f32(w0, v0, g0, float(lr), float(mu), float(wd))
+    L = np.longdouble
+    assert np.finfo(L).nmant >= 63
+    inner = (L(wd) * w0.astype(L) + g0.astype(L)).astype(np.float32)
+    v_ref = (L(mu) * v0.astype(L) + inner.astype(L)).astype(np.float32)
+    w_ref = (-L(lr) * v_ref.astype(L) + w0.astype(L)).astype(np.float32)
+    assert np.array_equal(v.view(np.int32), v_ref.view(np.int32))
+    assert np.array_equal(w.view(np.int32), w_ref.view(np.int32))
+    # and it is the fp64 step up to fp32 rounding
+    w64, v64 = oracle.sgd(w0, v0, g0, float(lr), float(mu), float(wd))
+    assert np.max(np.abs(w - w64)) <= 4 * np.finfo(np.float32).eps * np.max(np.abs(w64))

@@ -89,3 +89,10 @@ def test_softmax_xent_matches_torch():
     lt.backward()
     assert loss == pytest.approx(lt.item(), rel=1e-13)
     assert np.allclose(dz, zt.grad.numpy(), rtol=1e-12, atol=1e-15)
+
+
+def test_learning_rate_schedule():
+    # Sec. 4: 0.1, divided by 10 at epochs 30, 40 and 50
+    from paper_1701_00485_amd.networks import lr_at
+    assert [lr_at(e) for e in (0, 29, 30, 39, 40, 49, 50, 57)] == pytest.approx(
+        [0.1, 0.1, 0.01, 0.01, 1e-3, 1e-3, 1e-4, 1e-4])
