@@ -481,6 +481,9 @@ def main():
         result["small_workloads"] = small_configs(dev)
         result["weight_streaming"] = weight_streaming(dev)
         result["fused_update_quantize"] = fused_update(dev)
+    from paper_1701_00485_amd import memory
+    result["model_size"] = {k: {f: v[f] for f in ("params", "fp64_bytes", "tbn_bytes", "fp64_over_tbn")}
+                            for k, v in memory.memory_table().items()}
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
     print(json.dumps(result), flush=True)
