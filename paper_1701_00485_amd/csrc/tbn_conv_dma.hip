@@ -146,12 +146,14 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
         er = rs / a.S;
         es = rs - er * a.S;
     }
-    // code block of this wave (waves < NBLK copy one 1 KiB block per stage)
-    const int fb = n0 / 64 + wave;
-    const bool copies_codes = wave < NBLK;
+    // code block of this wave: wave w copies the 1 KiB block w % NBLK of each stage (with
+    // fewer than four blocks some waves copy the same block into the same place, identical
+    // bytes), so that every wave issues the same number of DMAs per stage and the waits
+    // below are compile-time counts
+    const int cblk = wave % NBLK;
+    const int fb = n0 / 64 + cblk;
     const bool codes_valid = fb < KB;
-    const bool copies_pairs = BWD && wave == 0;
-    const int dmas = AR + (copies_codes ? 1 : 0) + (copies_pairs ? 1 : 0);  // per stage, this wave
+    constexpr int DMAS = AR + 1 + (BWD ? 1 : 0);  // per stage, every wave
 
     auto issue = [&](int chunk) {
         const uint32_t st = smem_base + (uint32_t)(((chunk - c_begin) % STAGES) * L::BYTES);
@@ -205,16 +207,15 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
                 }
             }
         }
-        if (copies_codes) {
+        {
             const uint32_t off = codes_valid ? (uint32_t)(((int64_t)fb * nchunks + chunk) * 1024 + lane * 16)
                                              : 0x80000000u;
-            dma_b128(rs_c, st + L::B + (uint32_t)(wave * 1024), off);
+            dma_b128(rs_c, st + L::B + (uint32_t)(cblk * 1024), off);
         }
         if constexpr (BWD) {
-            if (copies_pairs) {
-                const uint32_t off = lane < 32 ? (uint32_t)(chunk * 128 + lane * 4) : 0x80000000u;
-                dma_b32(rs_p, st + L::P, off);
-            }
+            // the stage's 32 bf16 scale pairs (every wave writes the same 128 bytes)
+            const uint32_t off = lane < 32 ? (uint32_t)(chunk * 128 + lane * 4) : 0x80000000u;
+            dma_b32(rs_p, st + L::P, off);
         }
     };
 
@@ -245,9 +246,12 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
     for (int c = 0; c < STAGES - 1; ++c)
         if (c < nloc) issue(c_begin + c);
     for (int il = 0; il < nloc; ++il) {
-        // this wave's DMAs of stage il landed (later stages may still be in flight)
-        const int later = min(nloc - 1 - il, STAGES - 2);
-        wait_vmcnt(later * dmas);
+        // this wave's DMAs of stage il landed (later stages may still be in flight; in the
+        // last stages simply everything)
+        if (il + STAGES - 2 < nloc)
+            wait_vmcnt((STAGES - 2) * DMAS);
+        else
+            wait_vmcnt(0);
         __syncthreads();  // ... and every other wave's; all reads of stage il-1 are done
         if (il + STAGES - 1 < nloc) issue(c_begin + il + STAGES - 1);  // into stage il-1's buffer
         const uint8_t* st = smem + (il % STAGES) * L::BYTES;

@@ -76,7 +76,9 @@ __device__ __forceinline__ uint32_t load_patch(const ConvGemmArgs& a, const uint
     return okmask;
 }
 
-template <int CP, bool X32>
+// TT: 16-element reduction steps per filter row (T / 16), so that the reduction loop is
+// one flat, unrolled sequence whose operand reads run one step ahead of the MFMAs.
+template <int CP, bool X32, int TT>
 __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, const ThinGeom g) {
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
     uint16_t* wl = reinterpret_cast<uint16_t*>(lds + g.w_off);  // [FB][WPITCH]
@@ -210,21 +212,32 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
                 for (int v = 0; v < 16; ++v) acc[u][t][v] = 0.0f;
         const uint16_t* abase = cur + ((wave * a.sh) * g.PW + l32 * a.sw) * CP + 8 * half;
         const int arow4 = 4 * a.sh * g.PW * CP;  // patch offset of output row + 4
+        const int arowr = g.PW * CP;             // patch offset of filter row r + 1
         const uint16_t* bbase = wl + l32 * g.WPITCH + 8 * half;
-        for (int r = 0; r < R; ++r) {
-            const uint16_t* ar = abase + r * g.PW * CP;
-            const uint16_t* br = bbase + r * g.T;
-            for (int t0 = 0; t0 < g.T; t0 += 16) {
-                const bf16x8 a0 = load8<CP>(ar + t0);
-                const bf16x8 a1 = load8<CP>(ar + arow4 + t0);
-                const bf16x8 b0 = *reinterpret_cast<const bf16x8*>(br + t0);
-                const bf16x8 b1 = *reinterpret_cast<const bf16x8*>(br + 32 * g.WPITCH + t0);
-                acc[0][0] = mfma32(b0, a0, acc[0][0]);
-                acc[0][1] = mfma32(b1, a0, acc[0][1]);
-                acc[1][0] = mfma32(b0, a1, acc[1][0]);
-                acc[1][1] = mfma32(b1, a1, acc[1][1]);
+        // flat reduction steps j = r * TT + t (16 elements each); the filters are contiguous
+        // in j, the patch advances a row every TT steps
+        const int J = R * TT;
+        bf16x8 a0 = load8<CP>(abase), a1 = load8<CP>(abase + arow4);
+        bf16x8 b0 = *reinterpret_cast<const bf16x8*>(bbase);
+        bf16x8 b1 = *reinterpret_cast<const bf16x8*>(bbase + 32 * g.WPITCH);
+        for (int j = 0; j < J; ++j) {
+            const bf16x8 ca0 = a0, ca1 = a1, cb0 = b0, cb1 = b1;
+            if (j + 1 < J) {
+                const int jn = j + 1;
+                const uint16_t* an = abase + (jn / TT) * arowr + 16 * (jn % TT);
+                a0 = load8<CP>(an);
+                a1 = load8<CP>(an + arow4);
+                b0 = *reinterpret_cast<const bf16x8*>(bbase + 16 * jn);
+                b1 = *reinterpret_cast<const bf16x8*>(bbase + 32 * g.WPITCH + 16 * jn);
             }
+            acc[0][0] = mfma32(cb0, ca0, acc[0][0]);
+            acc[0][1] = mfma32(cb1, ca0, acc[0][1]);
+            acc[1][0] = mfma32(cb0, ca1, acc[1][0]);
+            acc[1][1] = mfma32(cb1, ca1, acc[1][1]);
         }
+        // the next tile's patch goes to the other buffer now: its loads were issued before
+        // the MFMAs, and waiting for them here does not also wait for this tile's stores
+        if (more) write_patch(nxt, pv, okm);
 
         // ---- epilogue: lane holds pixel l32 and filters 32 t + 8 g + 4 half + 0..3 ----
 #pragma unroll
@@ -278,7 +291,6 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
                 }
             }
         }
-        if (more) write_patch(nxt, pv, okm);
         __syncthreads();  // the next patch is complete; every wave is done with this one
     }
 }
@@ -316,7 +328,7 @@ bool conv_thin_plan(const ConvGemmArgs& a, ThinGeom* g) {
     t.div_rowlen = make_fastdiv((uint32_t)t.rowlen);
     t.div_c = make_fastdiv((uint32_t)a.C);
     const int64_t xelems = (int64_t)a.N * a.H * a.W * a.C;
-    if (t.lds_bytes > 96 * 1024 || a.R > 64 || nb * 1024 > 4 * 32 * SPITCH * 4 || t.ept > kElemsPerThread ||
+    if (t.lds_bytes > 96 * 1024 || a.R > 64 || t.T > 128 || nb * 1024 > 4 * 32 * SPITCH * 4 || t.ept > kElemsPerThread ||
         t.PH * t.PW * t.CP >= 0xFFFF || t.PH > 63 || t.PW > 1023 || xelems >= 0x7FFFFFFF)
         return false;
     t.tiles_p = (a.P + TP - 1) / TP;
@@ -328,14 +340,16 @@ bool conv_thin_plan(const ConvGemmArgs& a, ThinGeom* g) {
 
 hipError_t launch_conv_thin(const ConvGemmArgs& a, const ThinGeom& g, hipStream_t stream) {
     const bool x32 = a.x_f32 != 0;
-    const void* fn = x32 ? (g.CP == 1 ? reinterpret_cast<const void*>(&conv_thin_kernel<1, true>)
-                            : g.CP == 2 ? reinterpret_cast<const void*>(&conv_thin_kernel<2, true>)
-                            : g.CP == 4 ? reinterpret_cast<const void*>(&conv_thin_kernel<4, true>)
-                                        : reinterpret_cast<const void*>(&conv_thin_kernel<8, true>))
-                         : (g.CP == 1 ? reinterpret_cast<const void*>(&conv_thin_kernel<1, false>)
-                            : g.CP == 2 ? reinterpret_cast<const void*>(&conv_thin_kernel<2, false>)
-                            : g.CP == 4 ? reinterpret_cast<const void*>(&conv_thin_kernel<4, false>)
-                                        : reinterpret_cast<const void*>(&conv_thin_kernel<8, false>));
+    const int tt = g.T / 16;
+    const void* fn = nullptr;
+#define TBN_THIN_PICK(cp, x, t) \
+    if (g.CP == cp && x32 == x && tt == t) fn = reinterpret_cast<const void*>(&conv_thin_kernel<cp, x, t>);
+#define TBN_THIN_PICK_T(cp, x) TBN_THIN_PICK(cp, x, 1) TBN_THIN_PICK(cp, x, 2) TBN_THIN_PICK(cp, x, 4) TBN_THIN_PICK(cp, x, 8)
+    TBN_THIN_PICK_T(1, true) TBN_THIN_PICK_T(2, true) TBN_THIN_PICK_T(4, true) TBN_THIN_PICK_T(8, true)
+    TBN_THIN_PICK_T(1, false) TBN_THIN_PICK_T(2, false) TBN_THIN_PICK_T(4, false) TBN_THIN_PICK_T(8, false)
+#undef TBN_THIN_PICK_T
+#undef TBN_THIN_PICK
+    if (!fn) return hipErrorInvalidValue;
     if (g.lds_bytes > 65536 &&
         hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, g.lds_bytes) != hipSuccess)
         return hipErrorInvalidConfiguration;
@@ -350,25 +364,10 @@ hipError_t launch_conv_thin(const ConvGemmArgs& a, const ThinGeom& g, hipStream_
     int64_t cap = (int64_t)per_cu * cus / kb;
     if (cap < 1) cap = 1;
     const dim3 grid((unsigned)(g.ntiles < cap ? g.ntiles : cap), (unsigned)kb);
-#define TBN_THIN_LAUNCH(cp, x)                                                                       \
-    hipLaunchKernelGGL((conv_thin_kernel<cp, x>), grid, dim3(256), g.lds_bytes, stream, a, g)
-    if (x32) {
-        switch (g.CP) {
-            case 1: TBN_THIN_LAUNCH(1, true); break;
-            case 2: TBN_THIN_LAUNCH(2, true); break;
-            case 4: TBN_THIN_LAUNCH(4, true); break;
-            default: TBN_THIN_LAUNCH(8, true); break;
-        }
-    } else {
-        switch (g.CP) {
-            case 1: TBN_THIN_LAUNCH(1, false); break;
-            case 2: TBN_THIN_LAUNCH(2, false); break;
-            case 4: TBN_THIN_LAUNCH(4, false); break;
-            default: TBN_THIN_LAUNCH(8, false); break;
-        }
-    }
-#undef TBN_THIN_LAUNCH
-    return hipGetLastError();
+    ConvGemmArgs ka = a;
+    ThinGeom kg = g;
+    void* args[] = {&ka, &kg};
+    return hipLaunchKernel(fn, grid, dim3(256), args, (size_t)g.lds_bytes, stream);
 }
 
 }  // namespace tbn

@@ -194,6 +194,8 @@ CONV_CASES = [
     (2, 9, 9, 2, 16, 3, 3, 1, 0),           # 2 channels, no padding
     (1, 1, 1, 16, 8, 3, 3, 1, 1),           # 1x1 image under a 3x3 window: only the centre tap
     (2, 5, 5, 8, 1, 3, 3, 1, 1),            # a single filter
+    (2, 20, 24, 3, 20, 5, 11, 1, 2),        # C = 3, 11 taps per filter row (64-element rows)
+    (1, 12, 12, 7, 16, 3, 9, 1, 1),         # C = 7, 9 taps per row (128-element rows)
 ]
 
 
