@@ -125,12 +125,16 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
     int er = 0, es = 0, ec = 0;
     // uniform path: (r, s) and first channel of the next stage (the same for every lane)
     int ur = 0, us = 0, uc = 0;
-    int32_t rb2[AR];        // uniform path: row offset plus this lane's channel offset
+    // uniform path, kept incrementally: utap = r * S + s, utoff2 = byte offset of (r, s, c0)
+    // relative to a row's (h0, w0) = 2 * ((r * W + s) * C + c0)
+    int utap = 0;
+    uint32_t utoff2 = 0;
+    uint32_t rb2s[AR];      // uniform path: byte offset of the row plus this lane's segment
     uint32_t nmask[AR][2];  // uniform path: complement of rmask (bit set = tap outside)
     if constexpr (UNI) {
 #pragma unroll
         for (int j = 0; j < AR; ++j) {
-            rb2[j] = rbase[j] + 8 * lseg;
+            rb2s[j] = (uint32_t)(rbase[j] + 8 * lseg) << 1;
             nmask[j][0] = ~rmask[j][0];
             nmask[j][1] = ~rmask[j][1];
         }
@@ -139,6 +143,8 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
         uc = e0 - rs * C;
         ur = rs / a.S;
         us = rs - ur * a.S;
+        utap = rs;
+        utoff2 = (uint32_t)((ur * a.W + us) * C + uc) << 1;
     } else {
         const int e0 = c_begin * BK + lseg * 8;
         const int rs = e0 / C;
@@ -155,35 +161,39 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
     const bool codes_valid = fb < KB;
     constexpr int DMAS = AR + 1 + (BWD ? 1 : 0);  // per stage, every wave
 
+    const uint32_t row_step2 = (uint32_t)((a.W - a.S) * C) << 1;  // next filter row, in bytes
+    int islot = 0;  // ring slot of the next stage to issue
     auto issue = [&](int chunk) {
-        const uint32_t st = smem_base + (uint32_t)(((chunk - c_begin) % STAGES) * L::BYTES);
+        const uint32_t st = smem_base + (uint32_t)(islot * L::BYTES);
+        islot = islot + 1 == STAGES ? 0 : islot + 1;
         if constexpr (UNI) {
             // out-of-image taps (and the padding stage past the filter, tap clamped to
             // bit 63, which is clear in rmask because R*S <= 63) get offset bit 31 set,
             // beyond the buffer, so the hardware returns zeros
-            const int tap = min(ur * a.S + us, 63);
-            const int32_t toff = (ur * a.W + us) * C + uc;
+            const int tap = min(utap, 63);
             if (tap < 32) {
 #pragma unroll
                 for (int j = 0; j < AR; ++j) {
-                    const uint32_t out = (nmask[j][0] >> tap) & 1u;
-                    dma_b128(rs_x, st + L::A + (uint32_t)(8 * (wave + 4 * j) * ROWB),
-                             ((uint32_t)(rb2[j] + toff) << 1) | (out << 31));
+                    const uint32_t out = (nmask[j][0] << (31 - tap)) & 0x80000000u;
+                    dma_b128(rs_x, st + L::A + (uint32_t)(8 * (wave + 4 * j) * ROWB), (rb2s[j] + utoff2) | out);
                 }
             } else {
 #pragma unroll
                 for (int j = 0; j < AR; ++j) {
-                    const uint32_t out = (nmask[j][1] >> (tap - 32)) & 1u;
-                    dma_b128(rs_x, st + L::A + (uint32_t)(8 * (wave + 4 * j) * ROWB),
-                             ((uint32_t)(rb2[j] + toff) << 1) | (out << 31));
+                    const uint32_t out = (nmask[j][1] << (63 - tap)) & 0x80000000u;
+                    dma_b128(rs_x, st + L::A + (uint32_t)(8 * (wave + 4 * j) * ROWB), (rb2s[j] + utoff2) | out);
                 }
             }
+            // next stage: 64 channels on; past the last channel the next tap (s + 1), past
+            // the last tap of a filter row the first tap of the next row
             uc += BK;
+            utoff2 += 2 * BK;
             if (uc == C) {
                 uc = 0;
+                ++utap;
                 if (++us == a.S) {
                     us = 0;
-                    ++ur;
+                    utoff2 += row_step2;
                 }
             }
         } else {
@@ -245,6 +255,7 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
 #pragma unroll
     for (int c = 0; c < STAGES - 1; ++c)
         if (c < nloc) issue(c_begin + c);
+    int cslot = 0;  // ring slot of the stage being multiplied
     for (int il = 0; il < nloc; ++il) {
         // this wave's DMAs of stage il landed (later stages may still be in flight; in the
         // last stages simply everything)
@@ -254,7 +265,8 @@ __global__ __launch_bounds__(256, 2) void conv_dma_kernel(const ConvGemmArgs a) 
             wait_vmcnt(0);
         __syncthreads();  // ... and every other wave's; all reads of stage il-1 are done
         if (il + STAGES - 1 < nloc) issue(c_begin + il + STAGES - 1);  // into stage il-1's buffer
-        const uint8_t* st = smem + (il % STAGES) * L::BYTES;
+        const uint8_t* st = smem + cslot * L::BYTES;
+        cslot = cslot + 1 == STAGES ? 0 : cslot + 1;
         u32x4 braw[TN];
 #pragma unroll
         for (int t = 0; t < TN; ++t) braw[t] = *reinterpret_cast<const u32x4*>(st + L::B + bcol + 32 * 16 * t);
