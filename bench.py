@@ -318,7 +318,8 @@ def fused_update(dev, reps=20):
     """The update step fused with the next quantisation (one pass over the real weights:
     12 B read + 8.25 B written per weight) against SGD followed by a separate quantisation
     (16 B read + 8.25 B written), on the training layer and on a 4096 x 4608 filter set
-    (18.9 M weights, larger than the last-level cache)."""
+    (18.9 M weights, larger than the last-level cache); also the stochastic discretisation
+    (weights and uniform numbers read, 8 B, codes written, 0.25 B per weight)."""
     import torch
 
     import paper_1701_00485_amd as tbn
@@ -340,8 +341,14 @@ def fused_update(dev, reps=20):
             tbn.sgd_step(w, v, gr, 1e-6, 0.9, 1e-4)
             tbn.quantize(w, codes, alpha, want_counts=False)
 
+        uni = torch.rand(K, n, device=dev, generator=g)
+
+        def stochastic():
+            tbn.quantize_variant(w, 1.0, uni, codes=codes, alpha=alpha, want_counts=False)
+
         rec = {}
-        for label, fn, byts in (("fused", fused, 20.25), ("separate", separate, 24.25)):
+        for label, fn, byts in (("fused", fused, 20.25), ("separate", separate, 24.25),
+                                ("stochastic_quantize", stochastic, 8.25)):
             for _ in range(3):
                 fn()
             torch.cuda.synchronize()

@@ -113,6 +113,23 @@ tbn_status tbn_quantize(const float* w, int64_t k, int64_t n, uint32_t* codes, f
                         int32_t* counts, hipStream_t stream);
 
 /*
+ * Variants of the discretisation step (Sec. 2 chooses the deterministic rule of Eq. 3 "for
+ * simplicity"; the scale is then the optimum of Eq. 4 for the chosen codes).
+ *   threshold  t > 0 (finite): the magnitude-2 boundary of Eq. 3 moved from 1 to t,
+ *              W~_i = -2 if W_i < -t; -1 if -t <= W_i <= 0; 1 if 0 < W_i <= t; 2 if W_i > t.
+ *              t = 1 with uniform == NULL is exactly tbn_quantize.
+ *   uniform    optional [K][n] fp32 numbers in [0, 1) (NULL = deterministic): stochastic
+ *              discretisation.  a = clamp(W_i, -2, 2); if a > 1: 2 when u < a - 1, else 1;
+ *              if a < -1: -2 when u < -1 - a, else -1; otherwise 1 when 2u < a + 1, else
+ *              -1 (all fp32), so that E[W~_i] = clamp(W_i, -2, 2).  Requires t = 1
+ *              (TBN_ERR_UNSUPPORTED otherwise).
+ *   alpha      sum_i W_i W~_i / sum_i W~_i^2 (fp64 sums, one rounding to fp32): Eq. 5 for the
+ *              deterministic rules.  codes, counts: as tbn_quantize (counts by |W~_i|).
+ */
+tbn_status tbn_quantize_variant(const float* w, int64_t k, int64_t n, float threshold, const float* uniform,
+                                uint32_t* codes, float* alpha, int32_t* counts, hipStream_t stream);
+
+/*
  * Forward pass of a two-bit layer (Sec. 2 Eq. 1, I * (alpha W~) = (alpha I) (+) W~;
  * Algorithm 1, forward step):  y[n,p,q,k] = alpha_k * sum_{r,s,c} x[n, p*sh-ph+r,
  * q*sw-pw+s, c] * W~[k,r,s,c], then the optional epilogue.  The products with the codes

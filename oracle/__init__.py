@@ -72,6 +72,8 @@ def _load():
     lib.orc_conv_bwd_weight_sampled_bf16.restype = ctypes.c_int
     lib.orc_sgd.argtypes = [p, p, p, i64, ctypes.c_double, ctypes.c_double, ctypes.c_double]
     lib.orc_sgd.restype = None
+    lib.orc_quantize_variant.argtypes = [p, i64, i64, ctypes.c_float, p, p, p, p, p, p]
+    lib.orc_quantize_variant.restype = ctypes.c_int
     lib.orc_sgd_f32.argtypes = [p, p, p, i64, ctypes.c_float, ctypes.c_float, ctypes.c_float]
     lib.orc_sgd_f32.restype = None
     lib.orc_maxpool_fwd.argtypes = [p, p, p, p]
@@ -174,6 +176,30 @@ def quantize(w: np.ndarray) -> Quantized:
         raise OracleError("non-finite weight: outside the method's domain")
     if st != 0:
         raise OracleError("quantize: bad shape")
+    return out
+
+
+def quantize_variant(w: np.ndarray, threshold: float = 1.0, uniform=None) -> Quantized:
+    """Discretisation variants: magnitude threshold `threshold`, or stochastic rounding
+    driven by `uniform` ([K][n] fp32 in [0, 1)); alpha = sum W c / sum c^2."""
+    w = _c(w, np.float32)
+    if w.ndim != 2:
+        raise OracleError("quantize_variant expects [K][n]")
+    K, n = w.shape
+    u = None if uniform is None else _c(uniform, np.float32).reshape(K, n)
+    out = Quantized()
+    out.codes = np.zeros((K, n), np.int8)
+    out.alpha64 = np.zeros(K, np.float64)
+    out.alpha = np.zeros(K, np.float32)
+    out.b1_size = np.zeros(K, np.int64)
+    out.b2_size = np.zeros(K, np.int64)
+    st = _load().orc_quantize_variant(_ptr(w), K, n, float(threshold), None if u is None else _ptr(u),
+                                      _ptr(out.codes), _ptr(out.alpha64), _ptr(out.alpha), _ptr(out.b1_size),
+                                      _ptr(out.b2_size))
+    if st == 1:
+        raise OracleError("non-finite weight: outside the method's domain")
+    if st != 0:
+        raise OracleError("quantize_variant: bad shape or threshold")
     return out
 
 

@@ -120,6 +120,66 @@ int orc_quantize(const float* w, int64_t K, int64_t n, int8_t* codes, double* al
     return status;
 }
 
+/* Discretisation variants (Sec. 2 adopts the deterministic rule "for simplicity"):
+ *   threshold t > 0 (uniform == NULL): the rule of Eq. (3) with the magnitude boundary at t
+ *     instead of 1: -2 if W < -t, -1 if -t <= W <= 0, 1 if 0 < W <= t, 2 if W > t;
+ *   uniform != NULL (t must be 1): stochastic rounding of a = clamp(W, -2, 2) to one of its
+ *     two neighbouring levels among {-2, -1, 1, 2}, the upper one with probability equal
+ *     to the distance from the lower one over the gap, so that E[code] = a.  Every decision
+ *     is an fp32 comparison of the given uniform number u in [0, 1).
+ * The scale is the minimiser of J(alpha) = ||W - alpha W~||^2 (Eq. 4) for the chosen codes:
+ * dJ/dalpha = 0 gives alpha = sum_i W_i W~_i / sum_i W~_i^2, which for the deterministic
+ * rules equals Eq. (5).  Sums in fp64 in index order, one rounding to fp32. */
+static int orc_stochastic_one(float w, float u) {
+    float a = fminf(fmaxf(w, -2.0f), 2.0f);
+    if (a > 1.0f) return (u < a - 1.0f) ? 2 : 1;
+    if (a < -1.0f) return (u < -1.0f - a) ? -2 : -1;
+    return (u + u < a + 1.0f) ? 1 : -1;
+}
+
+int orc_quantize_variant(const float* w, int64_t K, int64_t n, float t, const float* uniform,
+                         int8_t* codes, double* alpha64, float* alpha32, int64_t* b1_size,
+                         int64_t* b2_size) {
+    if (K < 0 || n <= 0 || !(t > 0.0f) || (uniform && t != 1.0f)) return ORC_ERR_SHAPE;
+    int status = ORC_OK;
+    for (int64_t k = 0; k < K; ++k) {
+        const float* wk = w + k * n;
+        int finite = 1;
+        for (int64_t i = 0; i < n; ++i)
+            if (!isfinite(wk[i])) finite = 0;
+        if (!finite) {
+            status = ORC_ERR_NONFINITE;
+            continue;
+        }
+        double num = 0.0;
+        int64_t nb1 = 0, nb2 = 0;
+        for (int64_t i = 0; i < n; ++i) {
+            const float x = wk[i];
+            int c;
+            if (uniform) {
+                c = orc_stochastic_one(x, uniform[k * n + i]);
+            } else if (x < -t) {
+                c = -2;
+            } else if (x <= 0.0f) {
+                c = -1;
+            } else if (x <= t) {
+                c = 1;
+            } else {
+                c = 2;
+            }
+            codes[k * n + i] = (int8_t)c;
+            num += (double)x * (double)c;
+            if (c == 2 || c == -2) nb2 += 1; else nb1 += 1;
+        }
+        const double a = num / (double)(nb1 + 4 * nb2);
+        if (alpha64) alpha64[k] = a;
+        if (alpha32) alpha32[k] = (float)a;
+        if (b1_size) b1_size[k] = nb1;
+        if (b2_size) b2_size[k] = nb2;
+    }
+    return status;
+}
+
 /* ------------------------------------------------------------------------------------ */
 /* Two-bit packed storage (this project's format; the paper fixes only that the four     */
 /* values fit in two bits).                                                              */

@@ -7,6 +7,7 @@ call raises; there is no fallback.
 
 Calls (same names as the C ABI, without the ``tbn_`` prefix):
   quantize(w)                      Sec. 2 Eq. (3)-(5)   -> packed codes, alpha, counts
+  quantize_variant(w, threshold, uniform)  other thresholds / stochastic discretisation
   conv2d_fwd(desc, x, codes, alpha) Sec. 2 Eq. (1)       -> y
   conv2d_bwd_data(desc, dy, codes, alpha)  Sec. 3        -> dx
   conv2d_bwd_weight(desc, x, dy)    Sec. 3 (straight-through) -> dW
@@ -77,6 +78,7 @@ def load():
         "tbn_packed_words": ([i64, i64], i64),
         "tbn_workspace_size": ([i32, vp, vp], i32),
         "tbn_quantize": ([vp, i64, i64, vp, vp, vp, vp], i32),
+        "tbn_quantize_variant": ([vp, i64, i64, f32, vp, vp, vp, vp, vp], i32),
         "tbn_conv2d_fwd": ([vp, vp, i32, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_conv2d_fwd_dense": ([vp, vp, i32, vp, vp, vp, i32, vp], i32),
         "tbn_conv2d_bwd_data": ([vp, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
@@ -104,7 +106,7 @@ def load():
 
 def exported_symbols():
     return sorted(["tbn_status_str", "tbn_last_error", "tbn_conv_out_dims", "tbn_packed_words",
-                   "tbn_workspace_size", "tbn_quantize", "tbn_conv2d_fwd", "tbn_conv2d_fwd_dense",
+                   "tbn_workspace_size", "tbn_quantize", "tbn_quantize_variant", "tbn_conv2d_fwd", "tbn_conv2d_fwd_dense",
                    "tbn_conv2d_bwd_data",
                    "tbn_conv2d_bwd_weight", "tbn_sgd_step", "tbn_sgd_step_quantize", "tbn_pool_out_dims", "tbn_maxpool2d_fwd",
                    "tbn_maxpool2d_bwd", "tbn_avgpool_global", "tbn_batchnorm_workspace_size",
@@ -182,6 +184,31 @@ def quantize(w: torch.Tensor, codes=None, alpha=None, counts=None, want_counts=T
     _numel(alpha, K, "alpha")
     pc = _dev(counts, "counts", (torch.int32,)) if counts is not None else None
     _call("tbn_quantize", pw, K, n, _dev(codes, "codes", (torch.int32,)),
+          _dev(alpha, "alpha", (torch.float32,)), pc, _stream())
+    return codes, alpha, counts
+
+
+def quantize_variant(w: torch.Tensor, threshold=1.0, uniform=None, codes=None, alpha=None, counts=None,
+                     want_counts=True):
+    """Discretisation variants: magnitude threshold `threshold` (Eq. 3 has 1), or stochastic
+    discretisation driven by `uniform` ([K][n] fp32 in [0, 1)).  Returns (codes, alpha, counts)."""
+    K = w.shape[0]
+    n = w.numel() // K
+    pw = _dev(w, "w", (torch.float32,))
+    pu = None
+    if uniform is not None:
+        _numel(uniform, K * n, "uniform")
+        pu = _dev(uniform, "uniform", (torch.float32,))
+    if codes is None:
+        codes = torch.empty(packed_words(K, n), dtype=torch.int32, device=w.device)
+    if alpha is None:
+        alpha = torch.empty(K, dtype=torch.float32, device=w.device)
+    if counts is None and want_counts:
+        counts = torch.empty((K, 2), dtype=torch.int32, device=w.device)
+    _numel(codes, packed_words(K, n), "codes")
+    _numel(alpha, K, "alpha")
+    pc = _dev(counts, "counts", (torch.int32,)) if counts is not None else None
+    _call("tbn_quantize_variant", pw, K, n, float(threshold), pu, _dev(codes, "codes", (torch.int32,)),
           _dev(alpha, "alpha", (torch.float32,)), pc, _stream())
     return codes, alpha, counts
 

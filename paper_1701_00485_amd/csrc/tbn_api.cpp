@@ -4,6 +4,7 @@
 
 #include <cstdint>
 #include <cstdio>
+#include <cstring>
 #include <string>
 
 #include "tbn.h"
@@ -183,6 +184,25 @@ tbn_status tbn_quantize(const float* w, int64_t k, int64_t n, uint32_t* codes, f
         return fail(TBN_ERR_ALIGN, "misaligned pointer");
     hipError_t e = tbn::launch_quantize(w, k, n, codes, alpha, counts, stream);
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_quantize");
+}
+
+tbn_status tbn_quantize_variant(const float* w, int64_t k, int64_t n, float threshold, const float* uniform,
+                                uint32_t* codes, float* alpha, int32_t* counts, hipStream_t stream) {
+    if (!w || !codes || !alpha) return fail(TBN_ERR_NULL, "w, codes and alpha are required");
+    if (k <= 0 || n <= 0) return fail(TBN_ERR_SHAPE, "k and n must be positive");
+    if (n > kI32Max || k > kI32Max / 2) return fail(TBN_ERR_SHAPE, "k or n too large");
+    if (!(threshold > 0.0f) || !(threshold < 3.4028235e38f))
+        return fail(TBN_ERR_SHAPE, "threshold must be positive and finite");
+    if (uniform && threshold != 1.0f)
+        return fail(TBN_ERR_UNSUPPORTED, "stochastic discretisation uses the threshold 1");
+    if (!aligned4(w) || !aligned16(codes) || !aligned4(alpha) || (counts && !aligned4(counts)) ||
+        (uniform && !aligned4(uniform)))
+        return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    uint32_t thr_bits;
+    memcpy(&thr_bits, &threshold, 4);
+    hipError_t e = tbn::launch_quantize_variant(w, k, n, tbn::QuantVariant{thr_bits, uniform}, codes, alpha, counts,
+                                                stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_quantize_variant");
 }
 
 tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt, const uint32_t* codes,

@@ -61,6 +61,16 @@ struct SgdArgs {
 hipError_t launch_sgd_quantize(const SgdArgs& sgd, int64_t K, int64_t n, uint32_t* codes, float* alpha,
                                int32_t* counts, hipStream_t stream);
 
+// Discretisation variant: thr_bits = bit pattern of the magnitude threshold t > 0 (1.0f is
+// Eq. 3), uni = per-weight uniform numbers in [0, 1) for stochastic discretisation (null:
+// deterministic).
+struct QuantVariant {
+    uint32_t thr_bits;
+    const float* uni;
+};
+hipError_t launch_quantize_variant(const float* w, int64_t K, int64_t n, const QuantVariant& var, uint32_t* codes,
+                                   float* alpha, int32_t* counts, hipStream_t stream);
+
 hipError_t launch_conv_gemm(const ConvGemmArgs& a, hipStream_t stream);
 
 // LDS-DMA variant (bf16 x, C % 8 == 0, R*S <= 63, x < 2 GiB).  Its plan picks the tile

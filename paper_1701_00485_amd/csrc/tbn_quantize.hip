@@ -44,11 +44,22 @@ __device__ __forceinline__ void sgd_update(float& w, float& v, float g, float lr
 // order through LDS.  With SGD, each element is first updated in place (w, v from their
 // gradient g) and the updated weight is what Eq. (3)-(5) see: the next iteration's
 // quantisation fused into this iteration's update, one pass over the filter.
-template <bool SGD>
+//
+// Variants of the discretisation (Sec. 2 adopts the deterministic rule "for simplicity"):
+//   * threshold t (QuantVariant::thr_bits, the bit pattern of t > 0): |W| > t selects the
+//     magnitude 2 instead of |W| > 1;
+//   * STOCH: stochastic discretisation with caller-supplied uniform numbers u in [0, 1):
+//     W is clamped to [-2, 2] and rounded to one of its two neighbouring levels with the
+//     probabilities that make the expected code equal W (between -1 and 1 the neighbours
+//     are -1 and 1).  All decisions are fp32 comparisons.
+// The scale is in every case the optimum of Eq. (4) for the chosen codes,
+// alpha = sum_i W_i c_i / sum_i c_i^2, which for the deterministic rules is Eq. (5).
+template <bool SGD, bool STOCH>
 __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__ w, int64_t K,
                                                        int64_t n, uint32_t* __restrict__ codes,
                                                        float* __restrict__ alpha,
-                                                       int32_t* __restrict__ counts, SgdArgs sgd) {
+                                                       int32_t* __restrict__ counts, SgdArgs sgd,
+                                                       QuantVariant var) {
     __shared__ double sh1[4], sh2[4];
     __shared__ int64_t shn[4];
     const int lane = threadIdx.x & 63;
@@ -99,11 +110,38 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
             // denormal mode: |W| > 1, and W > 0 (false for both zeros and for NaN).
             const uint32_t abits = u[j] & 0x7FFFFFFFu;
             const bool nan = abits > 0x7F800000u;
-            const bool mag = in && !nan && abits > 0x3F800000u;
-            const bool neg = in && !(!nan && !(u[j] >> 31) && abits != 0u);
-            if (in) {
-                const double a = (double)__uint_as_float(abits);
-                if (mag) s2 += a; else s1 += a;  // a NaN weight makes alpha NaN
+            bool mag, neg;
+            if constexpr (STOCH) {
+                const int64_t i = c * 64 + lane;
+                const float uu = var.uni[k * n + (in ? i : 0)];
+                const float a = fminf(fmaxf(__uint_as_float(u[j]), -2.0f), 2.0f);
+                if (nan) {
+                    mag = false;
+                    neg = true;
+                } else if (a > 1.0f) {
+                    mag = uu < a - 1.0f;
+                    neg = false;
+                } else if (a < -1.0f) {
+                    mag = uu < -1.0f - a;
+                    neg = true;
+                } else {
+                    mag = false;
+                    neg = !(uu + uu < a + 1.0f);
+                }
+                mag = mag && in;
+                neg = neg && in;
+                if (in) {  // W_i * sign(c_i), summed per magnitude
+                    const double wv = (double)__uint_as_float(u[j]);
+                    const double a2 = neg ? -wv : wv;
+                    if (mag) s2 += a2; else s1 += a2;
+                }
+            } else {
+                mag = in && !nan && abits > var.thr_bits;
+                neg = in && !(!nan && !(u[j] >> 31) && abits != 0u);
+                if (in) {
+                    const double a = (double)__uint_as_float(abits);
+                    if (mag) s2 += a; else s1 += a;  // a NaN weight makes alpha NaN
+                }
             }
             const uint64_t M = __ballot(mag);
             const uint64_t S = __ballot(neg);
@@ -145,17 +183,26 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
 
 hipError_t launch_quantize(const float* w, int64_t K, int64_t n, uint32_t* codes, float* alpha,
                            int32_t* counts, hipStream_t stream) {
+    return launch_quantize_variant(w, K, n, QuantVariant{0x3F800000u, nullptr}, codes, alpha, counts, stream);
+}
+
+hipError_t launch_quantize_variant(const float* w, int64_t K, int64_t n, const QuantVariant& var, uint32_t* codes,
+                                   float* alpha, int32_t* counts, hipStream_t stream) {
     const int64_t kpad = (K + 63) / 64 * 64;
-    hipLaunchKernelGGL(quantize_kernel<false>, dim3((unsigned)kpad), dim3(256), 0, stream, w, K, n, codes, alpha,
-                       counts, SgdArgs{});
+    if (var.uni)
+        hipLaunchKernelGGL((quantize_kernel<false, true>), dim3((unsigned)kpad), dim3(256), 0, stream, w, K, n, codes,
+                           alpha, counts, SgdArgs{}, var);
+    else
+        hipLaunchKernelGGL((quantize_kernel<false, false>), dim3((unsigned)kpad), dim3(256), 0, stream, w, K, n, codes,
+                           alpha, counts, SgdArgs{}, var);
     return hipGetLastError();
 }
 
 hipError_t launch_sgd_quantize(const SgdArgs& sgd, int64_t K, int64_t n, uint32_t* codes, float* alpha,
                                int32_t* counts, hipStream_t stream) {
     const int64_t kpad = (K + 63) / 64 * 64;
-    hipLaunchKernelGGL(quantize_kernel<true>, dim3((unsigned)kpad), dim3(256), 0, stream, sgd.w, K, n, codes,
-                       alpha, counts, sgd);
+    hipLaunchKernelGGL((quantize_kernel<true, false>), dim3((unsigned)kpad), dim3(256), 0, stream, sgd.w, K, n,
+                       codes, alpha, counts, sgd, QuantVariant{0x3F800000u, nullptr});
     return hipGetLastError();
 }
 

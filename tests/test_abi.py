@@ -72,6 +72,10 @@ def test_argument_errors_before_launch():
     assert lib.tbn_quantize(good, 0, 4, good, good, None, None) == 2
     assert lib.tbn_sgd_step(good, good, good, 0, 0.1, 0.9, 0.0, None) == 2
     assert lib.tbn_sgd_step_quantize(good, good, good, 0, 4, 0.1, 0.9, 0.0, good, good, None, None) == 2
+    assert lib.tbn_quantize_variant(good, 4, 4, 0.0, None, good, good, None, None) == 2
+    assert lib.tbn_quantize_variant(good, 4, 4, float("inf"), None, good, good, None, None) == 2
+    assert lib.tbn_quantize_variant(good, 4, 4, 0.5, good, good, good, None, None) == 3
+    assert lib.tbn_quantize_variant(good, 4, 4, 1.0, vp(0x1001), good, good, None, None) == 4
     assert lib.tbn_sgd_step_quantize(good, good, good, 4, 4, 0.1, 0.9, 0.0, bad, good, None, None) == 4
     assert lib.tbn_sgd_step_quantize(good, None, good, 4, 4, 0.1, 0.9, 0.0, good, good, None, None) == 1
     # stride-2 backward-data is not implemented

@@ -147,6 +147,36 @@ def test_sgd_step_quantize_parity(tbn, K, n):
     assert nerr(w_new.ravel(), w64) <= 1e-6
 
 
+VARIANT_CASES = [
+    # K, n, weight std, threshold, stochastic
+    (32, 25, 0.05, 0.05, False), (130, 2304, 1.0, 0.5, False), (7, 4608, 1.0, 2.0, False),
+    (65, 129, 1.0, 1.0, True), (256, 2304, 1.0, 1.0, True), (3, 5, 3.0, 1.0, True), (1, 1, 1.0, 0.7, False),
+]
+
+
+@pytest.mark.parametrize("K,n,std,t,stoch", VARIANT_CASES)
+def test_quantize_variant_parity(tbn, K, n, std, t, stoch):
+    """Discretisation variants against the oracle: codes and counts bit-exact, alpha within
+    1 ulp.  Threshold cases include weights exactly at +-t and one ulp either side."""
+    log("quantize_variant K=%d n=%d std=%g t=%g stochastic=%s" % (K, n, std, t, stoch))
+    w = synth.normal(1, "qv_w%d_%d" % (K, n), (K, n), std)
+    if not stoch and K * n >= 6:
+        tt = np.float32(t)
+        w.flat[:6] = [tt, -tt, np.nextafter(tt, np.float32(9)), np.nextafter(-tt, np.float32(-9)),
+                      np.nextafter(tt, np.float32(0)), 0.0]
+    u = np.minimum(synth.uniform(1, "qv_u%d_%d" % (K, n), (K, n)), np.float32(1 - 2 ** -24)) if stoch else None
+    q = oracle.quantize_variant(w, t, u)
+    codes, alpha, counts = tbn.quantize_variant(to_dev(w), t, None if u is None else to_dev(u))
+    torch.cuda.synchronize()
+    assert np.array_equal(words_np(codes), oracle.pack(q.codes)), "packed codes differ"
+    assert np.array_equal(counts.cpu().numpy(), np.stack([q.b1_size, q.b2_size], 1)), "counts differ"
+    d = ulp_diff(alpha.cpu().numpy(), q.alpha)
+    assert d.max() <= 1, "alpha differs by %d ulp" % d.max()
+    if not stoch and t == 1.0:
+        c2, a2, _ = tbn.quantize(to_dev(w))
+        assert torch.equal(c2, codes) and torch.equal(a2, alpha)
+
+
 def test_quantize_bit_pattern_sweep(tbn):
     # Every fp32 sign/exponent/top-7-fraction pattern with 16 low-fraction variants:
     # 2^16 * 16 values, finite ones compared with the oracle; NaN -> code -1 by contract.

@@ -191,3 +191,60 @@ def test_pack_roundtrip_and_bf16_rule(K, n):
 def test_pack_rejects_bad_codes():
     with pytest.raises(oracle.OracleError):
         oracle.pack(np.array([[0, 1]], np.int8))
+
+
+# ---------------------------------------------------------------------------------------
+# Discretisation variants (Sec. 2 chooses the deterministic rule for simplicity)
+# ---------------------------------------------------------------------------------------
+def test_variant_threshold_one_is_eq3():
+    w = synth.normal(0, "var_eq3", (40, 300), 1.0)
+    a, b = oracle.quantize(w), oracle.quantize_variant(w, 1.0)
+    assert np.array_equal(a.codes, b.codes)
+    assert np.array_equal(a.b2_size, b.b2_size)
+    assert np.max(np.abs(a.alpha64 - b.alpha64) / a.alpha64) < 1e-14
+
+
+def test_variant_threshold_hand_values():
+    # t = 0.5: -2 below -0.5, -1 on [-0.5, 0], 1 on (0, 0.5], 2 above 0.5
+    w = np.array([[-0.75, -0.5, -0.25, 0.0, 0.25, 0.5, 0.75]], np.float32)
+    q = oracle.quantize_variant(w, 0.5)
+    assert q.codes[0].tolist() == [-2, -1, -1, -1, 1, 1, 2]
+    # alpha = sum W c / sum c^2 = (1.5 + 0.5 + 0.25 + 0 + 0.25 + 0.5 + 1.5) / (4 + 1 + 1 + 1 + 1 + 1 + 4)
+    assert q.alpha64[0] == pytest.approx(4.5 / 13, rel=1e-15)
+
+
+def test_variant_alpha_is_the_least_squares_scale():
+    # whatever the codes, alpha minimises ||W - alpha c||^2: the numpy least-squares fit
+    w = synth.normal(0, "var_ls", (12, 257), 0.8)
+    u = synth.uniform(0, "var_ls_u", (12, 257))
+    for q in (oracle.quantize_variant(w, 0.3), oracle.quantize_variant(w, 1.0, u)):
+        for k in range(12):
+            c = q.codes[k].astype(np.float64)[:, None]
+            fit = np.linalg.lstsq(c, w[k].astype(np.float64), rcond=None)[0][0]
+            assert q.alpha64[k] == pytest.approx(fit, rel=1e-12)
+
+
+def test_stochastic_hand_values():
+    w = np.array([[1.5, 1.5, -1.25, -1.25, 0.0, 0.0, 0.5, 0.5, 3.0, -7.0]], np.float32)
+    u = np.array([[0.49, 0.51, 0.24, 0.26, 0.49, 0.5, 0.74, 0.76, 0.999, 0.999]], np.float32)
+    q = oracle.quantize_variant(w, 1.0, u)
+    # 1.5 -> 2 with probability 0.5; -1.25 -> -2 with probability 0.25; 0 -> 1 with
+    # probability 0.5; 0.5 -> 1 with probability 0.75; beyond +-2 always +-2
+    assert q.codes[0].tolist() == [2, 1, -2, -1, 1, -1, 1, -1, 2, -2]
+
+
+def test_stochastic_rounding_is_unbiased():
+    # E[code] = clamp(W, -2, 2): averaged over 40000 draws per weight, within 5 standard errors
+    vals = np.array([-2.5, -1.75, -1.0, -0.6, -0.0, 0.3, 0.99, 1.01, 1.5, 1.9, 2.0], np.float32)
+    draws = 40000
+    w = np.repeat(vals[None, :], draws, axis=0).T.copy()
+    u = np.minimum(synth.uniform(0, "var_unbiased", w.shape), np.float32(1 - 2 ** -24))  # [0, 1)
+    q = oracle.quantize_variant(w, 1.0, u)
+    mean = q.codes.astype(np.float64).mean(axis=1)
+    target = np.clip(vals.astype(np.float64), -2, 2)
+    se = np.maximum(q.codes.astype(np.float64).std(axis=1), 1e-3) / np.sqrt(draws)
+    assert np.all(np.abs(mean - target) <= 5 * se + 1e-12), (mean, target)
+    # only the two levels around each weight ever occur
+    for row, v in zip(q.codes, vals):
+        lo, hi = {True: (-2, -1), False: (-1, 1)}[bool(v < -1)] if v <= 1 else (1, 2)
+        assert set(np.unique(row)).issubset({lo, hi})
