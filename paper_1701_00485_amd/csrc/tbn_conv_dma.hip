@@ -515,6 +515,7 @@ hipError_t launch_dma_mode(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
         case 16: return launch_dma_cfg<256, 128, 1, 4, 2, BWD>(a, stream);
         case 18: return launch_dma_cfg<64, 128, 1, 4, 4, BWD>(a, stream);
         case 19: return launch_dma_cfg<256, 256, 2, 2, 3, BWD>(a, stream);
+        case 17: return launch_dma_cfg<256, 256, 2, 2, 4, BWD>(a, stream);
         default: return launch_dma_cfg<128, 256, 1, 4, 3, BWD>(a, stream);
     }
 }
@@ -525,7 +526,7 @@ void cfg_tile(int cfg, int* bm, int* bn) {
         case 14: *bm = 128; *bn = 64; return;
         case 18: *bm = 64; *bn = 128; return;
         case 16: *bm = 256; *bn = 128; return;
-        case 19: *bm = 256; *bn = 256; return;
+        case 17: case 19: *bm = 256; *bn = 256; return;
         default: *bm = 128; *bn = 256; return;
     }
 }
@@ -547,10 +548,6 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
     int bm, bn;
     if (p.cfg < 10) {
         p.cfg = a.Kf > 128 ? 10 : (a.Kf > 64 ? 12 : 14);
-        // at least 256 filters and two full rounds of 256 x 256 tiles: one block per CU with
-        // 128 x 128 accumulators per wave (half the LDS operand reads per MFMA of the
-        // 128 x 256 tile, and less sensitive to the memory system)
-        if (a.Kf >= 256 && a.Kf % 256 == 0 && (M + 255) / 256 * (a.Kf / 256) >= 512) p.cfg = 19;
         cfg_tile(p.cfg, &bm, &bn);
         // too few tiles for one wave of blocks: shorter tiles (64 pixels x 128 filters, a
         // four-deep ring) when there are at least 128 filters, else 128 x 64; then split
