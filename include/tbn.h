@@ -94,7 +94,10 @@ tbn_status tbn_conv_out_dims(const tbn_conv_desc* desc, int32_t* p, int32_t* q);
 int64_t tbn_packed_words(int64_t k, int64_t n);
 
 /* Bytes of caller-provided workspace `op` needs for `desc` (0 = none needed).
- * Pass the same op and geometry to the corresponding call. */
+ * Pass the same op and geometry to the corresponding call.  TBN_OP_FWD: fp32 partial sums
+ * of a split reduction, or, for inputs with fewer than 8 channels and at least 2^20
+ * elements, a zero-bordered bf16 copy of the input with the channels padded to a power of
+ * two (the forward call writes it first); the size covers either input dtype. */
 tbn_status tbn_workspace_size(tbn_op op, const tbn_conv_desc* desc, size_t* bytes);
 
 /*

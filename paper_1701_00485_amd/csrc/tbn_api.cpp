@@ -164,7 +164,13 @@ tbn_status tbn_workspace_size(tbn_op op, const tbn_conv_desc* desc, size_t* byte
     if (st != TBN_OK) return st;
     if (!bytes) return fail(TBN_ERR_NULL, "bytes is NULL");
     switch (op) {
-        case TBN_OP_FWD: *bytes = tbn::conv_gemm_partial_bytes(fwd_args(g, TBN_BF16, TBN_BF16)); return TBN_OK;
+        case TBN_OP_FWD: {
+            // the same geometry may take another path for fp32 input: size for both
+            const size_t b16 = tbn::conv_gemm_partial_bytes(fwd_args(g, TBN_BF16, TBN_BF16));
+            const size_t b32 = tbn::conv_gemm_partial_bytes(fwd_args(g, TBN_F32, TBN_BF16));
+            *bytes = b16 > b32 ? b16 : b32;
+            return TBN_OK;
+        }
         case TBN_OP_BWD_DATA: *bytes = (size_t)bwd_data_ws(g).total; return TBN_OK;
         case TBN_OP_BWD_WEIGHT: {
             const int splits = wgrad_splits(g);

@@ -394,7 +394,11 @@ size_t conv_gemm_partial_bytes(const ConvGemmArgs& a) {
     const int cfg = conv_tile_override();
     FcStreamPlan fp;
     ThinGeom tg;
-    return choose_path(a, cfg, &fp, &tg) == PATH_DMA ? plan_conv_dma(a, cfg).partial_bytes : 0;
+    switch (choose_path(a, cfg, &fp, &tg)) {
+        case PATH_DMA: return plan_conv_dma(a, cfg).partial_bytes;
+        case PATH_THIN: return tg.dma ? (size_t)tg.ws_bytes : 0;
+        default: return 0;
+    }
 }
 
 hipError_t launch_conv_gemm(const ConvGemmArgs& args, hipStream_t stream) {

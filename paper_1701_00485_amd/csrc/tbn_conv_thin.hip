@@ -13,7 +13,12 @@
 //   * applies alpha (and the optional scale, bias, residual, ReLU) in fp32 and writes
 //     16-byte rows through a small per-wave LDS transpose.
 // Blocks are persistent over the output tiles, so the filter decode is paid once per block.
+// For large inputs (the image stems) a first kernel writes the input once into workspace as
+// a zero-bordered copy with the padded channel count, and the patches are then copied from it
+// straight into LDS in whole 16-byte pieces (LDS-DMA): no per-element bounds checks or
+// address arithmetic remain in the tile loop.
 #include "tbn_device.h"
+#include "tbn_dma.h"
 #include "tbn_kernels.h"
 
 namespace tbn {
@@ -76,9 +81,46 @@ __device__ __forceinline__ uint32_t load_patch(const ConvGemmArgs& a, const uint
     return okmask;
 }
 
+// The zero-bordered copy of the input: xp[n][h'][w'][c] = x[n][h' - ph][w' - pw][c] inside
+// the image and for c < C, else 0 (bf16).  One thread per padded pixel, CP elements each.
+template <int CP, bool X32>
+__global__ __launch_bounds__(256) void thin_pad_kernel(const ConvGemmArgs a, const ThinGeom g, uint16_t* xp) {
+    const int64_t total = (int64_t)a.N * g.Hp * g.Wp;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= total) return;
+    const int64_t hw = (int64_t)g.Hp * g.Wp;
+    const int n = (int)(i / hw);
+    const int rem = (int)(i - (int64_t)n * hw);
+    const int hp = rem / g.Wp, wp = rem - (rem / g.Wp) * g.Wp;
+    const int h = hp - a.ph, w = wp - a.pw;
+    const bool in = (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+    const int64_t src = (((int64_t)n * a.H + h) * a.W + w) * a.C;
+    uint32_t v[CP];
+#pragma unroll
+    for (int c = 0; c < CP; ++c) {
+        uint32_t e = 0;
+        if (in && c < a.C)
+            e = X32 ? f32_to_bf16_bits(reinterpret_cast<const float*>(a.x)[src + c])
+                    : reinterpret_cast<const uint16_t*>(a.x)[src + c];
+        v[c] = e;
+    }
+    uint16_t* dst = xp + i * CP;
+    if constexpr (CP == 1) {
+        dst[0] = (uint16_t)v[0];
+    } else if constexpr (CP == 2) {
+        *reinterpret_cast<uint32_t*>(dst) = v[0] | (v[1] << 16);
+    } else if constexpr (CP == 4) {
+        *reinterpret_cast<u32x2*>(dst) = u32x2{v[0] | (v[1] << 16), v[2] | (v[3] << 16)};
+    } else {
+        *reinterpret_cast<u32x4*>(dst) =
+            u32x4{v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16)};
+    }
+}
+
 // TT: 16-element reduction steps per filter row (T / 16), so that the reduction loop is
 // one flat, unrolled sequence whose operand reads run one step ahead of the MFMAs.
-template <int CP, bool X32, int TT>
+// DMA: patches copied from the zero-bordered workspace copy (a.partial) with LDS-DMA.
+template <int CP, bool X32, int TT, bool DMA>
 __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, const ThinGeom g) {
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
     uint16_t* wl = reinterpret_cast<uint16_t*>(lds + g.w_off);  // [FB][WPITCH]
@@ -148,8 +190,10 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
     };
 
     // channel-padding slots of the patch stay zero; data elements are rewritten per tile
-    for (int i = tid; i < 2 * g.pbuf; i += 256) pl[i] = 0;
-    __syncthreads();  // zeros in place before any thread writes patch data
+    if constexpr (!DMA) {
+        for (int i = tid; i < 2 * g.pbuf; i += 256) pl[i] = 0;
+    }
+    __syncthreads();  // zeros (and the decoded filters) in place before the first patch
     const uint32_t img_elems = (uint32_t)a.H * a.W * a.C;
 
     uint32_t desc[kElemsPerThread];
@@ -178,32 +222,8 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
             }
         }
     };
-    int64_t tile = blockIdx.x;
-    int64_t img;
-    int p0, q0;
-    if (tile < g.ntiles) {
-        uint32_t pv[kElemsPerThread];
-        origin(tile, &img, &p0, &q0);
-        const uint32_t okm = load_patch<CP, X32>(a, desc, (uint32_t)img * img_elems, p0 * a.sh - a.ph,
-                                                 q0 * a.sw - a.pw, pv);
-        write_patch(pl, pv, okm);
-    }
-    __syncthreads();
-    for (int it = 0; tile < g.ntiles; tile += gridDim.x, ++it) {
-        uint16_t* cur = pl + (it & 1) * g.pbuf;
-        uint16_t* nxt = pl + ((it + 1) & 1) * g.pbuf;
-        const int64_t cimg = img;
-        const int cp0 = p0, cq0 = q0;
-        const bool more = tile + gridDim.x < g.ntiles;
-        // next tile's loads (the current tile's again on the last pass, unused: no branch, so
-        // nothing makes the compiler wait for them), consumed after the MFMAs and stores
-        uint32_t pv[kElemsPerThread];
-        origin(more ? tile + gridDim.x : tile, &img, &p0, &q0);
-        const uint32_t okm =
-            load_patch<CP, X32>(a, desc, (uint32_t)img * img_elems, p0 * a.sh - a.ph, q0 * a.sw - a.pw, pv);
-
-        // wave w computes output rows w and w + 4 of the tile
-        f32x16 acc[2][2];
+    // the tile's reduction: wave w computes output rows w and w + 4 of the tile
+    auto tile_mfma = [&](const uint16_t* cur, f32x16 (&acc)[2][2]) {
 #pragma unroll
         for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -235,10 +255,9 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
             acc[1][0] = mfma32(cb0, ca1, acc[1][0]);
             acc[1][1] = mfma32(cb1, ca1, acc[1][1]);
         }
-        // the next tile's patch goes to the other buffer now: its loads were issued before
-        // the MFMAs, and waiting for them here does not also wait for this tile's stores
-        if (more) write_patch(nxt, pv, okm);
+    };
 
+    auto tile_epilogue = [&](const f32x16 (&acc)[2][2], int64_t cimg, int cp0, int cq0) {
         // ---- epilogue: lane holds pixel l32 and filters 32 t + 8 g + 4 half + 0..3 ----
 #pragma unroll
         for (int ut = 0; ut < 4; ++ut) {
@@ -291,6 +310,89 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
                 }
             }
         }
+    };
+
+    if constexpr (DMA) {
+        // byte offsets, relative to the patch origin in the zero-bordered copy, of the pieces
+        // this lane copies: piece k = 64 (4 i + wave) + lane of the patch is row k / ppr,
+        // 16-byte column k % ppr, and lands at LDS byte 16 k of the patch buffer (pieces past
+        // the patch get an out-of-range offset and land as zeros in the buffer's tail)
+        constexpr int kMaxNi = 8;
+        uint32_t prel[kMaxNi];
+#pragma unroll
+        for (int i = 0; i < kMaxNi; ++i) {
+            const int k = 64 * (4 * i + wave) + lane;
+            const int r = k / g.ppr, j = k - (k / g.ppr) * g.ppr;
+            prel[i] = (i < g.ni && k < g.npieces) ? (uint32_t)((r * g.Wp * CP + 8 * j) * 2) : 0x80000000u;
+        }
+        const v4i rs_xp = make_rsrc(a.partial, (uint32_t)g.ws_bytes);
+        auto issue_patch = [&](int64_t t, uint16_t* buf) {
+            int64_t im;
+            int tp0, tq0;
+            origin(t, &im, &tp0, &tq0);
+            const uint32_t toff = (uint32_t)((((int64_t)im * g.Hp + (int64_t)tp0 * a.sh) * g.Wp + (int64_t)tq0 * a.sw) * CP * 2);
+            const uint32_t base = lds_addr(buf);
+#pragma unroll
+            for (int i = 0; i < kMaxNi; ++i) {
+                if (i < g.ni)
+                    dma_b128(rs_xp, base + (uint32_t)(64 * (4 * i + wave)) * 16u,
+                             prel[i] >= 0x80000000u ? 0x80000000u : prel[i] + toff);
+            }
+        };
+        int64_t tile = blockIdx.x;
+        if (tile < g.ntiles) issue_patch(tile, pl);
+        wait_vmcnt(0);
+        __syncthreads();
+        for (int it = 0; tile < g.ntiles; tile += gridDim.x, ++it) {
+            uint16_t* cur = pl + (it & 1) * g.pbuf;
+            uint16_t* nxt = pl + ((it + 1) & 1) * g.pbuf;
+            int64_t cimg;
+            int cp0, cq0;
+            origin(tile, &cimg, &cp0, &cq0);
+            const bool more = tile + gridDim.x < g.ntiles;
+            // the next tile's patch is copied into the other buffer while this one computes
+            if (more) issue_patch(tile + gridDim.x, nxt);
+            f32x16 acc[2][2];
+            tile_mfma(cur, acc);
+            // this wave's pieces of the next patch have landed (and the previous tile's
+            // stores, issued a whole reduction ago, are done)
+            wait_vmcnt(0);
+            tile_epilogue(acc, cimg, cp0, cq0);
+            __syncthreads();  // the next patch is complete; every wave is done with this one
+        }
+        return;
+    }
+    int64_t tile = blockIdx.x;
+    int64_t img;
+    int p0, q0;
+    if (tile < g.ntiles) {
+        uint32_t pv[kElemsPerThread];
+        origin(tile, &img, &p0, &q0);
+        const uint32_t okm = load_patch<CP, X32>(a, desc, (uint32_t)img * img_elems, p0 * a.sh - a.ph,
+                                                 q0 * a.sw - a.pw, pv);
+        write_patch(pl, pv, okm);
+    }
+    __syncthreads();
+    for (int it = 0; tile < g.ntiles; tile += gridDim.x, ++it) {
+        uint16_t* cur = pl + (it & 1) * g.pbuf;
+        uint16_t* nxt = pl + ((it + 1) & 1) * g.pbuf;
+        const int64_t cimg = img;
+        const int cp0 = p0, cq0 = q0;
+        const bool more = tile + gridDim.x < g.ntiles;
+        // next tile's loads (the current tile's again on the last pass, unused: no branch, so
+        // nothing makes the compiler wait for them), consumed after the MFMAs and stores
+        uint32_t pv[kElemsPerThread];
+        origin(more ? tile + gridDim.x : tile, &img, &p0, &q0);
+        const uint32_t okm =
+            load_patch<CP, X32>(a, desc, (uint32_t)img * img_elems, p0 * a.sh - a.ph, q0 * a.sw - a.pw, pv);
+
+        f32x16 acc[2][2];
+        tile_mfma(cur, acc);
+        // the next tile's patch goes to the other buffer now: its loads were issued before
+        // the MFMAs, and waiting for them here does not also wait for this tile's stores
+        if (more) write_patch(nxt, pv, okm);
+
+        tile_epilogue(acc, cimg, cp0, cq0);
         __syncthreads();  // the next patch is complete; every wave is done with this one
     }
 }
@@ -316,9 +418,35 @@ bool conv_thin_plan(const ConvGemmArgs& a, ThinGeom* g) {
     t.WPITCH = t.RT + 8;
     t.PH = (TP - 1) * a.sh + a.R;
     t.PW = (TQ - 1) * a.sw + (a.S > t.T / t.CP ? a.S : t.T / t.CP);
+    t.tiles_p = (a.P + TP - 1) / TP;
+    t.tiles_q = (a.Q + TQ - 1) / TQ;
+    t.ntiles = (int64_t)a.N * t.tiles_p * t.tiles_q;
+    const int64_t xelems = (int64_t)a.N * a.H * a.W * a.C;
+    // large inputs (one million elements and up): zero-bordered copy + LDS-DMA patches, the
+    // patch rows widened to whole 16-byte pieces; small ones (where a second launch would
+    // cost more than it saves) load their patches element by element
+    t.dma = xelems >= (1 << 20) ? 1 : 0;
+    if (t.dma) {
+        const int step = t.CP >= 8 ? 1 : 8 / t.CP;  // pixels per 16-byte piece
+        t.PW = (t.PW + step - 1) / step * step;
+        t.Hp = (t.tiles_p - 1) * TP * a.sh + t.PH;
+        t.Wp = (t.tiles_q - 1) * TQ * a.sw + t.PW;
+        if (t.Hp < a.H + a.ph) t.Hp = a.H + a.ph;
+        if (t.Wp < a.W + a.pw) t.Wp = (a.W + a.pw + step - 1) / step * step;
+        t.ppr = t.PW * t.CP / 8;
+        t.npieces = t.PH * t.ppr;
+        t.ni = (t.npieces + 255) / 256;
+        t.ws_bytes = ((int64_t)a.N * t.Hp * t.Wp * t.CP * 2 + 255) / 256 * 256;
+        if (t.ni > 8 || t.ws_bytes >= 0x7FFFFFF0ll) t.dma = 0;
+    }
+    if (!t.dma) {
+        t.PW = (TQ - 1) * a.sw + (a.S > t.T / t.CP ? a.S : t.T / t.CP);
+        t.ws_bytes = 0;
+    }
     t.w_off = 0;
     t.p_off = round16(FB * t.WPITCH * 2);
-    t.pbuf = round16(t.PH * t.PW * t.CP * 2) / 2;  // bf16 elements per patch buffer
+    // bf16 elements per patch buffer: the patch (DMA: every piece the copies write)
+    t.pbuf = t.dma ? t.ni * 256 * 8 : round16(t.PH * t.PW * t.CP * 2) / 2;
     t.s_off = t.p_off + 2 * t.pbuf * 2;
     t.lds_bytes = t.s_off + 4 * 32 * SPITCH * 4;
     const int nb = (a.R * a.S * a.C + 63) / 64;  // code blocks staged in the epilogue area
@@ -327,13 +455,10 @@ bool conv_thin_plan(const ConvGemmArgs& a, ThinGeom* g) {
     t.ept = (t.nelem + 255) / 256;
     t.div_rowlen = make_fastdiv((uint32_t)t.rowlen);
     t.div_c = make_fastdiv((uint32_t)a.C);
-    const int64_t xelems = (int64_t)a.N * a.H * a.W * a.C;
-    if (t.lds_bytes > 96 * 1024 || a.R > 64 || t.T > 128 || nb * 1024 > 4 * 32 * SPITCH * 4 || t.ept > kElemsPerThread ||
-        t.PH * t.PW * t.CP >= 0xFFFF || t.PH > 63 || t.PW > 1023 || xelems >= 0x7FFFFFFF)
+    if (t.lds_bytes > 96 * 1024 || a.R > 64 || t.T > 128 || nb * 1024 > 4 * 32 * SPITCH * 4 ||
+        (!t.dma && t.ept > kElemsPerThread) || t.PH * t.PW * t.CP >= 0xFFFF || t.PH > 63 || t.PW > 1023 ||
+        xelems >= 0x7FFFFFFF)
         return false;
-    t.tiles_p = (a.P + TP - 1) / TP;
-    t.tiles_q = (a.Q + TQ - 1) / TQ;
-    t.ntiles = (int64_t)a.N * t.tiles_p * t.tiles_q;
     *g = t;
     return true;
 }
@@ -342,13 +467,40 @@ hipError_t launch_conv_thin(const ConvGemmArgs& a, const ThinGeom& g, hipStream_
     const bool x32 = a.x_f32 != 0;
     const int tt = g.T / 16;
     const void* fn = nullptr;
-#define TBN_THIN_PICK(cp, x, t) \
-    if (g.CP == cp && x32 == x && tt == t) fn = reinterpret_cast<const void*>(&conv_thin_kernel<cp, x, t>);
-#define TBN_THIN_PICK_T(cp, x) TBN_THIN_PICK(cp, x, 1) TBN_THIN_PICK(cp, x, 2) TBN_THIN_PICK(cp, x, 4) TBN_THIN_PICK(cp, x, 8)
-    TBN_THIN_PICK_T(1, true) TBN_THIN_PICK_T(2, true) TBN_THIN_PICK_T(4, true) TBN_THIN_PICK_T(8, true)
-    TBN_THIN_PICK_T(1, false) TBN_THIN_PICK_T(2, false) TBN_THIN_PICK_T(4, false) TBN_THIN_PICK_T(8, false)
+#define TBN_THIN_PICK(cp, x, t, d) \
+    if (g.CP == cp && x32 == x && tt == t && (g.dma != 0) == d) fn = reinterpret_cast<const void*>(&conv_thin_kernel<cp, x, t, d>);
+#define TBN_THIN_PICK_T(cp, x, d) TBN_THIN_PICK(cp, x, 1, d) TBN_THIN_PICK(cp, x, 2, d) TBN_THIN_PICK(cp, x, 4, d) TBN_THIN_PICK(cp, x, 8, d)
+    TBN_THIN_PICK_T(1, true, false) TBN_THIN_PICK_T(2, true, false) TBN_THIN_PICK_T(4, true, false) TBN_THIN_PICK_T(8, true, false)
+    TBN_THIN_PICK_T(1, false, false) TBN_THIN_PICK_T(2, false, false) TBN_THIN_PICK_T(4, false, false) TBN_THIN_PICK_T(8, false, false)
 #undef TBN_THIN_PICK_T
 #undef TBN_THIN_PICK
+    if (g.dma) {
+        // the DMA kernel reads the bf16 zero-bordered copy whatever the input dtype
+#define TBN_THIN_PICK_D(cp, t) if (g.CP == cp && tt == t) fn = reinterpret_cast<const void*>(&conv_thin_kernel<cp, false, t, true>);
+        TBN_THIN_PICK_D(1, 1) TBN_THIN_PICK_D(1, 2) TBN_THIN_PICK_D(1, 4) TBN_THIN_PICK_D(1, 8)
+        TBN_THIN_PICK_D(2, 1) TBN_THIN_PICK_D(2, 2) TBN_THIN_PICK_D(2, 4) TBN_THIN_PICK_D(2, 8)
+        TBN_THIN_PICK_D(4, 1) TBN_THIN_PICK_D(4, 2) TBN_THIN_PICK_D(4, 4) TBN_THIN_PICK_D(4, 8)
+        TBN_THIN_PICK_D(8, 1) TBN_THIN_PICK_D(8, 2) TBN_THIN_PICK_D(8, 4) TBN_THIN_PICK_D(8, 8)
+#undef TBN_THIN_PICK_D
+        if (!a.partial) return hipErrorInvalidValue;
+        const int64_t pix = (int64_t)a.N * g.Hp * g.Wp;
+        const dim3 pgrid((unsigned)((pix + 255) / 256));
+        uint16_t* xp = reinterpret_cast<uint16_t*>(a.partial);
+#define TBN_PAD(cp, x) hipLaunchKernelGGL((thin_pad_kernel<cp, x>), pgrid, dim3(256), 0, stream, a, g, xp)
+        switch (g.CP * 2 + (x32 ? 1 : 0)) {
+            case 2: TBN_PAD(1, false); break;
+            case 3: TBN_PAD(1, true); break;
+            case 4: TBN_PAD(2, false); break;
+            case 5: TBN_PAD(2, true); break;
+            case 8: TBN_PAD(4, false); break;
+            case 9: TBN_PAD(4, true); break;
+            case 16: TBN_PAD(8, false); break;
+            default: TBN_PAD(8, true); break;
+        }
+#undef TBN_PAD
+        const hipError_t pe = hipGetLastError();
+        if (pe != hipSuccess) return pe;
+    }
     if (!fn) return hipErrorInvalidValue;
     if (g.lds_bytes > 65536 &&
         hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, g.lds_bytes) != hipSuccess)

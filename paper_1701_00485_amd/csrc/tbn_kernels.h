@@ -102,6 +102,12 @@ struct ThinGeom {
     int32_t pbuf;  // bf16 elements per patch buffer (two buffers)
     int32_t rowlen, nelem, ept;  // input elements per patch row, per patch, per thread
     FastDiv div_rowlen, div_c;
+    // large inputs: the input is first written once into workspace as a zero-bordered NHWC
+    // copy with CP channels [N][Hp][Wp][CP] bf16, from which every patch is a block of whole
+    // 16-byte pieces copied straight into LDS (ppr pieces per patch row, npieces per patch,
+    // ni copy instructions per wave)
+    int32_t dma, Hp, Wp, ppr, npieces, ni;
+    int64_t ws_bytes;
 };
 bool conv_thin_plan(const ConvGemmArgs& a, ThinGeom* g);
 hipError_t launch_conv_thin(const ConvGemmArgs& a, const ThinGeom& g, hipStream_t stream);

@@ -104,6 +104,15 @@ def test_workspace_sizes():
     assert tbn.workspace_size(tbn.OP_BWD_DATA, d) == codes_pairs + wf
 
 
+def test_stem_workspace_is_the_bordered_copy():
+    # 7x7/2 stem over 64 x 224 x 224 x 3: 14 x 4 tiles of 8 x 32 outputs; the bordered copy
+    # spans (14-1)*8*2 + 21 = 229 rows and (4-1)*32*2 + 70 = 262 columns of 4 channels
+    d = tbn.ConvDesc(64, 224, 224, 3, 64, 7, 7, 2, 3)
+    assert tbn.workspace_size(tbn.OP_FWD, d) == (64 * 229 * 262 * 4 * 2 + 255) // 256 * 256
+    # small inputs load their patches directly: no workspace
+    assert tbn.workspace_size(tbn.OP_FWD, tbn.ConvDesc(16, 28, 28, 1, 32, 5, 5, 1, 2)) == 0
+
+
 def test_forward_workspace_checked():
     lib = tbn.load()
     good = ctypes.c_void_p(0x100000)

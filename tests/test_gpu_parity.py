@@ -256,6 +256,38 @@ def test_fwd_parity(tbn, g, out):
     assert e <= (1e-4 if out == "f32" else TOL)
 
 
+@pytest.mark.parametrize("g,xdt", [((8, 224, 224, 3, 64, 7, 7, 2, 3), "bf16"),   # ResNet stem, batch 8
+                                    ((7, 224, 224, 3, 40, 7, 7, 2, 3), "f32"),    # fp32 input, ragged filters
+                                    ((16, 256, 256, 1, 32, 5, 5, 1, 2), "bf16"),  # one channel
+                                    ((4, 257, 263, 5, 24, 3, 3, 2, 1), "bf16")])  # 5 channels, odd sizes
+def test_fwd_thin_bordered_copy(tbn, g, xdt):
+    """Inputs of 2^20 elements and more with fewer than 8 channels: the input is first written
+    into workspace as a zero-bordered copy and the patches are copied from it."""
+    log("fwd thin bordered copy %s %s" % (g, xdt))
+    n, h, w, c, k, r, s, st, pd = g
+    assert n * h * w * c >= 1 << 20
+    desc = tbn.ConvDesc(*g)
+    assert tbn.workspace_size(tbn.OP_FWD, desc) > 0
+    d = oracle.ConvDesc(*g)
+    wr = synth.normal(2, "bw%s" % (g,), (k, r * s * c), 1.0)
+    q = oracle.quantize(wr)
+    codes, alpha, _ = tbn.quantize(to_dev(wr))
+    if xdt == "f32":
+        x = synth.normal(2, "bx%s" % (g,), (n, h, w, c))
+        xin, xref = to_dev(x), oracle.round_bf16(x)
+    else:
+        xb = synth.normal_bf16(2, "bx%s" % (g,), (n, h, w, c))
+        xin, xref = bf16_dev(xb), oracle.bf16_bits_to_f64(xb)
+    y = tbn.conv2d_fwd(desc, xin, codes, alpha, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    imgs = [0, n - 1]
+    ref = oracle.conv_fwd(oracle.ConvDesc(len(imgs), h, w, c, k, r, s, st, pd), xref[imgs], q.codes,
+                          q.alpha.astype(np.float64))
+    e = nerr(y.cpu().numpy()[imgs], ref)
+    log("  images %s: normalised max error %.3e" % (imgs, e))
+    assert e <= 1e-4
+
+
 def test_fwd_fp32_input_single_layer(tbn):
     # 16 x 1 x 28 x 28 fp32 uniform[0,1) input, 32 filters 5x5, pad 2, N(0, 0.05) masters.
     g = (16, 28, 28, 1, 32, 5, 5, 1, 2)
