@@ -78,14 +78,16 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
     const int n = a.R * a.S * C;
     const int nchunks = (n + BK - 1) / BK;
     const int KB = (a.Kf + 63) / 64;
-    const int tilesN = (a.Kf + BN - 1) / BN;
-    const int64_t tiles = ((M + BM - 1) / BM) * tilesN;
-    // XCD-aware order over (split, tile); each split reduces a contiguous range of stages
-    const int64_t work = xcd_remap(blockIdx.x, gridDim.x);
-    const int split = (int)(work / tiles);
-    const int64_t tile = work % tiles;
-    const int64_t m0 = (tile / tilesN) * BM;
-    const int n0 = (int)(tile % tilesN) * BN;
+    const uint32_t tilesN = (uint32_t)(a.Kf + BN - 1) / BN;
+    const uint32_t tiles = (uint32_t)((M + BM - 1) / BM) * tilesN;
+    // XCD-aware order over (split, tile); each split reduces a contiguous range of stages.
+    // Block counts are below 2^31 (checked by the host), so 32-bit magic-number divisions.
+    const uint32_t work = (uint32_t)xcd_remap(blockIdx.x, gridDim.x);
+    const int split = (int)fdiv(work, a.div_tiles);
+    const uint32_t tile = work - (uint32_t)split * tiles;
+    const uint32_t mtile = fdiv(tile, a.div_tilesN);
+    const int64_t m0 = (int64_t)mtile * BM;
+    const int n0 = (int)(tile - mtile * tilesN) * BN;
     const int c_begin = split * a.chunks_per_split;
     const int c_end = min(c_begin + a.chunks_per_split, nchunks);
     const int nloc = c_end - c_begin;
@@ -112,11 +114,17 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
             const uint32_t q = pq - p * (uint32_t)a.Q;
             const int h0 = (int)p * a.sh - a.ph, w0 = (int)q * a.sw - a.pw;
             rbase[j] = ((int32_t)img * a.H + h0) * a.W * C + w0 * C;
-            uint64_t wbits = 0;
-            for (int s = 0; s < a.S; ++s)
-                if ((unsigned)(w0 + s) < (unsigned)a.W) wbits |= 1ull << s;
-            for (int r = 0; r < a.R; ++r)
-                if ((unsigned)(h0 + r) < (unsigned)a.H) mask |= wbits << (r * a.S);
+            // in-image taps: s in [slo, shi), r in [rlo, rhi); the row's bits wbits
+            // replicated at every in-image r by one multiplication with the pattern
+            // sum_r 2^(r*S) (its groups of S bits never overlap, R*S <= 63)
+            const int slo = max(0, -w0), shi = min(a.S, a.W - w0);
+            const int rlo = max(0, -h0), rhi = min(a.R, a.H - h0);
+            if (shi > slo && rhi > rlo) {
+                const uint64_t wbits = (1ull << shi) - (1ull << slo);
+                const uint64_t rowsel = (1ull << (rhi * a.S)) - (1ull << (rlo * a.S));
+                const uint64_t rep = ((uint64_t)a.rep_hi << 32) | a.rep_lo;
+                mask = wbits * (rep & rowsel);
+            }
         }
         rmask[j][0] = (uint32_t)mask;
         rmask[j][1] = (uint32_t)(mask >> 32);
@@ -140,13 +148,15 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
             nmask[j][0] = ~rmask[j][0];
             nmask[j][1] = ~rmask[j][1];
         }
-        const int e0 = c_begin * BK;
-        const int rs = e0 / C;
-        uc = e0 - rs * C;
-        ur = rs / a.S;
-        us = rs - ur * a.S;
-        utap = rs;
-        utoff2 = (uint32_t)((ur * a.W + us) * C + uc) << 1;
+        if (c_begin != 0) {  // a later reduction split: its first (r, s, c)
+            const int e0 = c_begin * BK;
+            const int rs = e0 / C;
+            uc = e0 - rs * C;
+            ur = rs / a.S;
+            us = rs - ur * a.S;
+            utap = rs;
+            utoff2 = (uint32_t)((ur * a.W + us) * C + uc) << 1;
+        }
     } else {
         const int e0 = c_begin * BK + lseg * 8;
         const int rs = e0 / C;
@@ -495,9 +505,18 @@ __global__ __launch_bounds__(256) void conv_split_epilogue_kernel(const ConvGemm
 }
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool BWD>
-hipError_t launch_dma_cfg(const ConvGemmArgs& a, hipStream_t stream) {
+hipError_t launch_dma_cfg(const ConvGemmArgs& args, hipStream_t stream) {
+    ConvGemmArgs a = args;
     const int64_t M = (int64_t)a.N * a.P * a.Q;
-    const int64_t tiles = ((M + BM - 1) / BM) * ((a.Kf + BN - 1) / BN);
+    const int64_t tilesN = (a.Kf + BN - 1) / BN;
+    const int64_t tiles = ((M + BM - 1) / BM) * tilesN;
+    if (tiles * a.splits >= 0x7FFFFFFFll) return hipErrorInvalidValue;
+    a.div_tiles = make_fastdiv((uint32_t)tiles);
+    a.div_tilesN = make_fastdiv((uint32_t)tilesN);
+    uint64_t rep = 0;
+    for (int r = 0; r < a.R; ++r) rep |= 1ull << (r * a.S);
+    a.rep_lo = (uint32_t)rep;
+    a.rep_hi = (uint32_t)(rep >> 32);
     const dim3 grid((unsigned)(tiles * a.splits));
     if (a.C % 64 == 0)
         hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, true>), grid, dim3(256), 0, stream, a);

@@ -46,6 +46,11 @@ struct ConvGemmArgs {
     float* partial;           // split-K: fp32 partial sums [splits][M][Kf] (workspace)
     int32_t splits;           // split-K: number of reduction ranges (1 = none)
     int32_t chunks_per_split; // split-K: 64-element stages per range
+    // LDS-DMA kernel: division by the tile count and by the column-tile count (the block
+    // index -> (split, tile) -> (row tile, column tile) maps), and the 64-bit pattern
+    // sum_{r < R} 2^(r*S) that replicates a filter row's in-image taps over its rows
+    FastDiv div_tiles, div_tilesN;
+    uint32_t rep_lo, rep_hi;
 };
 
 hipError_t launch_quantize(const float* w, int64_t K, int64_t n, uint32_t* codes, float* alpha,
