@@ -316,35 +316,43 @@ __global__ __launch_bounds__(256) void repack_bwd_kernel(const uint32_t* __restr
                                                          int32_t R, int32_t S, int32_t C,
                                                          uint32_t* __restrict__ codes_t,
                                                          uint32_t* __restrict__ apair) {
-    const int64_t n = (int64_t)R * S * C;        // elements of a forward filter
-    const int64_t nt = (int64_t)R * S * K;       // elements of a transposed filter
-    const int64_t nb = (n + 63) / 64;
-    const int64_t nbt = (nt + 63) / 64;
-    const int64_t cb = (C + 63) / 64;
-    const int64_t words = cb * nbt * 256;
-    const int64_t pairs = nbt * 32;
+    // every count below is < 2^31 (R*S*C and R*S*K < 2^30, checked by the host)
+    const uint32_t n = (uint32_t)(R * S * C);     // elements of a forward filter
+    const uint32_t nt = (uint32_t)(R * S * K);    // elements of a transposed filter
+    const uint32_t nb = (n + 63) / 64;
+    const uint32_t nbt = (nt + 63) / 64;
+    const uint32_t cb = (uint32_t)(C + 63) / 64;
+    const int64_t words = (int64_t)cb * nbt * 256;
+    const int64_t pairs = (int64_t)nbt * 32;
     const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (gid < words) {
-        const int64_t wsub = gid & 3;
-        const int64_t cc = (gid >> 2) & 63;
-        const int64_t eb = (gid >> 8) % nbt;
-        const int64_t cblk = (gid >> 8) / nbt;
-        const int64_t c = cblk * 64 + cc;
+        const uint32_t g32 = (uint32_t)gid;
+        const uint32_t wsub = g32 & 3;
+        const uint32_t cc = (g32 >> 2) & 63;
+        const uint32_t eb = (g32 >> 8) % nbt;
+        const uint32_t cblk = (g32 >> 8) / nbt;
+        const uint32_t c = cblk * 64 + cc;
         uint32_t word = 0;
-        if (c < C) {
-            for (int e = 0; e < 16; ++e) {
-                const int64_t et = eb * 64 + wsub * 16 + e;  // (r', s', k) of the flipped filter
-                if (et >= nt) break;
-                const int64_t k = et % K;
-                const int64_t rs = et / K;
-                const int64_t rr = R - 1 - rs / S, ss = S - 1 - rs % S;
-                const int64_t i = (rr * S + ss) * C + c;       // element of forward filter k
-                const uint32_t src = codes[((k / 64 * nb + i / 64) * 64 + k % 64) * 4 + (i % 64) / 16];
-                const int ei = (int)(i % 16), hi = ei & 1, j = ei >> 1;
+        uint32_t et = eb * 64 + wsub * 16;  // first (r', s', k) of the flipped filter in this word
+        if (c < (uint32_t)C && et < nt) {
+            // walk k, carrying into s' and r' (one division per word, none per element)
+            uint32_t k = et % (uint32_t)K, rs = et / (uint32_t)K;
+            uint32_t rp = rs / (uint32_t)S, sp = rs - rp * (uint32_t)S;
+            for (int e = 0; e < 16 && et < nt; ++e, ++et) {
+                const uint32_t i = ((R - 1 - rp) * S + (S - 1 - sp)) * C + c;  // element of forward filter k
+                const uint32_t src = codes[(((k >> 6) * nb + (i >> 6)) * 64 + (k & 63)) * 4 + ((i & 63) >> 4)];
+                const int ei = (int)(i & 15), hi = ei & 1, j = ei >> 1;
                 const uint32_t mag = (src >> (16 * hi + j)) & 1u;
                 const uint32_t neg = (src >> (16 * hi + 8 + j)) & 1u;
                 const int eh = e & 1, ej = e >> 1;
                 word |= (mag << (16 * eh + ej)) | (neg << (16 * eh + 8 + ej));
+                if (++k == (uint32_t)K) {
+                    k = 0;
+                    if (++sp == (uint32_t)S) {
+                        sp = 0;
+                        ++rp;
+                    }
+                }
             }
         }
         codes_t[gid] = word;
@@ -352,9 +360,9 @@ __global__ __launch_bounds__(256) void repack_bwd_kernel(const uint32_t* __restr
     if (gid < pairs) {
         uint32_t v = 0;
         for (int h = 0; h < 2; ++h) {
-            const int64_t et = 2 * gid + h;
+            const uint32_t et = 2 * (uint32_t)gid + h;
             if (et < nt) {
-                uint32_t b = f32_to_bf16_bits(alpha[et % K]);
+                uint32_t b = f32_to_bf16_bits(alpha[et % (uint32_t)K]);
                 if ((b & 0x7F80u) == 0) b = 0;  // a denormal scale is flushed: exponent + 1 would not double it
                 v |= b << (16 * h);
             }
