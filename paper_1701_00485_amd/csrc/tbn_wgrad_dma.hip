@@ -305,22 +305,45 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
     // pixels PAIRS wave + jj and that + NPAIR.  Computed for the next stage while the
     // MFMAs of the current one run.
     uint32_t o_dy[PAIRS], o_x[PAIRS];
+    // the PAIRS pixels of a lane are consecutive: the first is located by division, the
+    // others step q (and carry into p and the image)
+    const int q_step = a.sw, p_step = a.sh;
     auto table = [&](int st_i) {
+        const int64_t m0 = m_begin + (int64_t)st_i * PIXR + PAIRS * wave + NPAIR * half;
+        uint32_t mm = m0 < m_end ? (uint32_t)m0 : 0u;
+        uint32_t img = fdiv(mm, ka.div_pq);
+        const uint32_t pq = mm - img * PQ;
+        uint32_t p = fdiv(pq, ka.div_q);
+        uint32_t q_ = pq - p * (uint32_t)a.Q;
+        int h = (int)p * a.sh - a.ph + xr, w = (int)q_ * a.sw - a.pw + xs;
 #pragma unroll
         for (int jj = 0; jj < PAIRS; ++jj) {
-            const int64_t m = m_begin + (int64_t)st_i * PIXR + PAIRS * wave + jj + NPAIR * half;
-            const bool mok = m < m_end;
-            const uint32_t mm = mok ? (uint32_t)m : 0u;
-            uint32_t img;
-            int h, w;
-            locate(mm, xr, xs, &img, &h, &w);
-            o_dy[jj] = mok ? (mm * (uint32_t)K * 2u + dy_col) | dy_bad : 0x80000000u;
+            const bool mok = m0 + jj < m_end;
+            const uint32_t mj = mm + jj;
+            o_dy[jj] = mok ? (mj * (uint32_t)K * 2u + dy_col) | dy_bad : 0x80000000u;
             const bool ok = mok && x_ok && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
             o_x[jj] = ok ? (img * HWC + (uint32_t)((h * a.W + w) * C + xc)) * 2u : 0x80000000u;
+            if (jj + 1 < PAIRS) {  // next output pixel
+                ++q_;
+                w += q_step;
+                if (q_ == (uint32_t)a.Q) {
+                    q_ = 0;
+                    w -= a.Q * q_step;
+                    ++p;
+                    h += p_step;
+                    if (p == (uint32_t)a.P) {
+                        p = 0;
+                        h -= a.P * p_step;
+                        ++img;
+                    }
+                }
+            }
         }
     };
-    auto issue = [&](int st_i) {
-        const uint32_t st = smem_base + (uint32_t)((st_i % STAGES) * PR_STAGE);
+    int islot = 0;  // ring slot of the next stage to issue
+    auto issue = [&](int) {
+        const uint32_t st = smem_base + (uint32_t)(islot * PR_STAGE);
+        islot = islot + 1 == STAGES ? 0 : islot + 1;
 #pragma unroll
         for (int jj = 0; jj < PAIRS; ++jj) {
             const int j = PAIRS * wave + jj;  // pair slot (wave-uniform)
@@ -367,10 +390,13 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
     const int g = lane >> 4, i16 = lane & 15;
     const int rho = 8 * (g >> 1) + (i16 >> 2);
     const uint32_t col_off = (uint32_t)((16 * (g & 1) + 4 * (i16 & 3)) * 2);
-    auto row_off = [&](int u) {
+    uint32_t ro_u[PIXR / 16];  // per step u: this lane's byte offset inside a stage operand
+#pragma unroll
+    for (int u = 0; u < PIXR / 16; ++u) {
         const int r = 16 * u + rho;
-        return (uint32_t)((r % NPAIR) * PP + (r / NPAIR) * 512) + col_off;
-    };
+        ro_u[u] = (uint32_t)((r % NPAIR) * PP + (r / NPAIR) * 512) + col_off;
+    }
+    auto row_off = [&](int u) { return ro_u[u]; };
     const uint32_t a_base = (uint32_t)(wm * 128 * 2);
     const uint32_t b_base = (uint32_t)PR_OP + (uint32_t)(wn * 32 * TN * 2);
     auto operand = [&](uint32_t addr) {
@@ -400,17 +426,22 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
         }
     }
     table(STAGES - 1);
+    int cslot = 0;  // ring slot of the stage being multiplied
     for (int it = 0; it < nst; ++it) {
-        // this wave's DMAs of stage `it` landed (later stages may still be in flight)
-        const int later = min(nst - 1 - it, STAGES - 2);
-        wait_vmcnt(later * (kDmas + 1) + 1);
+        // this wave's DMAs of stage `it` landed (later stages and the prefetch issued with
+        // stage `it` may still be in flight; in the last stages simply everything)
+        if (it + STAGES - 2 < nst)
+            wait_vmcnt((STAGES - 2) * (kDmas + 1) + 1);
+        else
+            wait_vmcnt(0);
         __syncthreads();  // ... and every other wave's; all reads of stage it-1 are done
         if (it + STAGES - 1 < nst) {
             issue(it + STAGES - 1);  // into stage it-1's buffer
             prefetch(it + STAGES - 1 + pf_dist);
             table(it + STAGES);      // the offsets of the next copy, during the MFMAs
         }
-        const uint32_t st = smem_base + (uint32_t)((it % STAGES) * PR_STAGE);
+        const uint32_t st = smem_base + (uint32_t)(cslot * PR_STAGE);
+        cslot = cslot + 1 == STAGES ? 0 : cslot + 1;
         bf16x8 af[2][TM], bf[2][TN];
         auto load = [&](int u, int b) {
             const uint32_t ro = row_off(u);
