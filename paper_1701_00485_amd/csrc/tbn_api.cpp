@@ -73,7 +73,10 @@ int wgrad_splits(const Geometry& g) {
     const int64_t chunks = (g.N * g.P * g.Q + 63) / 64;
     const int64_t target = dma ? plan.resident_blocks : 1024;
     int64_t splits = target / tiles;
-    const int64_t max_by_len = chunks / 16 > 0 ? chunks / 16 : 1;  // >= 16 chunks per split
+    // at least 16 chunks per split for the LDS-DMA kernel, 4 for the register-staged one
+    // (its first-layer shapes have one output tile and a long reduction)
+    const int64_t min_chunks = dma ? 16 : 4;
+    const int64_t max_by_len = chunks / min_chunks > 0 ? chunks / min_chunks : 1;
     if (splits > max_by_len) splits = max_by_len;
     if (splits > 256) splits = 256;
     if (splits < 1) splits = 1;

@@ -231,6 +231,29 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
     dw[i] = s;
 }
 
+// Few outputs with many splits (first layers: K x R*S*C of a few thousand): G threads
+// per output each add every G-th split, then the G sums are added in group order (fixed,
+// so the result is the same on every run).
+template <int G>
+__global__ __launch_bounds__(256) void split_reduce_groups_kernel(const float* __restrict__ part,
+                                                                  int32_t splits, int64_t count,
+                                                                  float* __restrict__ dw, int32_t accumulate) {
+    constexpr int OPB = 256 / G;  // outputs per block
+    __shared__ float sh[256];
+    const int o = threadIdx.x % OPB, g = threadIdx.x / OPB;
+    const int64_t i = (int64_t)blockIdx.x * OPB + o;
+    float s = 0.0f;
+    if (i < count)
+        for (int z = g; z < splits; z += G) s += part[(int64_t)z * count + i];
+    sh[threadIdx.x] = s;
+    __syncthreads();
+    if (g == 0 && i < count) {
+        float t = accumulate ? dw[i] : 0.0f;
+        for (int gg = 0; gg < G; ++gg) t += sh[gg * OPB + o];
+        dw[i] = t;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_wgrad(const WgradArgs& a, hipStream_t stream) {
@@ -251,8 +274,13 @@ hipError_t launch_wgrad(const WgradArgs& a, hipStream_t stream) {
 
 hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, float* dw,
                                int32_t accumulate, hipStream_t stream) {
-    hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, stream, partials,
-                       splits, count, dw, accumulate);
+    if (count < 65536 && splits >= 32) {
+        hipLaunchKernelGGL(split_reduce_groups_kernel<16>, dim3((unsigned)((count + 15) / 16)), dim3(256), 0, stream,
+                           partials, splits, count, dw, accumulate);
+    } else {
+        hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, stream,
+                           partials, splits, count, dw, accumulate);
+    }
     return hipGetLastError();
 }
 
