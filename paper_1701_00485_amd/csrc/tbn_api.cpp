@@ -278,7 +278,22 @@ tbn_status tbn_conv2d_fwd_dense(const tbn_conv_desc* desc, const void* x, tbn_dt
     a.ph = (int32_t)g.ph; a.pw = (int32_t)g.pw; a.P = (int32_t)g.P; a.Q = (int32_t)g.Q;
     a.x_f32 = xt == TBN_F32;
     a.y_f32 = yt == TBN_F32;
-    hipError_t e = tbn::launch_conv_dense(a, stream);
+    // few input channels: the thin-input MFMA kernel with the real filters staged as bf16
+    // (inputs small enough to need no workspace); otherwise the vector-ALU kernel
+    tbn::ConvGemmArgs t = fwd_args(g, xt, yt);
+    t.x = x;
+    t.wdense = w;
+    t.scale = a.scale;
+    t.bias = a.bias;
+    t.residual = a.residual;
+    t.relu = a.relu;
+    t.y = y;
+    tbn::ThinGeom tg;
+    hipError_t e;
+    if (tbn::conv_thin_plan(t, &tg) && !tg.dma)
+        e = tbn::launch_conv_thin(t, tg, stream);
+    else
+        e = tbn::launch_conv_dense(a, stream);
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_fwd_dense");
 }
 

@@ -137,15 +137,29 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
     const int NB = (n + 63) / 64;
     const int k0 = blockIdx.y * FB;
 
-    // ---- the block's packed codes (NB KiB, contiguous in the blocked layout) into LDS,
-    //      then decoded as bf16 W~, zero at padding taps / channels / filters ----
+    // ---- the block's filters into LDS as bf16, zero at padding taps / channels / filters:
+    //      the packed codes (NB KiB, contiguous in the blocked layout) decoded to W~, or
+    //      the real filters of a full-precision layer rounded to bf16 ----
     uint32_t* cw = reinterpret_cast<uint32_t*>(lds + g.s_off);
-    {
-        const u32x4* src = reinterpret_cast<const u32x4*>(a.codes + (int64_t)blockIdx.y * NB * 256);
-        for (int i = tid; i < NB * 64; i += 256) reinterpret_cast<u32x4*>(cw)[i] = src[i];
-    }
-    __syncthreads();
-    {
+    if (a.wdense) {
+        // a full-precision layer: its real filters rounded to bf16 (nearest even)
+        const int f = tid >> 2;
+        const bool fk = k0 + f < K;
+        for (int j = tid & 3; j < g.WPITCH; j += 4) {
+            uint32_t v = 0;
+            if (j < g.RT && fk) {
+                const int r = j >> g.logT, t = j & (g.T - 1);
+                const int s = t / CP, c = t & (CP - 1);
+                if (s < S && c < C) v = f32_to_bf16_bits(a.wdense[(int64_t)(k0 + f) * n + (r * S + s) * C + c]);
+            }
+            wl[f * g.WPITCH + j] = (uint16_t)v;
+        }
+    } else {
+        {
+            const u32x4* src = reinterpret_cast<const u32x4*>(a.codes + (int64_t)blockIdx.y * NB * 256);
+            for (int i = tid; i < NB * 64; i += 256) reinterpret_cast<u32x4*>(cw)[i] = src[i];
+        }
+        __syncthreads();
         const int f = tid >> 2;  // 4 threads per filter row
         const bool fk = k0 + f < K;
         for (int j = tid & 3; j < g.WPITCH; j += 4) {

@@ -51,6 +51,9 @@ struct ConvGemmArgs {
     // sum_{r < R} 2^(r*S) that replicates a filter row's in-image taps over its rows
     FastDiv div_tiles, div_tilesN;
     uint32_t rep_lo, rep_hi;
+    // thin-input kernel only: real-valued filters [Kf][R][S][C] fp32 (rounded to bf16 as
+    // they are staged) in place of the packed codes, for a layer kept in full precision
+    const float* wdense;
 };
 
 hipError_t launch_quantize(const float* w, int64_t K, int64_t n, uint32_t* codes, float* alpha,

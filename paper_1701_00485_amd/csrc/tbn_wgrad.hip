@@ -227,7 +227,16 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= count) return;
     float s = accumulate ? dw[i] : 0.0f;
-    for (int z = 0; z < splits; ++z) s += part[(int64_t)z * count + i];
+    // eight partials loaded together, then added in split order
+    int z = 0;
+    for (; z + 8 <= splits; z += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(z + u) * count + i];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; z < splits; ++z) s += part[(int64_t)z * count + i];
     dw[i] = s;
 }
 

@@ -327,7 +327,8 @@ def test_fwd_epilogue(tbn, g):
 
 
 DENSE_CASES = [(4, 32, 32, 3, 128, 3, 3, 1, 1), (2, 9, 9, 3, 5, 3, 3, 2, 1), (2, 12, 11, 40, 24, 3, 3, 1, 1),
-               (1, 20, 20, 70, 16, 3, 3, 1, 1)]  # the last reduces over 630 > one LDS fill of 512
+               (1, 20, 20, 70, 16, 3, 3, 1, 1),  # reduces over 630 > one LDS fill of 512 (vector-ALU kernel)
+               (2, 14, 14, 1, 32, 5, 5, 1, 2), (2, 10, 9, 7, 70, 3, 3, 1, 1)]  # thin MFMA kernel, two filter blocks
 
 
 @pytest.mark.parametrize("g", DENSE_CASES)
