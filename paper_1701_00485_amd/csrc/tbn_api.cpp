@@ -83,6 +83,19 @@ int wgrad_splits(const Geometry& g) {
     return (int)splits;
 }
 
+// bwd_weight of an input with C < 8 channels (and K % 8 == 0): run on the LDS-DMA kernel
+// over the input copied into 8 channels.  Workspace: the 8-channel input, then the split
+// partials of the 8-channel gradient.
+bool wgrad_pad8(const Geometry& g, Geometry* g8) {
+    if (g.C >= 8 || g.K % 8 != 0) return false;
+    *g8 = g;
+    g8->C = 8;
+    if (g8->R * g8->S * 8 > kI32Max / 2) return false;
+    return tbn::wgrad_dma_eligible(wgrad_args(*g8));
+}
+
+int64_t pad8_x_bytes(const Geometry& g) { return round_up(g.N * g.H * g.W * 16, 256); }
+
 struct BwdDataWs {
     int64_t codes_bytes, apair_off, apair_bytes, partial_off, partial_bytes, total;
 };
@@ -176,6 +189,11 @@ tbn_status tbn_workspace_size(tbn_op op, const tbn_conv_desc* desc, size_t* byte
         }
         case TBN_OP_BWD_DATA: *bytes = (size_t)bwd_data_ws(g).total; return TBN_OK;
         case TBN_OP_BWD_WEIGHT: {
+            Geometry g8;
+            if (wgrad_pad8(g, &g8)) {
+                *bytes = (size_t)pad8_x_bytes(g) + (size_t)wgrad_splits(g8) * (size_t)(g.K * g.R * g.S * 8) * 4;
+                return TBN_OK;
+            }
             const int splits = wgrad_splits(g);
             *bytes = splits > 1 ? (size_t)splits * (size_t)(g.K * g.R * g.S * g.C) * 4 : 0;
             return TBN_OK;
@@ -333,6 +351,32 @@ tbn_status tbn_conv2d_bwd_weight(const tbn_conv_desc* desc, const void* x, const
     if (st != TBN_OK) return st;
     if (!x || !dy || !dw) return fail(TBN_ERR_NULL, "x, dy and dw are required");
     if (!aligned16(x) || !aligned16(dy) || !aligned16(dw)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
+    Geometry g8;
+    if (wgrad_pad8(g, &g8)) {
+        // few input channels: 8-channel copy of x, 8-channel gradient, channels < C kept
+        const int splits = wgrad_splits(g8);
+        const int64_t xb = pad8_x_bytes(g);
+        const size_t need = (size_t)xb + (size_t)splits * (size_t)(g.K * g.R * g.S * 8) * 4;
+        if (!ws || ws_bytes < need) return fail(TBN_ERR_WORKSPACE, "workspace too small");
+        if (!aligned16(ws)) return fail(TBN_ERR_ALIGN, "workspace must be 16-byte aligned");
+        uint16_t* x8 = reinterpret_cast<uint16_t*>(ws);
+        float* part = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(ws) + xb);
+        hipError_t e = tbn::launch_pad_channels8(reinterpret_cast<const uint16_t*>(x), g.N * g.H * g.W, (int32_t)g.C,
+                                                 x8, stream);
+        if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_weight (channel copy)");
+        tbn::WgradArgs a = wgrad_args(g8);
+        a.x = x8;
+        a.dy = reinterpret_cast<const uint16_t*>(dy);
+        a.out = part;
+        const int64_t chunks = (g.N * g.P * g.Q + 63) / 64;
+        a.splits = splits;
+        a.chunks_per_split = (int32_t)((chunks + splits - 1) / splits);
+        a.accumulate = 0;
+        e = tbn::launch_wgrad(a, stream);
+        if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_weight");
+        e = tbn::launch_split_reduce_compact(part, splits, g.K * g.R * g.S, (int32_t)g.C, dw, accumulate, stream);
+        return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_bwd_weight (reduce)");
+    }
     const int splits = wgrad_splits(g);
     const int64_t count = g.K * g.R * g.S * g.C;
     const bool direct = splits == 1;  // one split writes (or adds to) dw itself

@@ -160,6 +160,12 @@ struct WgradDmaPlan {
 WgradDmaPlan wgrad_dma_plan(int K, int J);
 hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream);
 
+// Filter gradient of an input with C < 8 channels on the LDS-DMA kernel: the input copied
+// into 8 channels (zeros beyond C), then the 8-channel gradient's split partials summed
+// into the C-channel dw.
+hipError_t launch_pad_channels8(const uint16_t* x, int64_t pixels, int32_t C, uint16_t* x8, hipStream_t stream);
+hipError_t launch_split_reduce_compact(const float* partials, int32_t splits, int64_t rows, int32_t C, float* dw,
+                                       int32_t accumulate, hipStream_t stream);
 hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, float* dw,
                                int32_t accumulate, hipStream_t stream);
 

@@ -263,7 +263,63 @@ __global__ __launch_bounds__(256) void split_reduce_groups_kernel(const float* _
     }
 }
 
+// Input with C < 8 channels copied into an 8-channel layout (zeros in channels C..7), so
+// that the filter gradient can run on the LDS-DMA kernel.  One thread per pixel.
+__global__ __launch_bounds__(256) void pad_channels8_kernel(const uint16_t* __restrict__ x, int64_t pixels, int32_t C,
+                                                            uint16_t* __restrict__ x8) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= pixels) return;
+    uint32_t v[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) v[c] = c < C ? x[i * C + c] : 0u;
+    reinterpret_cast<u32x4*>(x8)[i] =
+        u32x4{v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16)};
+}
+
+// Sum of the split partials of an 8-channel filter gradient [splits][rows][8], keeping
+// channels c < C: dw[row][c] (+)= sum_z part[z][row][c], G threads per output adding every
+// G-th split, combined in group order (fixed).
+template <int G>
+__global__ __launch_bounds__(256) void split_reduce_compact_kernel(const float* __restrict__ part, int32_t splits,
+                                                                   int64_t rows, int32_t C, float* __restrict__ dw,
+                                                                   int32_t accumulate) {
+    constexpr int OPB = 256 / G;
+    __shared__ float sh[256];
+    const int o = threadIdx.x % OPB, g = threadIdx.x / OPB;
+    const int64_t i = (int64_t)blockIdx.x * OPB + o;  // output (row, c)
+    const int64_t count = rows * C;
+    const int64_t src = (i / C) * 8 + i % C;
+    float s = 0.0f;
+    if (i < count)
+        for (int z = g; z < splits; z += G) s += part[(int64_t)z * rows * 8 + src];
+    sh[threadIdx.x] = s;
+    __syncthreads();
+    if (g == 0 && i < count) {
+        float t = accumulate ? dw[i] : 0.0f;
+        for (int gg = 0; gg < G; ++gg) t += sh[gg * OPB + o];
+        dw[i] = t;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_pad_channels8(const uint16_t* x, int64_t pixels, int32_t C, uint16_t* x8, hipStream_t stream) {
+    hipLaunchKernelGGL(pad_channels8_kernel, dim3((unsigned)((pixels + 255) / 256)), dim3(256), 0, stream, x, pixels, C,
+                       x8);
+    return hipGetLastError();
+}
+
+hipError_t launch_split_reduce_compact(const float* partials, int32_t splits, int64_t rows, int32_t C, float* dw,
+                                       int32_t accumulate, hipStream_t stream) {
+    const int64_t count = rows * C;
+    if (count < 65536 && splits >= 32)
+        hipLaunchKernelGGL(split_reduce_compact_kernel<16>, dim3((unsigned)((count + 15) / 16)), dim3(256), 0, stream,
+                           partials, splits, rows, C, dw, accumulate);
+    else
+        hipLaunchKernelGGL(split_reduce_compact_kernel<1>, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, stream,
+                           partials, splits, rows, C, dw, accumulate);
+    return hipGetLastError();
+}
 
 hipError_t launch_wgrad(const WgradArgs& a, hipStream_t stream) {
     if (wgrad_dma_eligible(a)) return launch_wgrad_dma(a, stream);
