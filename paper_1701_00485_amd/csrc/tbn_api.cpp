@@ -96,6 +96,19 @@ bool wgrad_pad8(const Geometry& g, Geometry* g8) {
 
 int64_t pad8_x_bytes(const Geometry& g) { return round_up(g.N * g.H * g.W * 16, 256); }
 
+// A gradient with K % 8 != 0 channels (a 10-way classifier): dy copied into Kp = K rounded
+// up to 8 channels (zeros beyond K) so that both backward passes run on the LDS-DMA
+// kernels.  `gk` is the geometry with Kp filters.
+bool grad_padk(const Geometry& g, Geometry* gk) {
+    if (g.K % 8 == 0 || g.C % 8 != 0) return false;
+    *gk = g;
+    gk->K = round_up(g.K, 8);
+    if (gk->R * gk->S * gk->K > kI32Max / 2) return false;
+    return true;
+}
+
+int64_t padk_dy_bytes(const Geometry& gk) { return round_up(gk.N * gk.P * gk.Q * gk.K * 2, 256); }
+
 struct BwdDataWs {
     int64_t codes_bytes, apair_off, apair_bytes, partial_off, partial_bytes, total;
 };
@@ -187,11 +200,20 @@ tbn_status tbn_workspace_size(tbn_op op, const tbn_conv_desc* desc, size_t* byte
             *bytes = b16 > b32 ? b16 : b32;
             return TBN_OK;
         }
-        case TBN_OP_BWD_DATA: *bytes = (size_t)bwd_data_ws(g).total; return TBN_OK;
+        case TBN_OP_BWD_DATA: {
+            Geometry gk;
+            *bytes = grad_padk(g, &gk) ? (size_t)(round_up(bwd_data_ws(gk).total, 256) + padk_dy_bytes(gk))
+                                       : (size_t)bwd_data_ws(g).total;
+            return TBN_OK;
+        }
         case TBN_OP_BWD_WEIGHT: {
             Geometry g8;
             if (wgrad_pad8(g, &g8)) {
                 *bytes = (size_t)pad8_x_bytes(g) + (size_t)wgrad_splits(g8) * (size_t)(g.K * g.R * g.S * 8) * 4;
+                return TBN_OK;
+            }
+            if (grad_padk(g, &g8) && tbn::wgrad_dma_eligible(wgrad_args(g8))) {
+                *bytes = (size_t)padk_dy_bytes(g8) + (size_t)wgrad_splits(g8) * (size_t)(g8.K * g.R * g.S * g.C) * 4;
                 return TBN_OK;
             }
             const int splits = wgrad_splits(g);
@@ -325,16 +347,30 @@ tbn_status tbn_conv2d_bwd_data(const tbn_conv_desc* desc, const void* dy, const 
     if (g.sh != 1 || g.sw != 1) return fail(TBN_ERR_UNSUPPORTED, "backward-data supports stride 1 only");
     if (!aligned16(dy) || !aligned16(codes) || !aligned16(dx) || !aligned4(alpha))
         return fail(TBN_ERR_ALIGN, "dy, codes and dx must be 16-byte aligned");
-    const BwdDataWs w = bwd_data_ws(g);
-    if (!ws || ws_bytes < (size_t)w.total) return fail(TBN_ERR_WORKSPACE, "workspace too small");
+    // K % 8 != 0: the GEMM runs over dy copied into Kp channels (workspace, after the rest)
+    Geometry gk;
+    const bool padk = grad_padk(g, &gk);
+    const Geometry& gg = padk ? gk : g;
+    const BwdDataWs w = bwd_data_ws(gg);
+    const int64_t dy_off = round_up(w.total, 256);  // the Kp-channel copy of dy (padk only)
+    const int64_t total = padk ? dy_off + padk_dy_bytes(gk) : w.total;
+    if (!ws || ws_bytes < (size_t)total) return fail(TBN_ERR_WORKSPACE, "workspace too small");
     if (!aligned16(ws)) return fail(TBN_ERR_ALIGN, "workspace must be 16-byte aligned");
     uint32_t* codes_t = reinterpret_cast<uint32_t*>(ws);
     uint32_t* apair = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(ws) + w.apair_off);
-    hipError_t e = tbn::launch_repack_bwd(codes, alpha, (int32_t)g.K, (int32_t)g.R, (int32_t)g.S, (int32_t)g.C,
-                                          codes_t, apair, stream);
+    hipError_t e = tbn::launch_repack_bwd(codes, alpha, (int32_t)gg.K, (int32_t)g.K, (int32_t)g.R, (int32_t)g.S,
+                                          (int32_t)g.C, codes_t, apair, stream);
     if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_data (repack)");
-    tbn::ConvGemmArgs a = bwd_data_args(g, dxt);
-    a.x = dy;
+    const void* dyk = dy;
+    if (padk) {
+        uint16_t* dyp = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(ws) + dy_off);
+        e = tbn::launch_pad_channels(reinterpret_cast<const uint16_t*>(dy), g.N * g.P * g.Q, (int32_t)g.K,
+                                     (int32_t)gk.K, dyp, stream);
+        if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_data (channel copy)");
+        dyk = dyp;
+    }
+    tbn::ConvGemmArgs a = bwd_data_args(gg, dxt);
+    a.x = dyk;
     a.codes = codes_t;
     a.apair = apair;
     a.colscale = nullptr;
@@ -361,8 +397,8 @@ tbn_status tbn_conv2d_bwd_weight(const tbn_conv_desc* desc, const void* x, const
         if (!aligned16(ws)) return fail(TBN_ERR_ALIGN, "workspace must be 16-byte aligned");
         uint16_t* x8 = reinterpret_cast<uint16_t*>(ws);
         float* part = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(ws) + xb);
-        hipError_t e = tbn::launch_pad_channels8(reinterpret_cast<const uint16_t*>(x), g.N * g.H * g.W, (int32_t)g.C,
-                                                 x8, stream);
+        hipError_t e = tbn::launch_pad_channels(reinterpret_cast<const uint16_t*>(x), g.N * g.H * g.W, (int32_t)g.C, 8,
+                                                x8, stream);
         if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_weight (channel copy)");
         tbn::WgradArgs a = wgrad_args(g8);
         a.x = x8;
@@ -375,6 +411,32 @@ tbn_status tbn_conv2d_bwd_weight(const tbn_conv_desc* desc, const void* x, const
         e = tbn::launch_wgrad(a, stream);
         if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_weight");
         e = tbn::launch_split_reduce_compact(part, splits, g.K * g.R * g.S, (int32_t)g.C, dw, accumulate, stream);
+        return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_bwd_weight (reduce)");
+    }
+    if (grad_padk(g, &g8) && tbn::wgrad_dma_eligible(wgrad_args(g8))) {
+        // K % 8 != 0: dy copied into Kp channels; rows k < K of the Kp-row partials summed
+        const int splits = wgrad_splits(g8);
+        const int64_t dyb = padk_dy_bytes(g8);
+        const int64_t J = g.R * g.S * g.C;
+        const size_t need = (size_t)dyb + (size_t)splits * (size_t)(g8.K * J) * 4;
+        if (!ws || ws_bytes < need) return fail(TBN_ERR_WORKSPACE, "workspace too small");
+        if (!aligned16(ws)) return fail(TBN_ERR_ALIGN, "workspace must be 16-byte aligned");
+        uint16_t* dyp = reinterpret_cast<uint16_t*>(ws);
+        float* part = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(ws) + dyb);
+        hipError_t e = tbn::launch_pad_channels(reinterpret_cast<const uint16_t*>(dy), g.N * g.P * g.Q, (int32_t)g.K,
+                                                (int32_t)g8.K, dyp, stream);
+        if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_weight (channel copy)");
+        tbn::WgradArgs a = wgrad_args(g8);
+        a.x = reinterpret_cast<const uint16_t*>(x);
+        a.dy = dyp;
+        a.out = part;
+        const int64_t chunks = (g.N * g.P * g.Q + 63) / 64;
+        a.splits = splits;
+        a.chunks_per_split = (int32_t)((chunks + splits - 1) / splits);
+        a.accumulate = 0;
+        e = tbn::launch_wgrad(a, stream);
+        if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_weight");
+        e = tbn::launch_split_reduce(part, splits, g.K * J, g8.K * J, dw, accumulate, stream);
         return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_bwd_weight (reduce)");
     }
     const int splits = wgrad_splits(g);
@@ -396,7 +458,7 @@ tbn_status tbn_conv2d_bwd_weight(const tbn_conv_desc* desc, const void* x, const
     hipError_t e = tbn::launch_wgrad(a, stream);
     if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_weight");
     if (!direct) {
-        e = tbn::launch_split_reduce(reinterpret_cast<const float*>(ws), splits, count, dw, accumulate, stream);
+        e = tbn::launch_split_reduce(reinterpret_cast<const float*>(ws), splits, count, count, dw, accumulate, stream);
         if (e != hipSuccess) return hip_fail(e, "tbn_conv2d_bwd_weight (reduce)");
     }
     return TBN_OK;

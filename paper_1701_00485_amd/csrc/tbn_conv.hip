@@ -311,8 +311,10 @@ hipError_t launch_mode(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
 }
 
 // ---------------- backward-data operand preparation ----------------
+// K may exceed the layer's Kreal filters (a gradient padded to a multiple of 8 channels):
+// filters k >= Kreal read the zero padding bits of the last 64-filter block and get scale 0.
 __global__ __launch_bounds__(256) void repack_bwd_kernel(const uint32_t* __restrict__ codes,
-                                                         const float* __restrict__ alpha, int32_t K,
+                                                         const float* __restrict__ alpha, int32_t K, int32_t Kreal,
                                                          int32_t R, int32_t S, int32_t C,
                                                          uint32_t* __restrict__ codes_t,
                                                          uint32_t* __restrict__ apair) {
@@ -362,7 +364,8 @@ __global__ __launch_bounds__(256) void repack_bwd_kernel(const uint32_t* __restr
         for (int h = 0; h < 2; ++h) {
             const uint32_t et = 2 * (uint32_t)gid + h;
             if (et < nt) {
-                uint32_t b = f32_to_bf16_bits(alpha[et % (uint32_t)K]);
+                const uint32_t kk = et % (uint32_t)K;
+                uint32_t b = kk < (uint32_t)Kreal ? f32_to_bf16_bits(alpha[kk]) : 0u;
                 if ((b & 0x7F80u) == 0) b = 0;  // a denormal scale is flushed: exponent + 1 would not double it
                 v |= b << (16 * h);
             }
@@ -429,14 +432,14 @@ hipError_t launch_conv_gemm(const ConvGemmArgs& args, hipStream_t stream) {
     return vec ? launch_mode<A_VEC8, false>(a, cfg, stream) : launch_mode<A_SCALAR, false>(a, cfg, stream);
 }
 
-hipError_t launch_repack_bwd(const uint32_t* codes, const float* alpha, int32_t K, int32_t R, int32_t S,
-                             int32_t C, uint32_t* codes_t, uint32_t* apair, hipStream_t stream) {
+hipError_t launch_repack_bwd(const uint32_t* codes, const float* alpha, int32_t K, int32_t Kreal, int32_t R,
+                             int32_t S, int32_t C, uint32_t* codes_t, uint32_t* apair, hipStream_t stream) {
     const int64_t nt = (int64_t)R * S * K;
     const int64_t nbt = (nt + 63) / 64;
     const int64_t words = (int64_t)((C + 63) / 64) * nbt * 256;
     const int64_t total = words > nbt * 32 ? words : nbt * 32;
     hipLaunchKernelGGL(repack_bwd_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream, codes,
-                       alpha, K, R, S, C, codes_t, apair);
+                       alpha, K, Kreal, R, S, C, codes_t, apair);
     return hipGetLastError();
 }
 

@@ -130,10 +130,10 @@ hipError_t launch_fc_stream(const ConvGemmArgs& a, const FcStreamPlan& p, hipStr
 
 // Re-pack the codes of K filters [K][R][S][C] into the codes of the C filters of the
 // transposed, spatially flipped layer [C][R][S][K] (backward-data operand), and build
-// the bf16 scale pairs of that layer's element pairs.
-hipError_t launch_repack_bwd(const uint32_t* codes, const float* alpha, int32_t K, int32_t R,
-                             int32_t S, int32_t C, uint32_t* codes_t, uint32_t* apair,
-                             hipStream_t stream);
+// the bf16 scale pairs of that layer's element pairs; filters Kreal..K-1 (channel padding
+// of the gradient) get scale 0.
+hipError_t launch_repack_bwd(const uint32_t* codes, const float* alpha, int32_t K, int32_t Kreal, int32_t R,
+                             int32_t S, int32_t C, uint32_t* codes_t, uint32_t* apair, hipStream_t stream);
 
 struct WgradArgs {
     const uint16_t* x;        // NHWC [N][H][W][C] bf16
@@ -160,13 +160,15 @@ struct WgradDmaPlan {
 WgradDmaPlan wgrad_dma_plan(int K, int J);
 hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream);
 
-// Filter gradient of an input with C < 8 channels on the LDS-DMA kernel: the input copied
-// into 8 channels (zeros beyond C), then the 8-channel gradient's split partials summed
-// into the C-channel dw.
-hipError_t launch_pad_channels8(const uint16_t* x, int64_t pixels, int32_t C, uint16_t* x8, hipStream_t stream);
+// Channel counts the LDS-DMA kernels cannot take (C < 8 inputs, K % 8 != 0 gradients): the
+// tensor copied into Cp channels (a multiple of 8, zeros beyond C); for the filter gradient
+// of a C < 8 input, the 8-channel gradient's split partials summed into the C-channel dw.
+hipError_t launch_pad_channels(const uint16_t* x, int64_t pixels, int32_t C, int32_t Cp, uint16_t* xp,
+                               hipStream_t stream);
 hipError_t launch_split_reduce_compact(const float* partials, int32_t splits, int64_t rows, int32_t C, float* dw,
                                        int32_t accumulate, hipStream_t stream);
-hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, float* dw,
+// partials [splits][stride]: dw[i] (+)= sum_z partials[z][i] for i < count
+hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, int64_t stride, float* dw,
                                int32_t accumulate, hipStream_t stream);
 
 struct DenseConvArgs {

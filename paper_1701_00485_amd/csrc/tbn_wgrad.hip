@@ -221,8 +221,9 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradKernelArgs ka) {
     }
 }
 
+// partials [splits][stride] (the first `count` of each split are summed)
 __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part, int32_t splits,
-                                                           int64_t count, float* __restrict__ dw,
+                                                           int64_t count, int64_t stride, float* __restrict__ dw,
                                                            int32_t accumulate) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= count) return;
@@ -232,11 +233,11 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
     for (; z + 8 <= splits; z += 8) {
         float v[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(z + u) * count + i];
+        for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(z + u) * stride + i];
 #pragma unroll
         for (int u = 0; u < 8; ++u) s += v[u];
     }
-    for (; z < splits; ++z) s += part[(int64_t)z * count + i];
+    for (; z < splits; ++z) s += part[(int64_t)z * stride + i];
     dw[i] = s;
 }
 
@@ -245,7 +246,7 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
 // so the result is the same on every run).
 template <int G>
 __global__ __launch_bounds__(256) void split_reduce_groups_kernel(const float* __restrict__ part,
-                                                                  int32_t splits, int64_t count,
+                                                                  int32_t splits, int64_t count, int64_t stride,
                                                                   float* __restrict__ dw, int32_t accumulate) {
     constexpr int OPB = 256 / G;  // outputs per block
     __shared__ float sh[256];
@@ -253,7 +254,7 @@ __global__ __launch_bounds__(256) void split_reduce_groups_kernel(const float* _
     const int64_t i = (int64_t)blockIdx.x * OPB + o;
     float s = 0.0f;
     if (i < count)
-        for (int z = g; z < splits; z += G) s += part[(int64_t)z * count + i];
+        for (int z = g; z < splits; z += G) s += part[(int64_t)z * stride + i];
     sh[threadIdx.x] = s;
     __syncthreads();
     if (g == 0 && i < count) {
@@ -263,16 +264,20 @@ __global__ __launch_bounds__(256) void split_reduce_groups_kernel(const float* _
     }
 }
 
-// Input with C < 8 channels copied into an 8-channel layout (zeros in channels C..7), so
-// that the filter gradient can run on the LDS-DMA kernel.  One thread per pixel.
-__global__ __launch_bounds__(256) void pad_channels8_kernel(const uint16_t* __restrict__ x, int64_t pixels, int32_t C,
-                                                            uint16_t* __restrict__ x8) {
+// An NHWC tensor with C channels copied into Cp channels (Cp a multiple of 8, zeros in
+// channels C..Cp-1), so that the LDS-DMA kernels (8-channel granularity) apply.  One thread
+// per pixel and 8-channel group.
+__global__ __launch_bounds__(256) void pad_channels_kernel(const uint16_t* __restrict__ x, int64_t pixels, int32_t C,
+                                                           int32_t Cp, uint16_t* __restrict__ xp) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (i >= pixels) return;
+    const int groups = Cp / 8;
+    if (i >= pixels * groups) return;
+    const int64_t pix = i / groups;
+    const int c0 = (int)(i - pix * groups) * 8;
     uint32_t v[8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) v[c] = c < C ? x[i * C + c] : 0u;
-    reinterpret_cast<u32x4*>(x8)[i] =
+    for (int c = 0; c < 8; ++c) v[c] = c0 + c < C ? x[pix * C + c0 + c] : 0u;
+    *reinterpret_cast<u32x4*>(xp + pix * Cp + c0) =
         u32x4{v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16)};
 }
 
@@ -303,9 +308,11 @@ __global__ __launch_bounds__(256) void split_reduce_compact_kernel(const float* 
 
 }  // namespace
 
-hipError_t launch_pad_channels8(const uint16_t* x, int64_t pixels, int32_t C, uint16_t* x8, hipStream_t stream) {
-    hipLaunchKernelGGL(pad_channels8_kernel, dim3((unsigned)((pixels + 255) / 256)), dim3(256), 0, stream, x, pixels, C,
-                       x8);
+hipError_t launch_pad_channels(const uint16_t* x, int64_t pixels, int32_t C, int32_t Cp, uint16_t* xp,
+                               hipStream_t stream) {
+    const int64_t n = pixels * (Cp / 8);
+    hipLaunchKernelGGL(pad_channels_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, x, pixels, C, Cp,
+                       xp);
     return hipGetLastError();
 }
 
@@ -337,14 +344,14 @@ hipError_t launch_wgrad(const WgradArgs& a, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, float* dw,
+hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, int64_t stride, float* dw,
                                int32_t accumulate, hipStream_t stream) {
     if (count < 65536 && splits >= 32) {
         hipLaunchKernelGGL(split_reduce_groups_kernel<16>, dim3((unsigned)((count + 15) / 16)), dim3(256), 0, stream,
-                           partials, splits, count, dw, accumulate);
+                           partials, splits, count, stride, dw, accumulate);
     } else {
         hipLaunchKernelGGL(split_reduce_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, stream,
-                           partials, splits, count, dw, accumulate);
+                           partials, splits, count, stride, dw, accumulate);
     }
     return hipGetLastError();
 }

@@ -410,7 +410,9 @@ def test_fc_stream_weight_streaming_size(tbn):
     assert e <= 1e-4
 
 
-BWD_CASES = [c for c in CONV_CASES if c[7] == 1] + [(2, 8, 8, 64, 64, 3, 3, 1, 0), (2, 6, 6, 64, 64, 5, 5, 1, 4)]
+BWD_CASES = [c for c in CONV_CASES if c[7] == 1] + [(2, 8, 8, 64, 64, 3, 3, 1, 0), (2, 6, 6, 64, 64, 5, 5, 1, 4),
+                                                    (4, 4, 4, 512, 10, 4, 4, 1, 0),   # 10-way classifier over 4x4
+                                                    (3, 9, 9, 16, 13, 3, 3, 1, 1)]    # 13 filters: 16-channel copy
 
 
 @pytest.mark.parametrize("g", BWD_CASES)
