@@ -61,6 +61,10 @@ def _load():
     lib.orc_conv_fwd.restype = ctypes.c_int
     lib.orc_conv_fwd_dense.argtypes = [p, p, p, p]
     lib.orc_conv_fwd_dense.restype = ctypes.c_int
+    lib.orc_quantize_act_i8.argtypes = [p, i64, ctypes.c_float, p]
+    lib.orc_quantize_act_i8.restype = None
+    lib.orc_conv_fwd_i8.argtypes = [p, p, p, p, ctypes.c_float, ctypes.c_int, p, p]
+    lib.orc_conv_fwd_i8.restype = ctypes.c_int
     lib.orc_conv_bwd_data.argtypes = [p, p, p, p, p]
     lib.orc_conv_bwd_data.restype = ctypes.c_int
     lib.orc_conv_bwd_weight.argtypes = [p, p, p, p]
@@ -256,6 +260,35 @@ def conv_fwd_dense(desc: ConvDesc, x: np.ndarray, w: np.ndarray) -> np.ndarray:
     if _load().orc_conv_fwd_dense(_ptr(desc.as_array()), _ptr(x), _ptr(w), _ptr(y)) != 0:
         raise OracleError("conv_fwd_dense failed")
     return y
+
+
+# --------------------------------------------------------------------------------------
+# Integer-activation variant of Eq. (1): the input replaced by s * q, q int8 (an extension)
+# --------------------------------------------------------------------------------------
+def quantize_act_i8(x: np.ndarray, inv_scale) -> np.ndarray:
+    """q = clamp(round-half-even(fp32(x * inv_scale)), -127, 127), NaN -> 0; x fp32 values."""
+    x = _c(x, np.float32)
+    q = np.zeros(x.shape, np.int8)
+    _load().orc_quantize_act_i8(_ptr(x), x.size, float(np.float32(inv_scale)), _ptr(q))
+    return q
+
+
+def conv_fwd_i8(desc: ConvDesc, xq: np.ndarray, codes: np.ndarray, alpha: np.ndarray, x_scale,
+                relu: bool = False):
+    """Forward pass on int8 activation codes: returns (y fp32 NHWC, exact int64 sums).
+    y = fp32(acc) * fp32(alpha_k * x_scale), then max(., 0) when relu."""
+    P, Q = desc.out_dims()
+    xq = _c(xq, np.int8)
+    codes = _c(codes, np.int8)
+    alpha = _c(alpha, np.float32)
+    if xq.size != desc.n * desc.h * desc.w * desc.c or codes.size != desc.k * desc.r * desc.s * desc.c:
+        raise OracleError("conv_fwd_i8: operand sizes do not match the geometry")
+    y = np.zeros((desc.n, P, Q, desc.k), np.float32)
+    acc = np.zeros((desc.n, P, Q, desc.k), np.int64)
+    if _load().orc_conv_fwd_i8(_ptr(desc.as_array()), _ptr(xq), _ptr(codes), _ptr(alpha),
+                               float(np.float32(x_scale)), 1 if relu else 0, _ptr(acc), _ptr(y)) != 0:
+        raise OracleError("conv_fwd_i8 failed")
+    return y, acc
 
 
 def conv_bwd_data(desc: ConvDesc, dy: np.ndarray, codes: np.ndarray, alpha: np.ndarray) -> np.ndarray:

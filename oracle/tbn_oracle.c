@@ -17,6 +17,8 @@
  *     filter used as the real-weight gradient : Sec. 3 (text) and Algorithm 1 (backward,
  *     update)
  *   - SGD with momentum and weight decay  : Sec. 4 (training set-up)
+ *   - integer-activation forward variant  : Eq. (1) with the input replaced by int8 codes
+ *     times one scale (an extension; see orc_conv_fwd_i8)
  * The 2-bit packed layout is this project's own storage format (the paper only says the
  * four values fit in two bits, abstract and Sec. 1); its definition is restated next to
  * the packer below.
@@ -327,6 +329,73 @@ int orc_conv_fwd_dense(const int32_t* d, const double* x, const double* wts, dou
                         }
                     }
                     y[((nn * P + p) * Q + q) * K + k] = acc;
+                }
+            }
+        }
+    }
+    return ORC_OK;
+}
+
+/*
+ * Integer-activation variant of the forward pass (an extension: the paper keeps the
+ * activations in full precision and motivates the two-bit filters by arithmetic that needs
+ * no multiplier, Sec. 1).  The input I of Eq. (1) is replaced by s * q with q an int8 code
+ * per activation and s one positive fp32 scale per tensor, chosen by the caller.
+ *
+ * Activation codes: v = x * inv in fp32 (inv = the caller's fp32 reciprocal of s), then
+ * q = v rounded to the nearest integer, ties to even, limited to [-127, 127]; a NaN
+ * activation gets q = 0.
+ */
+void orc_quantize_act_i8(const float* x, int64_t count, float inv, int8_t* q) {
+    for (int64_t i = 0; i < count; ++i) {
+        const float v = x[i] * inv; /* one fp32 rounding */
+        if (isnan(v)) {
+            q[i] = 0;
+            continue;
+        }
+        float r = nearbyintf(v); /* default rounding mode: nearest, ties to even */
+        if (r > 127.0f) r = 127.0f;
+        if (r < -127.0f) r = -127.0f;
+        q[i] = (int8_t)r;
+    }
+}
+
+/*
+ * Forward pass on int8 activation codes (Eq. 1 with I = s q and the scale applied after
+ * the multiplication-free sum):  acc[n,p,q,k] = sum_{r,s,c} q[n, p*sh-ph+r, q*sw-pw+s, c]
+ * * W~[k,r,s,c] in exact integer arithmetic (zero padding), then, in fp32,
+ * y = float(acc) * (alpha_k * s) with the scale product rounded first, and max(y, 0) when
+ * relu != 0.  acc (optional) receives the exact sums.
+ */
+int orc_conv_fwd_i8(const int32_t* d, const int8_t* xq, const int8_t* codes, const float* alpha, float s,
+                    int relu, int64_t* acc_out, float* y) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t N = d[DN], H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t nn = 0; nn < N; ++nn) {
+        for (int64_t p = 0; p < P; ++p) {
+            for (int64_t q = 0; q < Q; ++q) {
+                for (int64_t k = 0; k < K; ++k) {
+                    int64_t acc = 0;
+                    for (int64_t r = 0; r < R; ++r) {
+                        const int64_t h = p * sh - ph + r;
+                        if (h < 0 || h >= H) continue;
+                        for (int64_t t = 0; t < S; ++t) {
+                            const int64_t w = q * sw - pw + t;
+                            if (w < 0 || w >= W) continue;
+                            const int8_t* xp = xq + ((nn * H + h) * W + w) * C;
+                            const int8_t* cp = codes + ((k * R + r) * S + t) * C;
+                            for (int64_t c = 0; c < C; ++c) acc += (int64_t)xp[c] * (int64_t)cp[c];
+                        }
+                    }
+                    const int64_t o = ((nn * P + p) * Q + q) * K + k;
+                    const float scale = alpha[k] * s;
+                    float v = (float)acc * scale;
+                    if (relu && !(v > 0.0f)) v = 0.0f;
+                    y[o] = v;
+                    if (acc_out) acc_out[o] = acc;
                 }
             }
         }
