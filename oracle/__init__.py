@@ -65,6 +65,8 @@ def _load():
     lib.orc_quantize_act_i8.restype = None
     lib.orc_conv_fwd_i8.argtypes = [p, p, p, p, ctypes.c_float, ctypes.c_int, p, p]
     lib.orc_conv_fwd_i8.restype = ctypes.c_int
+    lib.orc_conv_fwd_i8_sampled.argtypes = [p, p, p, p, ctypes.c_float, ctypes.c_int, p, i64, p]
+    lib.orc_conv_fwd_i8_sampled.restype = ctypes.c_int
     lib.orc_conv_bwd_data.argtypes = [p, p, p, p, p]
     lib.orc_conv_bwd_data.restype = ctypes.c_int
     lib.orc_conv_bwd_weight.argtypes = [p, p, p, p]
@@ -289,6 +291,23 @@ def conv_fwd_i8(desc: ConvDesc, xq: np.ndarray, codes: np.ndarray, alpha: np.nda
                                float(np.float32(x_scale)), 1 if relu else 0, _ptr(acc), _ptr(y)) != 0:
         raise OracleError("conv_fwd_i8 failed")
     return y, acc
+
+
+def conv_fwd_i8_sampled(desc: ConvDesc, xq: np.ndarray, codes: np.ndarray, alpha: np.ndarray, x_scale,
+                        idx: np.ndarray, relu: bool = False) -> np.ndarray:
+    """conv_fwd_i8's y at flat output indices idx (into [N][P][Q][K]), fp32."""
+    xq = _c(xq, np.int8)
+    codes = _c(codes, np.int8)
+    alpha = _c(alpha, np.float32)
+    idx = _c(idx, np.int64)
+    if xq.size != desc.n * desc.h * desc.w * desc.c or codes.size != desc.k * desc.r * desc.s * desc.c:
+        raise OracleError("conv_fwd_i8_sampled: operand sizes do not match the geometry")
+    y = np.zeros(idx.size, np.float32)
+    if _load().orc_conv_fwd_i8_sampled(_ptr(desc.as_array()), _ptr(xq), _ptr(codes), _ptr(alpha),
+                                       float(np.float32(x_scale)), 1 if relu else 0, _ptr(idx), idx.size,
+                                       _ptr(y)) != 0:
+        raise OracleError("conv_fwd_i8_sampled: index out of range")
+    return y
 
 
 def conv_bwd_data(desc: ConvDesc, dy: np.ndarray, codes: np.ndarray, alpha: np.ndarray) -> np.ndarray:

@@ -403,6 +403,39 @@ int orc_conv_fwd_i8(const int32_t* d, const int8_t* xq, const int8_t* codes, con
     return ORC_OK;
 }
 
+/* The same at `count` flat output indices idx (into [N][P][Q][K]); y[i] for idx[i]. */
+int orc_conv_fwd_i8_sampled(const int32_t* d, const int8_t* xq, const int8_t* codes, const float* alpha, float s,
+                            int relu, const int64_t* idx, int64_t count, float* y) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t N = d[DN], H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+    for (int64_t i = 0; i < count; ++i)
+        if (idx[i] < 0 || idx[i] >= N * P * Q * K) return ORC_ERR_SHAPE;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < count; ++i) {
+        const int64_t o = idx[i];
+        const int64_t k = o % K, q = (o / K) % Q, p = (o / (K * Q)) % P, nn = o / (K * Q * P);
+        int64_t acc = 0;
+        for (int64_t r = 0; r < R; ++r) {
+            const int64_t h = p * sh - ph + r;
+            if (h < 0 || h >= H) continue;
+            for (int64_t t = 0; t < S; ++t) {
+                const int64_t w = q * sw - pw + t;
+                if (w < 0 || w >= W) continue;
+                const int8_t* xp = xq + ((nn * H + h) * W + w) * C;
+                const int8_t* cp = codes + ((k * R + r) * S + t) * C;
+                for (int64_t c = 0; c < C; ++c) acc += (int64_t)xp[c] * (int64_t)cp[c];
+            }
+        }
+        const float scale = alpha[k] * s;
+        float v = (float)acc * scale;
+        if (relu && !(v > 0.0f)) v = 0.0f;
+        y[i] = v;
+    }
+    return ORC_OK;
+}
+
 /*
  * Backward pass to the layer input through the approximate filters W^ = alpha W~
  * (Sec. 3: both passes use the approximate filters; Algorithm 1, backward step).

@@ -124,3 +124,12 @@ def test_i8_relu_only_clears_negatives():
     yr, _ = oracle.conv_fwd_i8(desc, xq, codes, alpha, 0.01, relu=True)
     assert np.array_equal(yr, np.where(y > 0, y, 0.0).astype(np.float32))
     assert (y < 0).any() and (y > 0).any()
+
+
+@pytest.mark.parametrize("relu", [False, True])
+def test_i8_sampled_equals_full(relu):
+    desc, xq, codes, alpha = _int_problem((2, 9, 7, 32, 11, 3, 3, 2, 1), "i8-sampled")
+    y, _ = oracle.conv_fwd_i8(desc, xq, codes, alpha, 0.02, relu=relu)
+    idx = synth.sample_indices(0, "i8-sampled-idx", y.size, 300)
+    ys = oracle.conv_fwd_i8_sampled(desc, xq, codes, alpha, 0.02, idx, relu=relu)
+    assert np.array_equal(ys, y.ravel()[idx])
