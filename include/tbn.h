@@ -150,6 +150,33 @@ tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt
                           void* y, tbn_dtype yt, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Integer-activation variant of the forward pass (an extension of Sec. 2 Eq. 1: the paper
+ * keeps activations in full precision; its Sec. 1 motivates the two-bit filters by
+ * arithmetic without multipliers).  The input I is represented as s * q, q int8, and the
+ * layer runs on the int8 matrix cores, where the products q * W~ and their int32 sums are
+ * exact.
+ *
+ * tbn_quantize_act_i8: activation codes q = clamp(round-half-even(x * inv_scale), -127, 127)
+ *   with the product rounded to fp32 first; a NaN input gets 0.  x: `count` elements of
+ *   dtype xt (any layout: elementwise); q: `count` int8.  inv_scale finite and > 0
+ *   (typically 127 / max|x| over a calibration set), else TBN_ERR_SHAPE.
+ *
+ * tbn_conv2d_fwd_i8: y[n,p,q,k] = act(float(acc) * float(alpha_k * x_scale)) with
+ *   acc = sum_{r,s,c} q[n, p*sh-ph+r, q*sw-pw+s, c] * W~[k,r,s,c] exact (zero padding),
+ *   the scale product rounded to fp32 first; relu != 0 applies max(., 0).
+ *   x      NHWC [N][H][W][C] int8 codes (for example from tbn_quantize_act_i8); x_scale =
+ *          the s with x ~ s * q (1 / inv_scale), finite.
+ *   codes  TBN2 packed codes of the K filters (n = R*S*C); alpha [K] fp32.
+ *   y      NHWC [N][P][Q][K], dtype yt (bf16 rounded to nearest even, or fp32).
+ *   Needs C % 16 == 0, R*S <= 63, 254 * R*S*C < 2^31 (int32 sums) and x and the codes
+ *   below 2 GiB; TBN_ERR_UNSUPPORTED otherwise.  No workspace.
+ */
+tbn_status tbn_quantize_act_i8(const void* x, tbn_dtype xt, int64_t count, float inv_scale, int8_t* q,
+                               hipStream_t stream);
+tbn_status tbn_conv2d_fwd_i8(const tbn_conv_desc* desc, const int8_t* x, const uint32_t* codes, const float* alpha,
+                             float x_scale, int32_t relu, void* y, tbn_dtype yt, hipStream_t stream);
+
+/*
  * Forward pass of a layer kept in full precision (Eq. 1 with the real filters; the first
  * convolution of the CIFAR-shaped network stays unquantised):
  *   y[n,p,q,k] = sum_{r,s,c} x[n, p*sh-ph+r, q*sw-pw+s, c] * bf16(w[k,r,s,c]),

@@ -81,6 +81,8 @@ def load():
         "tbn_quantize_variant": ([vp, i64, i64, f32, vp, vp, vp, vp, vp], i32),
         "tbn_conv2d_fwd": ([vp, vp, i32, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_conv2d_fwd_dense": ([vp, vp, i32, vp, vp, vp, i32, vp], i32),
+        "tbn_quantize_act_i8": ([vp, i32, i64, f32, vp, vp], i32),
+        "tbn_conv2d_fwd_i8": ([vp, vp, vp, vp, f32, i32, vp, i32, vp], i32),
         "tbn_conv2d_bwd_data": ([vp, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_conv2d_bwd_weight": ([vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_sgd_step": ([vp, vp, vp, i64, f32, f32, f32, vp], i32),
@@ -107,6 +109,7 @@ def load():
 def exported_symbols():
     return sorted(["tbn_status_str", "tbn_last_error", "tbn_conv_out_dims", "tbn_packed_words",
                    "tbn_workspace_size", "tbn_quantize", "tbn_quantize_variant", "tbn_conv2d_fwd", "tbn_conv2d_fwd_dense",
+                   "tbn_quantize_act_i8", "tbn_conv2d_fwd_i8",
                    "tbn_conv2d_bwd_data",
                    "tbn_conv2d_bwd_weight", "tbn_sgd_step", "tbn_sgd_step_quantize", "tbn_pool_out_dims", "tbn_maxpool2d_fwd",
                    "tbn_maxpool2d_bwd", "tbn_avgpool_global", "tbn_batchnorm_workspace_size",
@@ -242,6 +245,33 @@ def conv2d_fwd(desc: ConvDesc, x, codes, alpha, y=None, out_dtype=torch.bfloat16
           ctypes.byref(ep) if ep is not None else None, _dev(y, "y", (torch.bfloat16, torch.float32)),
           _dtype_code(y.dtype), _dev(ws, "ws") if ws is not None else None,
           ws.numel() * ws.element_size() if ws is not None else 0, _stream())
+    return y
+
+
+def quantize_act_i8(x: torch.Tensor, inv_scale: float, q=None):
+    """int8 activation codes q = clamp(round-half-even(x * inv_scale), -127, 127) (NaN -> 0),
+    elementwise over a bf16 or fp32 tensor; returns q (int8, x's shape)."""
+    if q is None:
+        q = torch.empty(x.shape, dtype=torch.int8, device=x.device)
+    _numel(q, x.numel(), "q")
+    _call("tbn_quantize_act_i8", _dev(x, "x", (torch.bfloat16, torch.float32)), _dtype_code(x.dtype), x.numel(),
+          float(inv_scale), _dev(q, "q", (torch.int8,)), _stream())
+    return q
+
+
+def conv2d_fwd_i8(desc: ConvDesc, xq, codes, alpha, x_scale: float, y=None, out_dtype=torch.bfloat16, relu=False):
+    """Forward pass on int8 activation codes (int8 matrix cores):
+    y = act(float(xq conv W~) * float(alpha_k * x_scale)), NHWC."""
+    P, Q = desc.out_dims()
+    _numel(xq, desc.n * desc.h * desc.w * desc.c, "xq")
+    _numel(codes, packed_words(desc.k, desc.r * desc.s * desc.c), "codes")
+    _numel(alpha, desc.k, "alpha")
+    if y is None:
+        y = torch.empty((desc.n, P, Q, desc.k), dtype=out_dtype, device=xq.device)
+    _numel(y, desc.n * P * Q * desc.k, "y")
+    _call("tbn_conv2d_fwd_i8", ctypes.byref(desc), _dev(xq, "xq", (torch.int8,)), _dev(codes, "codes", (torch.int32,)),
+          _dev(alpha, "alpha", (torch.float32,)), float(x_scale), 1 if relu else 0,
+          _dev(y, "y", (torch.bfloat16, torch.float32)), _dtype_code(y.dtype), _stream())
     return y
 
 

@@ -1,0 +1,468 @@
+// tbn_conv_i8.hip -- forward pass of a two-bit layer on int8 activation codes: Eq. (1) with
+// the input replaced by s * q (q int8, one fp32 scale s per tensor), on the gfx950 int8
+// matrix cores (v_mfma_i32_32x32x32_i8).  The codes {-2, -1, 1, 2} are exact int8 values
+// and the int32 accumulation of their products with q is exact, so the sum is the integer
+// definition itself; only the final scaling rounds.  Also the activation-code kernel
+// q = clamp(round-half-even(x * inv), -127, 127).
+//
+// The convolution follows the bf16 LDS-DMA kernel (implicit GEMM; activation rows and
+// packed-code blocks copied to LDS by buffer loads in LDS-DMA mode, a three-deep ring with
+// compile-time vmcnt waits, swizzled 128-byte rows, XCD-aware tile order), with a stage of
+// 128 reduction elements: 128 int8 channels per activation row and two 64-element code
+// chunks per filter.
+//   * Lane-half h of the MFMA takes the 16-channel segments u + 4h of a row in the stage's
+//     four MFMA steps u, so that over the stage its filter operand is code chunk h: one
+//     16-byte LDS read per 32 filters per stage, one packed word per step.
+//   * A packed word (16 codes: bit j magnitude and bit 8 + j sign of element 2j, bits 16 + j
+//     and 24 + j of element 2j + 1) becomes 16 int8 values with two byte permutes, three
+//     bitfield merges and, per 4 values, a shift, a mask and a 4-entry byte lookup
+//     (v_perm_b32).
+//   * The epilogue converts the int32 sums to fp32 (exact below 2^24), multiplies by
+//     fp32(alpha_k * s), optionally clamps at 0 and stores bf16 or fp32 through an LDS
+//     staging tile with 16-byte stores.
+//
+// M0 is written by the DMA helper; nothing else in these kernels uses M0.
+#include <cstdlib>
+
+#include "tbn_device.h"
+#include "tbn_dma.h"
+#include "tbn_kernels.h"
+
+namespace tbn {
+
+namespace {
+
+constexpr int BK = 128;    // int8 reduction elements per stage
+constexpr int ROWB = 128;  // LDS bytes per activation row of a stage
+
+template <int BM, int BN>
+struct I8Layout {
+    static constexpr int A = 0;            // BM rows x 128 B
+    static constexpr int B = BM * ROWB;    // code chunk 0 of the BN filters, then chunk 1
+    static constexpr int BYTES = B + 2 * BN * 16;
+};
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ i32x16 mfma_i8(i32x4 a, i32x4 b, i32x16 c) {
+    return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+}
+
+// The 16 codes of one packed word as int8, element e in byte e % 4 of dword e / 4.
+__device__ __forceinline__ i32x4 decode_i8(uint32_t w) {
+    // bytes (magnitude even, magnitude odd, magnitude even, magnitude odd) and the same
+    // for the sign planes; both sources are w, so the byte order of the pair is immaterial
+    const uint32_t pm = __builtin_amdgcn_perm(w, w, 0x02000200u);
+    const uint32_t ps = __builtin_amdgcn_perm(w, w, 0x03010301u);
+    // element 4d + b: its magnitude to bit 2d of byte b, its sign to bit 2d + 1
+    const uint32_t m = (pm & 0x0000FFFFu) | ((pm >> 1) & 0xFFFF0000u);
+    const uint32_t s = ((ps << 1) & 0x0000FFFFu) | (ps & 0xFFFF0000u);
+    const uint32_t z = (m & 0x55555555u) | (s & 0xAAAAAAAAu);
+    constexpr uint32_t LUT = 0xFEFF0201u;  // index magnitude + 2 sign -> 1, 2, -1, -2
+    i32x4 r;
+    r.x = (int)__builtin_amdgcn_perm(LUT, LUT, z & 0x03030303u);
+    r.y = (int)__builtin_amdgcn_perm(LUT, LUT, (z >> 2) & 0x03030303u);
+    r.z = (int)__builtin_amdgcn_perm(LUT, LUT, (z >> 4) & 0x03030303u);
+    r.w = (int)__builtin_amdgcn_perm(LUT, LUT, (z >> 6) & 0x03030303u);
+    return r;
+}
+
+// UNI: C % 128 == 0, so all 128 elements of a stage share one tap (r, s) and the tap
+// bookkeeping is wave-uniform.  Otherwise C % 16 == 0 and every lane tracks the tap of its
+// own 16-channel segment.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool UNI>
+__global__ __launch_bounds__(256, 2) void conv_i8_kernel(const ConvI8Args a) {
+    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+    constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr int AR = BM / 32;    // activation DMAs per wave per stage (8 rows each)
+    constexpr int NBLK = BN / 64;  // 1 KiB code blocks per chunk
+    using L = I8Layout<BM, BN>;
+    static_assert(WAVES_M * WAVES_N == 4, "four waves per block");
+    static_assert(TM >= 1 && TN >= 1 && BM % 32 == 0 && BN % 64 == 0 && NBLK <= 4, "tile shape");
+    static_assert(STAGES * L::BYTES >= 4 * 32 * (WN + 4) * 4, "epilogue staging fits in the ring");
+
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * L::BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WAVES_N;
+    const int wn = wave % WAVES_N;
+    const int half = lane >> 5;
+    const int l32 = lane & 31;
+
+    const int64_t PQ = (int64_t)a.P * a.Q;
+    const int64_t M = (int64_t)a.N * PQ;
+    const int C = a.C;
+    const int n = a.R * a.S * C;
+    const int nst = (n + BK - 1) / BK;  // stages
+    const int nch = (n + 63) / 64;      // 64-element code chunks
+    const int KB = (a.K + 63) / 64;
+    const uint32_t tilesN = (uint32_t)(a.K + BN - 1) / BN;
+    const uint32_t tile = (uint32_t)xcd_remap(blockIdx.x, gridDim.x);
+    const uint32_t mtile = fdiv(tile, a.div_tilesN);
+    const int64_t m0 = (int64_t)mtile * BM;
+    const int n0 = (int)(tile - mtile * tilesN) * BN;
+
+    const v4i rs_x = make_rsrc(a.x, (uint32_t)((int64_t)a.N * a.H * a.W * C));
+    const v4i rs_c = make_rsrc(a.codes, (uint32_t)((int64_t)KB * nch * 1024));
+    const uint32_t smem_base = lds_addr(smem);
+
+    // ---- activation rows this lane fills: row = 8 * (wave + 4 j) + lane / 8 ----
+    int32_t rbase[AR];      // byte offset of the row's (h0, w0) in x (may be negative)
+    uint32_t rmask[AR][2];  // bit r*S + s set iff tap (r, s) lies inside the image
+#pragma unroll
+    for (int j = 0; j < AR; ++j) {
+        const int64_t m = m0 + 8 * (wave + 4 * j) + (lane >> 3);
+        uint64_t mask = 0;
+        rbase[j] = 0;
+        if (m < M) {
+            const uint32_t mm = (uint32_t)m;  // < 2^31, checked by the host
+            const uint32_t img = fdiv(mm, a.div_pq);
+            const uint32_t pq = mm - img * (uint32_t)PQ;
+            const uint32_t p = fdiv(pq, a.div_q);
+            const uint32_t q = pq - p * (uint32_t)a.Q;
+            const int h0 = (int)p * a.sh - a.ph, w0 = (int)q * a.sw - a.pw;
+            rbase[j] = ((int32_t)img * a.H + h0) * a.W * C + w0 * C;
+            // in-image taps s in [slo, shi), r in [rlo, rhi): the row's bits replicated at
+            // every in-image r by a multiplication with sum_r 2^(r*S) (R*S <= 63)
+            const int slo = max(0, -w0), shi = min(a.S, a.W - w0);
+            const int rlo = max(0, -h0), rhi = min(a.R, a.H - h0);
+            if (shi > slo && rhi > rlo) {
+                const uint64_t wbits = (1ull << shi) - (1ull << slo);
+                const uint64_t rowsel = (1ull << (rhi * a.S)) - (1ull << (rlo * a.S));
+                const uint64_t rep = ((uint64_t)a.rep_hi << 32) | a.rep_lo;
+                mask = wbits * (rep & rowsel);
+            }
+        }
+        rmask[j][0] = (uint32_t)mask;
+        rmask[j][1] = (uint32_t)(mask >> 32);
+    }
+    // logical 16-byte segment this lane loads (its LDS slot is lane % 8 of the row; rows
+    // swizzled by (row / 2) % 8)
+    const int lseg = (lane & 7) ^ ((4 * (wave & 1)) | ((lane >> 4) & 3));
+    int er = 0, es = 0, ec = 0;  // general path: (r, s, c) of this lane's next segment
+    int us = 0, uc = 0, utap = 0;  // uniform path: s, first channel and tap of the next stage
+    uint32_t utoff = 0;            // uniform path: byte offset of (r, s, c0) from a row's (h0, w0)
+    uint32_t rbs[AR];              // uniform path: row offset plus this lane's segment
+    uint32_t nmask[AR][2];         // uniform path: complement of rmask
+    if constexpr (UNI) {
+#pragma unroll
+        for (int j = 0; j < AR; ++j) {
+            rbs[j] = (uint32_t)(rbase[j] + 16 * lseg);
+            nmask[j][0] = ~rmask[j][0];
+            nmask[j][1] = ~rmask[j][1];
+        }
+    } else {
+        const int e0 = lseg * 16;
+        const int rs = e0 / C;
+        ec = e0 - rs * C;
+        er = rs / a.S;
+        es = rs - er * a.S;
+    }
+    // code blocks of this wave: block wave % NBLK of both chunks of each stage (with fewer
+    // than four blocks some waves copy identical bytes to the same place), so that every
+    // wave issues the same number of DMAs per stage and the waits are compile-time counts
+    const int cblk = wave % NBLK;
+    const int fb = n0 / 64 + cblk;
+    const bool codes_valid = fb < KB;
+    constexpr int DMAS = AR + 2;
+
+    const uint32_t row_step = (uint32_t)((a.W - a.S) * C);  // to the next filter row, bytes
+    int islot = 0;
+    auto issue = [&](int stage) {
+        const uint32_t st = smem_base + (uint32_t)(islot * L::BYTES);
+        islot = islot + 1 == STAGES ? 0 : islot + 1;
+        if constexpr (UNI) {
+            // out-of-image taps and the taps past the filter (clamped to bit 63, clear
+            // because R*S <= 63) get offset bit 31 set: the hardware returns zeros
+            const int tap = min(utap, 63);
+            if (tap < 32) {
+#pragma unroll
+                for (int j = 0; j < AR; ++j) {
+                    const uint32_t out = (nmask[j][0] << (31 - tap)) & 0x80000000u;
+                    dma_b128(rs_x, st + L::A + (uint32_t)(8 * (wave + 4 * j) * ROWB), (rbs[j] + utoff) | out);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < AR; ++j) {
+                    const uint32_t out = (nmask[j][1] << (63 - tap)) & 0x80000000u;
+                    dma_b128(rs_x, st + L::A + (uint32_t)(8 * (wave + 4 * j) * ROWB), (rbs[j] + utoff) | out);
+                }
+            }
+            uc += BK;
+            utoff += BK;
+            if (uc == C) {
+                uc = 0;
+                ++utap;
+                if (++us == a.S) {
+                    us = 0;
+                    utoff += row_step;
+                }
+            }
+        } else {
+            const int tap = min(er * a.S + es, 63);
+            const int tword = tap >> 5, tbit = tap & 31;
+            const int32_t toff = (er * a.W + es) * C + ec;
+#pragma unroll
+            for (int j = 0; j < AR; ++j) {
+                const bool ok = ((tword ? rmask[j][1] : rmask[j][0]) >> tbit) & 1u;
+                const uint32_t off = ok ? (uint32_t)(rbase[j] + toff) : 0x80000000u;
+                dma_b128(rs_x, st + L::A + (uint32_t)(8 * (wave + 4 * j) * ROWB), off);
+            }
+            ec += BK;
+            while (ec >= C) {
+                ec -= C;
+                if (++es == a.S) {
+                    es = 0;
+                    ++er;
+                }
+            }
+        }
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) {
+            const int ch = 2 * stage + cc;
+            const uint32_t off = (codes_valid && ch < nch) ? (uint32_t)(((int64_t)fb * nch + ch) * 1024 + lane * 16)
+                                                           : 0x80000000u;
+            dma_b128(rs_c, st + L::B + (uint32_t)((cc * NBLK + cblk) * 1024), off);
+        }
+    };
+
+    // ---- operand addressing inside a stage ----
+    const int sw = (l32 >> 1) & 7;
+    int seg_off[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) seg_off[u] = 16 * ((u + 4 * half) ^ sw);
+    const int arow = (wm * WM + l32) * ROWB;
+    const int bcol = half * NBLK * 1024 + (wn * WN + l32) * 16;  // code chunk `half`
+
+    i32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][t][v] = 0;
+
+#pragma unroll
+    for (int c = 0; c < STAGES - 1; ++c)
+        if (c < nst) issue(c);
+    int cslot = 0;
+    for (int il = 0; il < nst; ++il) {
+        if (il + STAGES - 2 < nst)
+            wait_vmcnt((STAGES - 2) * DMAS);
+        else
+            wait_vmcnt(0);
+        __syncthreads();  // every wave's copies of stage il landed; reads of il-1 are done
+        if (il + STAGES - 1 < nst) issue(il + STAGES - 1);
+        const uint8_t* st = smem + cslot * L::BYTES;
+        cslot = cslot + 1 == STAGES ? 0 : cslot + 1;
+        u32x4 braw[TN];
+#pragma unroll
+        for (int t = 0; t < TN; ++t) braw[t] = *reinterpret_cast<const u32x4*>(st + L::B + bcol + 32 * 16 * t);
+        i32x4 afs[4][TM];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                afs[u][i] = *reinterpret_cast<const i32x4*>(st + L::A + arow + 32 * i * ROWB + seg_off[u]);
+        __builtin_amdgcn_sched_barrier(0);  // keep the LDS reads ahead of the MFMAs
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            i32x4 bfr[TN];
+#pragma unroll
+            for (int t = 0; t < TN; ++t) bfr[t] = decode_i8(braw[t][u]);
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int t = 0; t < TN; ++t) acc[i][t] = mfma_i8(bfr[t], afs[u][i], acc[i][t]);
+        }
+    }
+
+    // ---- epilogue.  The MFMA computed the transposed tile (filters x pixels): lane l of
+    //      tile (i, t) holds pixel 32 i + l % 32 and, for each v / 4, filters
+    //      32 t + 8 (v / 4) + 4 (l / 32) + 0..3.  Each 32-pixel tile row is staged through
+    //      LDS as fp32, then every lane scales 8 consecutive channels of one pixel. ----
+    __syncthreads();
+    constexpr int PITCH = WN + 4;
+    float* stage = reinterpret_cast<float*>(smem) + wave * 32 * PITCH;
+    const int K = a.K;
+    constexpr int CG = WN / 8;
+    constexpr int RPP = 64 / CG;
+    const int gcol = lane % CG;
+    const int grow = lane / CG;
+    const int col0 = n0 + wn * WN + 8 * gcol;
+    float cs[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cs[e] = col0 + e < K ? a.alpha[col0 + e] * a.x_scale : 0.0f;
+    const bool vec_store = (K % 8) == 0;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int t = 0; t < TN; ++t)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<f32x4*>(&stage[l32 * PITCH + 32 * t + 8 * g + 4 * half]) =
+                    f32x4{(float)acc[i][t][4 * g], (float)acc[i][t][4 * g + 1], (float)acc[i][t][4 * g + 2],
+                          (float)acc[i][t][4 * g + 3]};
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+#pragma unroll
+        for (int pass = 0; pass < 32 / RPP; ++pass) {
+            const int r = pass * RPP + grow;
+            const int64_t row = m0 + wm * WM + 32 * i + r;
+            if (row >= M || col0 >= K) continue;
+            const f32x4 lo = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol]);
+            const f32x4 hi = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol + 4]);
+            float v8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v8[e] = v8[e] * cs[e];
+            if (a.relu) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v8[e] = fmaxf(v8[e], 0.0f);
+            }
+            const int64_t o = row * K + col0;
+            if (a.y_f32) {
+                float* yp = reinterpret_cast<float*>(a.y) + o;
+                if (vec_store) {
+                    *reinterpret_cast<f32x4*>(yp) = f32x4{v8[0], v8[1], v8[2], v8[3]};
+                    *reinterpret_cast<f32x4*>(yp + 4) = f32x4{v8[4], v8[5], v8[6], v8[7]};
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (col0 + e < K) yp[e] = v8[e];
+                }
+            } else {
+                uint16_t* yp = reinterpret_cast<uint16_t*>(a.y) + o;
+                if (vec_store) {
+                    *reinterpret_cast<u32x4*>(yp) = u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]),
+                                                          pack_bf16x2(v8[4], v8[5]), pack_bf16x2(v8[6], v8[7])};
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (col0 + e < K) yp[e] = (uint16_t)f32_to_bf16_bits(v8[e]);
+                }
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // reads of this tile row done before it is overwritten
+    }
+}
+
+// q = clamp(round-half-even(x * inv), -127, 127), NaN -> 0; 16 elements per thread.
+template <bool F32>
+__global__ __launch_bounds__(256) void quantize_act_i8_kernel(const void* __restrict__ x, int64_t count, float inv,
+                                                              int8_t* __restrict__ q) {
+    const int64_t i0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 16;
+    if (i0 >= count) return;
+    float v[16];
+    const bool full = i0 + 16 <= count;
+    if (full) {
+        if constexpr (F32) {
+            const f32x4* p = reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(x) + i0);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const f32x4 t = p[j];
+                v[4 * j] = t.x; v[4 * j + 1] = t.y; v[4 * j + 2] = t.z; v[4 * j + 3] = t.w;
+            }
+        } else {
+            const u32x4* p = reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(x) + i0);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const u32x4 t = p[j];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    v[8 * j + 2 * e] = bf16_bits_to_f32(t[e] & 0xFFFFu);
+                    v[8 * j + 2 * e + 1] = bf16_bits_to_f32(t[e] >> 16);
+                }
+            }
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int64_t i = i0 + e < count ? i0 + e : i0;
+            v[e] = F32 ? reinterpret_cast<const float*>(x)[i] : bf16_bits_to_f32(reinterpret_cast<const uint16_t*>(x)[i]);
+        }
+    }
+    uint32_t word[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const float t = v[e] * inv;
+        const float r = fminf(fmaxf(rintf(t), -127.0f), 127.0f);
+        const int c = t != t ? 0 : (int)r;
+        word[e / 4] |= ((uint32_t)c & 0xFFu) << (8 * (e % 4));
+    }
+    if (full) {
+        *reinterpret_cast<u32x4*>(q + i0) = u32x4{word[0], word[1], word[2], word[3]};
+    } else {
+        for (int e = 0; i0 + e < count; ++e) q[i0 + e] = (int8_t)((word[e / 4] >> (8 * (e % 4))) & 0xFFu);
+    }
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES>
+hipError_t launch_i8_cfg(const ConvI8Args& args, hipStream_t stream) {
+    ConvI8Args a = args;
+    const int64_t M = (int64_t)a.N * a.P * a.Q;
+    const int64_t tilesN = (a.K + BN - 1) / BN;
+    const int64_t tiles = ((M + BM - 1) / BM) * tilesN;
+    if (tiles >= 0x7FFFFFFFll) return hipErrorInvalidValue;
+    a.div_tilesN = make_fastdiv((uint32_t)tilesN);
+    uint64_t rep = 0;
+    for (int r = 0; r < a.R; ++r) rep |= 1ull << (r * a.S);
+    a.rep_lo = (uint32_t)rep;
+    a.rep_hi = (uint32_t)(rep >> 32);
+    const dim3 grid((unsigned)tiles);
+    if (a.C % BK == 0)
+        hipLaunchKernelGGL((conv_i8_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, true>), grid, dim3(256), 0, stream, a);
+    else
+        hipLaunchKernelGGL((conv_i8_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, false>), grid, dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool conv_i8_eligible(const ConvI8Args& a) {
+    const int64_t n = (int64_t)a.R * a.S * a.C;
+    const int64_t xbytes = (int64_t)a.N * a.H * a.W * a.C;
+    const int64_t cbytes = (int64_t)((a.K + 63) / 64) * ((n + 63) / 64) * 1024;
+    // int32 sums: |sum| <= 127 * 2 * n
+    return a.C % 16 == 0 && a.R * a.S <= 63 && n * 254 < 0x7FFFFFFFll && xbytes < 0x7FFFFFF0ll &&
+           cbytes < 0x7FFFFFF0ll;
+}
+
+int conv_i8_tile(const ConvI8Args& a) {
+    const char* e = getenv("TBN_I8_TILE");
+    if (e && atoi(e) >= 1 && atoi(e) <= 4) return atoi(e);
+    const int64_t M = (int64_t)a.N * a.P * a.Q;
+    int cfg = a.K > 128 ? 1 : (a.K > 64 ? 2 : 3);
+    const int bm = 128, bn = cfg == 1 ? 256 : (cfg == 2 ? 128 : 64);
+    // too few tiles for one wave of blocks: 64-pixel x 128-filter tiles
+    if (((M + bm - 1) / bm) * ((a.K + bn - 1) / bn) < 384 && a.K >= 128) cfg = 4;
+    return cfg;
+}
+
+hipError_t launch_conv_i8(const ConvI8Args& args, hipStream_t stream) {
+    if (!conv_i8_eligible(args)) return hipErrorInvalidValue;
+    ConvI8Args a = args;
+    a.div_q = make_fastdiv((uint32_t)a.Q);
+    a.div_pq = make_fastdiv((uint32_t)a.P * (uint32_t)a.Q);
+    switch (conv_i8_tile(a)) {
+        case 2: return launch_i8_cfg<128, 128, 2, 2, 3>(a, stream);
+        case 3: return launch_i8_cfg<128, 64, 2, 2, 3>(a, stream);
+        case 4: return launch_i8_cfg<64, 128, 1, 4, 4>(a, stream);
+        default: return launch_i8_cfg<128, 256, 1, 4, 3>(a, stream);
+    }
+}
+
+hipError_t launch_quantize_act_i8(const void* x, int x_f32, int64_t count, float inv, int8_t* q,
+                                  hipStream_t stream) {
+    const int64_t threads = (count + 15) / 16;
+    const int64_t blocks = (threads + 255) / 256;
+    if (blocks >= 0x7FFFFFFFll) return hipErrorInvalidValue;
+    if (x_f32)
+        hipLaunchKernelGGL(quantize_act_i8_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream, x, count, inv, q);
+    else
+        hipLaunchKernelGGL(quantize_act_i8_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream, x, count, inv, q);
+    return hipGetLastError();
+}
+
+}  // namespace tbn

@@ -171,6 +171,28 @@ hipError_t launch_split_reduce_compact(const float* partials, int32_t splits, in
 hipError_t launch_split_reduce(const float* partials, int32_t splits, int64_t count, int64_t stride, float* dw,
                                int32_t accumulate, hipStream_t stream);
 
+// Forward pass on int8 activation codes (int8 MFMA): y = act(float(sum q * W~) *
+// float(alpha_k * x_scale)), NHWC, bf16 or fp32 output.  Needs C % 16 == 0, R*S <= 63,
+// int32-safe sums and tensors below 2 GiB (conv_i8_eligible); no workspace.
+struct ConvI8Args {
+    const int8_t* x;          // NHWC [N][H][W][C] int8 codes
+    const uint32_t* codes;    // TBN2 codes of K filters of n = R*S*C elements
+    const float* alpha;       // [K]
+    void* y;                  // NHWC [N][P][Q][K]
+    float x_scale;
+    int32_t N, H, W, C, K, R, S, sh, sw, ph, pw, P, Q;
+    int32_t relu, y_f32;
+    FastDiv div_q, div_pq, div_tilesN;
+    uint32_t rep_lo, rep_hi;  // sum_{r < R} 2^(r*S)
+};
+bool conv_i8_eligible(const ConvI8Args& a);
+// Tile shape (1: 128 x 256, 2: 128 x 128, 3: 128 x 64, 4: 64 x 128); TBN_I8_TILE forces one.
+int conv_i8_tile(const ConvI8Args& a);
+hipError_t launch_conv_i8(const ConvI8Args& a, hipStream_t stream);
+// q = clamp(round-half-even(x * inv), -127, 127), NaN -> 0; x bf16 or fp32.
+hipError_t launch_quantize_act_i8(const void* x, int x_f32, int64_t count, float inv, int8_t* q,
+                                  hipStream_t stream);
+
 struct DenseConvArgs {
     const void* x;
     const float* w;          // [K][R][S][C] fp32, rounded to bf16 on load
