@@ -28,6 +28,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PEAK_INT8_TOPS = 5000.0     # MI355X dense int8 MFMA
 
 LAYER = dict(n=128, h=56, w=56, c=256, k=256, r=3, s=3, stride=1, pad=1)
 LR, MOMENTUM, WD = 0.1, 0.9, 1e-4
@@ -365,6 +366,52 @@ def fused_update(dev, reps=20):
     return out
 
 
+def int8_forward(dev, desc, x, codes, alpha, conv_flops, reps=20):
+    """The integer-activation variant of the forward pass on the training layer: activation
+    codes (2 B read + 1 B written per activation) and the forward pass on the int8 matrix
+    cores, timed with HIP events on the stream they run on.  The activation scale is fixed
+    once from max|x| (a calibration step, outside the timed region)."""
+    import torch
+
+    import paper_1701_00485_amd as tbn
+
+    stream = torch.cuda.current_stream()
+    amax = float(x.float().abs().max())
+    x_scale = amax / 127.0
+    xq = torch.empty(x.shape, dtype=torch.int8, device=dev)
+    P, Q = desc.out_dims()
+    y = torch.empty((desc.n, P, Q, desc.k), dtype=torch.bfloat16, device=dev)
+
+    def quant():
+        tbn.quantize_act_i8(x, 127.0 / amax, q=xq)
+
+    def conv():
+        tbn.conv2d_fwd_i8(desc, xq, codes, alpha, x_scale, y=y)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    us_q = timed(quant)
+    us_c = timed(conv)
+    tops = conv_flops / (us_c * 1e-6) / 1e12
+    gbs = 3.0 * x.numel() / (us_q * 1e-6) / 1e9
+    return {
+        "shape": "conv3x3 256->256 ch, 56x56, pad 1, batch 128; int8 activations, bf16 output",
+        "act_quantize": {"us": round(us_q, 2), "achieved_GBs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)},
+        "conv_fwd_i8": {"us": round(us_c, 2), "achieved_TOPS": round(tops, 1), "peak_TOPS": PEAK_INT8_TOPS,
+                        "frac": round(tops / PEAK_INT8_TOPS, 4)},
+    }
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -482,6 +529,8 @@ def main():
             "traffic": measured_traffic(dom),
         },
     }
+    result["int8_forward"] = int8_forward(dev, desc, x, codes, alpha, conv_flops)
+    result["int8_forward"]["bf16_fwd_us"] = round(per_kernel["fwd"] * 1e3, 2)
     if not args.no_resnet:
         result["resnet18_fwd"] = resnet18_fwd(dev)
     if not args.no_small:
