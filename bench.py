@@ -271,8 +271,18 @@ def small_configs(dev, steps=20, warmup=3):
         xb = torch.from_numpy(mk().view(np.int16)).to(dev).view(torch.bfloat16)
         lab = torch.from_numpy(synth.labels(2, "bench_lab", batch, 10).astype(np.int32)).to(dev)
         ms = timed(lambda: net.step(xb, lab), steps)
+        # the same iteration captured once as a HIP graph and replayed (no host launch work)
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            net.step(xb, lab)
+        torch.cuda.synchronize()
+        gms = timed(graph.replay, steps)
         out[name] = {"batch": batch, "ms_per_iteration": round(ms, 4), "images_per_s": round(batch / (ms * 1e-3), 1),
-                     "effective_tflops": round(cls.train_flops(batch) / (ms * 1e-3) / 1e12, 2)}
+                     "effective_tflops": round(cls.train_flops(batch) / (ms * 1e-3) / 1e12, 2),
+                     "graph_ms_per_iteration": round(gms, 4),
+                     "graph_images_per_s": round(batch / (gms * 1e-3), 1)}
     return out
 
 

@@ -247,7 +247,8 @@ class _Trainer:
             return  # the previous step's fused update already quantised the new weights
         for l in self.two_bit_layers():
             l.quantize()
-            self._rec(trace, "quantize", l, w=l.w.clone(), codes=l.codes.clone(), alpha=l.alpha.clone())
+            if trace is not None:
+                self._rec(trace, "quantize", l, w=l.w.clone(), codes=l.codes.clone(), alpha=l.alpha.clone())
 
     def _update_two_bit(self, trace, layer, g, fused):
         """SGD on a two-bit layer's real filters; with `fused`, the same pass also

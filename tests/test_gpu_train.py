@@ -274,3 +274,44 @@ def test_lenet_training_loss_curve(tbn):
     means = losses.reshape(6, 10).mean(axis=1)
     assert np.all(np.diff(means) < 0), means
     assert losses[-5:].mean() < losses[0] - 0.1, losses
+
+
+def _state(net):
+    """Every tensor a training iteration updates."""
+    ts = []
+    for l in net.two_bit_layers():
+        ts += [l.w, l.v, l.codes, l.alpha]
+    for conv in getattr(net, "convs", [])[:1]:
+        ts += [conv.w, conv.v]  # the full-precision first layer
+    for bn in getattr(net, "bns", []):
+        ts += [bn.gamma, bn.beta, bn.vg, bn.vb]
+    return ts
+
+
+@pytest.mark.parametrize("name", ["lenet", "vgg"])
+def test_training_iteration_graph_replay(tbn, name):
+    """One training iteration captured as a HIP graph and replayed: every replay equals an
+    eager iteration of an identically initialised network bit for bit (loss and every
+    updated tensor), with eager work and synchronisations between the replays."""
+    from paper_1701_00485_amd.networks import LeNet, VGGSmall
+    cls, batch, mk = (LeNet, 64, _lenet_batch) if name == "lenet" else (VGGSmall, 16, _vgg_batch)
+    x, lab = mk(batch, "graph")
+    eager, graphed = cls(), cls()
+    le, lg = eager.step(x, lab), graphed.step(x, lab)  # first iteration eager on both
+    torch.cuda.synchronize()
+    assert torch.equal(le, lg)
+    stream = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        loss_g = graphed.step(x, lab)
+    torch.cuda.synchronize()
+    for it in range(4):
+        graph.replay()
+        le = eager.step(x, lab)
+        torch.cuda.synchronize()
+        log("%s graph replay %d: loss %.5f (eager %.5f)" % (name, it, float(loss_g.item()), float(le.item())))
+        assert torch.equal(loss_g, le), it
+        for a, b in zip(_state(eager), _state(graphed)):
+            assert torch.equal(a, b), it
