@@ -307,9 +307,9 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
             for (int i = 0; i < TM; ++i)
                 af[i] = *reinterpret_cast<const bf16x8*>(st + L::A + arow + 32 * i * ROWB + seg_off[u]);
         };
-        if constexpr (TM <= 4) {
-            // all of the stage's A operands are read up front so that LDS latency
-            // overlaps the decode and the first MFMAs
+        if constexpr (TM <= 4 && TM * TN < 8) {
+            // small wave tiles: all of the stage's A operands are read up front so that
+            // LDS latency overlaps the decode and the first MFMAs
             bf16x8 afs[4][TM];
 #pragma unroll
             for (int u = 0; u < 4; ++u) read_a(u, afs[u]);
@@ -322,6 +322,31 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(bfr[t], afs[u][i], acc[i][t]);
+            }
+        } else if constexpr (TM <= 4) {
+            // 8 or more MFMAs per step: the A operands of step u + 1 are read during step u,
+            // one read after each of the first TM MFMAs (measured ~3% faster in the
+            // backward-data pass of the training layer than reading the stage up front)
+            bf16x8 afs[4][TM];
+            read_a(0, afs[0]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (u + 1 < 4) read_a(u + 1, afs[u + 1]);
+                bf16x8 bfr[TN];
+                decode_b(u, bfr);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(bfr[t], afs[u][i], acc[i][t]);
+                if (u + 1 < 4) {
+#pragma unroll
+                    for (int k = 0; k < TM; ++k) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
         } else {
             // tall wave tiles: A operands one 16-element step ahead
