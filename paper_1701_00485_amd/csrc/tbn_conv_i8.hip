@@ -262,21 +262,50 @@ __global__ __launch_bounds__(256, 2) void conv_i8_kernel(const ConvI8Args a) {
 #pragma unroll
         for (int t = 0; t < TN; ++t) braw[t] = *reinterpret_cast<const u32x4*>(st + L::B + bcol + 32 * 16 * t);
         i32x4 afs[4][TM];
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
+        auto read_a = [&](int u) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
                 afs[u][i] = *reinterpret_cast<const i32x4*>(st + L::A + arow + 32 * i * ROWB + seg_off[u]);
-        __builtin_amdgcn_sched_barrier(0);  // keep the LDS reads ahead of the MFMAs
+        };
+        if constexpr (TM * TN < 8) {
+            // small wave tiles: the stage's A operands up front
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            i32x4 bfr[TN];
+            for (int u = 0; u < 4; ++u) read_a(u);
+            __builtin_amdgcn_sched_barrier(0);  // keep the LDS reads ahead of the MFMAs
 #pragma unroll
-            for (int t = 0; t < TN; ++t) bfr[t] = decode_i8(braw[t][u]);
+            for (int u = 0; u < 4; ++u) {
+                i32x4 bfr[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+                for (int t = 0; t < TN; ++t) bfr[t] = decode_i8(braw[t][u]);
 #pragma unroll
-                for (int t = 0; t < TN; ++t) acc[i][t] = mfma_i8(bfr[t], afs[u][i], acc[i][t]);
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int t = 0; t < TN; ++t) acc[i][t] = mfma_i8(bfr[t], afs[u][i], acc[i][t]);
+            }
+        } else {
+            // the next step's A operands read between the current step's MFMAs, one read
+            // after each of the first TM MFMAs
+            read_a(0);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (u + 1 < 4) read_a(u + 1);
+                i32x4 bfr[TN];
+#pragma unroll
+                for (int t = 0; t < TN; ++t) bfr[t] = decode_i8(braw[t][u]);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int t = 0; t < TN; ++t) acc[i][t] = mfma_i8(bfr[t], afs[u][i], acc[i][t]);
+                if (u + 1 < 4) {
+#pragma unroll
+                    for (int k = 0; k < TM; ++k) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+                        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
     }
 
