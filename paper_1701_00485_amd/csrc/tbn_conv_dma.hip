@@ -324,26 +324,37 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
                     for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(bfr[t], afs[u][i], acc[i][t]);
             }
         } else if constexpr (TM <= 4) {
-            // 8 or more MFMAs per step: the A operands of step u + 1 are read during step u,
-            // one read after each of the first TM MFMAs (measured ~3% faster in the
-            // backward-data pass of the training layer than reading the stage up front)
+            // 8 or more MFMAs per step: the A operands of step u + 1 are read and its filter
+            // operand decoded while the MFMAs of step u run (one LDS read and two decode ops
+            // after each MFMA); measured ~3-4% faster in the backward-data pass and ~1-2% in
+            // the forward pass of the training layer than reading and decoding each step
+            // right before its MFMAs
             bf16x8 afs[4][TM];
+            bf16x8 bfr[2][TN];
             read_a(0, afs[0]);
+            decode_b(0, bfr[0]);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                if (u + 1 < 4) read_a(u + 1, afs[u + 1]);
-                bf16x8 bfr[TN];
-                decode_b(u, bfr);
+                if (u + 1 < 4) {
+                    read_a(u + 1, afs[u + 1]);
+                    decode_b(u + 1, bfr[(u + 1) & 1]);
+                }
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
-                    for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(bfr[t], afs[u][i], acc[i][t]);
+                    for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(bfr[u & 1][t], afs[u][i], acc[i][t]);
                 if (u + 1 < 4) {
 #pragma unroll
                     for (int k = 0; k < TM; ++k) {
                         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
                         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+                        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // two decode ops
+                    }
+#pragma unroll
+                    for (int k = TM; k < TM * TN; ++k) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
