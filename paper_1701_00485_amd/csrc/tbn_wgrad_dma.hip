@@ -20,7 +20,7 @@
 //   * pixel-major (wide layers): each pixel's 256 dy channels / 256 x columns form one
 //     512-byte row of the stage, two pixels per 1088-byte slot, so that one 64-lane DMA
 //     instruction copies two pixels' contiguous bytes and the requests cover whole cache
-//     lines; 48-pixel stages, three deep, with an L2 prefetch of a later stage;
+//     lines; 48-pixel stages, three deep (an L2 prefetch of a later stage is an option);
 //   * segment-major (K < 128): 64-pixel stages, two deep; for every 8-channel segment the
 //     64 pixels' 16-byte pieces are contiguous (one DMA instruction, lane = pixel),
 //     segments 1088 bytes apart; with few valid dy channels this issues fewer copies.
@@ -256,7 +256,7 @@ constexpr int PP = 1088;  // bytes per pair of pixel rows
 // PIXR pixels per stage (a multiple of 16), STAGES-deep ring; 2 x 4 waves of 128 x 64,
 // two waves per SIMD.  (One wave per SIMD with 128 x 128 wave tiles reads a third less
 // from LDS per MFMA but measured slower: the stage boundaries are no longer covered.)
-template <int PIXR, int STAGES>
+template <int PIXR, int STAGES, bool PF>
 __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs ka) {
     const WgradArgs& a = ka.a;
     constexpr int WAVES = 8;
@@ -436,14 +436,14 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][t][v] = 0.0f;
 
-    // every issue() is followed by one prefetch; a stage's copies are complete once at most
-    // the copies and prefetches issued after them are outstanding
+    // with PF every issue() is followed by one prefetch; a stage's copies are complete once
+    // at most the copies (and prefetches) issued after them are outstanding
 #pragma unroll
     for (int c = 0; c < STAGES - 1; ++c) {
         table(c);
         if (c < nst) {
             issue(c);
-            prefetch(c + pf_dist);
+            if constexpr (PF) prefetch(c + pf_dist);
         }
     }
     table(STAGES - 1);
@@ -452,13 +452,13 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
         // this wave's DMAs of stage `it` landed (later stages and the prefetch issued with
         // stage `it` may still be in flight; in the last stages simply everything)
         if (it + STAGES - 2 < nst)
-            wait_vmcnt((STAGES - 2) * (kDmas + 1) + 1);
+            wait_vmcnt(PF ? (STAGES - 2) * (kDmas + 1) + 1 : (STAGES - 2) * kDmas);
         else
             wait_vmcnt(0);
         __syncthreads();  // ... and every other wave's; all reads of stage it-1 are done
         if (it + STAGES - 1 < nst) {
             issue(it + STAGES - 1);  // into stage it-1's buffer
-            prefetch(it + STAGES - 1 + pf_dist);
+            if constexpr (PF) prefetch(it + STAGES - 1 + pf_dist);
             table(it + STAGES);      // the offsets of the next copy, during the MFMAs
         }
         const uint32_t st = smem_base + (uint32_t)(cslot * PR_STAGE);
@@ -533,15 +533,22 @@ hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream) {
     ka.a = a;
     ka.div_q = make_fastdiv((uint32_t)a.Q);
     ka.div_pq = make_fastdiv((uint32_t)a.P * (uint32_t)a.Q);
+    // L2 prefetch of a later stage: off by default (measured ~9% slower on the training
+    // layer once the reads and MFMAs are interleaved); TBN_WGRAD_PF=<stages ahead> turns it on
     const char* pf = getenv("TBN_WGRAD_PF");
-    ka.pf_dist = pf ? atoi(pf) : 3;  // stages ahead (measured: 3 with 48-pixel stages)
+    ka.pf_dist = pf ? atoi(pf) : 0;
     const WgradDmaPlan p = wgrad_dma_plan(a.K, a.R * a.S * a.C);
     const dim3 grid((unsigned)(p.tiles * a.splits));
     if (p.cfg == 1) {
         switch (p.pix) {
-            case 32: hipLaunchKernelGGL((wgrad_rows_kernel<32, 4>), grid, dim3(512), 0, stream, ka); break;
-            case 64: hipLaunchKernelGGL((wgrad_rows_kernel<64, 2>), grid, dim3(512), 0, stream, ka); break;
-            default: hipLaunchKernelGGL((wgrad_rows_kernel<48, 3>), grid, dim3(512), 0, stream, ka); break;
+            case 32: hipLaunchKernelGGL((wgrad_rows_kernel<32, 4, false>), grid, dim3(512), 0, stream, ka); break;
+            case 64: hipLaunchKernelGGL((wgrad_rows_kernel<64, 2, false>), grid, dim3(512), 0, stream, ka); break;
+            default:
+                if (ka.pf_dist > 0)
+                    hipLaunchKernelGGL((wgrad_rows_kernel<48, 3, true>), grid, dim3(512), 0, stream, ka);
+                else
+                    hipLaunchKernelGGL((wgrad_rows_kernel<48, 3, false>), grid, dim3(512), 0, stream, ka);
+                break;
         }
     } else {
         hipLaunchKernelGGL(wgrad_seg_kernel, grid, dim3(512), 0, stream, ka);

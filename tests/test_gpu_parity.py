@@ -445,13 +445,14 @@ def test_bwd_weight_parity(tbn, g, accumulate):
     assert e <= 1e-4
 
 
-@pytest.mark.parametrize("cfg,pix", [(0, 48), (1, 32), (1, 48), (1, 64)])
-def test_bwd_weight_tile_shapes(tbn, cfg, pix, monkeypatch):
+@pytest.mark.parametrize("cfg,pix,pf", [(0, 48, 0), (1, 32, 0), (1, 48, 0), (1, 64, 0), (1, 48, 3)])
+def test_bwd_weight_tile_shapes(tbn, cfg, pix, pf, monkeypatch):
     # every tile / stage geometry of the transposing-read weight-gradient kernels (the
     # 48-pixel stages do not divide the 64-pixel split ranges: the last stage of a range is
-    # partial)
+    # partial), and the optional L2 prefetch
     monkeypatch.setenv("TBN_WGRAD_CFG", str(cfg))
     monkeypatch.setenv("TBN_WGRAD_PIX", str(pix))
+    monkeypatch.setenv("TBN_WGRAD_PF", str(pf))
     for g in [(2, 14, 14, 256, 256, 3, 3, 1, 1), (3, 12, 12, 128, 136, 3, 3, 2, 1), (5, 9, 7, 64, 96, 3, 3, 1, 1),
               (2, 16, 16, 64, 128, 1, 1, 2, 0)]:
         d, P, Q, xb, dyb, _ = _conv_inputs(g, 5)
