@@ -47,6 +47,8 @@ def _load():
     i64 = ctypes.c_int64
     lib.orc_round_bf16.argtypes = [p, i64, p]
     lib.orc_round_bf16.restype = None
+    lib.orc_codes_of_bits.argtypes = [ctypes.c_uint64, i64, p]
+    lib.orc_codes_of_bits.restype = None
     lib.orc_quantize.argtypes = [p, i64, i64, p, p, p, p, p, p, p]
     lib.orc_quantize.restype = ctypes.c_int
     lib.orc_packed_words.argtypes = [i64, i64]
@@ -182,6 +184,14 @@ def quantize(w: np.ndarray) -> Quantized:
         raise OracleError("non-finite weight: outside the method's domain")
     if st != 0:
         raise OracleError("quantize: bad shape")
+    return out
+
+
+def codes_of_bits(start: int, count: int) -> np.ndarray:
+    """Eq. (3) codes of the fp32 values with bit patterns start .. start + count - 1
+    (int8; NaN patterns, outside the method, get 0)."""
+    out = np.empty(count, np.int8)
+    _load().orc_codes_of_bits(int(start), int(count), _ptr(out))
     return out
 
 

@@ -72,6 +72,21 @@ static int orc_discretize_one(double w) {
 }
 
 /*
+ * Eq. (3) codes of the fp32 values whose bit patterns are start, start + 1, ...,
+ * start + count - 1 (taken modulo 2^32), for the exhaustive check of the discretisation
+ * over every fp32 value.  A NaN is outside the method and gets the marker 0.
+ */
+void orc_codes_of_bits(uint64_t start, int64_t count, int8_t* codes) {
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < count; ++i) {
+        const uint32_t b = (uint32_t)(start + (uint64_t)i);
+        float f;
+        memcpy(&f, &b, sizeof f);
+        codes[i] = isnan(f) ? 0 : (int8_t)orc_discretize_one((double)f);
+    }
+}
+
+/*
  * Quantise K filters of n real weights each (w is [K][n], row k = filter k).
  * Writes codes [K][n] in {-2,-1,1,2}, the optimal scale alpha [K] (fp64, and its
  * single round-to-nearest fp32 value), the sizes |B1|, |B2| and the sums over B1 and

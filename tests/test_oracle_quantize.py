@@ -248,3 +248,19 @@ def test_stochastic_rounding_is_unbiased():
     for row, v in zip(q.codes, vals):
         lo, hi = {True: (-2, -1), False: (-1, 1)}[bool(v < -1)] if v <= 1 else (1, 2)
         assert set(np.unique(row)).issubset({lo, hi})
+
+
+def test_codes_of_bits_follow_eq3():
+    # the bit-pattern form used by the exhaustive GPU check: hand values at the boundaries
+    # (just below / at / above +1 and -1, both zeros, denormals, infinities, NaN marker)
+    pats = {0x3F7FFFFF: 1, 0x3F800000: 1, 0x3F800001: 2, 0xBF7FFFFF: -1, 0xBF800000: -1, 0xBF800001: -2,
+            0x00000000: -1, 0x80000000: -1, 0x00000001: 1, 0x80000001: -1, 0x7F800000: 2, 0xFF800000: -2,
+            0x7FC00000: 0, 0xFFC00001: 0, 0x7F7FFFFF: 2, 0xFF7FFFFF: -2}
+    for b, want in pats.items():
+        assert int(oracle.codes_of_bits(b, 1)[0]) == want, hex(b)
+    # and it agrees with the quantiser's codes on every finite value of a strided sweep
+    start, count = 0x3E000000, 1 << 20
+    got = oracle.codes_of_bits(start, count)
+    w = (np.arange(start, start + count, dtype=np.uint64).astype(np.uint32)).view(np.float32).reshape(256, -1)
+    assert np.all(np.isfinite(w))
+    assert np.array_equal(got.reshape(256, -1), oracle.quantize(w).codes)
