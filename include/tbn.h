@@ -93,6 +93,14 @@ tbn_status tbn_conv_out_dims(const tbn_conv_desc* desc, int32_t* p, int32_t* q);
  * (ceil(K/64) * ceil(n/64) * 256), or -1 if K or n <= 0. */
 int64_t tbn_packed_words(int64_t k, int64_t n);
 
+/* uint32 words that one filter row of n elements occupies in the TBN2 layout: the row is
+ * padded to whole 64-code groups of 4 words, 4 * ceil(n/64); -1 if n <= 0. */
+int64_t tbn_packed_row_words(int64_t n);
+
+/* Bytes of the packed codes of K filters of n elements (4 * tbn_packed_words(k, n) =
+ * 1024 * ceil(K/64) * ceil(n/64)), or -1 if K or n <= 0. */
+int64_t tbn_packed_bytes(int64_t k, int64_t n);
+
 /* Bytes of caller-provided workspace `op` needs for `desc` (0 = none needed).
  * Pass the same op and geometry to the corresponding call.  TBN_OP_FWD: fp32 partial sums
  * of a split reduction, or, for inputs with fewer than 8 channels and at least 2^20

@@ -76,6 +76,8 @@ def load():
         "tbn_last_error": ([], ctypes.c_char_p),
         "tbn_conv_out_dims": ([vp, vp, vp], i32),
         "tbn_packed_words": ([i64, i64], i64),
+        "tbn_packed_row_words": ([i64], i64),
+        "tbn_packed_bytes": ([i64, i64], i64),
         "tbn_workspace_size": ([i32, vp, vp], i32),
         "tbn_quantize": ([vp, i64, i64, vp, vp, vp, vp], i32),
         "tbn_quantize_variant": ([vp, i64, i64, f32, vp, vp, vp, vp, vp], i32),
@@ -108,6 +110,7 @@ def load():
 
 def exported_symbols():
     return sorted(["tbn_status_str", "tbn_last_error", "tbn_conv_out_dims", "tbn_packed_words",
+                   "tbn_packed_row_words", "tbn_packed_bytes",
                    "tbn_workspace_size", "tbn_quantize", "tbn_quantize_variant", "tbn_conv2d_fwd", "tbn_conv2d_fwd_dense",
                    "tbn_quantize_act_i8", "tbn_conv2d_fwd_i8",
                    "tbn_conv2d_bwd_data",
@@ -154,6 +157,14 @@ def _dtype_code(dt):
 
 def packed_words(k: int, n: int) -> int:
     return int(load().tbn_packed_words(k, n))
+
+
+def packed_row_words(n: int) -> int:
+    return int(load().tbn_packed_row_words(n))
+
+
+def packed_bytes(k: int, n: int) -> int:
+    return int(load().tbn_packed_bytes(k, n))
 
 
 def workspace_size(op: int, desc: ConvDesc) -> int:

@@ -187,6 +187,16 @@ int64_t tbn_packed_words(int64_t k, int64_t n) {
     return ((k + 63) / 64) * ((n + 63) / 64) * 256;
 }
 
+int64_t tbn_packed_row_words(int64_t n) {
+    if (n <= 0) return -1;
+    return (n + 63) / 64 * 4;
+}
+
+int64_t tbn_packed_bytes(int64_t k, int64_t n) {
+    const int64_t w = tbn_packed_words(k, n);
+    return w < 0 ? -1 : 4 * w;
+}
+
 tbn_status tbn_workspace_size(tbn_op op, const tbn_conv_desc* desc, size_t* bytes) {
     Geometry g;
     tbn_status st = check_desc(desc, &g);

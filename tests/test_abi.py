@@ -54,6 +54,10 @@ def test_bad_geometry(g):
 def test_packed_words_match_oracle(K, n):
     assert tbn.packed_words(K, n) == oracle.packed_words(K, n)
     assert tbn.packed_words(0, n) == -1
+    # one filter row: whole 64-code groups of 4 words; K filters: 1 KiB per 64 x 64 block
+    assert tbn.packed_row_words(n) == 4 * -(-n // 64)
+    assert tbn.packed_bytes(K, n) == 4 * oracle.packed_words(K, n) == 1024 * -(-K // 64) * -(-n // 64)
+    assert tbn.packed_row_words(0) == -1 and tbn.packed_bytes(K, 0) == -1
 
 
 def test_argument_errors_before_launch():

@@ -73,6 +73,30 @@ def _boundary_weights(K, n, name):
     return out.astype(np.float32)
 
 
+def test_codes_of_every_fp32_bit_pattern(tbn):
+    """Eq. 3 on all 2^32 fp32 bit patterns (16 chunks of 2^28 weights, quantised as 65536
+    filters of 4096): the GPU's codes equal the oracle's for every non-NaN value, and a NaN
+    gets -1 (the documented choice; NaN is outside the method)."""
+    CH = 1 << 28
+    K, n = CH // 4096, 4096
+    for c in range(16):
+        start = c * CH
+        v = torch.arange(start, start + CH, dtype=torch.int64, device="cuda")
+        v = torch.where(v >= 2 ** 31, v - 2 ** 32, v).to(torch.int32)
+        w = v.view(torch.float32).view(K, n)
+        codes, _, _ = tbn.quantize(w, want_counts=False)
+        torch.cuda.synchronize()
+        del v, w
+        got = oracle.unpack(words_np(codes), K, n).ravel()
+        ref = oracle.codes_of_bits(start, CH)
+        nan = ref == 0
+        bad = int(np.count_nonzero(got[~nan] != ref[~nan]))
+        log("bit patterns 0x%08x..0x%08x: %d NaN, %d mismatches" % (start, start + CH - 1, int(nan.sum()), bad))
+        assert bad == 0
+        assert np.all(got[nan] == -1)
+        del codes, got, ref, nan
+
+
 QCASES = [
     # K, n, distribution
     (1, 1, "n1"), (32, 25, "n0.05"), (64, 800, "n0.05"), (10, 512, "n1"), (130, 2304, "n1"),
