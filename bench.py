@@ -88,6 +88,16 @@ def measured_traffic(op):
     return None
 
 
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(budget_s: float):
     """The fp64 oracle on a bounded slice of the same step: quantise and SGD over the whole
     layer, and the three convolutions on as many images of the batch as fit in `budget_s`
@@ -127,6 +137,8 @@ def cpu_baseline(budget_s: float):
         "value": round(3 * conv_flops / step_s / 1e12, 6),
         "unit": "TFLOP/s",
         "cores": int(os.environ.get("OMP_NUM_THREADS", threads)),
+        "affinity_cores": threads,
+        "cpu_model": _cpu_model(),
         "kind": "oracle",
         "sample": "fp64 oracle: quantise + SGD over the full 256x3x3x256 layer, fwd/bwd_data/bwd_weight "
                   "on %d of 128 images (mean per image scaled x128); measured %.1f s, extrapolated %.0f s "
