@@ -85,7 +85,7 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
         for (int u = 0; u < kU; ++u) {
             int ib = 4 * (step0 + u) + g;
             ib = ib < NB ? ib : NB - 1;  // in bounds; its activations are zero past n
-            w[u] = codes[(int64_t)ib * 64];
+            w[u] = __builtin_nontemporal_load(&codes[(int64_t)ib * 64]);  // read once: streaming
         }
     };
     const uint32_t half_one = __builtin_amdgcn_readfirstlane(0x3F003F00u);  // bf16 (0.5, 0.5)
