@@ -235,6 +235,39 @@ class _Trainer:
         if trace is not None:
             trace.append((kind, info, t))
 
+    def named_state(self):
+        """The training state by name: real weights and momenta of every layer, batch-norm
+        parameters and their momenta.  The codes and scales are not part of it: they are a
+        function of the real weights (Eq. 3-5) and are recomputed after a restore."""
+        out, seen = {}, []
+        for l in list(getattr(self, "convs", [])) + self.two_bit_layers():
+            if any(l is o for o in seen):
+                continue
+            seen.append(l)
+            out[l.name + ".w"], out[l.name + ".v"] = l.w, l.v
+        for bn in getattr(self, "bns", []):
+            for f in ("gamma", "beta", "vg", "vb"):
+                out["%s.%s" % (bn.name, f)] = getattr(bn, f)
+        return out
+
+    def save(self, path):
+        """Checkpoint the training state and the learning rate to an .npz file."""
+        arrays = {k: t.detach().cpu().numpy() for k, t in self.named_state().items()}
+        np.savez(path, lr=np.float64(self.lr), **arrays)
+
+    def load(self, path):
+        """Restore a checkpoint written by save(); the next step re-quantises the restored
+        weights, so training continues bit-identically to an uninterrupted run."""
+        with np.load(path) as data:  # plain arrays only (no pickled objects)
+            for k, t in self.named_state().items():
+                src = torch.from_numpy(data[k])
+                if tuple(src.shape) != tuple(t.shape):
+                    raise ValueError("checkpoint tensor %s has shape %s, expected %s" % (k, tuple(src.shape),
+                                                                                       tuple(t.shape)))
+                t.copy_(src.to(t.device))
+            self.lr = float(data["lr"])
+        self._codes_current = False
+
     def _sgd(self, trace, name, w, v, g, wd):
         if trace is not None:
             w0, v0 = w.clone(), v.clone()

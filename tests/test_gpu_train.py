@@ -315,3 +315,28 @@ def test_training_iteration_graph_replay(tbn, name):
         assert torch.equal(loss_g, le), it
         for a, b in zip(_state(eager), _state(graphed)):
             assert torch.equal(a, b), it
+
+
+@pytest.mark.parametrize("name,fused", [("lenet", True), ("vgg", False)])
+def test_checkpoint_resume_is_bit_exact(tbn, name, fused, tmp_path):
+    """Two iterations, a checkpoint, two more; a fresh network restored from the checkpoint
+    runs the same two iterations bit for bit (losses and every updated tensor)."""
+    from paper_1701_00485_amd.networks import LeNet, VGGSmall
+    cls, batch, mk = (LeNet, 64, _lenet_batch) if name == "lenet" else (VGGSmall, 16, _vgg_batch)
+    x, lab = mk(batch, "ckpt")
+    a = cls()
+    for _ in range(2):
+        a.step(x, lab, fused=fused)
+    path = str(tmp_path / "ckpt.npz")
+    a.save(path)
+    la = [float(a.step(x, lab, fused=fused).item()) for _ in range(2)]
+    b = cls(stream=7)  # different initial weights, overwritten by the restore
+    b.load(path)
+    lb = [float(b.step(x, lab, fused=fused).item()) for _ in range(2)]
+    torch.cuda.synchronize()
+    log("%s resume: losses %s / %s" % (name, la, lb))
+    assert la == lb
+    sa, sb = a.named_state(), b.named_state()
+    assert sa.keys() == sb.keys()
+    for k in sa:
+        assert torch.equal(sa[k], sb[k]), k
