@@ -52,7 +52,7 @@ typedef enum tbn_status {
     TBN_OK = 0,
     TBN_ERR_NULL = 1,        /* a required pointer is NULL */
     TBN_ERR_SHAPE = 2,       /* a size or geometry is invalid (<= 0, empty output, overflow) */
-    TBN_ERR_UNSUPPORTED = 3, /* valid request this build does not implement */
+    TBN_ERR_UNSUPPORTED = 3, /* valid request the library does not implement */
     TBN_ERR_ALIGN = 4,       /* a pointer is not 16-byte aligned */
     TBN_ERR_WORKSPACE = 5,   /* workspace missing or smaller than tbn_workspace_size() */
     TBN_ERR_HIP = 6          /* a HIP launch failed; see tbn_last_error() */
