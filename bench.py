@@ -291,10 +291,20 @@ def small_configs(dev, steps=20, warmup=3):
             net.step(xb, lab)
         torch.cuda.synchronize()
         gms = timed(graph.replay, steps)
+        # the update fused with the next iteration's quantisation (one pass over the real
+        # weights; the iteration then has no separate quantisation), eager and as a graph
+        fms = timed(lambda: net.step(xb, lab, fused=True), steps)
+        fgraph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(fgraph, stream=side):
+            net.step(xb, lab, fused=True)
+        torch.cuda.synchronize()
+        fgms = timed(fgraph.replay, steps)
         out[name] = {"batch": batch, "ms_per_iteration": round(ms, 4), "images_per_s": round(batch / (ms * 1e-3), 1),
                      "effective_tflops": round(cls.train_flops(batch) / (ms * 1e-3) / 1e12, 2),
                      "graph_ms_per_iteration": round(gms, 4),
-                     "graph_images_per_s": round(batch / (gms * 1e-3), 1)}
+                     "graph_images_per_s": round(batch / (gms * 1e-3), 1),
+                     "fused_update_ms_per_iteration": round(fms, 4),
+                     "fused_update_graph_ms_per_iteration": round(fgms, 4)}
     return out
 
 
