@@ -257,7 +257,9 @@ tbn_status tbn_sgd_step_quantize(float* w, float* v, const float* g, int64_t k, 
 /* ------------------------------------------------------------------------------------ */
 
 /* Pooling geometry: input N x H x W x C, square window k, stride, zero-size padding
- * (padded positions never win a maximum).  P = (H + 2*pad - k)/stride + 1 (floor). */
+ * (padded positions never win a maximum).  P = (H + 2*pad - k)/stride + 1 (floor).
+ * TBN_ERR_SHAPE if H*W, H + 2*pad + stride or W + 2*pad + stride exceeds 2^31 - 1 (positions
+ * and argmax are 32-bit) or the input or output has more than 2^40 elements. */
 typedef struct tbn_pool_desc {
     int32_t n, h, w, c, k, stride, pad;
 } tbn_pool_desc;
@@ -275,7 +277,8 @@ tbn_status tbn_maxpool2d_fwd(const tbn_pool_desc* desc, const void* x, void* y, 
 tbn_status tbn_maxpool2d_bwd(const tbn_pool_desc* desc, const void* dy, const int32_t* argmax, void* dx,
                              tbn_dtype dxt, hipStream_t stream);
 
-/* y[n][c] = mean over (h, w) of x[n][h][w][c] (fp32 sum); y has dtype yt. */
+/* y[n][c] = mean over (h, w) of x[n][h][w][c] (fp32 sum); y has dtype yt.  TBN_ERR_SHAPE
+ * if h*w > 2^31 - 1 or x has more than 2^40 elements. */
 tbn_status tbn_avgpool_global(int32_t n, int32_t h, int32_t w, int32_t c, const void* x, void* y, tbn_dtype yt,
                               hipStream_t stream);
 

@@ -31,6 +31,12 @@ constexpr int64_t kI32Max = 0x7FFFFFFF;
 
 int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
+// a * b * c > limit, for positive factors, without overflowing
+bool product_over(int64_t a, int64_t b, int64_t c, int64_t limit) {
+    int64_t ab, abc;
+    return __builtin_mul_overflow(a, b, &ab) || __builtin_mul_overflow(ab, c, &abc) || abc > limit;
+}
+
 struct Geometry {
     int64_t N, H, W, C, K, R, S, sh, sw, ph, pw, P, Q;
 };
@@ -47,10 +53,11 @@ tbn_status check_desc(const tbn_conv_desc* d, Geometry* g) {
     g->sh = d->stride_h; g->sw = d->stride_w; g->ph = d->pad_h; g->pw = d->pad_w;
     g->P = (hp - d->r) / d->stride_h + 1;
     g->Q = (wp - d->s) / d->stride_w + 1;
-    // index arithmetic inside the kernels is 32-bit for pixels and filter elements
-    if (g->N * g->P * g->Q > kI32Max || g->N * g->H * g->W > kI32Max)
+    // index arithmetic inside the kernels is 32-bit for pixels and filter elements (the
+    // products are formed with overflow checks: each factor alone may be near 2^32)
+    if (product_over(g->N, g->P, g->Q, kI32Max) || product_over(g->N, g->H, g->W, kI32Max))
         return fail(TBN_ERR_SHAPE, "more than 2^31 - 1 pixels");
-    if (g->R * g->S * g->C > kI32Max / 2 || g->R * g->S * g->K > kI32Max / 2)
+    if (product_over(g->R, g->S, g->C, kI32Max / 2) || product_over(g->R, g->S, g->K, kI32Max / 2))
         return fail(TBN_ERR_SHAPE, "filter has more than 2^30 elements");
     return TBN_OK;
 }
@@ -545,10 +552,18 @@ tbn_status check_pool(const tbn_pool_desc* d, tbn::PoolArgs* a) {
         return fail(TBN_ERR_SHAPE, "invalid pooling geometry");
     if (d->h + 2 * (int64_t)d->pad < d->k || d->w + 2 * (int64_t)d->pad < d->k)
         return fail(TBN_ERR_SHAPE, "window larger than the padded input");
-    if ((int64_t)d->n * d->h * d->w * d->c > ((int64_t)1 << 40)) return fail(TBN_ERR_SHAPE, "tensor too large");
+    // the kernels index window rows and columns, and the argmax position h*W + w, in 32 bits
+    if ((int64_t)d->h + 2 * (int64_t)d->pad + d->stride > kI32Max ||
+        (int64_t)d->w + 2 * (int64_t)d->pad + d->stride > kI32Max || product_over(d->h, d->w, 1, kI32Max))
+        return fail(TBN_ERR_SHAPE, "more than 2^31 - 1 positions per image");
+    const int64_t P = ((int64_t)d->h + 2 * (int64_t)d->pad - d->k) / d->stride + 1;
+    const int64_t Q = ((int64_t)d->w + 2 * (int64_t)d->pad - d->k) / d->stride + 1;
+    if (product_over((int64_t)d->n * d->c, d->h, d->w, (int64_t)1 << 40) ||
+        product_over((int64_t)d->n * d->c, P, Q, (int64_t)1 << 40))
+        return fail(TBN_ERR_SHAPE, "tensor too large");
     a->N = d->n; a->H = d->h; a->W = d->w; a->C = d->c; a->k = d->k; a->s = d->stride; a->pad = d->pad;
-    a->P = (d->h + 2 * d->pad - d->k) / d->stride + 1;
-    a->Q = (d->w + 2 * d->pad - d->k) / d->stride + 1;
+    a->P = (int32_t)P;
+    a->Q = (int32_t)Q;
     return TBN_OK;
 }
 
@@ -591,6 +606,8 @@ tbn_status tbn_avgpool_global(int32_t n, int32_t h, int32_t w, int32_t c, const 
                               hipStream_t stream) {
     if (!x || !y) return fail(TBN_ERR_NULL, "x and y are required");
     if (n <= 0 || h <= 0 || w <= 0 || c <= 0) return fail(TBN_ERR_SHAPE, "sizes must be positive");
+    if (product_over(h, w, 1, kI32Max)) return fail(TBN_ERR_SHAPE, "more than 2^31 - 1 positions per image");
+    if (product_over((int64_t)n * c, h, w, (int64_t)1 << 40)) return fail(TBN_ERR_SHAPE, "tensor too large");
     if (yt != TBN_BF16 && yt != TBN_F32) return fail(TBN_ERR_UNSUPPORTED, "unknown dtype");
     if (!aligned16(x) || !aligned16(y)) return fail(TBN_ERR_ALIGN, "misaligned pointer");
     hipError_t e = tbn::launch_avgpool(n, h * w, c, reinterpret_cast<const uint16_t*>(x), y, yt == TBN_F32, stream);

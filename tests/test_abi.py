@@ -160,6 +160,8 @@ def test_batchnorm_workspace_checked():
 @pytest.mark.parametrize("g,why", [
     ((1 << 16, 200, 200, 8, 8, 1, 1, 1, 0), "more than 2^31 - 1 pixels"),
     ((1, 8, 8, 1 << 26, 8, 5, 5, 1, 2), "filter has more than 2^30 elements"),
+    # N * P * Q = 2^22 * 2^21 * 2^21 = 2^64: wraps to 0 in 64-bit arithmetic
+    ((1 << 22, 2, 2, 8, 8, 1, 1, 1, (1 << 20) - 1), "more than 2^31 - 1 pixels"),
 ])
 def test_index_range_limits(g, why):
     # sizes whose pixel or filter indices would overflow the kernels' 32-bit arithmetic are
@@ -170,6 +172,23 @@ def test_index_range_limits(g, why):
     assert lib.tbn_conv2d_fwd(ctypes.byref(d), good, 0, good, good, None, good, 0, good, 1 << 40, None) == 2
     assert lib.tbn_last_error().decode() == why
     assert lib.tbn_conv2d_bwd_weight(ctypes.byref(d), good, good, good, 0, good, 1 << 40, None) == 2
+
+
+@pytest.mark.parametrize("pd,why", [
+    ((1, 1 << 16, 1 << 16, 8, 2, 2, 0), "more than 2^31 - 1 positions per image"),
+    ((1, 8, 8, 8, 2, 1, (1 << 30)), "more than 2^31 - 1 positions per image"),
+    ((1 << 30, 1 << 10, 1 << 10, 1 << 30, 2, 2, 0), "tensor too large"),  # 2^80 elements
+])
+def test_pool_index_range_limits(pd, why):
+    # pooling sizes beyond the kernels' 32-bit positions, or whose element count overflows
+    # 64-bit arithmetic, are rejected before any launch
+    lib = tbn.load()
+    good = ctypes.c_void_p(0x100000)
+    d = tbn.PoolDesc(*pd)
+    assert lib.tbn_maxpool2d_fwd(ctypes.byref(d), good, good, None, None) == 2
+    assert lib.tbn_last_error().decode() == why
+    assert lib.tbn_avgpool_global(1, 1 << 16, 1 << 16, 8, good, good, 0, None) == 2
+    assert lib.tbn_last_error().decode() == "more than 2^31 - 1 positions per image"
 
 
 def test_unknown_dtype_and_pool_geometry():
