@@ -288,16 +288,19 @@ def _state(net):
     return ts
 
 
-@pytest.mark.parametrize("name", ["lenet", "vgg"])
-def test_training_iteration_graph_replay(tbn, name):
+@pytest.mark.parametrize("name,fused", [("lenet", False), ("vgg", False), ("lenet", True), ("vgg", True)])
+def test_training_iteration_graph_replay(tbn, name, fused):
     """One training iteration captured as a HIP graph and replayed: every replay equals an
     eager iteration of an identically initialised network bit for bit (loss and every
-    updated tensor), with eager work and synchronisations between the replays."""
+    updated tensor), with eager work and synchronisations between the replays.  With
+    `fused` the captured iteration is the steady state of the fused update: no separate
+    quantisation, the update re-quantising each two-bit layer."""
     from paper_1701_00485_amd.networks import LeNet, VGGSmall
     cls, batch, mk = (LeNet, 64, _lenet_batch) if name == "lenet" else (VGGSmall, 16, _vgg_batch)
     x, lab = mk(batch, "graph")
     eager, graphed = cls(), cls()
-    le, lg = eager.step(x, lab), graphed.step(x, lab)  # first iteration eager on both
+    # first iteration eager on both
+    le, lg = eager.step(x, lab, fused=fused), graphed.step(x, lab, fused=fused)
     torch.cuda.synchronize()
     assert torch.equal(le, lg)
     stream = torch.cuda.current_stream()
@@ -305,11 +308,11 @@ def test_training_iteration_graph_replay(tbn, name):
     side.wait_stream(stream)
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=side):
-        loss_g = graphed.step(x, lab)
+        loss_g = graphed.step(x, lab, fused=fused)
     torch.cuda.synchronize()
     for it in range(4):
         graph.replay()
-        le = eager.step(x, lab)
+        le = eager.step(x, lab, fused=fused)
         torch.cuda.synchronize()
         log("%s graph replay %d: loss %.5f (eager %.5f)" % (name, it, float(loss_g.item()), float(le.item())))
         assert torch.equal(loss_g, le), it
