@@ -307,7 +307,10 @@ tbn_status tbn_relu_bwd(const void* y, const void* dy, int64_t count, void* dx, 
 
 /* Softmax cross-entropy over fp32 logits [n][classes] with int32 labels: loss[0] = mean
  * over the batch of logsumexp(z) - z[label]; dlogits (bf16) = (softmax(z) - onehot)/n.
- * loss_per_sample is caller workspace of n floats. */
+ * loss_per_sample is caller workspace of n floats.  Labels live in device memory and are
+ * not checked before the launch: a label outside [0, classes) gives that sample a NaN loss
+ * (so loss[0] is NaN) and the gradient softmax(z)/n with no one-hot term; nothing is read
+ * out of bounds. */
 tbn_status tbn_softmax_xent(const float* logits, const int32_t* labels, int32_t n, int32_t classes, float* loss,
                             float* loss_per_sample, void* dlogits, hipStream_t stream);
 

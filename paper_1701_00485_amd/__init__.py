@@ -99,6 +99,8 @@ def load():
                                     i32),
         "tbn_relu_bwd": ([vp, vp, i64, vp, vp], i32),
         "tbn_softmax_xent": ([vp, vp, i32, i32, vp, vp, vp, vp], i32),
+        "tbn_tuning_set": ([i32, i32], i32),
+        "tbn_tuning_get": ([i32], i32),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(lib, name)
@@ -116,7 +118,44 @@ def exported_symbols():
                    "tbn_conv2d_bwd_data",
                    "tbn_conv2d_bwd_weight", "tbn_sgd_step", "tbn_sgd_step_quantize", "tbn_pool_out_dims", "tbn_maxpool2d_fwd",
                    "tbn_maxpool2d_bwd", "tbn_avgpool_global", "tbn_batchnorm_workspace_size",
-                   "tbn_batchnorm_train_fwd", "tbn_batchnorm_train_bwd", "tbn_relu_bwd", "tbn_softmax_xent"])
+                   "tbn_batchnorm_train_fwd", "tbn_batchnorm_train_bwd", "tbn_relu_bwd", "tbn_softmax_xent",
+                   "tbn_tuning_set", "tbn_tuning_get"])
+
+
+# Test and tuning knobs of include/tbn_tuning.h (names -> tbn_knob values).  Production code
+# leaves them unset; the parity tests force every kernel variant through them.
+KNOBS = {"conv_tile": 0, "conv_splits": 1, "wgrad_cfg": 2, "wgrad_pix": 3, "wgrad_pf": 4, "i8_tile": 5}
+
+
+def tuning_get(name: str) -> int:
+    return int(load().tbn_tuning_get(KNOBS[name]))
+
+
+def tuning_set(name: str, value: int) -> None:
+    _call("tbn_tuning_set", KNOBS[name], int(value))
+
+
+class tuning:
+    """Context manager that sets knobs for its body and restores their previous values:
+    ``with tbn.tuning(conv_tile=18, conv_splits=3): ...``."""
+
+    def __init__(self, **knobs):
+        for k in knobs:
+            if k not in KNOBS:
+                raise KeyError("unknown tuning knob %r" % k)
+        self.knobs = {k: int(v) for k, v in knobs.items()}
+        self.saved = {}
+
+    def __enter__(self):
+        for k, v in self.knobs.items():
+            self.saved[k] = tuning_get(k)
+            tuning_set(k, v)
+        return self
+
+    def __exit__(self, *exc):
+        for k, v in self.saved.items():
+            tuning_set(k, v)
+        return False
 
 
 def _status_name(s: int) -> str:

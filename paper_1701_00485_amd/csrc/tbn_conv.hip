@@ -376,21 +376,15 @@ __global__ __launch_bounds__(256) void repack_bwd_kernel(const uint32_t* __restr
 
 }  // namespace
 
-// Tile-shape override for tuning and for the tests that cover every shape:
-// TBN_CONV_TILE=<index> (read at each launch; unset = the built-in choice).
-int conv_tile_override() {
-    const char* e = getenv("TBN_CONV_TILE");
-    return e ? atoi(e) : -1;
-}
+// Tile-shape and split overrides for tuning and for the tests that cover every shape (the
+// knobs of tbn_tuning.h; -1 = the built-in choice).
+int conv_tile_override() { return knob(KNOB_CONV_TILE); }
 
-int conv_splits_override() {
-    const char* e = getenv("TBN_CONV_SPLITS");
-    return e ? atoi(e) : -1;
-}
+int conv_splits_override() { return knob(KNOB_CONV_SPLITS); }
 
 // Which kernel runs a forward / backward-data GEMM: the weight-streaming kernel for a
 // fully-connected layer of at most 16 rows, the LDS-DMA implicit GEMM for C % 8 == 0, the
-// thin-input kernel for few channels, else the general one.  cfg (TBN_CONV_TILE) forces a
+// thin-input kernel for few channels, else the general one.  cfg (the tile knob) forces a
 // family: 0-1 general, 10-18 LDS-DMA tile shapes, 20 thin, 30 weight streaming.
 enum ConvPath { PATH_FC, PATH_DMA, PATH_THIN, PATH_GENERIC };
 

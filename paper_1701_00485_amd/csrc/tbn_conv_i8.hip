@@ -459,8 +459,8 @@ bool conv_i8_eligible(const ConvI8Args& a) {
 }
 
 int conv_i8_tile(const ConvI8Args& a) {
-    const char* e = getenv("TBN_I8_TILE");
-    if (e && atoi(e) >= 1 && atoi(e) <= 4) return atoi(e);
+    const int forced = knob(KNOB_I8_TILE);
+    if (forced >= 1 && forced <= 4) return forced;
     const int64_t M = (int64_t)a.N * a.P * a.Q;
     int cfg = a.K > 128 ? 1 : (a.K > 64 ? 2 : 3);
     const int bm = 128, bn = cfg == 1 ? 256 : (cfg == 2 ? 128 : 64);

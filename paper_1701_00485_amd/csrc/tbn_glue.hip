@@ -436,12 +436,15 @@ __global__ __launch_bounds__(64) void softmax_xent_kernel(const float* __restric
     for (int j = lane; j < K; j += 64) se += expf(zn[j] - mx);
     for (int off = 32; off >= 1; off >>= 1) se += __shfl_xor(se, off, 64);
     const float lse = mx + logf(se);
+    // a label outside [0, K) selects no logit: its loss is NaN and its gradient has no -1
+    // term, so the row is never read out of bounds
     const int lab = labels[n];
+    const bool lab_ok = lab >= 0 && lab < K;
     for (int j = lane; j < K; j += 64) {
         const float pj = expf(zn[j] - lse);
         dz[(int64_t)n * K + j] = (uint16_t)f32_to_bf16_bits((pj - (j == lab ? 1.0f : 0.0f)) / (float)N);
     }
-    if (lane == 0) loss_per_sample[n] = lse - zn[lab];
+    if (lane == 0) loss_per_sample[n] = lab_ok ? lse - zn[lab] : __builtin_nanf("");
 }
 
 // mean of the per-sample losses, summed in index order by one wave

@@ -6,6 +6,11 @@
 
 namespace tbn {
 
+// Test and tuning knobs (tbn_tuning.h); -1 = unset, the built-in choice.
+enum Knob { KNOB_CONV_TILE = 0, KNOB_CONV_SPLITS = 1, KNOB_WGRAD_CFG = 2, KNOB_WGRAD_PIX = 3, KNOB_WGRAD_PF = 4,
+            KNOB_I8_TILE = 5 };
+int knob(int which);
+
 // Unsigned division by a runtime constant d >= 1 for numerators below 2^31
 // (round-up multiplier: q = (mulhi(n, mul) + n) >> shift).
 struct FastDiv {
@@ -93,8 +98,8 @@ struct ConvPlan {
 bool conv_dma_eligible(const ConvGemmArgs& a);
 ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg);
 hipError_t launch_conv_dma(const ConvGemmArgs& a, const ConvPlan& plan, hipStream_t stream);
-// Tile-shape and reduction-split overrides for tuning and tests (TBN_CONV_TILE and
-// TBN_CONV_SPLITS environment variables, read at every call; -1 when unset).
+// Tile-shape and reduction-split overrides for tuning and tests (the knobs of
+// tbn_tuning.h, read once per call; -1 when unset).
 int conv_tile_override();
 int conv_splits_override();
 // Bytes of split-K partials the forward / backward-data GEMM of these arguments needs.
@@ -151,7 +156,7 @@ hipError_t launch_wgrad(const WgradArgs& a, hipStream_t stream);
 // 256 x 256 output tiles of 512 threads; launch_wgrad uses it when eligible.
 bool wgrad_dma_eligible(const WgradArgs& a);
 // Stage layout of the LDS-DMA weight-gradient kernel (1 = pixel-major rows for K >= 128,
-// 0 = segment-major; TBN_WGRAD_CFG forces one for tests), its output tiles and how many
+// 0 = segment-major; the stage-layout knob forces one for tests), its output tiles and how many
 // blocks are resident at once.
 struct WgradDmaPlan {
     int cfg, tiles, resident_blocks;
@@ -186,7 +191,7 @@ struct ConvI8Args {
     uint32_t rep_lo, rep_hi;  // sum_{r < R} 2^(r*S)
 };
 bool conv_i8_eligible(const ConvI8Args& a);
-// Tile shape (1: 128 x 256, 2: 128 x 128, 3: 128 x 64, 4: 64 x 128); TBN_I8_TILE forces one.
+// Tile shape (1: 128 x 256, 2: 128 x 128, 3: 128 x 64, 4: 64 x 128); the int8 tile knob forces one.
 int conv_i8_tile(const ConvI8Args& a);
 hipError_t launch_conv_i8(const ConvI8Args& a, hipStream_t stream);
 // q = clamp(round-half-even(x * inv), -127, 127), NaN -> 0; x bf16 or fp32.

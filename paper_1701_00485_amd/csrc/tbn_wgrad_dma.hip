@@ -517,14 +517,14 @@ WgradDmaPlan wgrad_dma_plan(int K, int J) {
     // pixel-major rows for wide layers; the segment-major stages waste less of the
     // 256-row tile's copy work when K is narrow
     p.cfg = K >= 128 ? 1 : 0;
-    const char* e = getenv("TBN_WGRAD_CFG");
-    if (e && (atoi(e) == 0 || atoi(e) == 1)) p.cfg = atoi(e);
+    const int forced = knob(KNOB_WGRAD_CFG);
+    if (forced == 0 || forced == 1) p.cfg = forced;
     p.tiles = ((K + TILE_K - 1) / TILE_K) * ((J + 255) / 256);
     p.resident_blocks = 256;  // one block per CU
     // pixel-major kernel: 48-pixel stages in a three-deep ring (measured best of 32 / 48 / 64)
     p.pix = 48;
-    const char* px = getenv("TBN_WGRAD_PIX");
-    if (px && (atoi(px) == 32 || atoi(px) == 64)) p.pix = atoi(px);
+    const int px = knob(KNOB_WGRAD_PIX);
+    if (px == 32 || px == 64) p.pix = px;
     return p;
 }
 
@@ -534,9 +534,10 @@ hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream) {
     ka.div_q = make_fastdiv((uint32_t)a.Q);
     ka.div_pq = make_fastdiv((uint32_t)a.P * (uint32_t)a.Q);
     // L2 prefetch of a later stage: off by default (measured ~9% slower on the training
-    // layer once the reads and MFMAs are interleaved); TBN_WGRAD_PF=<stages ahead> turns it on
-    const char* pf = getenv("TBN_WGRAD_PF");
-    ka.pf_dist = pf ? atoi(pf) : 0;
+    // layer once the reads and MFMAs are interleaved); the prefetch knob (stages ahead)
+    // turns it on
+    const int pf = knob(KNOB_WGRAD_PF);
+    ka.pf_dist = pf > 0 ? pf : 0;
     const WgradDmaPlan p = wgrad_dma_plan(a.K, a.R * a.S * a.C);
     const dim3 grid((unsigned)(p.tiles * a.splits));
     if (p.cfg == 1) {

@@ -28,3 +28,18 @@ def tbn():
     import paper_1701_00485_amd as tbn_mod
     tbn_mod.load()  # raises if libtbn.so is absent or does not load
     return tbn_mod
+
+
+@pytest.fixture
+def knobs(tbn):
+    """Setter of the library's test and tuning knobs (include/tbn_tuning.h) for one test;
+    every knob is restored to its previous value afterwards."""
+    saved = {k: tbn.tuning_get(k) for k in tbn.KNOBS}
+
+    def set_knobs(**kw):
+        for k, v in kw.items():
+            tbn.tuning_set(k, v)
+
+    yield set_knobs
+    for k, v in saved.items():
+        tbn.tuning_set(k, v)

@@ -14,8 +14,13 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def _declared():
-    text = open(os.path.join(ROOT, "include", "tbn.h")).read()
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\*?\s+\*?(tbn_[a-z_0-9]+)\(", text, re.M)))
+    names = set()
+    inc = os.path.join(ROOT, "include")
+    for f in sorted(os.listdir(inc)):
+        if f.endswith(".h"):
+            text = open(os.path.join(inc, f)).read()
+            names |= set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\*?\s+\*?(tbn_[a-z_0-9]+)\(", text, re.M))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_function():
@@ -25,6 +30,25 @@ def test_library_exports_every_declared_function():
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(tbn.exported_symbols()) == names
+
+
+def test_tuning_knobs_default_unset_and_round_trip():
+    # every knob starts unset (kernel choice from the geometry alone); the context manager
+    # restores the previous value; an unknown knob is rejected
+    lib = tbn.load()
+    for name in tbn.KNOBS:
+        assert tbn.tuning_get(name) == -1
+    with tbn.tuning(conv_tile=18, conv_splits=3):
+        assert tbn.tuning_get("conv_tile") == 18 and tbn.tuning_get("conv_splits") == 3
+        with tbn.tuning(conv_tile=12):
+            assert tbn.tuning_get("conv_tile") == 12
+        assert tbn.tuning_get("conv_tile") == 18
+    assert tbn.tuning_get("conv_tile") == -1 and tbn.tuning_get("conv_splits") == -1
+    assert lib.tbn_tuning_set(99, 1) == 2 and lib.tbn_tuning_get(99) == -1
+    # no environment variable reaches the kernel choice
+    src = os.path.join(ROOT, "paper_1701_00485_amd", "csrc")
+    for f in os.listdir(src):
+        assert "getenv" not in open(os.path.join(src, f)).read(), f
 
 
 def test_status_strings():

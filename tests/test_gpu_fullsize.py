@@ -6,6 +6,9 @@ buffers, workspaces and inputs, checked against the oracle:
   * 4096 sampled outputs of each contraction, each recomputed exactly by the oracle
     (a filter-gradient sample is a full reduction over the 401,408 output pixels);
   * the SGD update over every weight.
+The benchmark draws the real weights from N(0, 0.05^2), where Eq. 3 gives only the codes +-1;
+a second run with N(0, 1) weights (about a third of the codes +-2) covers the magnitude-2
+decode in the same launch configuration.
 """
 import os
 import sys
@@ -23,7 +26,8 @@ pytestmark = pytest.mark.gpu
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def test_training_layer_full_size(tbn):
+@pytest.mark.parametrize("w_std", [0.05, 1.0])
+def test_training_layer_full_size(tbn, w_std):
     sys.path.insert(0, ROOT)
     import bench
 
@@ -34,7 +38,7 @@ def test_training_layer_full_size(tbn):
     n = L["r"] * L["s"] * L["c"]
     xb = synth.normal_bf16(5, "x", (L["n"], L["h"], L["w"], L["c"]))
     dyb = synth.normal_bf16(5, "dy", (L["n"], P, Q, L["k"]))
-    w0 = synth.normal(5, "w", (L["k"], n), 0.05)
+    w0 = synth.normal(5, "w" if w_std == 0.05 else "w_std1", (L["k"], n), w_std)
 
     dev = torch.device("cuda")
     desc = tbn.ConvDesc(*g)
@@ -61,6 +65,10 @@ def test_training_layer_full_size(tbn):
 
     q = oracle.quantize(w0)
     assert np.array_equal(codes.cpu().numpy().view(np.uint32), oracle.pack(q.codes))
+    frac2 = float(np.mean(np.abs(q.codes) == 2))
+    log("full-size layer, real weights N(0, %g^2): %.1f%% of the codes are +-2" % (w_std, 100 * frac2))
+    if w_std >= 1.0:
+        assert frac2 > 0.25
     assert ulp_diff(alpha.cpu().numpy(), q.alpha).max() <= 1
     a64 = q.alpha.astype(np.float64)
 
@@ -70,19 +78,19 @@ def test_training_layer_full_size(tbn):
     idx = synth.sample_indices(5, "fwd_idx", y.numel(), 4096)
     ref = oracle.conv_fwd_sampled(d, xb.reshape(-1), q.codes, a64, idx)
     e = nerr(oracle.bf16_bits_to_f64(bits(y)[idx]), ref)
-    log("full-size fwd, 4096 samples: %.3e" % e)
+    log("full-size fwd (w std %g), 4096 samples: %.3e" % (w_std, e))
     assert e <= 1e-2
 
     idx = synth.sample_indices(5, "bd_idx", dx.numel(), 4096)
     ref = oracle.conv_bwd_data_sampled(d, dyb.reshape(-1), q.codes, a64, idx)
     e = nerr(oracle.bf16_bits_to_f64(bits(dx)[idx]), ref)
-    log("full-size bwd_data, 4096 samples: %.3e" % e)
+    log("full-size bwd_data (w std %g), 4096 samples: %.3e" % (w_std, e))
     assert e <= 1e-2
 
     idx = synth.sample_indices(5, "bw_idx", dw.numel(), 4096)
     ref = oracle.conv_bwd_weight_sampled(d, xb.reshape(-1), dyb.reshape(-1), idx)
     e = nerr(dw.cpu().numpy().reshape(-1)[idx], ref)
-    log("full-size bwd_weight, 4096 samples over 401408-term reductions: %.3e" % e)
+    log("full-size bwd_weight (w std %g), 4096 samples over 401408-term reductions: %.3e" % (w_std, e))
     assert e <= 1e-4
 
     w_ref, _ = oracle.sgd(w_before.cpu().numpy().astype(np.float64), np.zeros(w0.shape),

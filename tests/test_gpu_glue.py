@@ -104,3 +104,25 @@ def test_softmax_xent(tbn, N, K):
     torch.cuda.synchronize()
     assert float(loss.item()) == pytest.approx(loss_ref, rel=1e-5)
     assert nerr(dz.float().cpu().numpy(), dz_ref) <= 1e-2
+
+
+def test_softmax_xent_out_of_range_labels(tbn):
+    # a label outside [0, classes) is not bounds-checked before the launch; the kernel gives
+    # that sample a NaN loss and the gradient softmax(z)/n (no one-hot term) and reads
+    # nothing outside its row; the other samples are unaffected
+    N, K = 6, 10
+    z = synth.normal(12, "zbad", (N, K), 3.0)
+    lab = synth.labels(12, "lbad", N, K).astype(np.int32)
+    bad = lab.copy()
+    bad[1], bad[4] = -1, K
+    loss, dz = tbn.softmax_xent(to_dev(z), to_dev(bad))
+    torch.cuda.synchronize()
+    assert np.isnan(float(loss.item()))
+    zz = z.astype(np.float64)
+    p = np.exp(zz - zz.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    want = p.copy()
+    ok = np.array([i not in (1, 4) for i in range(N)])
+    want[np.arange(N)[ok], bad[ok]] -= 1.0
+    want /= N
+    assert nerr(dz.float().cpu().numpy(), want) <= 1e-2

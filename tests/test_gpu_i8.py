@@ -115,9 +115,9 @@ def test_conv_i8_parity(tbn, g, out, relu):
 
 
 @pytest.mark.parametrize("tile", [1, 2, 3, 4])
-def test_conv_i8_every_tile_shape(tbn, tile, monkeypatch):
+def test_conv_i8_every_tile_shape(tbn, tile, knobs):
     g = (3, 10, 11, 128, 200, 3, 3, 1, 1)
-    monkeypatch.setenv("TBN_I8_TILE", str(tile))
+    knobs(i8_tile=tile)
     log("conv_fwd_i8 tile %d %s" % (tile, g))
     d, xq, codes, alpha, words, x_scale = _problem(g, 5, full_range=True)
     ref, _ = oracle.conv_fwd_i8(d, xq, codes, alpha, x_scale)

@@ -470,13 +470,11 @@ def test_bwd_weight_parity(tbn, g, accumulate):
 
 
 @pytest.mark.parametrize("cfg,pix,pf", [(0, 48, 0), (1, 32, 0), (1, 48, 0), (1, 64, 0), (1, 48, 3)])
-def test_bwd_weight_tile_shapes(tbn, cfg, pix, pf, monkeypatch):
+def test_bwd_weight_tile_shapes(tbn, cfg, pix, pf, knobs):
     # every tile / stage geometry of the transposing-read weight-gradient kernels (the
     # 48-pixel stages do not divide the 64-pixel split ranges: the last stage of a range is
     # partial), and the optional L2 prefetch
-    monkeypatch.setenv("TBN_WGRAD_CFG", str(cfg))
-    monkeypatch.setenv("TBN_WGRAD_PIX", str(pix))
-    monkeypatch.setenv("TBN_WGRAD_PF", str(pf))
+    knobs(wgrad_cfg=cfg, wgrad_pix=pix, wgrad_pf=pf)
     for g in [(2, 14, 14, 256, 256, 3, 3, 1, 1), (3, 12, 12, 128, 136, 3, 3, 2, 1), (5, 9, 7, 64, 96, 3, 3, 1, 1),
               (2, 16, 16, 64, 128, 1, 1, 2, 0)]:
         d, P, Q, xb, dyb, _ = _conv_inputs(g, 5)
@@ -524,11 +522,11 @@ SPLIT_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1
 
 
 @pytest.mark.parametrize("splits", [1, 2, 7, 1000])
-def test_reduction_splits(tbn, splits, monkeypatch):
+def test_reduction_splits(tbn, splits, knobs):
     # the reduction split into ranges summed by the epilogue kernel: fused epilogue (scale,
     # bias, bf16 residual, ReLU) and fp32 output of fwd, and bwd_data, against the oracle;
     # 1000 clamps to one 64-element stage per range
-    monkeypatch.setenv("TBN_CONV_SPLITS", str(splits))
+    knobs(conv_splits=splits)
     for g in SPLIT_CASES:
         log("splits %d %s" % (splits, g))
         d, P, Q, xb, dyb, wr = _conv_inputs(g, 9)
@@ -563,9 +561,9 @@ TILE_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1)
 
 
 @pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 14, 16, 17, 18, 19, 20, 30])
-def test_every_tile_shape(tbn, tile, monkeypatch):
+def test_every_tile_shape(tbn, tile, knobs):
     # each tile shape of the convolution kernels against the oracle (fwd and bwd_data)
-    monkeypatch.setenv("TBN_CONV_TILE", str(tile))
+    knobs(conv_tile=tile)
     for g in TILE_CASES:
         log("tile %d %s" % (tile, g))
         d, P, Q, xb, dyb, wr = _conv_inputs(g, 8)

@@ -11,6 +11,9 @@
   through the per-layer checks.
 * At the benchmark batch (64) the same per-layer checks run on two sampled images, since the
   oracle is exact per image.
+* At batch 1 (the weight-bandwidth-bound configuration, whose tile shapes and reduction
+  splits differ from batch 2 and 64) every layer is checked in full, for the eager pass and
+  for the replays of the HIP graph the benchmark times.
 """
 import numpy as np
 import pytest
@@ -117,6 +120,41 @@ def test_resnet18_batch64_sampled_images(net):
     imgs = [int(i) for i in synth.sample_indices(4, "imgs", 64, 2)[:2]]
     worst = _check_layers(net, trace, imgs)
     log("resnet18 batch 64, images %s: worst per-layer normalised error %.3e" % (imgs, worst))
+
+
+def test_resnet18_batch1_layers_and_logits_eager_and_graph(net):
+    x_bits = synth.normal_bf16(4, "x1", (1, 224, 224, 3))
+    x = torch.from_numpy(x_bits.view(np.int16)).cuda().view(torch.bfloat16)
+    ref = _oracle_network(net, oracle.bf16_bits_to_f64(x_bits))
+    trace = []
+    logits = net.forward(x, trace)
+    torch.cuda.synchronize()
+    worst = _check_layers(net, trace, slice(0, 1))
+    e = nerr(logits.cpu().numpy(), ref)
+    log("resnet18 batch 1 eager: worst per-layer normalised error %.3e, logits %.3e" % (worst, e))
+    assert e <= 3e-2
+    # the same forward captured as a HIP graph: after each replay every traced layer output
+    # (graph-owned memory) is checked against the oracle again, from its replayed input
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    gtrace = []
+    with torch.cuda.stream(side):
+        net.forward(x)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            out = net.forward(x, gtrace)
+    torch.cuda.synchronize()
+    for i in range(2):
+        out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        worst = _check_layers(net, gtrace, slice(0, 1))
+        e = nerr(out.cpu().numpy(), ref)
+        log("resnet18 batch 1 graph replay %d: worst per-layer normalised error %.3e, logits %.3e" % (i, worst, e))
+        assert e <= 3e-2
+        net.forward(x)  # eager work between replays
+        torch.cuda.synchronize()
 
 
 def test_resnet18_batch1_graph_replays_match_eager(net):
