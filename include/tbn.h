@@ -158,6 +158,23 @@ tbn_status tbn_conv2d_fwd(const tbn_conv_desc* desc, const void* x, tbn_dtype xt
                           void* y, tbn_dtype yt, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * The forward pass without caller workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).
+ * Same arguments and results as tbn_conv2d_fwd (the same kernels run), except that the
+ * workspace is a static device array of TBN_NOALLOC_SCRATCH_BYTES owned by the library:
+ * one per device, held until the process ends, its address looked up on the first call on
+ * each device.  The call allocates nothing.  A layer whose tbn_workspace_size(TBN_OP_FWD)
+ * exceeds TBN_NOALLOC_SCRATCH_BYTES gets TBN_ERR_WORKSPACE (nothing queued); every batch-1
+ * layer of the workloads fits.  All calls on one device share its array: calls whose work
+ * overlaps in time on that device (other streams, other host threads) race on it and must
+ * be serialised by the caller; calls on one stream are ordered and safe.
+ */
+#define TBN_NOALLOC_SCRATCH_BYTES (8u << 20)
+tbn_status tbn_conv2d_fwd_noalloc(const tbn_conv_desc* desc, const void* x, tbn_dtype xt, const uint32_t* codes,
+                                  const float* alpha, const tbn_epilogue* ep, void* y, tbn_dtype yt,
+                                  hipStream_t stream);
+
+/*
  * Integer-activation variant of the forward pass (an extension of Sec. 2 Eq. 1: the paper
  * keeps activations in full precision; its Sec. 1 motivates the two-bit filters by
  * arithmetic without multipliers).  The input I is represented as s * q, q int8, and the

@@ -99,6 +99,7 @@ def load():
                                     i32),
         "tbn_relu_bwd": ([vp, vp, i64, vp, vp], i32),
         "tbn_softmax_xent": ([vp, vp, i32, i32, vp, vp, vp, vp], i32),
+        "tbn_conv2d_fwd_noalloc": ([vp, vp, i32, vp, vp, vp, vp, i32, vp], i32),
         "tbn_tuning_set": ([i32, i32], i32),
         "tbn_tuning_get": ([i32], i32),
     }
@@ -119,7 +120,7 @@ def exported_symbols():
                    "tbn_conv2d_bwd_weight", "tbn_sgd_step", "tbn_sgd_step_quantize", "tbn_pool_out_dims", "tbn_maxpool2d_fwd",
                    "tbn_maxpool2d_bwd", "tbn_avgpool_global", "tbn_batchnorm_workspace_size",
                    "tbn_batchnorm_train_fwd", "tbn_batchnorm_train_bwd", "tbn_relu_bwd", "tbn_softmax_xent",
-                   "tbn_tuning_set", "tbn_tuning_get"])
+                   "tbn_tuning_set", "tbn_tuning_get", "tbn_conv2d_fwd_noalloc"])
 
 
 # Test and tuning knobs of include/tbn_tuning.h (names -> tbn_knob values).  Production code
@@ -264,6 +265,34 @@ def quantize_variant(w: torch.Tensor, threshold=1.0, uniform=None, codes=None, a
     _call("tbn_quantize_variant", pw, K, n, float(threshold), pu, _dev(codes, "codes", (torch.int32,)),
           _dev(alpha, "alpha", (torch.float32,)), pc, _stream())
     return codes, alpha, counts
+
+
+NOALLOC_SCRATCH_BYTES = 8 << 20  # TBN_NOALLOC_SCRATCH_BYTES of include/tbn.h
+
+
+def conv2d_fwd_noalloc(desc: ConvDesc, x, codes, alpha, y, scale=None, bias=None, residual=None, relu=False):
+    """tbn_conv2d_fwd_noalloc: the forward pass with the library's static scratch as its
+    workspace (for callers that cannot allocate); `y` is caller-provided."""
+    P, Q = desc.out_dims()
+    _numel(x, desc.n * desc.h * desc.w * desc.c, "x")
+    _numel(codes, packed_words(desc.k, desc.r * desc.s * desc.c), "codes")
+    _numel(alpha, desc.k, "alpha")
+    _numel(y, desc.n * P * Q * desc.k, "y")
+    ep = None
+    if scale is not None or bias is not None or residual is not None or relu:
+        if residual is not None:
+            _numel(residual, y.numel(), "residual")
+            if residual.dtype != y.dtype:
+                raise TypeError("residual must have y's dtype")
+        ep = Epilogue(_dev(scale, "scale", (torch.float32,)).value if scale is not None else None,
+                      _dev(bias, "bias", (torch.float32,)).value if bias is not None else None,
+                      _dev(residual, "residual").value if residual is not None else None,
+                      1 if relu else 0)
+    _call("tbn_conv2d_fwd_noalloc", ctypes.byref(desc), _dev(x, "x", (torch.bfloat16, torch.float32)),
+          _dtype_code(x.dtype), _dev(codes, "codes", (torch.int32,)), _dev(alpha, "alpha", (torch.float32,)),
+          ctypes.byref(ep) if ep is not None else None, _dev(y, "y", (torch.bfloat16, torch.float32)),
+          _dtype_code(y.dtype), _stream())
+    return y
 
 
 def conv2d_fwd(desc: ConvDesc, x, codes, alpha, y=None, out_dtype=torch.bfloat16, scale=None, bias=None,

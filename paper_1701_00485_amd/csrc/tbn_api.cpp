@@ -162,6 +162,13 @@ tbn::ConvGemmArgs bwd_data_args(const Geometry& g, tbn_dtype dxt) {
 
 }  // namespace
 
+namespace tbn {
+tbn_status set_error(tbn_status s, const std::string& what) {
+    g_last_error = what;
+    return s;
+}
+}  // namespace tbn
+
 extern "C" {
 
 const char* tbn_status_str(tbn_status s) {

@@ -4,12 +4,19 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
+#include "tbn.h"
+
 namespace tbn {
 
 // Test and tuning knobs (tbn_tuning.h); -1 = unset, the built-in choice.
 enum Knob { KNOB_CONV_TILE = 0, KNOB_CONV_SPLITS = 1, KNOB_WGRAD_CFG = 2, KNOB_WGRAD_PIX = 3, KNOB_WGRAD_PF = 4,
             KNOB_I8_TILE = 5 };
 int knob(int which);
+
+// Record the detail of an error for tbn_last_error() on this thread; returns s.
+tbn_status set_error(tbn_status s, const std::string& what);
 
 // Unsigned division by a runtime constant d >= 1 for numerators below 2^31
 // (round-up multiplier: q = (mulhi(n, mul) + n) >> shift).
