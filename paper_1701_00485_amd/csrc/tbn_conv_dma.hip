@@ -566,6 +566,7 @@ hipError_t launch_dma_mode(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
     switch (cfg) {
         case 11: return launch_dma_cfg<128, 128, 1, 4, 3, BWD>(a, stream);
         case 12: return launch_dma_cfg<128, 128, 2, 2, 3, BWD>(a, stream);
+        case 13: return launch_dma_cfg<128, 128, 1, 4, 4, BWD>(a, stream);
         case 14: return launch_dma_cfg<128, 64, 2, 2, 3, BWD>(a, stream);
         case 16: return launch_dma_cfg<256, 128, 1, 4, 2, BWD>(a, stream);
         case 18: return launch_dma_cfg<64, 128, 1, 4, 4, BWD>(a, stream);
@@ -577,7 +578,7 @@ hipError_t launch_dma_mode(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
 
 void cfg_tile(int cfg, int* bm, int* bn) {
     switch (cfg) {
-        case 11: case 12: *bm = 128; *bn = 128; return;
+        case 11: case 12: case 13: *bm = 128; *bn = 128; return;
         case 14: *bm = 128; *bn = 64; return;
         case 18: *bm = 64; *bn = 128; return;
         case 16: *bm = 256; *bn = 128; return;
@@ -602,7 +603,10 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
     p.cfg = cfg;
     int bm, bn;
     if (p.cfg < 10) {
-        p.cfg = a.Kf > 128 ? 10 : (a.Kf > 64 ? 12 : 14);
+        // 65..128 filters: 128 x 128 tiles with one wave per 32 filters (each wave decodes
+        // only its own filters) and a four-deep ring, measured ~4-8% faster than two waves
+        // per 64 filters on the ResNet-18 layer-2 shapes
+        p.cfg = a.Kf > 128 ? 10 : (a.Kf > 64 ? 13 : 14);
         cfg_tile(p.cfg, &bm, &bn);
         // too few tiles for one wave of blocks: shorter tiles (64 pixels x 128 filters, a
         // four-deep ring) when there are at least 128 filters, else 128 x 64; then split

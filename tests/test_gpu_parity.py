@@ -560,7 +560,7 @@ TILE_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1)
               (3, 5, 5, 64, 80, 5, 5, 1, 0)]
 
 
-@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 14, 16, 17, 18, 19, 20, 30])
+@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 13, 14, 16, 17, 18, 19, 20, 30])
 def test_every_tile_shape(tbn, tile, knobs):
     # each tile shape of the convolution kernels against the oracle (fwd and bwd_data)
     knobs(conv_tile=tile)
