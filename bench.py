@@ -45,7 +45,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-resnet", action="store_true", help="skip the ResNet-18 forward figures")
     ap.add_argument("--no-small", action="store_true", help="skip the single-layer, LeNet and VGG figures")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="budget of the oracle's training-step sample")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain device copy of known size (HBM counter calibration)")
     return ap.parse_args()
@@ -99,16 +100,25 @@ def _cpu_model() -> str:
 
 
 def cpu_baseline(budget_s: float):
-    """The fp64 oracle on a bounded slice of the same step: quantise and SGD over the whole
-    layer, and the three convolutions on as many images of the batch as fit in `budget_s`
-    seconds (at least one; the work is linear in the batch, so the mean per-image time is
-    scaled by 128)."""
+    """The fp64 oracle (plain loops, OpenMP over the host cores) timed on the workloads, in
+    the same run as the GPU:
+      * the training step (the headline workload): quantise and SGD over the whole layer,
+        the three convolutions on as many images of the batch as fit in `budget_s` seconds
+        (at least one; the work is linear in the batch, so the mean per-image time is
+        scaled by 128);
+      * the single layer (16 x 28 x 28 x 1 -> 32 filters 5x5), whole, on one thread and on
+        all cores (median of several calls);
+      * one whole LeNet training iteration at batch 256;
+      * VGG-small training iterations on a slice of 4 images of the batch of 128, scaled
+        by 32 (the contractions are linear in the batch).
+    `value` is the training step's rate, in the metric's unit."""
     import oracle
     import synth
+    from oracle import nets
 
     L = LAYER
     threads = len(os.sched_getaffinity(0))
-    os.environ.setdefault("OMP_NUM_THREADS", str(threads))
+    oracle.set_threads(threads)
     d = oracle.ConvDesc(1, L["h"], L["w"], L["c"], L["k"], L["r"], L["s"], L["stride"], L["pad"])
     P, Q = d.out_dims()
     n = L["r"] * L["s"] * L["c"]
@@ -133,10 +143,10 @@ def cpu_baseline(budget_s: float):
     t_sgd = time.perf_counter() - t2
     step_s = t_quant + t_sgd + conv_s / images * L["n"]
     conv_flops, _, _ = layer_flops()
-    return {
+    out = {
         "value": round(3 * conv_flops / step_s / 1e12, 6),
         "unit": "TFLOP/s",
-        "cores": int(os.environ.get("OMP_NUM_THREADS", threads)),
+        "cores": threads,
         "affinity_cores": threads,
         "cpu_model": _cpu_model(),
         "kind": "oracle",
@@ -144,6 +154,55 @@ def cpu_baseline(budget_s: float):
                   "on %d of 128 images (mean per image scaled x128); measured %.1f s, extrapolated %.0f s "
                   "per step" % (images, t_quant + t_sgd + conv_s, step_s),
     }
+    configs = {"train_step_s": round(step_s, 2)}
+
+    # single layer, whole: one thread and all cores
+    d1 = oracle.ConvDesc(16, 28, 28, 1, 32, 5, 5, 1, 2)
+    x1 = oracle.round_bf16(synth.uniform(1, "x", (16, 28, 28, 1)))
+    q1 = oracle.quantize(synth.normal(1, "w", (32, 25), 0.05))
+    a1 = q1.alpha.astype(np.float64)
+    fl1 = 2.0 * 16 * 28 * 28 * 32 * 25
+    for label, nthr in (("single_thread", 1), ("all_cores", threads)):
+        oracle.set_threads(nthr)
+        ts = []
+        for _ in range(7):
+            t = time.perf_counter()
+            oracle.conv_fwd(d1, x1, q1.codes, a1)
+            ts.append(time.perf_counter() - t)
+        med = float(np.median(ts))
+        configs["single_layer_fwd_" + label] = {"us_per_call": round(med * 1e6, 1), "threads": nthr,
+                                               "tflops": round(fl1 / med / 1e12, 6)}
+    oracle.set_threads(threads)
+
+    # LeNet: one whole training iteration at batch 256
+    from paper_1701_00485_amd.networks import LeNet, VGGSmall
+    xl = oracle.bf16_bits_to_f64(synth.bf16_bits(synth.uniform(2, "bench_x", (256, 28, 28, 1))))
+    lab = synth.labels(2, "bench_lab", 256, 10)
+    wl = {name: synth.normal(2, name, (cout, k * k * cin), 0.05) for name, cin, cout, k, *_ in nets.LENET}
+    vl = {name: np.zeros(wv.shape) for name, wv in wl.items()}
+    t = time.perf_counter()
+    nets.lenet_iteration(xl, lab, wl, vl, LR)
+    t_lenet = time.perf_counter() - t
+    configs["lenet_iteration"] = {"s": round(t_lenet, 3), "images_per_s": round(256 / t_lenet, 1),
+                                  "tflops": round(LeNet.train_flops(256) / t_lenet / 1e12, 6), "batch": 256}
+
+    # VGG-small: iterations on 4 images, scaled to the batch of 128
+    nv = 4
+    xv = oracle.bf16_bits_to_f64(synth.normal_bf16(3, "bench_x", (nv, 32, 32, 3)))
+    labv = synth.labels(3, "bench_lab", nv, 10)
+    wv = {name: synth.normal(3, name, (cout, 9 * cin), 0.05) for name, cin, cout, _ in nets.VGG}
+    wv["fc"] = synth.normal(3, "fc", (10, 16 * 512), 0.05)
+    vv = {name: np.zeros(a.shape) for name, a in wv.items()}
+    bn = {name: (np.ones(cout), np.zeros(cout)) for name, _, cout, _ in nets.VGG}
+    bnv = {name: (np.zeros(cout), np.zeros(cout)) for name, _, cout, _ in nets.VGG}
+    t = time.perf_counter()
+    nets.vgg_iteration(xv, labv, wv, vv, bn, bnv, LR)
+    t_vgg = (time.perf_counter() - t) * (128 / nv)
+    configs["vgg_small_iteration"] = {"s": round(t_vgg, 2), "images_per_s": round(128 / t_vgg, 2),
+                                      "tflops": round(VGGSmall.train_flops(128) / t_vgg / 1e12, 6), "batch": 128,
+                                      "sample": "%d of 128 images, time scaled x%d" % (nv, 128 // nv)}
+    out["configs"] = configs
+    return out
 
 
 def resnet18_fwd(dev, steps=10, warmup=3):
@@ -516,8 +575,10 @@ def main():
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     ms_step = total_ms / args.steps
-    per_kernel = {nm: float(np.mean([events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]))
-                  for j, nm in enumerate(names)}
+    per_call = {nm: [events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)]
+                for j, nm in enumerate(names)}
+    per_kernel = {nm: float(np.median(v_)) for nm, v_ in per_call.items()}
+    step_times = [events[i][0].elapsed_time(events[i][5]) for i in range(args.steps)]
 
     if args.copy_probe:
         a = torch.empty(256 * 1024 * 1024, dtype=torch.uint8, device=dev)
@@ -538,6 +599,7 @@ def main():
         "warmup": args.warmup,
         "warmup_steps_run": warm_run,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_median": round(float(np.median(step_times)), 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -551,6 +613,9 @@ def main():
             "parallelism": "none (1 GPU)",
         },
         "per_kernel_ms": {k: round(v_, 4) for k, v_ in per_kernel.items()},
+        "per_kernel_ms_min_max": {k: [round(min(v_), 4), round(max(v_), 4)] for k, v_ in per_call.items()},
+        "timing": "per-kernel and per-step figures are medians over the timed steps (HIP events on the "
+                  "stream the kernels run on); ms_per_step is the timed region divided by the steps",
         "roofline": {
             "bound": "mfma",
             "kernel": dom,

@@ -84,6 +84,10 @@ def _load():
     lib.orc_quantize_variant.restype = ctypes.c_int
     lib.orc_sgd_f32.argtypes = [p, p, p, i64, ctypes.c_float, ctypes.c_float, ctypes.c_float]
     lib.orc_sgd_f32.restype = None
+    lib.orc_set_threads.argtypes = [ctypes.c_int]
+    lib.orc_set_threads.restype = None
+    lib.orc_max_threads.argtypes = []
+    lib.orc_max_threads.restype = ctypes.c_int
     lib.orc_maxpool_fwd.argtypes = [p, p, p, p]
     lib.orc_maxpool_fwd.restype = ctypes.c_int
     lib.orc_maxpool_bwd.argtypes = [p, p, p, p]
@@ -143,6 +147,15 @@ class ConvDesc:
 # --------------------------------------------------------------------------------------
 # bf16 rounding of fp32 inputs (IEEE round-to-nearest-even on the dropped 16 bits)
 # --------------------------------------------------------------------------------------
+def set_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops (timing only; results do not depend on it)."""
+    _load().orc_set_threads(int(n))
+
+
+def max_threads() -> int:
+    return int(_load().orc_max_threads())
+
+
 def round_bf16(x: np.ndarray) -> np.ndarray:
     x = _c(x, np.float32)
     out = np.empty(x.shape, np.float64)

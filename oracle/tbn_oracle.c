@@ -28,6 +28,7 @@
  * identities); none is "parity unpinned".
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -789,3 +790,11 @@ double orc_softmax_xent(const double* z, const int64_t* labels, int64_t N, int64
     }
     return loss / (double)N;
 }
+
+/* Threads of the parallel loops (timing only: every routine gives the same result for any
+ * thread count, each output element being computed by one thread in a fixed order). */
+void orc_set_threads(int n) {
+    if (n >= 1) omp_set_num_threads(n);
+}
+
+int orc_max_threads(void) { return omp_get_max_threads(); }

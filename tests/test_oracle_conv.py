@@ -249,3 +249,25 @@ def test_sgd_f32_single_rounding_per_fused_op():
     # and it is the fp64 step up to fp32 rounding
     w64, v64 = oracle.sgd(w0, v0, g0, float(lr), float(mu), float(wd))
     assert np.max(np.abs(w - w64)) <= 4 * np.finfo(np.float32).eps * np.max(np.abs(w64))
+
+
+def test_results_do_not_depend_on_thread_count():
+    # the CPU baseline times the oracle single-threaded and on all cores; every output element
+    # is one thread's fixed-order sum, so the results are bit-identical either way
+    g = (3, 9, 8, 16, 24, 3, 3, 1, 1)
+    d = oracle.ConvDesc(*g)
+    x = synth.normal(20, "tx", g[:4]).astype(np.float64)
+    w = synth.normal(20, "tw", (24, 9 * 16), 0.7)
+    q = oracle.quantize(w)
+    P, Q = d.out_dims()
+    dy = synth.normal(20, "tdy", (3, P, Q, 24)).astype(np.float64)
+    n0 = oracle.max_threads()
+    outs = []
+    for n in (1, max(2, n0)):
+        oracle.set_threads(n)
+        outs.append((oracle.conv_fwd(d, x, q.codes, q.alpha.astype(np.float64)),
+                     oracle.conv_bwd_data(d, dy, q.codes, q.alpha.astype(np.float64)),
+                     oracle.conv_bwd_weight(d, x, dy)))
+    oracle.set_threads(n0)
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
