@@ -28,7 +28,6 @@
  * identities); none is "parity unpinned".
  */
 #include <math.h>
-#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -793,8 +792,13 @@ double orc_softmax_xent(const double* z, const int64_t* labels, int64_t N, int64
 
 /* Threads of the parallel loops (timing only: every routine gives the same result for any
  * thread count, each output element being computed by one thread in a fixed order). */
+#ifdef _OPENMP
+#include <omp.h>
 void orc_set_threads(int n) {
     if (n >= 1) omp_set_num_threads(n);
 }
-
 int orc_max_threads(void) { return omp_get_max_threads(); }
+#else
+void orc_set_threads(int n) { (void)n; }
+int orc_max_threads(void) { return 1; }
+#endif
