@@ -36,7 +36,10 @@ typedef enum tbn_knob {
     TBN_KNOB_WGRAD_PF = 4,
     /* int8-activation forward tile: 1 128x256, 2 128x128, 3 128x64, 4 64x128 */
     TBN_KNOB_I8_TILE = 5,
-    TBN_KNOB_COUNT = 6
+    /* weight-streaming forward: code loads in flight per wave (0 = 4 buffers of 2 loads of
+     * 16 bytes per lane, 1 = 2 x 4, 2 = 2 x 8, 3 = 3 x 4) */
+    TBN_KNOB_FC_VARIANT = 6,
+    TBN_KNOB_COUNT = 7
 } tbn_knob;
 
 /* Set a knob (value -1 restores the built-in choice).  TBN_ERR_SHAPE for an unknown knob. */

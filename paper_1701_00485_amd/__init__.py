@@ -125,7 +125,8 @@ def exported_symbols():
 
 # Test and tuning knobs of include/tbn_tuning.h (names -> tbn_knob values).  Production code
 # leaves them unset; the parity tests force every kernel variant through them.
-KNOBS = {"conv_tile": 0, "conv_splits": 1, "wgrad_cfg": 2, "wgrad_pix": 3, "wgrad_pf": 4, "i8_tile": 5}
+KNOBS = {"conv_tile": 0, "conv_splits": 1, "wgrad_cfg": 2, "wgrad_pix": 3, "wgrad_pf": 4, "i8_tile": 5,
+         "fc_variant": 6}
 
 
 def tuning_get(name: str) -> int:

@@ -137,6 +137,41 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
     const int NB = (n + 63) / 64;
     const int k0 = blockIdx.y * FB;
 
+    const int64_t PQt = (int64_t)g.tiles_p * g.tiles_q;
+    auto origin = [&](int64_t tile, int64_t* img, int* p0, int* q0) {
+        *img = tile / PQt;
+        const int rem = (int)(tile - *img * PQt);
+        const int tp = rem / g.tiles_q;
+        *p0 = tp * TP;
+        *q0 = (rem - tp * g.tiles_q) * TQ;
+    };
+    const uint32_t img_elems = (uint32_t)a.H * a.W * a.C;
+    uint32_t desc[kElemsPerThread];
+#pragma unroll
+    for (int i = 0; i < kElemsPerThread; ++i) {
+        const uint32_t e = tid + 256 * i;
+        desc[i] = 0xFFFFFFFFu;
+        if (!DMA && i < g.ept && e < (uint32_t)g.nelem) {
+            const uint32_t row = fdiv(e, g.div_rowlen);
+            const uint32_t j = e - row * (uint32_t)g.rowlen;
+            const uint32_t cell = fdiv(j, g.div_c);
+            const uint32_t c = j - cell * (uint32_t)C;
+            desc[i] = ((((row * g.PW) + cell) * CP + c) << 16) | (row << 10) | cell;
+        }
+    }
+    // element-wise patches: the first tile's loads are issued before anything else, so that
+    // their latency overlaps the filter decode below (one round trip to memory for both)
+    int64_t img = 0;
+    int p0 = 0, q0 = 0;
+    uint32_t pv0[kElemsPerThread];
+    uint32_t okm0 = 0;
+    if constexpr (!DMA) {
+        if (blockIdx.x < g.ntiles) {
+            origin(blockIdx.x, &img, &p0, &q0);
+            okm0 = load_patch<CP, X32>(a, desc, (uint32_t)img * img_elems, p0 * a.sh - a.ph, q0 * a.sw - a.pw, pv0);
+        }
+    }
+
     // ---- the block's filters into LDS as bf16, zero at padding taps / channels / filters:
     //      the packed codes (NB KiB, contiguous in the blocked layout) decoded to W~, or
     //      the real filters of a full-precision layer rounded to bf16 ----
@@ -193,36 +228,12 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
             bi[t][e] = ok && a.bias ? a.bias[col] : 0.0f;
         }
     const bool vec_store = (K % 8) == 0;
-    const int64_t PQt = (int64_t)g.tiles_p * g.tiles_q;
-
-    auto origin = [&](int64_t tile, int64_t* img, int* p0, int* q0) {
-        *img = tile / PQt;
-        const int rem = (int)(tile - *img * PQt);
-        const int tp = rem / g.tiles_q;
-        *p0 = tp * TP;
-        *q0 = (rem - tp * g.tiles_q) * TQ;
-    };
 
     // channel-padding slots of the patch stay zero; data elements are rewritten per tile
     if constexpr (!DMA) {
         for (int i = tid; i < 2 * g.pbuf; i += 256) pl[i] = 0;
     }
     __syncthreads();  // zeros (and the decoded filters) in place before the first patch
-    const uint32_t img_elems = (uint32_t)a.H * a.W * a.C;
-
-    uint32_t desc[kElemsPerThread];
-#pragma unroll
-    for (int i = 0; i < kElemsPerThread; ++i) {
-        const uint32_t e = tid + 256 * i;
-        desc[i] = 0xFFFFFFFFu;
-        if (i < g.ept && e < (uint32_t)g.nelem) {
-            const uint32_t row = fdiv(e, g.div_rowlen);
-            const uint32_t j = e - row * (uint32_t)g.rowlen;
-            const uint32_t cell = fdiv(j, g.div_c);
-            const uint32_t c = j - cell * (uint32_t)C;
-            desc[i] = ((((row * g.PW) + cell) * CP + c) << 16) | (row << 10) | cell;
-        }
-    }
 
     // the patch is double buffered in LDS: tile i computes from buffer i % 2 while the
     // loads of tile i + 1 are in flight; their values land in the other buffer at the end
@@ -377,15 +388,7 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
         return;
     }
     int64_t tile = blockIdx.x;
-    int64_t img;
-    int p0, q0;
-    if (tile < g.ntiles) {
-        uint32_t pv[kElemsPerThread];
-        origin(tile, &img, &p0, &q0);
-        const uint32_t okm = load_patch<CP, X32>(a, desc, (uint32_t)img * img_elems, p0 * a.sh - a.ph,
-                                                 q0 * a.sw - a.pw, pv);
-        write_patch(pl, pv, okm);
-    }
+    if (tile < g.ntiles) write_patch(pl, pv0, okm0);  // loaded at the top
     __syncthreads();
     for (int it = 0; tile < g.ntiles; tile += gridDim.x, ++it) {
         uint16_t* cur = pl + (it & 1) * g.pbuf;

@@ -14,7 +14,8 @@
 //   * codes are decoded in registers to exact bf16 +-0.5/+-1 (half the code: the pair
 //     comes from one shift and one and-or, against three ops for +-1/+-2), and 2 alpha
 //     scales the fp32 sum (exact); the loads of the next steps are issued before the
-//     MFMAs of the current ones, and four accumulators keep four MFMA chains in flight;
+//     MFMAs of the current ones (several buffers of loads in flight per wave), and four
+//     accumulators keep four MFMA chains in flight;
 //   * the activations of the batch (N x n bf16) sit in LDS, zero-padded to whole steps,
 //     plus one zero row that the unused batch columns read (no branch per read; those
 //     output columns are never stored);
@@ -25,8 +26,6 @@
 namespace tbn {
 
 namespace {
-
-constexpr int kU = 4;  // code loads (16 bytes per lane) in flight per wave and buffer
 
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
@@ -57,6 +56,8 @@ __device__ __forceinline__ bf16x8 decode8_half(uint32_t w, uint32_t base) {
     return as_bf16x8(r);
 }
 
+// KU code loads (16 bytes per lane) per buffer, NBUF buffers in flight per wave.
+template <int KU, int NBUF>
 __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, int32_t n, int32_t nsteps,
                                                         int32_t xpitch) {
     extern __shared__ __attribute__((aligned(16))) uint16_t xl[];  // [N + 1][xpitch] bf16
@@ -79,19 +80,19 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
     f32x4_t acc[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-    u32x4 wa[kU], wb[kU];
-    auto load = [&](u32x4 (&w)[kU], int step0) {
+    u32x4 wbuf[NBUF][KU];
+    auto load = [&](u32x4 (&w)[KU], int step0) {
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
+        for (int u = 0; u < KU; ++u) {
             int ib = 4 * (step0 + u) + g;
             ib = ib < NB ? ib : NB - 1;  // in bounds; its activations are zero past n
             w[u] = __builtin_nontemporal_load(&codes[(int64_t)ib * 64]);  // read once: streaming
         }
     };
     const uint32_t half_one = __builtin_amdgcn_readfirstlane(0x3F003F00u);  // bf16 (0.5, 0.5)
-    auto compute = [&](const u32x4 (&w)[kU], int step0) {
+    auto compute = [&](const u32x4 (&w)[KU], int step0) {
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
+        for (int u = 0; u < KU; ++u) {
             const uint16_t* xb = xrow + (4 * (step0 + u) + g) * 64;
             bf16x8 bx[8];  // the step's activation operands, read before its MFMAs
 #pragma unroll
@@ -103,10 +104,10 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
             }
         }
     };
-    // nsteps is a multiple of 2 kU (the host pads the activations in LDS to match); the
+    // nsteps is a multiple of NBUF KU (the host pads the activations in LDS to match); the
     // first code loads are in flight while the activations are staged
-    load(wa, 0);
-    load(wb, kU);
+#pragma unroll
+    for (int b = 0; b < NBUF; ++b) load(wbuf[b], b * KU);
     // ---- the batch's activations into LDS (zero beyond n, and the zero row) ----
     if (!a.x_f32 && n % 8 == 0) {
         // 16-byte pieces, the loads of a thread issued together
@@ -137,11 +138,12 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
         }
     }
     __syncthreads();
-    for (int st = 0; st < nsteps; st += 2 * kU) {
-        compute(wa, st);
-        if (st + 2 * kU < nsteps) load(wa, st + 2 * kU);
-        compute(wb, st + kU);
-        if (st + 3 * kU < nsteps) load(wb, st + 3 * kU);
+    for (int st = 0; st < nsteps; st += NBUF * KU) {
+#pragma unroll
+        for (int b = 0; b < NBUF; ++b) {
+            compute(wbuf[b], st + b * KU);
+            if (st + (NBUF + b) * KU < nsteps) load(wbuf[b], st + (NBUF + b) * KU);
+        }
     }
 
     // ---- epilogue: lane holds batch column f, filters 4 g .. 4 g + 3 of the wave's 16 ----
@@ -170,13 +172,22 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
 
 }  // namespace
 
+// (loads per buffer, buffers) of each variant; the tuning knob selects one for sweeps.  The
+// default keeps four buffers of two 16-byte loads in flight: measured 17.8 us per call on
+// the 8192 -> 32768 batch-1 layer against 18.3-19.1 us for two buffers of four loads,
+// 19.0 us for two of eight and 19.8 us for three of four (loads consumed in smaller groups
+// interleave better with the decode)
+constexpr int kVariants[4][2] = {{2, 4}, {4, 2}, {8, 2}, {4, 3}};
+
 bool fc_stream_plan(const ConvGemmArgs& a, FcStreamPlan* p) {
     // a fully-connected layer: the filter window covers the whole (unpadded) input map
     if (a.apair || a.N > 16 || a.P != 1 || a.Q != 1 || a.R != a.H || a.S != a.W || a.ph != 0 || a.pw != 0)
         return false;
+    const int forced = knob(KNOB_FC_VARIANT);
+    p->variant = forced >= 0 && forced < 4 ? forced : 0;
     const int64_t n = (int64_t)a.R * a.S * a.C;
     const int64_t nb = (n + 63) / 64;
-    const int64_t per = 4 * 2 * kU;  // element blocks consumed per loop iteration
+    const int64_t per = 4 * kVariants[p->variant][0] * kVariants[p->variant][1];  // element blocks per iteration
     const int64_t steps_blocks = (nb + per - 1) / per * per;
     const int64_t xpitch = steps_blocks * 64;
     const int64_t lds = (int64_t)(a.N + 1) * xpitch * 2;  // + the zero row
@@ -190,7 +201,12 @@ bool fc_stream_plan(const ConvGemmArgs& a, FcStreamPlan* p) {
 
 hipError_t launch_fc_stream(const ConvGemmArgs& a, const FcStreamPlan& p, hipStream_t stream) {
     const dim3 grid((unsigned)((a.Kf + 63) / 64));
-    hipLaunchKernelGGL(fc_stream_kernel, grid, dim3(256), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch);
+    switch (p.variant) {
+        case 1: hipLaunchKernelGGL((fc_stream_kernel<4, 2>), grid, dim3(256), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch); break;
+        case 2: hipLaunchKernelGGL((fc_stream_kernel<8, 2>), grid, dim3(256), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch); break;
+        case 3: hipLaunchKernelGGL((fc_stream_kernel<4, 3>), grid, dim3(256), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch); break;
+        default: hipLaunchKernelGGL((fc_stream_kernel<2, 4>), grid, dim3(256), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch); break;
+    }
     return hipGetLastError();
 }
 

@@ -12,7 +12,7 @@ namespace tbn {
 
 // Test and tuning knobs (tbn_tuning.h); -1 = unset, the built-in choice.
 enum Knob { KNOB_CONV_TILE = 0, KNOB_CONV_SPLITS = 1, KNOB_WGRAD_CFG = 2, KNOB_WGRAD_PIX = 3, KNOB_WGRAD_PF = 4,
-            KNOB_I8_TILE = 5 };
+            KNOB_I8_TILE = 5, KNOB_FC_VARIANT = 6 };
 int knob(int which);
 
 // Record the detail of an error for tbn_last_error() on this thread; returns s.
@@ -136,6 +136,7 @@ hipError_t launch_conv_thin(const ConvGemmArgs& a, const ThinGeom& g, hipStream_
 // for a batch of at most 16: codes streamed from HBM into 16x16x32 MFMAs.
 struct FcStreamPlan {
     int32_t n, nsteps, xpitch, lds_bytes;
+    int32_t variant;  // loads in flight per wave (tuning knob; 0 = built-in)
 };
 bool fc_stream_plan(const ConvGemmArgs& a, FcStreamPlan* p);
 hipError_t launch_fc_stream(const ConvGemmArgs& a, const FcStreamPlan& p, hipStream_t stream);

@@ -416,6 +416,21 @@ def test_fc_stream_parity(tbn, g):
     assert nerr(y.float().cpu().numpy(), ref) <= TOL
 
 
+@pytest.mark.parametrize("variant", [0, 1, 2, 3])
+def test_fc_stream_every_variant(tbn, variant, knobs):
+    # each load-buffering variant of the weight-streaming kernel (loads per buffer x buffers)
+    knobs(fc_variant=variant)
+    for g in [(1, 1, 1, 8192, 200, 1, 1, 1, 0), (16, 7, 7, 64, 72, 7, 7, 1, 0), (3, 1, 1, 520, 130, 1, 1, 1, 0)]:
+        d, P, Q, xb, _, wr = _conv_inputs(g, 11)
+        q = oracle.quantize(wr)
+        acc = oracle.conv_fwd(d, oracle.bf16_bits_to_f64(xb), q.codes, q.alpha.astype(np.float64))
+        codes, alpha, _ = tbn.quantize(to_dev(wr))
+        y = tbn.conv2d_fwd(tbn.ConvDesc(*g), bf16_dev(xb), codes, alpha, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        e = nerr(y.cpu().numpy(), acc)
+        assert e <= 1e-4, "variant %d %s: %.3e" % (variant, g, e)
+
+
 def test_fc_stream_weight_streaming_size(tbn):
     # 8192 -> 16384 at batch 1 (32 MiB of codes): sampled outputs against the oracle
     g = (1, 1, 1, 8192, 16384, 1, 1, 1, 0)
