@@ -49,6 +49,8 @@ def parse():
                     help="budget of the oracle's training-step sample")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain device copy of known size (HBM counter calibration)")
+    ap.add_argument("--only", choices=["resnet", "single", "lenet", "vgg", "ws", "int8", "fused"],
+                    help="profiling aid: run just this workload (no training step, no contract line)")
     return ap.parse_args()
 
 
@@ -296,7 +298,7 @@ def resnet18_fwd(dev, steps=10, warmup=3):
     return out
 
 
-def small_configs(dev, steps=20, warmup=3):
+def small_configs(dev, steps=20, warmup=3, which=("single", "lenet", "vgg")):
     """The smaller workloads: one two-bit layer on MNIST-shaped fp32 input (forward only,
     latency-bound), and full training iterations of the MNIST-shaped LeNet (batch 256) and
     the CIFAR-shaped VGG (batch 128)."""
@@ -322,6 +324,24 @@ def small_configs(dev, steps=20, warmup=3):
         return e0.elapsed_time(e1) / n
 
     # single layer: 16 x 28 x 28 x 1 fp32 U[0,1) -> 32 filters 5x5 pad 2, fp32 output
+    if "single" in which:
+        _single_layer(dev, out, timed)
+    for name, cls, batch, mk in (
+            ("lenet_train", LeNet, 256,
+             lambda: synth.bf16_bits(synth.uniform(2, "bench_x", (256, 28, 28, 1)))),
+            ("vgg_small_train", VGGSmall, 128, lambda: synth.normal_bf16(3, "bench_x", (128, 32, 32, 3)))):
+        if name.split("_")[0] not in which:
+            continue
+        _net_train(dev, out, timed, name, cls, batch, mk, steps)
+    return out
+
+
+def _single_layer(dev, out, timed):
+    import torch
+
+    import paper_1701_00485_amd as tbn
+    import synth
+
     d = tbn.ConvDesc(16, 28, 28, 1, 32, 5, 5, 1, 2)
     x = torch.from_numpy(synth.uniform(1, "x", (16, 28, 28, 1))).to(dev)
     w = torch.from_numpy(synth.normal(1, "w", (32, 25), 0.05)).to(dev)
@@ -334,37 +354,39 @@ def small_configs(dev, steps=20, warmup=3):
                                "effective_tflops": round(fl / (ms * 1e-3) / 1e12, 3),
                                "hbm_frac": round(byts / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
-    for name, cls, batch, mk in (
-            ("lenet_train", LeNet, 256,
-             lambda: synth.bf16_bits(synth.uniform(2, "bench_x", (256, 28, 28, 1)))),
-            ("vgg_small_train", VGGSmall, 128, lambda: synth.normal_bf16(3, "bench_x", (128, 32, 32, 3)))):
-        net = cls(device=dev)
-        xb = torch.from_numpy(mk().view(np.int16)).to(dev).view(torch.bfloat16)
-        lab = torch.from_numpy(synth.labels(2, "bench_lab", batch, 10).astype(np.int32)).to(dev)
-        ms = timed(lambda: net.step(xb, lab), steps)
-        # the same iteration captured once as a HIP graph and replayed (no host launch work)
-        side = torch.cuda.Stream()
-        side.wait_stream(stream)
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph, stream=side):
-            net.step(xb, lab)
-        torch.cuda.synchronize()
-        gms = timed(graph.replay, steps)
-        # the update fused with the next iteration's quantisation (one pass over the real
-        # weights; the iteration then has no separate quantisation), eager and as a graph
-        fms = timed(lambda: net.step(xb, lab, fused=True), steps)
-        fgraph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(fgraph, stream=side):
-            net.step(xb, lab, fused=True)
-        torch.cuda.synchronize()
-        fgms = timed(fgraph.replay, steps)
-        out[name] = {"batch": batch, "ms_per_iteration": round(ms, 4), "images_per_s": round(batch / (ms * 1e-3), 1),
-                     "effective_tflops": round(cls.train_flops(batch) / (ms * 1e-3) / 1e12, 2),
-                     "graph_ms_per_iteration": round(gms, 4),
-                     "graph_images_per_s": round(batch / (gms * 1e-3), 1),
-                     "fused_update_ms_per_iteration": round(fms, 4),
-                     "fused_update_graph_ms_per_iteration": round(fgms, 4)}
-    return out
+
+def _net_train(dev, out, timed, name, cls, batch, mk, steps):
+    import torch
+
+    import synth
+
+    stream = torch.cuda.current_stream()
+    net = cls(device=dev)
+    xb = torch.from_numpy(mk().view(np.int16)).to(dev).view(torch.bfloat16)
+    lab = torch.from_numpy(synth.labels(2, "bench_lab", batch, 10).astype(np.int32)).to(dev)
+    ms = timed(lambda: net.step(xb, lab), steps)
+    # the same iteration captured once as a HIP graph and replayed (no host launch work)
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        net.step(xb, lab)
+    torch.cuda.synchronize()
+    gms = timed(graph.replay, steps)
+    # the update fused with the next iteration's quantisation (one pass over the real
+    # weights; the iteration then has no separate quantisation), eager and as a graph
+    fms = timed(lambda: net.step(xb, lab, fused=True), steps)
+    fgraph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(fgraph, stream=side):
+        net.step(xb, lab, fused=True)
+    torch.cuda.synchronize()
+    fgms = timed(fgraph.replay, steps)
+    out[name] = {"batch": batch, "ms_per_iteration": round(ms, 4), "images_per_s": round(batch / (ms * 1e-3), 1),
+                 "effective_tflops": round(cls.train_flops(batch) / (ms * 1e-3) / 1e12, 2),
+                 "graph_ms_per_iteration": round(gms, 4),
+                 "graph_images_per_s": round(batch / (gms * 1e-3), 1),
+                 "fused_update_ms_per_iteration": round(fms, 4),
+                 "fused_update_graph_ms_per_iteration": round(fgms, 4)}
 
 
 def weight_streaming(dev, sets=8, reps=20):
@@ -503,6 +525,29 @@ def int8_forward(dev, desc, x, codes, alpha, conv_flops, reps=20):
     }
 
 
+def _only(section, dev):
+    """One workload alone (for kernel traces and counters of that workload)."""
+    if section == "resnet":
+        return resnet18_fwd(dev)
+    if section in ("single", "lenet", "vgg"):
+        return small_configs(dev, which=(section,))
+    if section == "ws":
+        return weight_streaming(dev)
+    if section == "fused":
+        return fused_update(dev)
+    import torch
+
+    import paper_1701_00485_amd as tbn
+    import synth
+    L = LAYER
+    conv_flops, P, Q = layer_flops()
+    desc = tbn.ConvDesc(L["n"], L["h"], L["w"], L["c"], L["k"], L["r"], L["s"], L["stride"], L["pad"])
+    x = torch.from_numpy(synth.normal_bf16(5, "x", (L["n"], L["h"], L["w"], L["c"])).view(np.int16)).to(dev)
+    w = torch.from_numpy(synth.normal(5, "w", (L["k"], L["r"] * L["s"] * L["c"]), 0.05)).to(dev)
+    codes, alpha, _ = tbn.quantize(w, want_counts=False)
+    return int8_forward(dev, desc, x.view(torch.bfloat16), codes, alpha, conv_flops)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -518,6 +563,9 @@ def main():
     tbn.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.only:
+        print(json.dumps({"only": args.only, "result": _only(args.only, dev)}), flush=True)
+        return
     L = LAYER
     conv_flops, P, Q = layer_flops()
     flops = 3 * conv_flops  # forward, backward-data and backward-weight contractions
