@@ -406,8 +406,9 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
         bi[e] = ok && a.bias ? a.bias[col] : 0.0f;
     }
     const bool vec_store = (Kf % 8) == 0;
-    const bool partial_out = a.splits > 1;  // raw fp32 sums of this split (Kf % 8 == 0)
-    float* part = partial_out ? a.partial + (int64_t)split * M * Kf : nullptr;
+    const bool partial_out = a.splits > 1;  // raw fp32 sums of this split, rows of Kp = round_up(Kf, 8)
+    const int Kp = (Kf + 7) & ~7;
+    float* part = partial_out ? a.partial + (int64_t)split * M * Kp : nullptr;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -428,8 +429,9 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
             const int64_t o = row * Kf + col0;
             if (partial_out) {
                 if (col0 < Kf) {
-                    *reinterpret_cast<f32x4*>(part + o) = lo;
-                    *reinterpret_cast<f32x4*>(part + o + 4) = hi;
+                    float* pp = part + row * Kp + col0;
+                    *reinterpret_cast<f32x4*>(pp) = lo;
+                    *reinterpret_cast<f32x4*>(pp + 4) = hi;
                 }
                 continue;
             }
@@ -487,26 +489,45 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
     }
 }
 
-// Sum of the split-K partials in split order, then the epilogue; one thread per 8 outputs.
+// Sum of the split-K partials in split order, then the epilogue; one thread per 8 outputs
+// (partial rows are Kp = round_up(Kf, 8) wide; columns past Kf are skipped).
 __global__ __launch_bounds__(256) void conv_split_epilogue_kernel(const ConvGemmArgs a) {
     const int64_t M = (int64_t)a.N * a.P * a.Q;
     const int Kf = a.Kf;
-    const int64_t groups = M * (Kf / 8);
+    const int Kp = (Kf + 7) & ~7;
+    const int64_t groups = M * (Kp / 8);
     const int64_t gi = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (gi >= groups) return;
-    const int64_t o = gi * 8;
-    const int col0 = (int)(o % Kf);
+    const int64_t row = gi / (Kp / 8);
+    const int col0 = (int)(gi - row * (Kp / 8)) * 8;
+    const int64_t po = row * Kp + col0;
     float v8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    for (int z = 0; z < a.splits; ++z) {
-        const float* pp = a.partial + (int64_t)z * M * Kf + o;
-        const f32x4 lo = *reinterpret_cast<const f32x4*>(pp);
-        const f32x4 hi = *reinterpret_cast<const f32x4*>(pp + 4);
+    auto add = [&](const f32x4& lo, const f32x4& hi) {
         v8[0] += lo.x; v8[1] += lo.y; v8[2] += lo.z; v8[3] += lo.w;
         v8[4] += hi.x; v8[5] += hi.y; v8[6] += hi.z; v8[7] += hi.w;
+    };
+    // eight splits' loads in flight at a time, added in split order
+    int z = 0;
+    for (; z + 8 <= a.splits; z += 8) {
+        f32x4 lo[8], hi[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const float* pp = a.partial + (int64_t)(z + u) * M * Kp + po;
+            lo[u] = *reinterpret_cast<const f32x4*>(pp);
+            hi[u] = *reinterpret_cast<const f32x4*>(pp + 4);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) add(lo[u], hi[u]);
     }
+    for (; z < a.splits; ++z) {
+        const float* pp = a.partial + (int64_t)z * M * Kp + po;
+        add(*reinterpret_cast<const f32x4*>(pp), *reinterpret_cast<const f32x4*>(pp + 4));
+    }
+    const bool full = col0 + 8 <= Kf;  // all 8 columns real (always when Kf % 8 == 0)
+    const int64_t o = row * Kf + col0;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        const int col = col0 + e;
+        const int col = col0 + e < Kf ? col0 + e : Kf - 1;  // past Kf: computed, never stored
         float sc = a.colscale ? a.colscale[col] : 1.0f;
         if (a.scale) sc *= a.scale[col];
         v8[e] = v8[e] * sc + (a.bias ? a.bias[col] : 0.0f);
@@ -515,28 +536,45 @@ __global__ __launch_bounds__(256) void conv_split_epilogue_kernel(const ConvGemm
         if (a.y_f32) {
             const float* rp = reinterpret_cast<const float*>(a.residual) + o;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v8[e] += rp[e];
-        } else {
+            for (int e = 0; e < 8; ++e)
+                if (col0 + e < Kf) v8[e] += rp[e];
+        } else if (full && (Kf % 8) == 0) {
             const u32x4 r8 = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.residual) + o);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 v8[2 * e] += bf16_bits_to_f32(r8[e] & 0xFFFFu);
                 v8[2 * e + 1] += bf16_bits_to_f32(r8[e] >> 16);
             }
+        } else {
+            const uint16_t* rp = reinterpret_cast<const uint16_t*>(a.residual) + o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (col0 + e < Kf) v8[e] += bf16_bits_to_f32(rp[e]);
         }
     }
     if (a.relu) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) v8[e] = fmaxf(v8[e], 0.0f);
     }
-    if (a.y_f32) {
-        float* yp = reinterpret_cast<float*>(a.y) + o;
-        *reinterpret_cast<f32x4*>(yp) = f32x4{v8[0], v8[1], v8[2], v8[3]};
-        *reinterpret_cast<f32x4*>(yp + 4) = f32x4{v8[4], v8[5], v8[6], v8[7]};
+    if ((Kf % 8) == 0) {
+        if (a.y_f32) {
+            float* yp = reinterpret_cast<float*>(a.y) + o;
+            *reinterpret_cast<f32x4*>(yp) = f32x4{v8[0], v8[1], v8[2], v8[3]};
+            *reinterpret_cast<f32x4*>(yp + 4) = f32x4{v8[4], v8[5], v8[6], v8[7]};
+        } else {
+            *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(a.y) + o) =
+                u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]), pack_bf16x2(v8[4], v8[5]),
+                      pack_bf16x2(v8[6], v8[7])};
+        }
     } else {
-        *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(a.y) + o) =
-            u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]), pack_bf16x2(v8[4], v8[5]),
-                  pack_bf16x2(v8[6], v8[7])};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            if (col0 + e >= Kf) break;
+            if (a.y_f32)
+                reinterpret_cast<float*>(a.y)[o + e] = v8[e];
+            else
+                reinterpret_cast<uint16_t*>(a.y)[o + e] = (uint16_t)f32_to_bf16_bits(v8[e]);
+        }
     }
 }
 
@@ -616,7 +654,7 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
     cfg_tile(p.cfg, &bm, &bn);
     const int64_t tiles = ((M + bm - 1) / bm) * ((a.Kf + bn - 1) / bn);
     int64_t splits = 1;
-    if (a.Kf % 8 == 0) {
+    {
         const int forced = conv_splits_override();
         if (forced > 0) {
             splits = forced;
@@ -635,7 +673,8 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
     }
     p.chunks_per_split = (int)((nchunks + splits - 1) / splits);
     p.splits = (int)((nchunks + p.chunks_per_split - 1) / p.chunks_per_split);
-    p.partial_bytes = p.splits > 1 ? (size_t)p.splits * (size_t)M * (size_t)a.Kf * 4 : 0;
+    // partial rows padded to whole 8-column groups
+    p.partial_bytes = p.splits > 1 ? (size_t)p.splits * (size_t)M * (size_t)((a.Kf + 7) & ~7) * 4 : 0;
     return p;
 }
 
@@ -646,7 +685,7 @@ hipError_t launch_conv_dma(const ConvGemmArgs& args, const ConvPlan& plan, hipSt
     if (a.splits > 1 && !a.partial) return hipErrorInvalidValue;
     hipError_t e = a.apair ? launch_dma_mode<true>(a, plan.cfg, stream) : launch_dma_mode<false>(a, plan.cfg, stream);
     if (e != hipSuccess || a.splits <= 1) return e;
-    const int64_t groups = (int64_t)a.N * a.P * a.Q * (a.Kf / 8);
+    const int64_t groups = (int64_t)a.N * a.P * a.Q * (((a.Kf + 7) & ~7) / 8);
     hipLaunchKernelGGL(conv_split_epilogue_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, stream, a);
     return hipGetLastError();
 }

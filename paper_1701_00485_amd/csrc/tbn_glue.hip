@@ -416,11 +416,26 @@ __global__ __launch_bounds__(256) void bn_bwd_apply_kernel(const uint16_t* __res
 }
 
 // gradient of ReLU applied after the fact: g = dy * [y > 0]
+// 8 elements (16 bytes of each tensor) per thread; the last thread takes the ragged tail
+// element by element
 __global__ __launch_bounds__(256) void relu_bwd_kernel(const uint16_t* __restrict__ y, const uint16_t* __restrict__ dy,
                                                        int64_t total, uint16_t* __restrict__ dx) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
     if (i >= total) return;
-    dx[i] = bf16_bits_to_f32(y[i]) > 0.0f ? dy[i] : (uint16_t)0;
+    if (i + 8 <= total) {
+        const u32x4 yv = *reinterpret_cast<const u32x4*>(y + i);
+        const u32x4 gv = *reinterpret_cast<const u32x4*>(dy + i);
+        u32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t lo = bf16_bits_to_f32(yv[e] & 0xFFFFu) > 0.0f ? (gv[e] & 0xFFFFu) : 0u;
+            const uint32_t hi = bf16_bits_to_f32(yv[e] >> 16) > 0.0f ? (gv[e] & 0xFFFF0000u) : 0u;
+            o[e] = lo | hi;
+        }
+        *reinterpret_cast<u32x4*>(dx + i) = o;
+    } else {
+        for (int64_t j = i; j < total; ++j) dx[j] = bf16_bits_to_f32(y[j]) > 0.0f ? dy[j] : (uint16_t)0;
+    }
 }
 
 // softmax cross-entropy, mean over the batch: one wave per sample (classes <= 64 * 32)
@@ -447,13 +462,22 @@ __global__ __launch_bounds__(64) void softmax_xent_kernel(const float* __restric
     if (lane == 0) loss_per_sample[n] = lab_ok ? lse - zn[lab] : __builtin_nanf("");
 }
 
-// mean of the per-sample losses, summed in index order by one wave
-__global__ __launch_bounds__(64) void mean_kernel(const float* __restrict__ v, int32_t n, float* __restrict__ out) {
+// mean of the per-sample losses, summed in index order by one thread; the block first
+// stages the values in LDS in chunks (parallel, coalesced loads), so that the serial sum
+// reads LDS instead of waiting on one global load per element
+__global__ __launch_bounds__(256) void mean_kernel(const float* __restrict__ v, int32_t n, float* __restrict__ out) {
+    constexpr int kChunk = 4096;
+    __shared__ float buf[kChunk];
     float acc = 0.0f;
-    if (threadIdx.x == 0) {
-        for (int i = 0; i < n; ++i) acc += v[i];
-        *out = acc / (float)n;
+    for (int base = 0; base < n; base += kChunk) {
+        const int len = n - base < kChunk ? n - base : kChunk;
+        for (int i = threadIdx.x; i < len; i += 256) buf[i] = v[base + i];
+        __syncthreads();
+        if (threadIdx.x == 0)
+            for (int i = 0; i < len; ++i) acc += buf[i];
+        __syncthreads();
     }
+    if (threadIdx.x == 0) *out = acc / (float)n;
 }
 
 unsigned blocks_for(int64_t total) { return (unsigned)((total + 255) / 256); }
@@ -560,14 +584,14 @@ hipError_t launch_bn_train_bwd(const uint16_t* x, const uint16_t* y, const uint1
 }
 
 hipError_t launch_relu_bwd(const uint16_t* y, const uint16_t* dy, int64_t total, uint16_t* dx, hipStream_t s) {
-    hipLaunchKernelGGL(relu_bwd_kernel, dim3(blocks_for(total)), dim3(256), 0, s, y, dy, total, dx);
+    hipLaunchKernelGGL(relu_bwd_kernel, dim3(blocks_for((total + 7) / 8)), dim3(256), 0, s, y, dy, total, dx);
     return hipGetLastError();
 }
 
 hipError_t launch_softmax_xent(const float* z, const int32_t* labels, int32_t N, int32_t K, float* loss,
                                float* loss_per_sample, uint16_t* dz, hipStream_t s) {
     hipLaunchKernelGGL(softmax_xent_kernel, dim3((unsigned)N), dim3(64), 0, s, z, labels, N, K, loss_per_sample, dz);
-    hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(64), 0, s, loss_per_sample, N, loss);
+    hipLaunchKernelGGL(mean_kernel, dim3(1), dim3(256), 0, s, loss_per_sample, N, loss);
     return hipGetLastError();
 }
 

@@ -85,17 +85,21 @@ def test_batchnorm_train(tbn, shape, relu):
     assert nerr(dx.float().cpu().numpy(), dx_ref) <= 1e-2
 
 
-def test_relu_bwd(tbn):
-    yb = synth.normal_bf16(12, "ry", (1000,))
+@pytest.mark.parametrize("count", [1000, 1003, 5, 4096 * 8 + 7])
+def test_relu_bwd(tbn, count):
+    # 8 elements per thread, a ragged tail element by element; ReLU'(0) = 0 (zeros and
+    # negative zeros in y)
+    yb = synth.normal_bf16(12, "ry%d" % count, (count,))
     yb = np.where(yb & 0x8000, np.uint16(0), yb).astype(np.uint16)
-    dyb = synth.normal_bf16(12, "rdy", (1000,))
+    yb[::7] = 0x8000  # -0.0
+    dyb = synth.normal_bf16(12, "rdy%d" % count, (count,))
     dx = tbn.relu_bwd(bf16_dev(yb), bf16_dev(dyb))
     torch.cuda.synchronize()
     want = np.where(oracle.bf16_bits_to_f64(yb) > 0, oracle.bf16_bits_to_f64(dyb), 0.0)
     assert np.array_equal(_bits_to_f64(dx), want)
 
 
-@pytest.mark.parametrize("N,K", [(256, 10), (128, 10), (3, 1000)])
+@pytest.mark.parametrize("N,K", [(256, 10), (128, 10), (3, 1000), (5000, 10)])
 def test_softmax_xent(tbn, N, K):
     z = synth.normal(12, "z%d" % N, (N, K), 3.0)
     lab = synth.labels(12, "l%d" % N, N, K)

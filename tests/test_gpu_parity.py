@@ -533,7 +533,10 @@ def test_repeat_runs_are_bitwise_identical(tbn):
 
 
 SPLIT_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1), (3, 12, 12, 128, 136, 3, 3, 2, 1),
-               (2, 7, 7, 512, 512, 3, 3, 1, 1)]
+               (2, 7, 7, 512, 512, 3, 3, 1, 1),
+               # filter counts that are not a multiple of 8 (a 10-way classifier as a 4x4 valid
+               # convolution; a ragged 13)
+               (3, 4, 4, 64, 10, 4, 4, 1, 0), (2, 9, 9, 16, 13, 3, 3, 1, 1)]
 
 
 @pytest.mark.parametrize("splits", [1, 2, 7, 1000])
