@@ -385,12 +385,12 @@ int conv_splits_override() { return knob(KNOB_CONV_SPLITS); }
 // Which kernel runs a forward / backward-data GEMM: the weight-streaming kernel for a
 // fully-connected layer of at most 16 rows, the LDS-DMA implicit GEMM for C % 8 == 0, the
 // thin-input kernel for few channels, else the general one.  cfg (the tile knob) forces a
-// family: 0-1 general, 10-18 LDS-DMA tile shapes, 20 thin, 30 weight streaming.
+// family: 0-1 general, 10-19 and 21-25 LDS-DMA tile shapes, 20 thin, 30 weight streaming.
 enum ConvPath { PATH_FC, PATH_DMA, PATH_THIN, PATH_GENERIC };
 
 static ConvPath choose_path(const ConvGemmArgs& a, int cfg, FcStreamPlan* fp, ThinGeom* tg) {
     if ((cfg < 0 || cfg == 30) && fc_stream_plan(a, fp)) return PATH_FC;
-    if (conv_dma_eligible(a) && (cfg < 0 || (cfg >= 10 && cfg < 20))) return PATH_DMA;
+    if (conv_dma_eligible(a) && (cfg < 0 || (cfg >= 10 && cfg < 20) || (cfg >= 21 && cfg <= 25))) return PATH_DMA;
     if ((cfg < 0 || cfg == 20) && conv_thin_plan(a, tg)) return PATH_THIN;
     return PATH_GENERIC;
 }

@@ -51,8 +51,14 @@ struct StageLayout {
 // bookkeeping is wave-uniform (scalar registers).
 // Tiles of 256 x 256 run one block per CU (one wave per SIMD, 128 x 128 accumulators each);
 // smaller tiles two.
-template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool BWD, bool UNI>
-__global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kernel(const ConvGemmArgs a) {
+// G > 1: the block is G groups of four waves; group g reduces its own contiguous range of
+// the tile's stages with its own LDS ring (the grid's reduction split s covers ranges
+// s G .. s G + G - 1), and at the end groups 1 .. G-1 hand their sums to group 0 through
+// LDS, which adds them in group order and runs the epilogue.  This gives a tile G waves
+// per SIMD where the grid has too few tiles for two blocks per CU, without partial sums in
+// memory or a second kernel.
+template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool BWD, bool UNI, int G>
+__global__ __launch_bounds__(256 * G, (BM * BN >= 65536 || G > 1) ? 1 : 2) void conv_dma_kernel(const ConvGemmArgs a) {
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int TM = WM / 32, TN = WN / 32;
     constexpr int AR = BM / 32;      // activation DMAs per wave per stage (8 rows each)
@@ -61,12 +67,17 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
     static_assert(WAVES_M * WAVES_N == 4, "four waves per block");
     static_assert(TM >= 1 && TN >= 1 && BM % 32 == 0 && BN % 64 == 0 && NBLK <= 4, "tile shape");
     static_assert(STAGES * L::BYTES >= 4 * 32 * (WN + 4) * 4, "epilogue staging fits in the ring");
+    // G > 1: the sums of groups 1 .. G-1 are handed over behind group 0's epilogue staging
+    constexpr int NACC = TM * TN * 16;  // accumulators per lane
+    constexpr int XOFF = ((4 * 32 * (WN + 4) * 4 + 1023) / 1024) * 1024;
+    static_assert(G == 1 || G * STAGES * L::BYTES >= XOFF + (G - 1) * 256 * NACC * 4, "group sums fit in LDS");
 
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[STAGES * L::BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[G * STAGES * L::BYTES];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int grp = G > 1 ? __builtin_amdgcn_readfirstlane(tid >> 8) : 0;  // group of four waves
+    const int wave = __builtin_amdgcn_readfirstlane((tid >> 6) & 3);     // wave within the group
     const int wm = wave / WAVES_N;
     const int wn = wave % WAVES_N;
     const int half = lane >> 5;
@@ -88,15 +99,19 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
     const uint32_t mtile = fdiv(tile, a.div_tilesN);
     const int64_t m0 = (int64_t)mtile * BM;
     const int n0 = (int)(tile - mtile * tilesN) * BN;
-    const int c_begin = split * a.chunks_per_split;
+    const int c_begin = (split * G + grp) * a.chunks_per_split;
     const int c_end = min(c_begin + a.chunks_per_split, nchunks);
-    const int nloc = c_end - c_begin;
+    const int nloc = max(c_end - c_begin, 0);
+    // every group runs the same number of iterations (and barriers); a group whose range is
+    // shorter skips the copies and MFMAs of the missing stages
+    const int niter = G > 1 ? a.chunks_per_split : nloc;
 
     const v4i rs_x = make_rsrc(a.x, (uint32_t)((int64_t)a.N * a.H * a.W * C * 2));
     const v4i rs_c = make_rsrc(a.codes, (uint32_t)((int64_t)KB * nchunks * 1024));
     v4i rs_p = rs_c;
     if constexpr (BWD) rs_p = make_rsrc(a.apair, (uint32_t)nchunks * 128u);
-    const uint32_t smem_base = lds_addr(smem);
+    uint8_t* const ring = smem + grp * (STAGES * L::BYTES);  // this group's LDS ring
+    const uint32_t smem_base = lds_addr(ring);
 
     // ---- activation rows this lane fills: row = 8 * (wave + 4 j) + lane / 8 ----
     int32_t rbase[AR];      // element offset of the row's (h0, w0) in x (may be negative)
@@ -268,7 +283,7 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
     for (int c = 0; c < STAGES - 1; ++c)
         if (c < nloc) issue(c_begin + c);
     int cslot = 0;  // ring slot of the stage being multiplied
-    for (int il = 0; il < nloc; ++il) {
+    for (int il = 0; il < niter; ++il) {
         // this wave's DMAs of stage il landed (later stages may still be in flight; in the
         // last stages simply everything)
         if (il + STAGES - 2 < nloc)
@@ -277,7 +292,8 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
             wait_vmcnt(0);
         __syncthreads();  // ... and every other wave's; all reads of stage il-1 are done
         if (il + STAGES - 1 < nloc) issue(c_begin + il + STAGES - 1);  // into stage il-1's buffer
-        const uint8_t* st = smem + cslot * L::BYTES;
+        if (G > 1 && il >= nloc) continue;  // past this group's range (wave-uniform)
+        const uint8_t* st = ring + cslot * L::BYTES;
         cslot = cslot + 1 == STAGES ? 0 : cslot + 1;
         u32x4 braw[TN];
 #pragma unroll
@@ -387,6 +403,40 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
     //      takes 8 consecutive channels of one pixel, applies y = act(acc * colscale *
     //      scale + bias + residual) and writes them with 16-byte stores. ----
     __syncthreads();  // every wave is done reading the ring
+    if constexpr (G > 1) {
+        // groups 1 .. G-1 store their sums (lane-contiguous 16-byte pieces), group 0 adds
+        // them in group order
+        f32x4* xch = reinterpret_cast<f32x4*>(smem + XOFF);
+        if (grp > 0) {
+            f32x4* dst = xch + (grp - 1) * (NACC / 4) * 256;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int t = 0; t < TN; ++t)
+#pragma unroll
+                    for (int g4 = 0; g4 < 4; ++g4)
+                        dst[(((i * TN + t) * 4 + g4) * 4 + wave) * 64 + lane] =
+                            f32x4{acc[i][t][4 * g4], acc[i][t][4 * g4 + 1], acc[i][t][4 * g4 + 2], acc[i][t][4 * g4 + 3]};
+        }
+        __syncthreads();
+        if (grp > 0) return;  // no barrier follows
+#pragma unroll 1
+        for (int gg = 1; gg < G; ++gg) {
+            const f32x4* src = xch + (gg - 1) * (NACC / 4) * 256;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int t = 0; t < TN; ++t)
+#pragma unroll
+                    for (int g4 = 0; g4 < 4; ++g4) {
+                        const f32x4 v = src[(((i * TN + t) * 4 + g4) * 4 + wave) * 64 + lane];
+                        acc[i][t][4 * g4] += v.x;
+                        acc[i][t][4 * g4 + 1] += v.y;
+                        acc[i][t][4 * g4 + 2] += v.z;
+                        acc[i][t][4 * g4 + 3] += v.w;
+                    }
+        }
+    }
     constexpr int PITCH = WN + 4;  // floats per staged pixel row
     float* stage = reinterpret_cast<float*>(smem) + wave * 32 * PITCH;
     const int Kf = a.Kf;
@@ -409,83 +459,104 @@ __global__ __launch_bounds__(256, (BM * BN >= 65536) ? 1 : 2) void conv_dma_kern
     const bool partial_out = a.splits > 1;  // raw fp32 sums of this split, rows of Kp = round_up(Kf, 8)
     const int Kp = (Kf + 7) & ~7;
     float* part = partial_out ? a.partial + (int64_t)split * M * Kp : nullptr;
+    // bf16 residual: the 16-byte loads of PRE_I tile rows (at most 8 per lane) are issued
+    // together before those rows are processed, so that their memory latency is paid once
+    // per group rather than once per pass
+    constexpr int NPASS = 32 / RPP;
+    constexpr int PRE_I = NPASS >= 8 ? 1 : (8 / NPASS < TM ? 8 / NPASS : TM);
+    static_assert(TM % PRE_I == 0, "residual prefetch groups");
+    const bool res_pre = a.residual && !a.y_f32 && vec_store && !partial_out && col0 < Kf;
+    const uint16_t* res16 = reinterpret_cast<const uint16_t*>(a.residual);
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
+    for (int i0 = 0; i0 < TM; i0 += PRE_I) {
+        u32x4 rpre[PRE_I][NPASS];
 #pragma unroll
-        for (int t = 0; t < TN; ++t)
+        for (int ii = 0; ii < PRE_I; ++ii)
 #pragma unroll
-            for (int g = 0; g < 4; ++g)
-                *reinterpret_cast<f32x4*>(&stage[l32 * PITCH + 32 * t + 8 * g + 4 * half]) =
-                    f32x4{acc[i][t][4 * g], acc[i][t][4 * g + 1], acc[i][t][4 * g + 2], acc[i][t][4 * g + 3]};
-        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS writes are visible to it
-#pragma unroll
-        for (int pass = 0; pass < 32 / RPP; ++pass) {
-            const int r = pass * RPP + grow;
-            const int64_t row = m0 + wm * WM + 32 * i + r;
-            if (row >= M) continue;
-            const f32x4 lo = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol]);
-            const f32x4 hi = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol + 4]);
-            float v8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-            const int64_t o = row * Kf + col0;
-            if (partial_out) {
-                if (col0 < Kf) {
-                    float* pp = part + row * Kp + col0;
-                    *reinterpret_cast<f32x4*>(pp) = lo;
-                    *reinterpret_cast<f32x4*>(pp + 4) = hi;
-                }
-                continue;
+            for (int pass = 0; pass < NPASS; ++pass) {
+                const int64_t row = m0 + wm * WM + 32 * (i0 + ii) + pass * RPP + grow;
+                rpre[ii][pass] = res_pre && row < M ? *reinterpret_cast<const u32x4*>(res16 + row * Kf + col0)
+                                                    : u32x4{0u, 0u, 0u, 0u};
             }
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v8[e] = v8[e] * cs[e] + bi[e];
-            if (a.residual) {
-                if (a.y_f32) {
-                    const float* rp = reinterpret_cast<const float*>(a.residual) + o;
+        for (int ii = 0; ii < PRE_I; ++ii) {
+            const int i = i0 + ii;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        if (col0 + e < Kf) v8[e] += rp[e];
-                } else {
-                    const uint16_t* rp = reinterpret_cast<const uint16_t*>(a.residual) + o;
-                    if (vec_store && col0 < Kf) {
-                        const u32x4 r8 = *reinterpret_cast<const u32x4*>(rp);
+            for (int t = 0; t < TN; ++t)
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            v8[2 * e] += bf16_bits_to_f32(r8[e] & 0xFFFFu);
-                            v8[2 * e + 1] += bf16_bits_to_f32(r8[e] >> 16);
+                for (int g = 0; g < 4; ++g)
+                    *reinterpret_cast<f32x4*>(&stage[l32 * PITCH + 32 * t + 8 * g + 4 * half]) =
+                        f32x4{acc[i][t][4 * g], acc[i][t][4 * g + 1], acc[i][t][4 * g + 2], acc[i][t][4 * g + 3]};
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS writes are visible to it
+#pragma unroll
+            for (int pass = 0; pass < 32 / RPP; ++pass) {
+                const int r = pass * RPP + grow;
+                const int64_t row = m0 + wm * WM + 32 * i + r;
+                if (row >= M) continue;
+                const f32x4 lo = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol]);
+                const f32x4 hi = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol + 4]);
+                float v8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+                const int64_t o = row * Kf + col0;
+                if (partial_out) {
+                    if (col0 < Kf) {
+                        float* pp = part + row * Kp + col0;
+                        *reinterpret_cast<f32x4*>(pp) = lo;
+                        *reinterpret_cast<f32x4*>(pp + 4) = hi;
+                    }
+                    continue;
+                }
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v8[e] = v8[e] * cs[e] + bi[e];
+                if (a.residual) {
+                    if (a.y_f32) {
+                        const float* rp = reinterpret_cast<const float*>(a.residual) + o;
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (col0 + e < Kf) v8[e] += rp[e];
+                    } else {
+                        const uint16_t* rp = reinterpret_cast<const uint16_t*>(a.residual) + o;
+                        if (vec_store && col0 < Kf) {
+                            const u32x4 r8 = rpre[ii][pass];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                v8[2 * e] += bf16_bits_to_f32(r8[e] & 0xFFFFu);
+                                v8[2 * e + 1] += bf16_bits_to_f32(r8[e] >> 16);
+                            }
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 8; ++e)
+                                if (col0 + e < Kf) v8[e] += bf16_bits_to_f32(rp[e]);
                         }
+                    }
+                }
+                if (a.relu) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v8[e] = fmaxf(v8[e], 0.0f);
+                }
+                if (a.y_f32) {
+                    float* yp = reinterpret_cast<float*>(a.y) + o;
+                    if (vec_store && col0 < Kf) {
+                        *reinterpret_cast<f32x4*>(yp) = f32x4{v8[0], v8[1], v8[2], v8[3]};
+                        *reinterpret_cast<f32x4*>(yp + 4) = f32x4{v8[4], v8[5], v8[6], v8[7]};
                     } else {
 #pragma unroll
                         for (int e = 0; e < 8; ++e)
-                            if (col0 + e < Kf) v8[e] += bf16_bits_to_f32(rp[e]);
+                            if (col0 + e < Kf) yp[e] = v8[e];
+                    }
+                } else {
+                    uint16_t* yp = reinterpret_cast<uint16_t*>(a.y) + o;
+                    if (vec_store && col0 < Kf) {
+                        *reinterpret_cast<u32x4*>(yp) = u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]),
+                                                              pack_bf16x2(v8[4], v8[5]), pack_bf16x2(v8[6], v8[7])};
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (col0 + e < Kf) yp[e] = (uint16_t)f32_to_bf16_bits(v8[e]);
                     }
                 }
             }
-            if (a.relu) {
-#pragma unroll
-                for (int e = 0; e < 8; ++e) v8[e] = fmaxf(v8[e], 0.0f);
-            }
-            if (a.y_f32) {
-                float* yp = reinterpret_cast<float*>(a.y) + o;
-                if (vec_store && col0 < Kf) {
-                    *reinterpret_cast<f32x4*>(yp) = f32x4{v8[0], v8[1], v8[2], v8[3]};
-                    *reinterpret_cast<f32x4*>(yp + 4) = f32x4{v8[4], v8[5], v8[6], v8[7]};
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        if (col0 + e < Kf) yp[e] = v8[e];
-                }
-            } else {
-                uint16_t* yp = reinterpret_cast<uint16_t*>(a.y) + o;
-                if (vec_store && col0 < Kf) {
-                    *reinterpret_cast<u32x4*>(yp) = u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]),
-                                                          pack_bf16x2(v8[4], v8[5]), pack_bf16x2(v8[6], v8[7])};
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        if (col0 + e < Kf) yp[e] = (uint16_t)f32_to_bf16_bits(v8[e]);
-                }
-            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);  // reads of this tile row done before it is overwritten
         }
-        __builtin_amdgcn_s_waitcnt(0xC07F);  // reads of this tile row done before it is overwritten
     }
 }
 
@@ -578,7 +649,7 @@ __global__ __launch_bounds__(256) void conv_split_epilogue_kernel(const ConvGemm
     }
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool BWD>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool BWD, int G = 1>
 hipError_t launch_dma_cfg(const ConvGemmArgs& args, hipStream_t stream) {
     ConvGemmArgs a = args;
     const int64_t M = (int64_t)a.N * a.P * a.Q;
@@ -593,9 +664,9 @@ hipError_t launch_dma_cfg(const ConvGemmArgs& args, hipStream_t stream) {
     a.rep_hi = (uint32_t)(rep >> 32);
     const dim3 grid((unsigned)(tiles * a.splits));
     if (a.C % 64 == 0)
-        hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, true>), grid, dim3(256), 0, stream, a);
+        hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, true, G>), grid, dim3(256 * G), 0, stream, a);
     else
-        hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, false>), grid, dim3(256), 0, stream, a);
+        hipLaunchKernelGGL((conv_dma_kernel<BM, BN, WAVES_M, WAVES_N, STAGES, BWD, false, G>), grid, dim3(256 * G), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -610,15 +681,25 @@ hipError_t launch_dma_mode(const ConvGemmArgs& a, int cfg, hipStream_t stream) {
         case 18: return launch_dma_cfg<64, 128, 1, 4, 4, BWD>(a, stream);
         case 19: return launch_dma_cfg<256, 256, 2, 2, 3, BWD>(a, stream);
         case 17: return launch_dma_cfg<256, 256, 2, 2, 4, BWD>(a, stream);
+        case 21: return launch_dma_cfg<64, 128, 1, 4, 4, BWD, 2>(a, stream);
+        case 22: return launch_dma_cfg<64, 128, 1, 4, 3, BWD, 4>(a, stream);
+        case 23: return launch_dma_cfg<128, 128, 1, 4, 4, BWD, 2>(a, stream);
+        case 24: return launch_dma_cfg<128, 64, 2, 2, 3, BWD, 2>(a, stream);
+        case 25: return launch_dma_cfg<64, 128, 1, 4, 3, BWD, 2>(a, stream);
         default: return launch_dma_cfg<128, 256, 1, 4, 3, BWD>(a, stream);
     }
 }
+
+// groups of four waves per block (each reducing its own range of stages)
+int cfg_groups(int cfg) { return cfg == 22 ? 4 : (cfg == 21 || cfg == 23 || cfg == 24 || cfg == 25) ? 2 : 1; }
 
 void cfg_tile(int cfg, int* bm, int* bn) {
     switch (cfg) {
         case 11: case 12: case 13: *bm = 128; *bn = 128; return;
         case 14: *bm = 128; *bn = 64; return;
-        case 18: *bm = 64; *bn = 128; return;
+        case 18: case 21: case 22: case 25: *bm = 64; *bn = 128; return;
+        case 23: *bm = 128; *bn = 128; return;
+        case 24: *bm = 128; *bn = 64; return;
         case 16: *bm = 256; *bn = 128; return;
         case 17: case 19: *bm = 256; *bn = 256; return;
         default: *bm = 128; *bn = 256; return;
@@ -650,6 +731,13 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
         // four-deep ring) when there are at least 128 filters, else 128 x 64; then split
         // the reduction
         if (((M + bm - 1) / bm) * ((a.Kf + bn - 1) / bn) < 384) p.cfg = a.Kf >= 128 ? 18 : 14;
+        // 128 .. 255 tiles of 64 x 128: one block per CU, so four groups of four waves per
+        // block (four waves per SIMD) instead of a reduction split; measured 23 vs 31-34 us
+        // on the 7 x 7 x 512 ResNet-18 layers at batch 64
+        if (p.cfg == 18) {
+            const int64_t t18 = ((M + 63) / 64) * ((a.Kf + 127) / 128);
+            if (t18 >= 128 && t18 < 256 && nchunks >= 16) p.cfg = 22;
+        }
     }
     cfg_tile(p.cfg, &bm, &bn);
     const int64_t tiles = ((M + bm - 1) / bm) * ((a.Kf + bn - 1) / bn);
@@ -658,12 +746,13 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
         const int forced = conv_splits_override();
         if (forced > 0) {
             splits = forced;
-        } else if (tiles < 384) {
+        } else if (tiles < 384 && cfg_groups(p.cfg) == 1) {
             // measured: the 64 x 128 tile split only below ~192 tiles (then to about 192
             // blocks with >= 6 stages each: a split costs a partial-sum pass), the 128 x 64
-            // tile to about 640 blocks with >= 3 stages each
+            // tile to about 640 blocks with >= 6 stages each (the 3 x 3 x 64 layer at batch 1,
+            // 9 stages, runs 8.8 us unsplit against 10.8 us in three ranges)
             const bool shortt = p.cfg == 18;
-            const int64_t target = shortt ? 192 : 640, min_stages = shortt ? 6 : 3;
+            const int64_t target = shortt ? 192 : 640, min_stages = 6;
             splits = (target + tiles - 1) / tiles;
             const int64_t max_splits = nchunks / min_stages > 0 ? nchunks / min_stages : 1;
             if (splits > max_splits) splits = max_splits;
@@ -671,8 +760,10 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
         if (splits > nchunks) splits = nchunks;
         if (splits < 1) splits = 1;
     }
-    p.chunks_per_split = (int)((nchunks + splits - 1) / splits);
-    p.splits = (int)((nchunks + p.chunks_per_split - 1) / p.chunks_per_split);
+    // each block's G groups take G consecutive ranges of chunks_per_split stages
+    const int G = cfg_groups(p.cfg);
+    p.chunks_per_split = (int)((nchunks + splits * G - 1) / (splits * G));
+    p.splits = (int)((nchunks + (int64_t)p.chunks_per_split * G - 1) / ((int64_t)p.chunks_per_split * G));
     // partial rows padded to whole 8-column groups
     p.partial_bytes = p.splits > 1 ? (size_t)p.splits * (size_t)M * (size_t)((a.Kf + 7) & ~7) * 4 : 0;
     return p;

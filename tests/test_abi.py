@@ -146,6 +146,11 @@ def test_workspace_sizes():
     assert wf > 0 and wf % (16 * 7 * 7 * 512 * 4) == 0
     codes_pairs = 8 * 72 * 1024 + 72 * 32 * 4
     assert tbn.workspace_size(tbn.OP_BWD_DATA, d) == codes_pairs + wf
+    # 196 tiles of 64 x 128 (the 7 x 7 x 512 layers at batch 64): groups of waves inside
+    # each block reduce the stage ranges, no partial sums in memory
+    d = tbn.ConvDesc(64, 7, 7, 512, 512, 3, 3, 1, 1)
+    assert tbn.workspace_size(tbn.OP_FWD, d) == 0
+    assert tbn.workspace_size(tbn.OP_BWD_DATA, d) == codes_pairs
 
 
 def test_stem_workspace_is_the_bordered_copy():

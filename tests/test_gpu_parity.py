@@ -573,12 +573,42 @@ def test_reduction_splits(tbn, splits, knobs):
             assert e <= TOL, "bwd_data splits %d %s: %.3e" % (splits, g, e)
 
 
+@pytest.mark.parametrize("tile,splits", [(21, 2), (22, 3), (23, 1000), (24, 7), (25, 2)])
+def test_grouped_tiles_with_splits(tbn, tile, splits, knobs):
+    # blocks of several four-wave groups (each reducing its own stage range) combined with a
+    # reduction split over the grid: fused epilogue and bwd_data against the oracle
+    knobs(conv_tile=tile, conv_splits=splits)
+    for g in SPLIT_CASES:
+        log("grouped tile %d splits %d %s" % (tile, splits, g))
+        d, P, Q, xb, dyb, wr = _conv_inputs(g, 10)
+        k = g[4]
+        q = oracle.quantize(wr)
+        a64 = q.alpha.astype(np.float64)
+        scale = synth.uniform(10, "sc", (k,), 0.5, 1.5)
+        bias = synth.normal(10, "bi", (k,), 0.1)
+        resb = synth.normal_bf16(10, "res", (g[0], P, Q, k))
+        acc = oracle.conv_fwd(d, oracle.bf16_bits_to_f64(xb), q.codes, a64)
+        ref = np.maximum(acc * scale.astype(np.float64) + bias + oracle.bf16_bits_to_f64(resb), 0.0)
+        codes, alpha, _ = tbn.quantize(to_dev(wr))
+        desc = tbn.ConvDesc(*g)
+        y = tbn.conv2d_fwd(desc, bf16_dev(xb), codes, alpha, out_dtype=torch.bfloat16, scale=to_dev(scale),
+                           bias=to_dev(bias), residual=bf16_dev(resb), relu=True)
+        torch.cuda.synchronize()
+        e = nerr(y.float().cpu().numpy(), ref)
+        assert e <= TOL, "fwd epilogue tile %d splits %d %s: %.3e" % (tile, splits, g, e)
+        if g[7] == 1:
+            dx = tbn.conv2d_bwd_data(desc, bf16_dev(dyb), codes, alpha, out_dtype=torch.float32)
+            torch.cuda.synchronize()
+            e = nerr(dx.cpu().numpy(), oracle.conv_bwd_data(d, oracle.bf16_bits_to_f64(dyb), q.codes, a64))
+            assert e <= TOL, "bwd_data tile %d splits %d %s: %.3e" % (tile, splits, g, e)
+
+
 TILE_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1), (2, 10, 10, 40, 24, 3, 3, 1, 1),
               (3, 12, 12, 128, 130, 3, 3, 2, 1), (2, 19, 17, 3, 40, 7, 7, 2, 3), (4, 1, 1, 512, 72, 1, 1, 1, 0),
               (3, 5, 5, 64, 80, 5, 5, 1, 0)]
 
 
-@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 13, 14, 16, 17, 18, 19, 20, 30])
+@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 13, 14, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 30])
 def test_every_tile_shape(tbn, tile, knobs):
     # each tile shape of the convolution kernels against the oracle (fwd and bwd_data)
     knobs(conv_tile=tile)

@@ -23,7 +23,7 @@ CASES = [
     ((1, 14, 14, 256, 256, 3, 3, 1, 1), True),    # ResNet-18 layer-3 shape at batch 1
     ((1, 7, 7, 512, 512, 3, 3, 1, 1), True),      # layer-4 shape, smaller input
     ((8, 224, 224, 3, 64, 7, 7, 2, 3), False),    # the stem at batch 8 (bordered input copy)
-    ((1, 56, 56, 64, 64, 3, 3, 1, 1), False),     # layer-1 shape, smaller input than the stem
+    ((1, 28, 28, 128, 128, 3, 3, 1, 1), False),   # layer-2 shape, smaller input than the stem
 ]
 
 
