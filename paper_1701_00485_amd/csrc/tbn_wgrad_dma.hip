@@ -25,6 +25,7 @@
 //     64 pixels' 16-byte pieces are contiguous (one DMA instruction, lane = pixel),
 //     segments 1088 bytes apart; with few valid dy channels this issues fewer copies.
 #include <cstdlib>
+#include <type_traits>
 
 #include "tbn_device.h"
 #include "tbn_dma.h"
@@ -59,6 +60,14 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 __device__ __forceinline__ v4i16 read_tr(uint32_t addr) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(uintptr_t)addr);
+}
+
+// Per-lane select by a wave-uniform 64-bit lane mask: bit i of `mask` set -> lane i gets
+// `if_set`.  One v_cndmask with the mask in a scalar register pair.
+__device__ __forceinline__ uint32_t lane_select(uint64_t mask, uint32_t if_clear, uint32_t if_set) {
+    uint32_t r;
+    asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(if_clear), "v"(if_set), "s"(mask));
+    return r;
 }
 
 // 8 consecutive pixels of one channel as an MFMA operand (two transposing reads).
@@ -329,7 +338,7 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
     // the PAIRS pixels of a lane are consecutive: the first is located by division, the
     // others step q (and carry into p and the image)
     const int q_step = a.sw, p_step = a.sh;
-    auto table = [&](int st_i) {
+    auto table_general = [&](int st_i) {
         const int64_t m0 = m_begin + (int64_t)st_i * PIXR + PAIRS * wave + NPAIR * half;
         uint32_t mm = m0 < m_end ? (uint32_t)m0 : 0u;
         uint32_t img = fdiv(mm, ka.div_pq);
@@ -360,6 +369,64 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
                 }
             }
         }
+    };
+    // Linear copies: a stride-1 convolution whose output has the input's size (P = H,
+    // Q = W) maps output pixel m and tap (r, s) to input pixel m + (r - ph) W + (s - pw),
+    // and with C % 256 == 0 the 256 columns of a block share one tap.  Then both halves'
+    // offsets are one wave-uniform pixel offset (the first pixel of the pair; the second
+    // lies NPAIR pixels on) plus a per-lane constant, and only the validity of the two
+    // pixels (inside the image for the tap, before the split's end) is tested, on the
+    // scalar unit; per copy one add and one select remain on the vector unit.
+    const bool lin = a.sh == 1 && a.sw == 1 && a.P == a.H && a.Q == a.W && C % 256 == 0;
+    const int tap = j0 / (lin ? C : 1);
+    const int tr = tap / a.S, ts = tap - (tap / a.S) * a.S;  // the block's tap (linear copies)
+    const uint32_t ldy = dy_col + (uint32_t)(half * NPAIR * K * 2);
+    const uint32_t lx = (uint32_t)(seg * 16 + half * NPAIR * C * 2);
+    const int32_t x_shift = ((tr - a.ph) * a.W + (ts - a.pw)) * C + (lin ? j0 - tap * C : 0);
+    const uint64_t dyok_lanes = __builtin_amdgcn_ballot_w64(dy_ok);
+    const uint32_t oob = 0x80000000u;
+    auto table_linear = [&](int st_i) {
+        // pixel A of pair jj is mA0 + jj (lanes 0-31), pixel B = A + NPAIR (lanes 32-63);
+        // M < 2^31, so 32-bit pixel indices
+        const int32_t mA0 = (int32_t)m_begin + st_i * PIXR + PAIRS * wave;
+        const int32_t rem = (int32_t)m_end - mA0;  // pixels of the split from mA0 on
+        uint64_t lx_ok[PAIRS], ld_ok[PAIRS];       // lanes whose copy is real (scalar masks)
+#pragma unroll
+        for (int jj = 0; jj < PAIRS; ++jj) lx_ok[jj] = ld_ok[jj] = 0;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+            const uint64_t lanes = hh ? 0xFFFFFFFF00000000ull : 0x00000000FFFFFFFFull;
+            const uint32_t m0 = NPAIR * hh < rem ? (uint32_t)(mA0 + NPAIR * hh) : 0u;
+            const uint32_t pq = m0 - fdiv(m0, ka.div_pq) * PQ;
+            uint32_t p = fdiv(pq, ka.div_q);
+            uint32_t q_ = pq - p * (uint32_t)a.Q;
+#pragma unroll
+            for (int jj = 0; jj < PAIRS; ++jj) {
+                const bool in = NPAIR * hh + jj < rem;
+                const bool inside = (unsigned)((int)p - a.ph + tr) < (unsigned)a.H &&
+                                    (unsigned)((int)q_ - a.pw + ts) < (unsigned)a.W;
+                ld_ok[jj] |= in ? lanes : 0ull;
+                lx_ok[jj] |= in && inside ? lanes : 0ull;
+                if (jj + 1 < PAIRS) {  // next output pixel (the image does not matter here)
+                    if (++q_ == (uint32_t)a.Q) {
+                        q_ = 0;
+                        if (++p == (uint32_t)a.P) p = 0;
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int jj = 0; jj < PAIRS; ++jj) {
+            const uint32_t mj = (uint32_t)(mA0 + jj);  // wraps harmlessly where masked off
+            o_dy[jj] = lane_select(ld_ok[jj] & dyok_lanes, oob, mj * (uint32_t)K * 2u + ldy);
+            o_x[jj] = lane_select(lx_ok[jj], oob, (mj * (uint32_t)C + (uint32_t)x_shift) * 2u + lx);
+        }
+    };
+    auto table = [&](int st_i) {
+        if (lin)
+            table_linear(st_i);
+        else
+            table_general(st_i);
     };
     int islot = 0;  // ring slot of the next stage to issue
     auto issue = [&](int) {
@@ -407,19 +474,26 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
 
     // transposing reads: lane (g = lane / 16, i = lane % 16) reads the 8 bytes of channels
     // 16 (g % 2) + 4 (i % 4) .. + 3 of stage pixel 16 u + 8 (g / 2) + i / 4 (+ 4 for the
-    // second read) in step u; stage pixel r sits at (r % NPAIR) * PP + (r / NPAIR) * 512
+    // second read) in step u; stage pixel r sits at (r % NPAIR) * PP + (r / NPAIR) * 512.
+    // One address register per (ring slot, step, operand), masked to the LDS size so that
+    // the compiler can prove it non-negative and fold the constant offsets of the other
+    // rows of the wave tile into the read instructions.
+    constexpr int NU = PIXR / 16;
     const int g = lane >> 4, i16 = lane & 15;
     const int rho = 8 * (g >> 1) + (i16 >> 2);
     const uint32_t col_off = (uint32_t)((16 * (g & 1) + 4 * (i16 & 3)) * 2);
-    uint32_t ro_u[PIXR / 16];  // per step u: this lane's byte offset inside a stage operand
-#pragma unroll
-    for (int u = 0; u < PIXR / 16; ++u) {
-        const int r = 16 * u + rho;
-        ro_u[u] = (uint32_t)((r % NPAIR) * PP + (r / NPAIR) * 512) + col_off;
-    }
-    auto row_off = [&](int u) { return ro_u[u]; };
     const uint32_t a_base = (uint32_t)(wm * 128 * 2);
     const uint32_t b_base = (uint32_t)PR_OP + (uint32_t)(wn * 32 * TN * 2);
+    uint32_t ra[STAGES][NU], rb[STAGES][NU];
+#pragma unroll
+    for (int sl = 0; sl < STAGES; ++sl)
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const int r = 16 * u + rho;
+            const uint32_t ro = (uint32_t)((r % NPAIR) * PP + (r / NPAIR) * 512) + col_off;
+            ra[sl][u] = (smem_base + (uint32_t)(sl * PR_STAGE) + a_base + ro) & 0x3FFFFu;
+            rb[sl][u] = (smem_base + (uint32_t)(sl * PR_STAGE) + b_base + ro) & 0x3FFFFu;
+        }
     auto operand = [&](uint32_t addr) {
         const v4i16 lo = read_tr(addr);
         const v4i16 hi = read_tr(addr + 4 * PP);
@@ -447,8 +521,10 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
         }
     }
     table(STAGES - 1);
-    int cslot = 0;  // ring slot of the stage being multiplied
-    for (int it = 0; it < nst; ++it) {
+    // one stage, in ring slot SL (a compile-time constant: the loop below is unrolled over
+    // the ring)
+    auto stage = [&](int it, auto slot) {
+        constexpr int SL = decltype(slot)::value;
         // this wave's DMAs of stage `it` landed (later stages and the prefetch issued with
         // stage `it` may still be in flight; in the last stages simply everything)
         if (it + STAGES - 2 < nst)
@@ -461,29 +537,36 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
             if constexpr (PF) prefetch(it + STAGES - 1 + pf_dist);
             table(it + STAGES);      // the offsets of the next copy, during the MFMAs
         }
-        const uint32_t st = smem_base + (uint32_t)(cslot * PR_STAGE);
-        cslot = cslot + 1 == STAGES ? 0 : cslot + 1;
         bf16x8 af[2][TM], bf[2][TN];
         auto load = [&](int u, int b) {
-            const uint32_t ro = row_off(u);
 #pragma unroll
-            for (int i = 0; i < TM; ++i) af[b][i] = operand(st + a_base + (uint32_t)(64 * i) + ro);
+            for (int i = 0; i < TM; ++i) af[b][i] = operand(ra[SL][u] + (uint32_t)(64 * i));
 #pragma unroll
-            for (int t = 0; t < TN; ++t) bf[b][t] = operand(st + b_base + (uint32_t)(64 * t) + ro);
+            for (int t = 0; t < TN; ++t) bf[b][t] = operand(rb[SL][u] + (uint32_t)(64 * t));
         };
         load(0, 0);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int u = 0; u < PIXR / 16; ++u) {
-            if (u + 1 < PIXR / 16) load(u + 1, (u + 1) & 1);
+        for (int u = 0; u < NU; ++u) {
+            if (u + 1 < NU) load(u + 1, (u + 1) & 1);
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(af[u & 1][i], bf[u & 1][t], acc[i][t]);
-            if (u + 1 < PIXR / 16) interleave_reads();
+            if (u + 1 < NU) interleave_reads();
             __builtin_amdgcn_sched_barrier(0);
         }
+    };
+    for (int it = 0; it < nst; it += STAGES) {
+        stage(it, std::integral_constant<int, 0>{});
+        if constexpr (STAGES > 1)
+            if (it + 1 < nst) stage(it + 1, std::integral_constant<int, 1>{});
+        if constexpr (STAGES > 2)
+            if (it + 2 < nst) stage(it + 2, std::integral_constant<int, 2>{});
+        if constexpr (STAGES > 3)
+            if (it + 3 < nst) stage(it + 3, std::integral_constant<int, 3>{});
     }
+    static_assert(STAGES <= 4, "ring unrolled up to four slots");
 
     float* out = a.out + (int64_t)split * K * J;
     const int l32 = lane & 31;

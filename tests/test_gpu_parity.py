@@ -488,10 +488,13 @@ def test_bwd_weight_parity(tbn, g, accumulate):
 def test_bwd_weight_tile_shapes(tbn, cfg, pix, pf, knobs):
     # every tile / stage geometry of the transposing-read weight-gradient kernels (the
     # 48-pixel stages do not divide the 64-pixel split ranges: the last stage of a range is
-    # partial), and the optional L2 prefetch
+    # partial), and the optional L2 prefetch; stride-1 same-size layers with C % 256 == 0
+    # take the linear copy addressing (ragged K, a pixel count that ends inside a stage's
+    # pixel pairs, 1x1 and 5x5 filters, images narrower than the filter)
     knobs(wgrad_cfg=cfg, wgrad_pix=pix, wgrad_pf=pf)
     for g in [(2, 14, 14, 256, 256, 3, 3, 1, 1), (3, 12, 12, 128, 136, 3, 3, 2, 1), (5, 9, 7, 64, 96, 3, 3, 1, 1),
-              (2, 16, 16, 64, 128, 1, 1, 2, 0)]:
+              (2, 16, 16, 64, 128, 1, 1, 2, 0), (2, 6, 7, 256, 136, 3, 3, 1, 1), (1, 5, 3, 512, 256, 3, 3, 1, 1),
+              (3, 4, 5, 256, 264, 1, 1, 1, 0), (2, 7, 9, 256, 128, 5, 5, 1, 2), (1, 2, 2, 256, 128, 3, 3, 1, 1)]:
         d, P, Q, xb, dyb, _ = _conv_inputs(g, 5)
         ref = oracle.conv_bwd_weight(d, oracle.bf16_bits_to_f64(xb), oracle.bf16_bits_to_f64(dyb))
         dw = tbn.conv2d_bwd_weight(tbn.ConvDesc(*g), bf16_dev(xb), bf16_dev(dyb))
