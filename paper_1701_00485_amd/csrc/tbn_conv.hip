@@ -384,13 +384,15 @@ int conv_splits_override() { return knob(KNOB_CONV_SPLITS); }
 
 // Which kernel runs a forward / backward-data GEMM: the weight-streaming kernel for a
 // fully-connected layer of at most 16 rows, the LDS-DMA implicit GEMM for C % 8 == 0, the
-// thin-input kernel for few channels, else the general one.  cfg (the tile knob) forces a
-// family: 0-1 general, 10-19 and 21-25 LDS-DMA tile shapes, 20 thin, 30 weight streaming.
-enum ConvPath { PATH_FC, PATH_DMA, PATH_THIN, PATH_GENERIC };
+// direct kernel for small few-channel layers, the thin-input kernel for other few-channel
+// ones, else the general one.  cfg (the tile knob) forces a family: 0-1 general, 10-19 and
+// 21-25 LDS-DMA tile shapes, 20 thin, 30 weight streaming, 40 direct.
+enum ConvPath { PATH_FC, PATH_DMA, PATH_DIRECT, PATH_THIN, PATH_GENERIC };
 
 static ConvPath choose_path(const ConvGemmArgs& a, int cfg, FcStreamPlan* fp, ThinGeom* tg) {
     if ((cfg < 0 || cfg == 30) && fc_stream_plan(a, fp)) return PATH_FC;
     if (conv_dma_eligible(a) && (cfg < 0 || (cfg >= 10 && cfg < 20) || (cfg >= 21 && cfg <= 25))) return PATH_DMA;
+    if ((cfg < 0 || cfg == 40) && conv_direct_eligible(a)) return PATH_DIRECT;
     if ((cfg < 0 || cfg == 20) && conv_thin_plan(a, tg)) return PATH_THIN;
     return PATH_GENERIC;
 }
@@ -418,6 +420,7 @@ hipError_t launch_conv_gemm(const ConvGemmArgs& args, hipStream_t stream) {
     switch (choose_path(a, cfg, &fp, &tg)) {
         case PATH_FC: return launch_fc_stream(a, fp, stream);
         case PATH_DMA: return launch_conv_dma(a, plan_conv_dma(a, cfg), stream);
+        case PATH_DIRECT: return launch_conv_direct(a, stream);
         case PATH_THIN: return launch_conv_thin(a, tg, stream);
         default: break;
     }

@@ -1,0 +1,203 @@
+// tbn_conv_direct.hip -- forward pass of a small two-bit layer (Sec. 2 Eq. 1) whose filters
+// have at most 64 elements over few input channels (3x3, 5x5, 7x7 or 1x1 shapes compiled):
+// single-channel MNIST-shaped layers and the first 3x3 layer over RGB.  Such a layer is a few hundred MFLOP at most, so the matrix cores
+// buy nothing; what costs time is latency (filter decode, input gather, output store in
+// sequence).  Here every thread owns one output pixel and 8 consecutive filters:
+//   * a block (four waves) covers 64 pixels and 32 filters; its filters are decoded once
+//     from the packed codes into LDS as fp32 +-1 / +-2 (element-major, so the 8 weights a
+//     thread needs for one element are one 32-byte broadcast read: every lane of a wave
+//     reads the same filters);
+//   * the thread first issues the loads of its R*S*C input values (zero outside the image;
+//     fp32 input rounded to bf16, nearest even, as in every other forward kernel), then the
+//     block decodes its filters while they are in flight, then the values are accumulated
+//     against the weights with fp32 FMAs (products exact, sums fp32);
+//   * alpha (the column scale) and the optional scale, bias, residual and ReLU are applied
+//     in fp32 and the 8 outputs written with 16-byte stores.
+#include "tbn_device.h"
+#include "tbn_kernels.h"
+
+namespace tbn {
+
+namespace {
+
+constexpr int DPIX = 64;   // output pixels per block (one per lane)
+constexpr int DFB = 32;    // filters per block (8 per wave)
+constexpr int DMAXN = 64;  // filter elements R*S*C
+
+// R x S filters over C channels (compile-time, so that the gather below is fully unrolled and
+// all of a thread's input loads are in flight together)
+template <int R, int S, int C, bool X32>
+__global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) {
+    constexpr int n = R * S * C;
+    static_assert(n <= DMAXN, "filter elements");
+    __shared__ __attribute__((aligned(16))) float wl[n * DFB];  // [element][filter]
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int grp = __builtin_amdgcn_readfirstlane(tid >> 6);  // filter group of the wave
+    constexpr int nchunks = (n + 63) / 64;
+    const int kb0 = blockIdx.y * DFB;
+
+    // the input values of this thread's pixel, loaded first so that their latency overlaps
+    // the filter decode (zero outside the image; fp32 input rounded to bf16)
+    const int64_t M = (int64_t)a.N * a.P * a.Q;
+    const int64_t m = (int64_t)blockIdx.x * DPIX + lane;
+    const bool live = m < M;
+    const uint32_t mm = live ? (uint32_t)m : 0u;  // < 2^31, checked by the host
+    const uint32_t img = fdiv(mm, a.div_pq);
+    const uint32_t pq = mm - img * (uint32_t)(a.P * a.Q);
+    const uint32_t p = fdiv(pq, a.div_q);
+    const uint32_t q = pq - p * (uint32_t)a.Q;
+    const int h0 = (int)p * a.sh - a.ph, w0 = (int)q * a.sw - a.pw;
+    // element index of tap (0, 0) (x has fewer than 2^31 elements, checked by the host; it
+    // may be negative here, only in-image taps are used)
+    const int32_t pix0 = (((int32_t)img * a.H + h0) * a.W + w0) * C;
+    // unconditional gather through a buffer resource: an out-of-image tap gets an offset
+    // beyond the buffer and the hardware returns zero, so no load sits behind a branch and
+    // all of them are in flight together
+    constexpr int ESZ = X32 ? 4 : 2;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<void*>(a.x), (short)0, (int)((int64_t)a.N * a.H * a.W * C * ESZ), 0x00020000);
+    float xv[n];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int s_ = 0; s_ < S; ++s_) {
+            const bool ok = live && (unsigned)(h0 + r) < (unsigned)a.H && (unsigned)(w0 + s_) < (unsigned)a.W;
+            const int off = ok ? (pix0 + (r * a.W + s_) * C) * ESZ : (int)0x80000000;
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+                uint32_t b;
+                if constexpr (X32)
+                    b = f32_to_bf16_bits(__uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, c * 4, 0)));
+                else
+                    b = __builtin_amdgcn_raw_buffer_load_b16(rs, off, c * 2, 0);
+                xv[(r * S + s_) * C + c] = bf16_bits_to_f32(b);
+            }
+        }
+
+    // the block's filters: element e of filter kb0 + f is bit (e % 16) / 2 (+ 16 for odd e)
+    // of word (e % 64) / 16 of the filter's 16-byte code row in chunk e / 64 (magnitude),
+    // the bit 8 above it the sign; weights of filters past Kf are zero
+    for (int i = tid; i < n * DFB; i += 256) {
+        const int e = i >> 5, f = i & (DFB - 1), k = kb0 + f;
+        float v = 0.0f;
+        if (k < a.Kf) {
+            const uint32_t w = a.codes[((int64_t)((k >> 6) * nchunks + (e >> 6)) * 64 + (k & 63)) * 4 + ((e & 63) >> 4)];
+            const int jj = (e & 15) >> 1, hh = e & 1;
+            const uint32_t mag = (w >> (16 * hh + jj)) & 1u, sg = (w >> (16 * hh + 8 + jj)) & 1u;
+            v = (mag ? 2.0f : 1.0f) * (sg ? -1.0f : 1.0f);
+        }
+        wl[i] = v;
+    }
+    __syncthreads();
+
+    const int k0 = kb0 + 8 * grp;
+    if (!live || k0 >= a.Kf) return;  // no barrier follows
+
+    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    const float* wg = wl + 8 * grp;
+#pragma unroll
+    for (int e = 0; e < n; ++e) {
+        // weights read four elements at a time (the fence keeps the compiler from hoisting
+        // all of them, which would cost ~200 registers and occupancy)
+        if (e % 4 == 0) __builtin_amdgcn_sched_barrier(0);
+        // the 8 weights of element e: the same address in every lane (broadcast)
+        const f32x4 lo = *reinterpret_cast<const f32x4*>(wg + e * DFB);
+        const f32x4 hi = *reinterpret_cast<const f32x4*>(wg + e * DFB + 4);
+        acc[0] = fmaf(xv[e], lo.x, acc[0]);
+        acc[1] = fmaf(xv[e], lo.y, acc[1]);
+        acc[2] = fmaf(xv[e], lo.z, acc[2]);
+        acc[3] = fmaf(xv[e], lo.w, acc[3]);
+        acc[4] = fmaf(xv[e], hi.x, acc[4]);
+        acc[5] = fmaf(xv[e], hi.y, acc[5]);
+        acc[6] = fmaf(xv[e], hi.z, acc[6]);
+        acc[7] = fmaf(xv[e], hi.w, acc[7]);
+        if (e % 4 == 3 || e == n - 1) {
+            // the sums so far are materialised here, so the FMAs cannot be moved past the
+            // next reads (which would keep every weight of the filter live at once)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) asm volatile("" : "+v"(acc[j]));
+        }
+    }
+
+    // ---- epilogue: y = act(acc * alpha * scale + bias + residual) ----
+    const int Kf = a.Kf;
+    const int64_t o = m * Kf + k0;
+    float v8[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int col = k0 + j < Kf ? k0 + j : Kf - 1;  // past Kf: computed, never stored
+        float sc = a.colscale ? a.colscale[col] : 1.0f;
+        if (a.scale) sc *= a.scale[col];
+        v8[j] = acc[j] * sc + (a.bias ? a.bias[col] : 0.0f);
+    }
+    const bool full = k0 + 8 <= Kf && Kf % 8 == 0;  // 16-byte aligned group of 8 real columns
+    if (a.residual) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (k0 + j < Kf)
+                v8[j] += a.y_f32 ? reinterpret_cast<const float*>(a.residual)[o + j]
+                                 : bf16_bits_to_f32(reinterpret_cast<const uint16_t*>(a.residual)[o + j]);
+    }
+    if (a.relu) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v8[j] = fmaxf(v8[j], 0.0f);
+    }
+    if (a.y_f32) {
+        float* yp = reinterpret_cast<float*>(a.y) + o;
+        if (full) {
+            *reinterpret_cast<f32x4*>(yp) = f32x4{v8[0], v8[1], v8[2], v8[3]};
+            *reinterpret_cast<f32x4*>(yp + 4) = f32x4{v8[4], v8[5], v8[6], v8[7]};
+        } else {
+            for (int j = 0; j < 8 && k0 + j < Kf; ++j) yp[j] = v8[j];
+        }
+    } else {
+        uint16_t* yp = reinterpret_cast<uint16_t*>(a.y) + o;
+        if (full) {
+            *reinterpret_cast<u32x4*>(yp) = u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]),
+                                                  pack_bf16x2(v8[4], v8[5]), pack_bf16x2(v8[6], v8[7])};
+        } else {
+            for (int j = 0; j < 8 && k0 + j < Kf; ++j) yp[j] = (uint16_t)f32_to_bf16_bits(v8[j]);
+        }
+    }
+}
+
+}  // namespace
+
+// filter shapes with a compiled kernel: 3x3 over 1..7 channels, 5x5 over 1..2, 7x7 over 1,
+// 1x1 over 1..8
+static const void* direct_kernel(int R, int S, int C, bool x32) {
+#define TBN_D(r, s, c) \
+    if (R == r && S == s && C == c) \
+        return x32 ? reinterpret_cast<const void*>(&conv_direct_kernel<r, s, c, true>) \
+                   : reinterpret_cast<const void*>(&conv_direct_kernel<r, s, c, false>);
+    TBN_D(3, 3, 1) TBN_D(3, 3, 2) TBN_D(3, 3, 3) TBN_D(3, 3, 4) TBN_D(3, 3, 5) TBN_D(3, 3, 6) TBN_D(3, 3, 7)
+    TBN_D(5, 5, 1) TBN_D(5, 5, 2) TBN_D(7, 7, 1)
+    TBN_D(1, 1, 1) TBN_D(1, 1, 2) TBN_D(1, 1, 3) TBN_D(1, 1, 4) TBN_D(1, 1, 5) TBN_D(1, 1, 6) TBN_D(1, 1, 7)
+    TBN_D(1, 1, 8)
+#undef TBN_D
+    return nullptr;
+}
+
+bool conv_direct_eligible(const ConvGemmArgs& a) {
+    // forward pass with packed codes, a compiled filter shape (at most 64 elements, C <= 8),
+    // and little work in total (at most 2^28 multiply-adds: beyond that the matrix-core
+    // kernels win)
+    const int64_t n = (int64_t)a.R * a.S * a.C;
+    const int64_t macs = (int64_t)a.N * a.P * a.Q * a.Kf * n;
+    return !a.apair && !a.wdense && direct_kernel(a.R, a.S, a.C, a.x_f32 != 0) != nullptr &&
+           macs <= (1ll << 28) && (int64_t)a.N * a.P * a.Q < 0x7FFFFFFFll &&
+           (int64_t)a.N * a.H * a.W * a.C < 0x7FFFFFFFll;
+}
+
+hipError_t launch_conv_direct(const ConvGemmArgs& a, hipStream_t stream) {
+    const void* fn = direct_kernel(a.R, a.S, a.C, a.x_f32 != 0);
+    if (!fn) return hipErrorInvalidValue;
+    const int64_t M = (int64_t)a.N * a.P * a.Q;
+    const dim3 grid((unsigned)((M + DPIX - 1) / DPIX), (unsigned)((a.Kf + DFB - 1) / DFB));
+    ConvGemmArgs ka = a;
+    void* args[] = {&ka};
+    return hipLaunchKernel(fn, grid, dim3(256), args, 0, stream);
+}
+
+}  // namespace tbn

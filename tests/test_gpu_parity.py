@@ -284,9 +284,11 @@ def test_fwd_parity(tbn, g, out):
                                     ((7, 224, 224, 3, 40, 7, 7, 2, 3), "f32"),    # fp32 input, ragged filters
                                     ((16, 256, 256, 1, 32, 5, 5, 1, 2), "bf16"),  # one channel
                                     ((4, 257, 263, 5, 24, 3, 3, 2, 1), "bf16")])  # 5 channels, odd sizes
-def test_fwd_thin_bordered_copy(tbn, g, xdt):
+def test_fwd_thin_bordered_copy(tbn, g, xdt, knobs):
     """Inputs of 2^20 elements and more with fewer than 8 channels: the input is first written
-    into workspace as a zero-bordered copy and the patches are copied from it."""
+    into workspace as a zero-bordered copy and the patches are copied from it (the thin-input
+    kernel forced, as small filters would otherwise take the direct kernel)."""
+    knobs(conv_tile=20)
     log("fwd thin bordered copy %s %s" % (g, xdt))
     n, h, w, c, k, r, s, st, pd = g
     assert n * h * w * c >= 1 << 20
@@ -310,6 +312,44 @@ def test_fwd_thin_bordered_copy(tbn, g, xdt):
     e = nerr(y.cpu().numpy()[imgs], ref)
     log("  images %s: normalised max error %.3e" % (imgs, e))
     assert e <= 1e-4
+
+
+@pytest.mark.parametrize("g,xdt", [((16, 28, 28, 1, 32, 5, 5, 1, 2), "f32"),   # the single-layer workload
+                                    ((3, 28, 28, 1, 20, 5, 5, 1, 0), "bf16"),   # LeNet conv1 shape, ragged K
+                                    ((2, 9, 9, 3, 72, 3, 3, 2, 1), "f32"),      # RGB 3x3 stride 2, two filter blocks
+                                    ((1, 13, 11, 7, 40, 3, 3, 1, 1), "bf16"),   # 7 channels (63 elements)
+                                    ((2, 10, 9, 1, 8, 7, 7, 1, 3), "bf16"),     # 7x7, one filter group
+                                    ((5, 6, 7, 4, 33, 1, 1, 1, 0), "f32")])     # 1x1, K one past 32
+def test_fwd_direct_small_layers(tbn, g, xdt):
+    """The direct fp32-FMA kernel (few channels, at most 64 filter elements): fused epilogue
+    (scale, bias, residual, ReLU) with bf16 output and plain fp32 output against the oracle."""
+    log("fwd direct %s %s" % (g, xdt))
+    n, h, w, c, k, r, s, st, pd = g
+    d = oracle.ConvDesc(*g)
+    P, Q = d.out_dims()
+    wr = synth.normal(11, "dw%s" % (g,), (k, r * s * c), 1.0)
+    q = oracle.quantize(wr)
+    codes, alpha, _ = tbn.quantize(to_dev(wr))
+    if xdt == "f32":
+        x = synth.normal(11, "dx%s" % (g,), (n, h, w, c))
+        xin, xref = to_dev(x), oracle.round_bf16(x)
+    else:
+        xb = synth.normal_bf16(11, "dx%s" % (g,), (n, h, w, c))
+        xin, xref = bf16_dev(xb), oracle.bf16_bits_to_f64(xb)
+    scale = synth.uniform(11, "dsc", (k,), 0.5, 1.5)
+    bias = synth.normal(11, "dbi", (k,), 0.1)
+    resb = synth.normal_bf16(11, "dres", (n, P, Q, k))
+    acc = oracle.conv_fwd(d, xref, q.codes, q.alpha.astype(np.float64))
+    desc = tbn.ConvDesc(*g)
+    y32 = tbn.conv2d_fwd(desc, xin, codes, alpha, out_dtype=torch.float32)
+    y = tbn.conv2d_fwd(desc, xin, codes, alpha, out_dtype=torch.bfloat16, scale=to_dev(scale), bias=to_dev(bias),
+                       residual=bf16_dev(resb), relu=True)
+    torch.cuda.synchronize()
+    e = nerr(y32.cpu().numpy(), acc)
+    assert e <= 1e-4, "fwd %s: %.3e" % (g, e)
+    ref = np.maximum(acc * scale.astype(np.float64) + bias + oracle.bf16_bits_to_f64(resb), 0.0)
+    e = nerr(y.float().cpu().numpy(), ref)
+    assert e <= TOL, "fwd epilogue %s: %.3e" % (g, e)
 
 
 def test_fwd_fp32_input_single_layer(tbn):
@@ -611,7 +651,7 @@ TILE_CASES = [(2, 14, 14, 256, 256, 3, 3, 1, 1), (2, 15, 13, 64, 96, 3, 3, 1, 1)
               (3, 5, 5, 64, 80, 5, 5, 1, 0)]
 
 
-@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 13, 14, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 30])
+@pytest.mark.parametrize("tile", [0, 1, 10, 11, 12, 13, 14, 16, 17, 18, 19, 20, 21, 22, 23, 24, 25, 30, 40])
 def test_every_tile_shape(tbn, tile, knobs):
     # each tile shape of the convolution kernels against the oracle (fwd and bwd_data)
     knobs(conv_tile=tile)
