@@ -56,14 +56,19 @@ __device__ __forceinline__ bf16x8 decode8_half(uint32_t w, uint32_t base) {
     return as_bf16x8(r);
 }
 
-// KU code loads (16 bytes per lane) per buffer, NBUF buffers in flight per wave.
-template <int KU, int NBUF>
-__global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, int32_t n, int32_t nsteps,
-                                                        int32_t xpitch) {
-    extern __shared__ __attribute__((aligned(16))) uint16_t xl[];  // [N + 1][xpitch] bf16
+// KU code loads (16 bytes per lane) per buffer, NBUF buffers in flight per wave; G groups
+// of four waves per block, group g reducing the g-th of G equal ranges of steps (more waves
+// per SIMD to keep loads in flight, no partial sums in memory: the groups add through LDS).
+template <int KU, int NBUF, int G>
+__global__ __launch_bounds__(256 * G) void fc_stream_kernel(const ConvGemmArgs a, int32_t n, int32_t nsteps,
+                                                            int32_t xpitch) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t xl[];  // [N + 1][xpitch] bf16, then group sums
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = (tid >> 6) & 3;
+    const int grp = G > 1 ? __builtin_amdgcn_readfirstlane(tid >> 8) : 0;
+    const int steps_g = nsteps / G;       // steps of each group (the host pads to a multiple)
+    const int step_base = grp * steps_g;
     const int N = a.N;
     const int K = a.Kf;
     const int NB = (n + 63) / 64;  // element blocks of a filter row
@@ -84,7 +89,7 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
     auto load = [&](u32x4 (&w)[KU], int step0) {
 #pragma unroll
         for (int u = 0; u < KU; ++u) {
-            int ib = 4 * (step0 + u) + g;
+            int ib = 4 * (step_base + step0 + u) + g;
             ib = ib < NB ? ib : NB - 1;  // in bounds; its activations are zero past n
             w[u] = __builtin_nontemporal_load(&codes[(int64_t)ib * 64]);  // read once: streaming
         }
@@ -93,7 +98,7 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
     auto compute = [&](const u32x4 (&w)[KU], int step0) {
 #pragma unroll
         for (int u = 0; u < KU; ++u) {
-            const uint16_t* xb = xrow + (4 * (step0 + u) + g) * 64;
+            const uint16_t* xb = xrow + (4 * (step_base + step0 + u) + g) * 64;
             bf16x8 bx[8];  // the step's activation operands, read before its MFMAs
 #pragma unroll
             for (int s = 0; s < 8; ++s) bx[s] = *reinterpret_cast<const bf16x8*>(xb + 8 * s);
@@ -113,11 +118,11 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
         // 16-byte pieces, the loads of a thread issued together
         const int pieces = (N + 1) * xpitch / 8;
         const int ppr = xpitch / 8;  // pieces per row
-        for (int i0 = tid; i0 < pieces; i0 += 256 * 8) {
+        for (int i0 = tid; i0 < pieces; i0 += 256 * G * 8) {
             u32x4 v[8];
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
-                const int i = i0 + 256 * u;
+                const int i = i0 + 256 * G * u;
                 const int r = i / ppr, e = (i - r * ppr) * 8;
                 const bool ok = i < pieces && r < N && e < n;
                 v[u] = ok ? *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.x) + (int64_t)r * n + e)
@@ -125,10 +130,10 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
             }
 #pragma unroll
             for (int u = 0; u < 8; ++u)
-                if (i0 + 256 * u < pieces) reinterpret_cast<u32x4*>(xl)[i0 + 256 * u] = v[u];
+                if (i0 + 256 * G * u < pieces) reinterpret_cast<u32x4*>(xl)[i0 + 256 * G * u] = v[u];
         }
     } else {
-        for (int i = tid; i < (N + 1) * xpitch; i += 256) {
+        for (int i = tid; i < (N + 1) * xpitch; i += 256 * G) {
             const int r = i / xpitch, e = i - (i / xpitch) * xpitch;
             uint16_t v = 0;
             if (e < n && r < N)
@@ -138,18 +143,27 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
         }
     }
     __syncthreads();
-    for (int st = 0; st < nsteps; st += NBUF * KU) {
+    for (int st = 0; st < steps_g; st += NBUF * KU) {
 #pragma unroll
         for (int b = 0; b < NBUF; ++b) {
             compute(wbuf[b], st + b * KU);
-            if (st + (NBUF + b) * KU < nsteps) load(wbuf[b], st + (NBUF + b) * KU);
+            if (st + (NBUF + b) * KU < steps_g) load(wbuf[b], st + (NBUF + b) * KU);
         }
+    }
+    f32x4_t t = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    if constexpr (G > 1) {
+        // groups 1 .. G-1 hand their sums to group 0, which adds them in group order
+        f32x4_t* xs = reinterpret_cast<f32x4_t*>(xl + (N + 1) * xpitch);
+        if (grp > 0) xs[((grp - 1) * 4 + wave) * 64 + lane] = t;
+        __syncthreads();
+        if (grp > 0) return;  // no barrier follows
+#pragma unroll
+        for (int gg = 1; gg < G; ++gg) t += xs[((gg - 1) * 4 + wave) * 64 + lane];
     }
 
     // ---- epilogue: lane holds batch column f, filters 4 g .. 4 g + 3 of the wave's 16 ----
     if (f >= N) return;
     const int k0 = kb * 64 + 16 * wave + 4 * g;
-    const f32x4_t t = (acc[0] + acc[1]) + (acc[2] + acc[3]);
     float v4[4] = {t.x, t.y, t.z, t.w};
     const int64_t o = (int64_t)f * K + k0;
 #pragma unroll
@@ -172,25 +186,30 @@ __global__ __launch_bounds__(256) void fc_stream_kernel(const ConvGemmArgs a, in
 
 }  // namespace
 
-// (loads per buffer, buffers) of each variant; the tuning knob selects one for sweeps.  The
-// default keeps four buffers of two 16-byte loads in flight: measured 17.8 us per call on
-// the 8192 -> 32768 batch-1 layer against 18.3-19.1 us for two buffers of four loads,
-// 19.0 us for two of eight and 19.8 us for three of four (loads consumed in smaller groups
-// interleave better with the decode)
-constexpr int kVariants[4][2] = {{2, 4}, {4, 2}, {8, 2}, {4, 3}};
+// (loads per buffer, buffers, groups) of each variant; the tuning knob selects one for
+// sweeps.  Measured on the 8192 -> 32768 batch-1 layer (two runs each): two groups with two
+// buffers of four 16-byte loads 17.6 us per call (the default, variant 5), one group with
+// four buffers of two 17.8-18.8 us, the other one- and two-group variants 18.0-19.8 us, four
+// groups 20.1 us (one block per CU).
+constexpr int kNumVariants = 8;
+constexpr int kVariants[kNumVariants][3] = {{2, 4, 1}, {4, 2, 1}, {8, 2, 1}, {4, 3, 1},
+                                            {2, 4, 2}, {4, 2, 2}, {2, 2, 4}, {2, 3, 2}};
 
 bool fc_stream_plan(const ConvGemmArgs& a, FcStreamPlan* p) {
     // a fully-connected layer: the filter window covers the whole (unpadded) input map
     if (a.apair || a.N > 16 || a.P != 1 || a.Q != 1 || a.R != a.H || a.S != a.W || a.ph != 0 || a.pw != 0)
         return false;
     const int forced = knob(KNOB_FC_VARIANT);
-    p->variant = forced >= 0 && forced < 4 ? forced : 0;
+    p->variant = forced >= 0 && forced < kNumVariants ? forced : 5;
     const int64_t n = (int64_t)a.R * a.S * a.C;
     const int64_t nb = (n + 63) / 64;
-    const int64_t per = 4 * kVariants[p->variant][0] * kVariants[p->variant][1];  // element blocks per iteration
+    const int G = kVariants[p->variant][2];
+    // element blocks per iteration of every group
+    const int64_t per = 4 * kVariants[p->variant][0] * kVariants[p->variant][1] * G;
     const int64_t steps_blocks = (nb + per - 1) / per * per;
     const int64_t xpitch = steps_blocks * 64;
-    const int64_t lds = (int64_t)(a.N + 1) * xpitch * 2;  // + the zero row
+    // + the zero row, then the group sums (16 bytes per lane of groups 1 .. G-1)
+    const int64_t lds = (int64_t)(a.N + 1) * xpitch * 2 + (int64_t)(G - 1) * 256 * 16;
     if (lds > 64 * 1024 || n > (1 << 24)) return false;
     p->n = (int32_t)n;
     p->nsteps = (int32_t)(steps_blocks / 4);
@@ -201,12 +220,19 @@ bool fc_stream_plan(const ConvGemmArgs& a, FcStreamPlan* p) {
 
 hipError_t launch_fc_stream(const ConvGemmArgs& a, const FcStreamPlan& p, hipStream_t stream) {
     const dim3 grid((unsigned)((a.Kf + 63) / 64));
+#define TBN_FC(ku, nb, g) \
+    hipLaunchKernelGGL((fc_stream_kernel<ku, nb, g>), grid, dim3(256 * g), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch)
     switch (p.variant) {
-        case 1: hipLaunchKernelGGL((fc_stream_kernel<4, 2>), grid, dim3(256), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch); break;
-        case 2: hipLaunchKernelGGL((fc_stream_kernel<8, 2>), grid, dim3(256), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch); break;
-        case 3: hipLaunchKernelGGL((fc_stream_kernel<4, 3>), grid, dim3(256), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch); break;
-        default: hipLaunchKernelGGL((fc_stream_kernel<2, 4>), grid, dim3(256), p.lds_bytes, stream, a, p.n, p.nsteps, p.xpitch); break;
+        case 1: TBN_FC(4, 2, 1); break;
+        case 2: TBN_FC(8, 2, 1); break;
+        case 3: TBN_FC(4, 3, 1); break;
+        case 4: TBN_FC(2, 4, 2); break;
+        case 6: TBN_FC(2, 2, 4); break;
+        case 7: TBN_FC(2, 3, 2); break;
+        case 0: TBN_FC(2, 4, 1); break;
+        default: TBN_FC(4, 2, 2); break;
     }
+#undef TBN_FC
     return hipGetLastError();
 }
 

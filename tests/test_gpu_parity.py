@@ -456,9 +456,9 @@ def test_fc_stream_parity(tbn, g):
     assert nerr(y.float().cpu().numpy(), ref) <= TOL
 
 
-@pytest.mark.parametrize("variant", [0, 1, 2, 3])
+@pytest.mark.parametrize("variant", list(range(8)))
 def test_fc_stream_every_variant(tbn, variant, knobs):
-    # each load-buffering variant of the weight-streaming kernel (loads per buffer x buffers)
+    # each variant of the weight-streaming kernel (loads per buffer x buffers x wave groups)
     knobs(fc_variant=variant)
     for g in [(1, 1, 1, 8192, 200, 1, 1, 1, 0), (16, 7, 7, 64, 72, 7, 7, 1, 0), (3, 1, 1, 520, 130, 1, 1, 1, 0)]:
         d, P, Q, xb, _, wr = _conv_inputs(g, 11)
