@@ -66,8 +66,8 @@ def layer_flops():
 
 # Which kernel carries each timed call, and the sources its HBM counters were taken on.
 KERNEL_OF_OP = {
-    "fwd": ("conv_dma_kernel<128, 256, 1, 4, 3, false, true>", ["tbn_conv_dma.hip", "tbn_dma.h", "tbn_device.h"]),
-    "bwd_data": ("conv_dma_kernel<128, 256, 1, 4, 3, true, true>", ["tbn_conv_dma.hip", "tbn_dma.h", "tbn_device.h"]),
+    "fwd": ("conv_dma_kernel<128, 256, 1, 4, 3, false, true, 1>", ["tbn_conv_dma.hip", "tbn_dma.h", "tbn_device.h"]),
+    "bwd_data": ("conv_dma_kernel<128, 256, 1, 4, 3, true, true, 1>", ["tbn_conv_dma.hip", "tbn_dma.h", "tbn_device.h"]),
     "bwd_weight": ("wgrad_rows_kernel", ["tbn_wgrad_dma.hip", "tbn_dma.h", "tbn_device.h"]),
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv3x3_256x256_56x56_b128_train_step_traffic.json")
