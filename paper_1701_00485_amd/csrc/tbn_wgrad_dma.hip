@@ -12,8 +12,8 @@
 //   * a block of 8 waves owns a 256 (k) x 256 (j) output tile; each wave 128 x 64 made of
 //     32x32 v_mfma_f32_32x32x16_bf16 tiles with fp32 accumulators;
 //   * stages of pixels in a ring of LDS buffers: the DMAs of later stages overlap the
-//     MFMAs of the current one, and the operands of each 16-pixel step are read during the
-//     previous one;
+//     MFMAs of the current one, and the operands of each 16-pixel step are read two steps
+//     earlier (the pixel-major kernel; one step in the segment-major one);
 //   * the pixel range is split over the grid (split-K): each split writes fp32 partials
 //     that a second kernel adds in a fixed order (deterministic result).
 // Two stage layouts:
@@ -80,20 +80,22 @@ __device__ __forceinline__ bf16x8 operand(uint32_t addr) {
 }
 
 // Instruction order of one 16-pixel step: its 8 MFMAs alternate with the 12 transposing
-// reads of the next step's operands (two after each of the first four MFMAs, one after
-// each of the others), so that the LDS reads are spread over the MFMA sequence instead of
-// issued in one burst (measured ~6% faster than the compiler's own order on the
-// 256 x 2304 training-layer gradient).
+// reads of a later step's operands (two after each of the first four MFMAs, one after each
+// of the others) and with the scalar work of the copy table, so that neither is issued in
+// one burst (the reads spread this way measured ~6% faster than the compiler's own order
+// on the 256 x 2304 training-layer gradient).
 __device__ __forceinline__ void interleave_reads() {
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
         __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // two LDS reads
+        __builtin_amdgcn_sched_group_barrier(0x004, 8, 0);  // scalar work of the copy table
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x004, 8, 0);
     }
 }
 
@@ -265,7 +267,8 @@ constexpr int PP = 1088;  // bytes per pair of pixel rows
 // PIXR pixels per stage (a multiple of 16), STAGES-deep ring; 2 x 4 waves of 128 x 64,
 // two waves per SIMD.  (One wave per SIMD with 128 x 128 wave tiles reads a third less
 // from LDS per MFMA but measured slower: the stage boundaries are no longer covered.)
-template <int PIXR, int STAGES, bool PF>
+// LIN: linear copy addressing (see below), chosen by the host.
+template <int PIXR, int STAGES, bool PF, bool LIN>
 __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs ka) {
     const WgradArgs& a = ka.a;
     constexpr int WAVES = 8;
@@ -377,56 +380,72 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
     // lies NPAIR pixels on) plus a per-lane constant, and only the validity of the two
     // pixels (inside the image for the tap, before the split's end) is tested, on the
     // scalar unit; per copy one add and one select remain on the vector unit.
-    const bool lin = a.sh == 1 && a.sw == 1 && a.P == a.H && a.Q == a.W && C % 256 == 0;
-    const int tap = j0 / (lin ? C : 1);
+    const int tap = j0 / (LIN ? C : 1);
     const int tr = tap / a.S, ts = tap - (tap / a.S) * a.S;  // the block's tap (linear copies)
     const uint32_t ldy = dy_col + (uint32_t)(half * NPAIR * K * 2);
     const uint32_t lx = (uint32_t)(seg * 16 + half * NPAIR * C * 2);
-    const int32_t x_shift = ((tr - a.ph) * a.W + (ts - a.pw)) * C + (lin ? j0 - tap * C : 0);
+    const int32_t x_shift = ((tr - a.ph) * a.W + (ts - a.pw)) * C + (LIN ? j0 - tap * C : 0);
     const uint64_t dyok_lanes = __builtin_amdgcn_ballot_w64(dy_ok);
     const uint32_t oob = 0x80000000u;
-    auto table_linear = [&](int st_i) {
-        // pixel A of pair jj is mA0 + jj (lanes 0-31), pixel B = A + NPAIR (lanes 32-63);
-        // M < 2^31, so 32-bit pixel indices
-        const int32_t mA0 = (int32_t)m_begin + st_i * PIXR + PAIRS * wave;
-        const int32_t rem = (int32_t)m_end - mA0;  // pixels of the split from mA0 on
-        uint64_t lx_ok[PAIRS], ld_ok[PAIRS];       // lanes whose copy is real (scalar masks)
-#pragma unroll
-        for (int jj = 0; jj < PAIRS; ++jj) lx_ok[jj] = ld_ok[jj] = 0;
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-            const uint64_t lanes = hh ? 0xFFFFFFFF00000000ull : 0x00000000FFFFFFFFull;
-            const uint32_t m0 = NPAIR * hh < rem ? (uint32_t)(mA0 + NPAIR * hh) : 0u;
-            const uint32_t pq = m0 - fdiv(m0, ka.div_pq) * PQ;
-            uint32_t p = fdiv(pq, ka.div_q);
-            uint32_t q_ = pq - p * (uint32_t)a.Q;
-#pragma unroll
-            for (int jj = 0; jj < PAIRS; ++jj) {
-                const bool in = NPAIR * hh + jj < rem;
-                const bool inside = (unsigned)((int)p - a.ph + tr) < (unsigned)a.H &&
-                                    (unsigned)((int)q_ - a.pw + ts) < (unsigned)a.W;
-                ld_ok[jj] |= in ? lanes : 0ull;
-                lx_ok[jj] |= in && inside ? lanes : 0ull;
-                if (jj + 1 < PAIRS) {  // next output pixel (the image does not matter here)
-                    if (++q_ == (uint32_t)a.Q) {
-                        q_ = 0;
-                        if (++p == (uint32_t)a.P) p = 0;
-                    }
-                }
-            }
-        }
+    // The linear table is built in two parts: a vector pass in which lane i tests stage
+    // pixel i (inside the split, and inside the image for the block's tap) and the wave
+    // collects the answers as one 64-bit mask, then per pair a few scalar bit tests that
+    // turn the mask bits of its two pixels into the lane masks of the selects.  The main
+    // loop places the parts between the MFMAs of different steps.
+    uint64_t xin = 0;  // bit i: stage pixel i is in the split and its tap inside the image
+    auto table_linear_mask = [&](int st_i) {
+        const int32_t s0 = (int32_t)m_begin + st_i * PIXR;  // first pixel of the stage (< 2^31)
+        const int32_t ms = s0 + lane;
+        const bool in = lane < PIXR && ms < (int32_t)m_end;
+        const uint32_t mm = in ? (uint32_t)ms : 0u;
+        const uint32_t pq = mm - fdiv(mm, ka.div_pq) * PQ;
+        const uint32_t p = fdiv(pq, ka.div_q);
+        const uint32_t q_ = pq - p * (uint32_t)a.Q;
+        const bool inside = (unsigned)((int)p - a.ph + tr) < (unsigned)a.H &&
+                            (unsigned)((int)q_ - a.pw + ts) < (unsigned)a.W;
+        xin = __builtin_amdgcn_ballot_w64(in && inside);
+    };
+    auto table_linear_select = [&](int st_i) {
+        const int32_t s0 = (int32_t)m_begin + st_i * PIXR;
+        const int32_t rem = (int32_t)m_end - s0;  // pixels of the split from the stage's first on
+        const int32_t mA0 = s0 + PAIRS * wave;
 #pragma unroll
         for (int jj = 0; jj < PAIRS; ++jj) {
+            // stage pixels of the pair: A (lanes 0-31) and B = A + NPAIR (lanes 32-63)
+            const int iA = PAIRS * wave + jj, iB = iA + NPAIR;
+            const uint64_t ld_ok = (iA < rem ? 0x00000000FFFFFFFFull : 0ull) | (iB < rem ? 0xFFFFFFFF00000000ull : 0ull);
+            const uint64_t lx_ok = (((xin >> iA) & 1ull) ? 0x00000000FFFFFFFFull : 0ull) |
+                                   (((xin >> iB) & 1ull) ? 0xFFFFFFFF00000000ull : 0ull);
             const uint32_t mj = (uint32_t)(mA0 + jj);  // wraps harmlessly where masked off
-            o_dy[jj] = lane_select(ld_ok[jj] & dyok_lanes, oob, mj * (uint32_t)K * 2u + ldy);
-            o_x[jj] = lane_select(lx_ok[jj], oob, (mj * (uint32_t)C + (uint32_t)x_shift) * 2u + lx);
+            o_dy[jj] = lane_select(ld_ok & dyok_lanes, oob, mj * (uint32_t)K * 2u + ldy);
+            o_x[jj] = lane_select(lx_ok, oob, (mj * (uint32_t)C + (uint32_t)x_shift) * 2u + lx);
         }
     };
     auto table = [&](int st_i) {
-        if (lin)
-            table_linear(st_i);
-        else
+        if constexpr (LIN) {
+            table_linear_mask(st_i);
+            table_linear_select(st_i);
+        } else {
             table_general(st_i);
+        }
+    };
+    // The table of stage Y is needed when Y is issued, two steps before the end of stage
+    // Y - STAGES, and may be built once stage Y-1 has been issued.  In stage `it` the
+    // linear table of stage it+STAGES+1 starts in the last step (the mask pass) and that of
+    // stage it+STAGES is finished in the first step (the selects); with two steps per stage
+    // all of it in the last step.  The general table is built whole in the last step.
+    constexpr int NSTEP = PIXR / 16;
+    auto table_part = [&](int it, int u) {
+        if constexpr (LIN) {
+            if (NSTEP == 2) {
+                if (u == 1) table(it + STAGES + 1);
+            } else {
+                if (u == NSTEP - 1) table_linear_mask(it + STAGES + 1);
+                if (u == 0) table_linear_select(it + STAGES);
+            }
+        } else {
+            if (u == NSTEP - 1) table_general(it + STAGES + 1);
+        }
     };
     int islot = 0;  // ring slot of the next stage to issue
     auto issue = [&](int) {
@@ -510,51 +529,96 @@ __global__ __launch_bounds__(512, 1) void wgrad_rows_kernel(const WgradDmaArgs k
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][t][v] = 0.0f;
 
-    // with PF every issue() is followed by one prefetch; a stage's copies are complete once
-    // at most the copies (and prefetches) issued after them are outstanding
+    // Pipeline: every ring slot is filled in the prologue; stage `it` is multiplied step by
+    // step with the operands of each step read two steps earlier.  Two steps before the end
+    // of stage `it` a barrier certifies that every wave is done reading stage `it` (the
+    // operands of its last two steps are already in registers) and that stage it+1 has
+    // landed; the copies of stage it + STAGES then go into stage it's slot, and the last
+    // two steps' MFMAs overlap the copies and the reads of stage it+1's first two steps.
+    // So no wave waits on LDS reads at a stage boundary, and every read has a whole step
+    // of MFMAs to complete.  With PF every issue() is followed by one prefetch; a stage's
+    // copies are complete once at most the copies (and prefetches) issued after them are
+    // outstanding.
 #pragma unroll
-    for (int c = 0; c < STAGES - 1; ++c) {
+    for (int c = 0; c < STAGES; ++c) {
         table(c);
         if (c < nst) {
             issue(c);
             if constexpr (PF) prefetch(c + pf_dist);
         }
     }
-    table(STAGES - 1);
+    table(STAGES);
+    // wait until stage x's copies landed, with the copies of the `later` stages issued after
+    // it (stages x+1 .. x+later) still allowed in flight; where fewer than that were issued
+    // (the last stages), wait for everything
+    auto wait_stage = [&](int x, auto later_c) {
+        constexpr int later = decltype(later_c)::value;
+        if (x + later < nst)
+            wait_vmcnt(PF ? later * (kDmas + 1) + 1 : later * kDmas);
+        else
+            wait_vmcnt(0);
+    };
+    // in the order the MFMAs use them (row 0 with every column first), so that the first
+    // MFMAs of a step wait only for the reads issued earliest
+    auto load = [&](int sl, int u, bf16x8* af, bf16x8* bf) {
+        af[0] = operand(ra[sl][u]);
+#pragma unroll
+        for (int t = 0; t < TN; ++t) bf[t] = operand(rb[sl][u] + (uint32_t)(64 * t));
+#pragma unroll
+        for (int i = 1; i < TM; ++i) af[i] = operand(ra[sl][u] + (uint32_t)(64 * i));
+    };
+    bf16x8 af[TM], bf[TN];    // operands of the next step to multiply
+    bf16x8 af1[TM], bf1[TN];  // ... and of the step after it
+    if (nst > 0) {
+        wait_stage(0, std::integral_constant<int, STAGES - 1>{});  // stages 0 .. STAGES-1 issued
+        __syncthreads();
+        load(0, 0, af, bf);
+        load(0, 1, af1, bf1);
+    }
     // one stage, in ring slot SL (a compile-time constant: the loop below is unrolled over
     // the ring)
     auto stage = [&](int it, auto slot) {
         constexpr int SL = decltype(slot)::value;
-        // this wave's DMAs of stage `it` landed (later stages and the prefetch issued with
-        // stage `it` may still be in flight; in the last stages simply everything)
-        if (it + STAGES - 2 < nst)
-            wait_vmcnt(PF ? (STAGES - 2) * (kDmas + 1) + 1 : (STAGES - 2) * kDmas);
-        else
-            wait_vmcnt(0);
-        __syncthreads();  // ... and every other wave's; all reads of stage it-1 are done
-        if (it + STAGES - 1 < nst) {
-            issue(it + STAGES - 1);  // into stage it-1's buffer
-            if constexpr (PF) prefetch(it + STAGES - 1 + pf_dist);
-            table(it + STAGES);      // the offsets of the next copy, during the MFMAs
-        }
-        bf16x8 af[2][TM], bf[2][TN];
-        auto load = [&](int u, int b) {
+        constexpr int SN = SL + 1 == STAGES ? 0 : SL + 1;
 #pragma unroll
-            for (int i = 0; i < TM; ++i) af[b][i] = operand(ra[SL][u] + (uint32_t)(64 * i));
-#pragma unroll
-            for (int t = 0; t < TN; ++t) bf[b][t] = operand(rb[SL][u] + (uint32_t)(64 * t));
-        };
-        load(0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int u = 0; u < NU; ++u) {
-            if (u + 1 < NU) load(u + 1, (u + 1) & 1);
+        for (int u = 0; u < NSTEP; ++u) {
+            bf16x8 naf[TM], nbf[TN];  // operands of step u + 2
+            if (u + 2 < NSTEP) {
+                load(SL, u + 2, naf, nbf);
+            } else {
+                if (u + 2 == NSTEP) {
+                    // stage it+1 landed (this wave's copies, then every wave's) and every
+                    // wave is done reading stage it
+                    wait_stage(it + 1, std::integral_constant<int, STAGES - 2>{});  // 0 .. it+STAGES-1 issued
+                    __syncthreads();
+                }
+                load(SN, u + 2 - NSTEP, naf, nbf);  // unused after the last stage
+            }
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(af[u & 1][i], bf[u & 1][t], acc[i][t]);
-            if (u + 1 < NU) interleave_reads();
+                for (int t = 0; t < TN; ++t) acc[i][t] = mfma32(af[i], bf[t], acc[i][t]);
+            // the copies of stage it + STAGES into stage it's slot, behind the MFMAs of the
+            // step that follows the barrier
+            if (u + 2 == NSTEP && it + STAGES < nst) {
+                issue(it + STAGES);
+                if constexpr (PF) prefetch(it + STAGES + pf_dist);
+            }
+            // copy offsets between the MFMAs (harmless past the last stage: nothing issues
+            // them)
+            table_part(it, u);
+            interleave_reads();
             __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                af[i] = af1[i];
+                af1[i] = naf[i];
+            }
+#pragma unroll
+            for (int t = 0; t < TN; ++t) {
+                bf[t] = bf1[t];
+                bf1[t] = nbf[t];
+            }
         }
     };
     for (int it = 0; it < nst; it += STAGES) {
@@ -611,6 +675,20 @@ WgradDmaPlan wgrad_dma_plan(int K, int J) {
     return p;
 }
 
+template <bool LIN>
+static void launch_rows(int pix, bool pf, dim3 grid, const WgradDmaArgs& ka, hipStream_t stream) {
+    switch (pix) {
+        case 32: hipLaunchKernelGGL((wgrad_rows_kernel<32, 4, false, LIN>), grid, dim3(512), 0, stream, ka); break;
+        case 64: hipLaunchKernelGGL((wgrad_rows_kernel<64, 2, false, LIN>), grid, dim3(512), 0, stream, ka); break;
+        default:
+            if (pf)
+                hipLaunchKernelGGL((wgrad_rows_kernel<48, 3, true, LIN>), grid, dim3(512), 0, stream, ka);
+            else
+                hipLaunchKernelGGL((wgrad_rows_kernel<48, 3, false, LIN>), grid, dim3(512), 0, stream, ka);
+            break;
+    }
+}
+
 hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream) {
     WgradDmaArgs ka;
     ka.a = a;
@@ -624,16 +702,13 @@ hipError_t launch_wgrad_dma(const WgradArgs& a, hipStream_t stream) {
     const WgradDmaPlan p = wgrad_dma_plan(a.K, a.R * a.S * a.C);
     const dim3 grid((unsigned)(p.tiles * a.splits));
     if (p.cfg == 1) {
-        switch (p.pix) {
-            case 32: hipLaunchKernelGGL((wgrad_rows_kernel<32, 4, false>), grid, dim3(512), 0, stream, ka); break;
-            case 64: hipLaunchKernelGGL((wgrad_rows_kernel<64, 2, false>), grid, dim3(512), 0, stream, ka); break;
-            default:
-                if (ka.pf_dist > 0)
-                    hipLaunchKernelGGL((wgrad_rows_kernel<48, 3, true>), grid, dim3(512), 0, stream, ka);
-                else
-                    hipLaunchKernelGGL((wgrad_rows_kernel<48, 3, false>), grid, dim3(512), 0, stream, ka);
-                break;
-        }
+        // linear copy addressing: stride 1, output the input's size, whole 256-column
+        // blocks of one tap
+        const bool lin = a.sh == 1 && a.sw == 1 && a.P == a.H && a.Q == a.W && a.C % 256 == 0;
+        if (lin)
+            launch_rows<true>(p.pix, ka.pf_dist > 0, grid, ka, stream);
+        else
+            launch_rows<false>(p.pix, ka.pf_dist > 0, grid, ka, stream);
     } else {
         hipLaunchKernelGGL(wgrad_seg_kernel, grid, dim3(512), 0, stream, ka);
     }
