@@ -282,12 +282,15 @@ def resnet18_fwd(dev, steps=10, warmup=3):
         torch.cuda.synchronize()
         graph.replay()
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        graph.replay()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) / steps * 1e3
+        reps = []  # median of five timed replays
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            graph.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            reps.append(e0.elapsed_time(e1) / steps * 1e3)
+        us = float(np.median(reps))
         del graph
         n, h, w, c = inp.shape
         fl = 2.0 * n * h * w * layer.cout * 9 * c

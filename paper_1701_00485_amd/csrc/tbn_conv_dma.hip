@@ -723,9 +723,9 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
     int bm, bn;
     if (p.cfg < 10) {
         // 65..128 filters: 128 x 128 tiles with one wave per 32 filters (each wave decodes
-        // only its own filters) and a four-deep ring, measured ~4-8% faster than two waves
-        // per 64 filters on the ResNet-18 layer-2 shapes
-        p.cfg = a.Kf > 128 ? 10 : (a.Kf > 64 ? 13 : 14);
+        // only its own filters), measured ~4-8% faster than two waves per 64 filters on the
+        // ResNet-18 layer-2 shapes, and a three-deep ring (there 4-8% faster than four deep)
+        p.cfg = a.Kf > 128 ? 10 : (a.Kf > 64 ? 11 : 14);
         cfg_tile(p.cfg, &bm, &bn);
         // too few tiles for one wave of blocks: shorter tiles (64 pixels x 128 filters, a
         // four-deep ring) when there are at least 128 filters, else 128 x 64; then split
