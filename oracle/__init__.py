@@ -69,6 +69,16 @@ def _load():
     lib.orc_conv_fwd_i8.restype = ctypes.c_int
     lib.orc_conv_fwd_i8_sampled.argtypes = [p, p, p, p, ctypes.c_float, ctypes.c_int, p, i64, p]
     lib.orc_conv_fwd_i8_sampled.restype = ctypes.c_int
+    lib.orc_fp8_value.argtypes = [ctypes.c_uint8]
+    lib.orc_fp8_value.restype = ctypes.c_double
+    lib.orc_fp8_encode.argtypes = [ctypes.c_float]
+    lib.orc_fp8_encode.restype = ctypes.c_uint8
+    lib.orc_quantize_act_fp8.argtypes = [p, i64, ctypes.c_float, p]
+    lib.orc_quantize_act_fp8.restype = None
+    lib.orc_conv_fwd_fp8.argtypes = [p, p, p, p, ctypes.c_float, ctypes.c_int, p]
+    lib.orc_conv_fwd_fp8.restype = ctypes.c_int
+    lib.orc_conv_fwd_fp8_sampled.argtypes = [p, p, p, p, ctypes.c_float, ctypes.c_int, p, i64, p]
+    lib.orc_conv_fwd_fp8_sampled.restype = ctypes.c_int
     lib.orc_conv_bwd_data.argtypes = [p, p, p, p, p]
     lib.orc_conv_bwd_data.restype = ctypes.c_int
     lib.orc_conv_bwd_weight.argtypes = [p, p, p, p]
@@ -330,6 +340,65 @@ def conv_fwd_i8_sampled(desc: ConvDesc, xq: np.ndarray, codes: np.ndarray, alpha
                                        float(np.float32(x_scale)), 1 if relu else 0, _ptr(idx), idx.size,
                                        _ptr(y)) != 0:
         raise OracleError("conv_fwd_i8_sampled: index out of range")
+    return y
+
+
+# --------------------------------------------------------------------------------------
+# fp8-activation variant of Eq. (1): the input replaced by s * f, f an E4M3 value (an
+# extension)
+# --------------------------------------------------------------------------------------
+def fp8_value(codes: np.ndarray) -> np.ndarray:
+    """float64 value of every E4M3 code (uint8 array); NaN for 0x7F and 0xFF."""
+    codes = np.asarray(codes, np.uint8)
+    lib = _load()
+    table = np.array([lib.orc_fp8_value(c) for c in range(256)], np.float64)
+    return table[codes]
+
+
+def fp8_encode_one(v) -> int:
+    """The E4M3 code of one fp32 value (nearest, ties to the even code, saturating at 448)."""
+    return int(_load().orc_fp8_encode(float(np.float32(v))))
+
+
+def quantize_act_fp8(x: np.ndarray, inv_scale) -> np.ndarray:
+    """codes = E4M3(fp32(x * inv_scale)), nearest with ties to even, saturating, NaN -> 0."""
+    x = _c(x, np.float32)
+    q = np.zeros(x.shape, np.uint8)
+    _load().orc_quantize_act_fp8(_ptr(x), x.size, float(np.float32(inv_scale)), _ptr(q))
+    return q
+
+
+def conv_fwd_fp8(desc: ConvDesc, xq: np.ndarray, codes: np.ndarray, alpha: np.ndarray, x_scale,
+                 relu: bool = False) -> np.ndarray:
+    """Forward pass on E4M3 activation codes: y = alpha_k * x_scale * sum f * W~ in fp64
+    (NHWC), then max(., 0) when relu."""
+    P, Q = desc.out_dims()
+    xq = _c(xq, np.uint8)
+    codes = _c(codes, np.int8)
+    alpha = _c(alpha, np.float32)
+    if xq.size != desc.n * desc.h * desc.w * desc.c or codes.size != desc.k * desc.r * desc.s * desc.c:
+        raise OracleError("conv_fwd_fp8: operand sizes do not match the geometry")
+    y = np.zeros((desc.n, P, Q, desc.k), np.float64)
+    if _load().orc_conv_fwd_fp8(_ptr(desc.as_array()), _ptr(xq), _ptr(codes), _ptr(alpha),
+                                float(np.float32(x_scale)), 1 if relu else 0, _ptr(y)) != 0:
+        raise OracleError("conv_fwd_fp8 failed")
+    return y
+
+
+def conv_fwd_fp8_sampled(desc: ConvDesc, xq: np.ndarray, codes: np.ndarray, alpha: np.ndarray, x_scale,
+                         idx: np.ndarray, relu: bool = False) -> np.ndarray:
+    """conv_fwd_fp8's y at flat output indices idx (into [N][P][Q][K]), fp64."""
+    xq = _c(xq, np.uint8)
+    codes = _c(codes, np.int8)
+    alpha = _c(alpha, np.float32)
+    idx = _c(idx, np.int64)
+    if xq.size != desc.n * desc.h * desc.w * desc.c or codes.size != desc.k * desc.r * desc.s * desc.c:
+        raise OracleError("conv_fwd_fp8_sampled: operand sizes do not match the geometry")
+    y = np.zeros(idx.size, np.float64)
+    if _load().orc_conv_fwd_fp8_sampled(_ptr(desc.as_array()), _ptr(xq), _ptr(codes), _ptr(alpha),
+                                        float(np.float32(x_scale)), 1 if relu else 0, _ptr(idx), idx.size,
+                                        _ptr(y)) != 0:
+        raise OracleError("conv_fwd_fp8_sampled failed")
     return y
 
 

@@ -19,6 +19,8 @@
  *   - SGD with momentum and weight decay  : Sec. 4 (training set-up)
  *   - integer-activation forward variant  : Eq. (1) with the input replaced by int8 codes
  *     times one scale (an extension; see orc_conv_fwd_i8)
+ *   - fp8-activation forward variant      : the same with E4M3 fp8 activation values (an
+ *     extension; see orc_conv_fwd_fp8)
  * The 2-bit packed layout is this project's own storage format (the paper only says the
  * four values fit in two bits, abstract and Sec. 1); its definition is restated next to
  * the packer below.
@@ -446,6 +448,124 @@ int orc_conv_fwd_i8_sampled(const int32_t* d, const int8_t* xq, const int8_t* co
         const float scale = alpha[k] * s;
         float v = (float)acc * scale;
         if (relu && !(v > 0.0f)) v = 0.0f;
+        y[i] = v;
+    }
+    return ORC_OK;
+}
+
+/*
+ * Eight-bit floating-point activation variant (an extension of the same kind as the int8
+ * one above): the input I of Eq. (1) is replaced by s * f with f an fp8 value in the E4M3
+ * format and the two-bit filter values used as they are (+-1 and +-2 are exact in any
+ * binary floating-point format with a 1-bit fraction, e.g. the 4-bit E2M1 one).
+ *
+ * E4M3 (the "fn" variant: no infinities): bit 7 sign, bits 6..3 exponent field e with bias
+ * 7, bits 2..0 fraction m.  e = 0: (-1)^sign * (m / 8) * 2^-6 (zero and subnormals);
+ * e = 1..15: (-1)^sign * (1 + m / 8) * 2^(e - 7), except the two codes with e = 15, m = 7
+ * (0x7F, 0xFF), which are NaN.  The largest finite magnitude is 1.75 * 2^8 = 448.
+ */
+double orc_fp8_value(uint8_t code) {
+    const int sign = code >> 7, e = (code >> 3) & 15, m = code & 7;
+    if (e == 15 && m == 7) return NAN;
+    const double mag = e == 0 ? ldexp(m / 8.0, -6) : ldexp(1.0 + m / 8.0, e - 7);
+    return sign ? -mag : mag;
+}
+
+/*
+ * Activation code of one value: v = x * inv in fp32 (inv = the caller's fp32 reciprocal of
+ * s), then the finite E4M3 value nearest to v, found by comparing v with every finite
+ * non-negative code (ties: the code with an even last fraction bit, i.e. the even code);
+ * |v| > 448 takes +-448 (saturation); the sign bit is the sign bit of v (so -0 and small
+ * negative values that round to zero keep it); a NaN gets code 0.
+ */
+uint8_t orc_fp8_encode(float v) {
+    if (isnan(v)) return 0;
+    const uint8_t sign = signbit(v) ? 0x80 : 0x00;
+    const double a = fabs((double)v);
+    if (a > 448.0) return sign | 0x7E;
+    int best = 0;
+    double best_d = INFINITY;
+    for (int c = 0; c < 0x7F; ++c) { /* 0x00 .. 0x7E: every finite non-negative code */
+        const double dist = fabs(orc_fp8_value((uint8_t)c) - a);
+        if (dist < best_d || (dist == best_d && (c & 1) == 0)) {
+            best_d = dist;
+            best = c;
+        }
+    }
+    return sign | (uint8_t)best;
+}
+
+void orc_quantize_act_fp8(const float* x, int64_t count, float inv, uint8_t* q) {
+    for (int64_t i = 0; i < count; ++i) q[i] = orc_fp8_encode(x[i] * inv); /* one fp32 rounding */
+}
+
+/*
+ * Forward pass on fp8 activation codes (Eq. 1 with I = s f):
+ *   y[n,p,q,k] = alpha_k * s * sum_{r,s,c} f[n, p*sh-ph+r, q*sw-pw+s, c] * W~[k,r,s,c]
+ * (zero padding), in double precision: every product is exact and so is the sum (the terms
+ * are multiples of 2^-9 below 2^10 in magnitude), then the two scales; max(y, 0) when
+ * relu != 0.  A NaN activation code makes its outputs NaN.
+ */
+int orc_conv_fwd_fp8(const int32_t* d, const uint8_t* xq, const int8_t* codes, const float* alpha, float s,
+                     int relu, double* y) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t N = d[DN], H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t nn = 0; nn < N; ++nn) {
+        for (int64_t p = 0; p < P; ++p) {
+            for (int64_t q = 0; q < Q; ++q) {
+                for (int64_t k = 0; k < K; ++k) {
+                    double acc = 0.0;
+                    for (int64_t r = 0; r < R; ++r) {
+                        const int64_t h = p * sh - ph + r;
+                        if (h < 0 || h >= H) continue;
+                        for (int64_t t = 0; t < S; ++t) {
+                            const int64_t w = q * sw - pw + t;
+                            if (w < 0 || w >= W) continue;
+                            const uint8_t* xp = xq + ((nn * H + h) * W + w) * C;
+                            const int8_t* cp = codes + ((k * R + r) * S + t) * C;
+                            for (int64_t c = 0; c < C; ++c) acc += orc_fp8_value(xp[c]) * (double)cp[c];
+                        }
+                    }
+                    double v = acc * (double)alpha[k] * (double)s;
+                    if (relu && !(v > 0.0)) v = 0.0;
+                    y[((nn * P + p) * Q + q) * K + k] = v;
+                }
+            }
+        }
+    }
+    return ORC_OK;
+}
+
+/* The same at `count` flat output indices idx (into [N][P][Q][K]); y[i] for idx[i]. */
+int orc_conv_fwd_fp8_sampled(const int32_t* d, const uint8_t* xq, const int8_t* codes, const float* alpha, float s,
+                             int relu, const int64_t* idx, int64_t count, double* y) {
+    int32_t P, Q;
+    if (orc_out_dims(d, &P, &Q) != ORC_OK) return ORC_ERR_SHAPE;
+    const int64_t N = d[DN], H = d[DH], W = d[DW], C = d[DC], K = d[DK], R = d[DR], S = d[DS];
+    const int64_t sh = d[DSH], sw = d[DSW], ph = d[DPH], pw = d[DPW];
+    for (int64_t i = 0; i < count; ++i)
+        if (idx[i] < 0 || idx[i] >= N * P * Q * K) return ORC_ERR_SHAPE;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < count; ++i) {
+        const int64_t o = idx[i];
+        const int64_t k = o % K, q = (o / K) % Q, p = (o / (K * Q)) % P, nn = o / (K * Q * P);
+        double acc = 0.0;
+        for (int64_t r = 0; r < R; ++r) {
+            const int64_t h = p * sh - ph + r;
+            if (h < 0 || h >= H) continue;
+            for (int64_t t = 0; t < S; ++t) {
+                const int64_t w = q * sw - pw + t;
+                if (w < 0 || w >= W) continue;
+                const uint8_t* xp = xq + ((nn * H + h) * W + w) * C;
+                const int8_t* cp = codes + ((k * R + r) * S + t) * C;
+                for (int64_t c = 0; c < C; ++c) acc += orc_fp8_value(xp[c]) * (double)cp[c];
+            }
+        }
+        double v = acc * (double)alpha[k] * (double)s;
+        if (relu && !(v > 0.0)) v = 0.0;
         y[i] = v;
     }
     return ORC_OK;
