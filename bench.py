@@ -29,6 +29,7 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 PEAK_INT8_TOPS = 5000.0     # MI355X dense int8 MFMA
+PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 
 LAYER = dict(n=128, h=56, w=56, c=256, k=256, r=3, s=3, stride=1, pad=1)
 LR, MOMENTUM, WD = 0.1, 0.9, 1e-4
@@ -49,7 +50,7 @@ def parse():
                     help="budget of the oracle's training-step sample")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain device copy of known size (HBM counter calibration)")
-    ap.add_argument("--only", choices=["resnet", "single", "lenet", "vgg", "ws", "int8", "fused"],
+    ap.add_argument("--only", choices=["resnet", "single", "lenet", "vgg", "ws", "int8", "fp8", "fused"],
                     help="profiling aid: run just this workload (no training step, no contract line)")
     return ap.parse_args()
 
@@ -541,6 +542,54 @@ def int8_forward(dev, desc, x, codes, alpha, conv_flops, reps=20):
     }
 
 
+def fp8_forward(dev, desc, x, codes, alpha, conv_flops, reps=20):
+    """The fp8-activation variant of the forward pass on the training layer: E4M3 activation
+    codes (2 B read + 1 B written per activation) and the forward pass on the scaled fp8 x
+    fp4 matrix cores, timed with HIP events on the stream they run on.  The activation scale
+    is fixed once from max|x| and the filter codes are repacked into the E2M1 layout once
+    (calibration and a once-per-weight-update step, outside the timed region)."""
+    import torch
+
+    import paper_1701_00485_amd as tbn
+
+    stream = torch.cuda.current_stream()
+    amax = float(x.float().abs().max())
+    x_scale = amax / 448.0
+    xq = torch.empty(x.shape, dtype=torch.uint8, device=dev)
+    f4 = tbn.repack_codes_fp4(codes)
+    P, Q = desc.out_dims()
+    y = torch.empty((desc.n, P, Q, desc.k), dtype=torch.bfloat16, device=dev)
+
+    def quant():
+        tbn.quantize_act_fp8(x, 448.0 / amax, q=xq)
+
+    def conv():
+        tbn.conv2d_fwd_fp8(desc, xq, f4, alpha, x_scale, y=y)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    us_q = timed(quant)
+    us_c = timed(conv)
+    tf = conv_flops / (us_c * 1e-6) / 1e12
+    gbs = 3.0 * x.numel() / (us_q * 1e-6) / 1e9
+    return {
+        "shape": "conv3x3 256->256 ch, 56x56, pad 1, batch 128; E4M3 activations x E2M1 two-bit codes, bf16 output",
+        "act_quantize": {"us": round(us_q, 2), "achieved_GBs": round(gbs, 1), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)},
+        "conv_fwd_fp8": {"us": round(us_c, 2), "achieved_TFLOPS": round(tf, 1), "peak_TFLOPS": PEAK_FP8_TFLOPS,
+                         "frac": round(tf / PEAK_FP8_TFLOPS, 4)},
+    }
+
+
 def _only(section, dev):
     """One workload alone (for kernel traces and counters of that workload)."""
     if section == "resnet":
@@ -561,6 +610,8 @@ def _only(section, dev):
     x = torch.from_numpy(synth.normal_bf16(5, "x", (L["n"], L["h"], L["w"], L["c"])).view(np.int16)).to(dev)
     w = torch.from_numpy(synth.normal(5, "w", (L["k"], L["r"] * L["s"] * L["c"]), 0.05)).to(dev)
     codes, alpha, _ = tbn.quantize(w, want_counts=False)
+    if section == "fp8":
+        return fp8_forward(dev, desc, x.view(torch.bfloat16), codes, alpha, conv_flops)
     return int8_forward(dev, desc, x.view(torch.bfloat16), codes, alpha, conv_flops)
 
 
@@ -692,6 +743,8 @@ def main():
     }
     result["int8_forward"] = int8_forward(dev, desc, x, codes, alpha, conv_flops)
     result["int8_forward"]["bf16_fwd_us"] = round(per_kernel["fwd"] * 1e3, 2)
+    result["fp8_forward"] = fp8_forward(dev, desc, x, codes, alpha, conv_flops)
+    result["fp8_forward"]["bf16_fwd_us"] = round(per_kernel["fwd"] * 1e3, 2)
     if not args.no_resnet:
         result["resnet18_fwd"] = resnet18_fwd(dev)
     if not args.no_small:

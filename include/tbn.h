@@ -202,6 +202,43 @@ tbn_status tbn_conv2d_fwd_i8(const tbn_conv_desc* desc, const int8_t* x, const u
                              float x_scale, int32_t relu, void* y, tbn_dtype yt, hipStream_t stream);
 
 /*
+ * Eight-bit floating-point activation variant of the forward pass (an extension of Sec. 2
+ * Eq. 1 of the same kind as the int8 one): the input I is represented as s * f with f an
+ * E4M3 value, and the layer runs on the scaled fp8 x fp4 matrix cores, where the filter
+ * values +-1 and +-2 are exact 4-bit E2M1 values and every product f * W~ is exact.
+ *
+ * tbn_quantize_act_fp8: activation codes f = E4M3(x * inv_scale), the product rounded to
+ *   fp32 first, then the nearest finite E4M3 value (ties to the even code), |value| > 448
+ *   saturating to +-448; the sign bit is kept for -0 and for values that round to zero; a
+ *   NaN input gets code 0.  E4M3: bit 7 sign, bits 6-3 exponent (bias 7, 0 = subnormal),
+ *   bits 2-0 fraction, no infinities, 0x7F and 0xFF NaN.  x: `count` elements of dtype xt
+ *   (elementwise); q: `count` bytes.  inv_scale finite and > 0 (typically 448 / max|x|),
+ *   else TBN_ERR_SHAPE.
+ *
+ * tbn_repack_codes_fp4: rewrites TBN2 packed codes (`words` 32-bit words, any number of
+ *   filters) into the E2M1 operand layout that tbn_conv2d_fwd_fp8 reads: the same 16 bytes
+ *   per filter and 64-element chunk, but word q of a chunk holds its elements 16 q + 8 r + j
+ *   (r = 0, 1; j = 0..7) as magnitude bit 4 j + 1 - r and sign bit 4 j + 3 - r.  Done once
+ *   per set of filters (after each quantisation); codes and out must not overlap.
+ *
+ * tbn_conv2d_fwd_fp8: y[n,p,q,k] = act(acc * fp32(alpha_k * x_scale)) with
+ *   acc = sum_{r,s,c} f[n, p*sh-ph+r, q*sw-pw+s, c] * W~[k,r,s,c] (zero padding), each
+ *   product exact and the sum in fp32 (order unspecified); relu != 0 applies max(., 0).
+ *   x      NHWC [N][H][W][C] E4M3 codes (for example from tbn_quantize_act_fp8); x_scale =
+ *          the s with x ~ s * f (1 / inv_scale), finite.
+ *   codes  the K filters' codes (n = R*S*C) in the E2M1 layout of tbn_repack_codes_fp4;
+ *          alpha [K] fp32.
+ *   y      NHWC [N][P][Q][K], dtype yt (bf16 rounded to nearest even, or fp32).
+ *   Needs C % 16 == 0, R*S <= 63 and x and the codes below 2 GiB; TBN_ERR_UNSUPPORTED
+ *   otherwise.  No workspace.
+ */
+tbn_status tbn_quantize_act_fp8(const void* x, tbn_dtype xt, int64_t count, float inv_scale, uint8_t* q,
+                                hipStream_t stream);
+tbn_status tbn_repack_codes_fp4(const uint32_t* codes, int64_t words, uint32_t* out, hipStream_t stream);
+tbn_status tbn_conv2d_fwd_fp8(const tbn_conv_desc* desc, const uint8_t* x, const uint32_t* codes, const float* alpha,
+                              float x_scale, int32_t relu, void* y, tbn_dtype yt, hipStream_t stream);
+
+/*
  * Forward pass of a layer kept in full precision (Eq. 1 with the real filters; the first
  * convolution of the CIFAR-shaped network stays unquantised):
  *   y[n,p,q,k] = sum_{r,s,c} x[n, p*sh-ph+r, q*sw-pw+s, c] * bf16(w[k,r,s,c]),

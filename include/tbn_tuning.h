@@ -36,10 +36,13 @@ typedef enum tbn_knob {
     TBN_KNOB_WGRAD_PF = 4,
     /* int8-activation forward tile: 1 128x256, 2 128x128, 3 128x64, 4 64x128 */
     TBN_KNOB_I8_TILE = 5,
-    /* weight-streaming forward: code loads in flight per wave (0 = 4 buffers of 2 loads of
-     * 16 bytes per lane, 1 = 2 x 4, 2 = 2 x 8, 3 = 3 x 4) */
+    /* weight-streaming forward: 0-7 select (16-byte code loads per buffer, buffers in flight
+     * per wave, groups of four waves per block) = (2,4,1) (4,2,1) (8,2,1) (4,3,1) (2,4,2)
+     * (4,2,2) (2,2,4) (2,3,2) */
     TBN_KNOB_FC_VARIANT = 6,
-    TBN_KNOB_COUNT = 7
+    /* fp8-activation forward tile: 1 128x256, 2 128x128, 3 128x64, 4 64x128 */
+    TBN_KNOB_FP8_TILE = 7,
+    TBN_KNOB_COUNT = 8
 } tbn_knob;
 
 /* Set a knob (value -1 restores the built-in choice).  TBN_ERR_SHAPE for an unknown knob. */

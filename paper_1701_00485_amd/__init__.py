@@ -85,6 +85,9 @@ def load():
         "tbn_conv2d_fwd_dense": ([vp, vp, i32, vp, vp, vp, i32, vp], i32),
         "tbn_quantize_act_i8": ([vp, i32, i64, f32, vp, vp], i32),
         "tbn_conv2d_fwd_i8": ([vp, vp, vp, vp, f32, i32, vp, i32, vp], i32),
+        "tbn_quantize_act_fp8": ([vp, i32, i64, f32, vp, vp], i32),
+        "tbn_repack_codes_fp4": ([vp, i64, vp, vp], i32),
+        "tbn_conv2d_fwd_fp8": ([vp, vp, vp, vp, f32, i32, vp, i32, vp], i32),
         "tbn_conv2d_bwd_data": ([vp, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_conv2d_bwd_weight": ([vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp], i32),
         "tbn_sgd_step": ([vp, vp, vp, i64, f32, f32, f32, vp], i32),
@@ -116,6 +119,7 @@ def exported_symbols():
                    "tbn_packed_row_words", "tbn_packed_bytes",
                    "tbn_workspace_size", "tbn_quantize", "tbn_quantize_variant", "tbn_conv2d_fwd", "tbn_conv2d_fwd_dense",
                    "tbn_quantize_act_i8", "tbn_conv2d_fwd_i8",
+                   "tbn_quantize_act_fp8", "tbn_repack_codes_fp4", "tbn_conv2d_fwd_fp8",
                    "tbn_conv2d_bwd_data",
                    "tbn_conv2d_bwd_weight", "tbn_sgd_step", "tbn_sgd_step_quantize", "tbn_pool_out_dims", "tbn_maxpool2d_fwd",
                    "tbn_maxpool2d_bwd", "tbn_avgpool_global", "tbn_batchnorm_workspace_size",
@@ -126,7 +130,7 @@ def exported_symbols():
 # Test and tuning knobs of include/tbn_tuning.h (names -> tbn_knob values).  Production code
 # leaves them unset; the parity tests force every kernel variant through them.
 KNOBS = {"conv_tile": 0, "conv_splits": 1, "wgrad_cfg": 2, "wgrad_pix": 3, "wgrad_pf": 4, "i8_tile": 5,
-         "fc_variant": 6}
+         "fc_variant": 6, "fp8_tile": 7}
 
 
 def tuning_get(name: str) -> int:
@@ -352,6 +356,44 @@ def conv2d_fwd_i8(desc: ConvDesc, xq, codes, alpha, x_scale: float, y=None, out_
     _call("tbn_conv2d_fwd_i8", ctypes.byref(desc), _dev(xq, "xq", (torch.int8,)), _dev(codes, "codes", (torch.int32,)),
           _dev(alpha, "alpha", (torch.float32,)), float(x_scale), 1 if relu else 0,
           _dev(y, "y", (torch.bfloat16, torch.float32)), _dtype_code(y.dtype), _stream())
+    return y
+
+
+def quantize_act_fp8(x: torch.Tensor, inv_scale: float, q=None):
+    """E4M3 activation codes f = E4M3(x * inv_scale) (nearest, ties to even, saturating at
+    +-448, NaN -> 0), elementwise over a bf16 or fp32 tensor; returns the codes (uint8)."""
+    if q is None:
+        q = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    _numel(q, x.numel(), "q")
+    _call("tbn_quantize_act_fp8", _dev(x, "x", (torch.bfloat16, torch.float32)), _dtype_code(x.dtype), x.numel(),
+          float(inv_scale), _dev(q, "q", (torch.uint8,)), _stream())
+    return q
+
+
+def repack_codes_fp4(codes, out=None):
+    """The packed codes rewritten in the E2M1 operand layout of conv2d_fwd_fp8 (int32, same size)."""
+    if out is None:
+        out = torch.empty_like(codes)
+    _numel(out, codes.numel(), "out")
+    _call("tbn_repack_codes_fp4", _dev(codes, "codes", (torch.int32,)), codes.numel(),
+          _dev(out, "out", (torch.int32,)), _stream())
+    return out
+
+
+def conv2d_fwd_fp8(desc: ConvDesc, xq, codes_fp4, alpha, x_scale: float, y=None, out_dtype=torch.bfloat16,
+                   relu=False):
+    """Forward pass on E4M3 activation codes (scaled fp8 x fp4 matrix cores):
+    y = act((f conv W~) * float(alpha_k * x_scale)), NHWC; codes_fp4 from repack_codes_fp4."""
+    P, Q = desc.out_dims()
+    _numel(xq, desc.n * desc.h * desc.w * desc.c, "xq")
+    _numel(codes_fp4, packed_words(desc.k, desc.r * desc.s * desc.c), "codes")
+    _numel(alpha, desc.k, "alpha")
+    if y is None:
+        y = torch.empty((desc.n, P, Q, desc.k), dtype=out_dtype, device=xq.device)
+    _numel(y, desc.n * P * Q * desc.k, "y")
+    _call("tbn_conv2d_fwd_fp8", ctypes.byref(desc), _dev(xq, "xq", (torch.uint8,)),
+          _dev(codes_fp4, "codes", (torch.int32,)), _dev(alpha, "alpha", (torch.float32,)), float(x_scale),
+          1 if relu else 0, _dev(y, "y", (torch.bfloat16, torch.float32)), _dtype_code(y.dtype), _stream())
     return y
 
 

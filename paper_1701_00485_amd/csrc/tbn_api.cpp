@@ -551,6 +551,56 @@ tbn_status tbn_conv2d_fwd_i8(const tbn_conv_desc* desc, const int8_t* x, const u
     return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_fwd_i8");
 }
 
+tbn_status tbn_quantize_act_fp8(const void* x, tbn_dtype xt, int64_t count, float inv_scale, uint8_t* q,
+                                hipStream_t stream) {
+    if (!x || !q) return fail(TBN_ERR_NULL, "x and q are required");
+    if (count <= 0) return fail(TBN_ERR_SHAPE, "count must be positive");
+    if (count > ((int64_t)1 << 40)) return fail(TBN_ERR_SHAPE, "count too large");
+    if (xt != TBN_BF16 && xt != TBN_F32) return fail(TBN_ERR_UNSUPPORTED, "unknown dtype");
+    if (!(inv_scale > 0.0f) || inv_scale > 3.4028235e38f) return fail(TBN_ERR_SHAPE, "inv_scale must be finite and positive");
+    if (!aligned16(x) || !aligned16(q)) return fail(TBN_ERR_ALIGN, "x and q must be 16-byte aligned");
+    hipError_t e = tbn::launch_quantize_act_fp8(x, xt == TBN_F32 ? 1 : 0, count, inv_scale, q, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_quantize_act_fp8");
+}
+
+tbn_status tbn_repack_codes_fp4(const uint32_t* codes, int64_t words, uint32_t* out, hipStream_t stream) {
+    if (!codes || !out) return fail(TBN_ERR_NULL, "codes and out are required");
+    if (words <= 0 || words > ((int64_t)1 << 40)) return fail(TBN_ERR_SHAPE, "words must be positive");
+    if (!aligned4(codes) || !aligned4(out)) return fail(TBN_ERR_ALIGN, "codes and out must be 4-byte aligned");
+    const uintptr_t c0 = (uintptr_t)codes, o0 = (uintptr_t)out, nb = (uintptr_t)words * 4;
+    if (c0 < o0 + nb && o0 < c0 + nb) return fail(TBN_ERR_SHAPE, "codes and out overlap");
+    hipError_t e = tbn::launch_repack_fp4(codes, words, out, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_repack_codes_fp4");
+}
+
+tbn_status tbn_conv2d_fwd_fp8(const tbn_conv_desc* desc, const uint8_t* x, const uint32_t* codes, const float* alpha,
+                              float x_scale, int32_t relu, void* y, tbn_dtype yt, hipStream_t stream) {
+    Geometry g;
+    tbn_status st = check_desc(desc, &g);
+    if (st != TBN_OK) return st;
+    if (!x || !codes || !alpha || !y) return fail(TBN_ERR_NULL, "x, codes, alpha and y are required");
+    if (yt != TBN_BF16 && yt != TBN_F32) return fail(TBN_ERR_UNSUPPORTED, "unknown dtype");
+    if (!(x_scale == x_scale) || x_scale > 3.4028235e38f || x_scale < -3.4028235e38f)
+        return fail(TBN_ERR_SHAPE, "x_scale must be finite");
+    if (!aligned16(x) || !aligned16(codes) || !aligned16(y) || !aligned4(alpha))
+        return fail(TBN_ERR_ALIGN, "x, codes and y must be 16-byte aligned");
+    tbn::ConvFp8Args a = {};
+    a.x = x;
+    a.codes = codes;
+    a.alpha = alpha;
+    a.y = y;
+    a.x_scale = x_scale;
+    a.N = (int32_t)g.N; a.H = (int32_t)g.H; a.W = (int32_t)g.W; a.C = (int32_t)g.C; a.K = (int32_t)g.K;
+    a.R = (int32_t)g.R; a.S = (int32_t)g.S; a.sh = (int32_t)g.sh; a.sw = (int32_t)g.sw;
+    a.ph = (int32_t)g.ph; a.pw = (int32_t)g.pw; a.P = (int32_t)g.P; a.Q = (int32_t)g.Q;
+    a.relu = relu ? 1 : 0;
+    a.y_f32 = yt == TBN_F32 ? 1 : 0;
+    if (!tbn::conv_fp8_eligible(a))
+        return fail(TBN_ERR_UNSUPPORTED, "fp8 forward needs C % 16 == 0, R*S <= 63 and tensors < 2 GiB");
+    hipError_t e = tbn::launch_conv_fp8(a, stream);
+    return e == hipSuccess ? TBN_OK : hip_fail(e, "tbn_conv2d_fwd_fp8");
+}
+
 namespace {
 
 tbn_status check_pool(const tbn_pool_desc* d, tbn::PoolArgs* a) {

@@ -12,7 +12,7 @@ namespace tbn {
 
 // Test and tuning knobs (tbn_tuning.h); -1 = unset, the built-in choice.
 enum Knob { KNOB_CONV_TILE = 0, KNOB_CONV_SPLITS = 1, KNOB_WGRAD_CFG = 2, KNOB_WGRAD_PIX = 3, KNOB_WGRAD_PF = 4,
-            KNOB_I8_TILE = 5, KNOB_FC_VARIANT = 6 };
+            KNOB_I8_TILE = 5, KNOB_FC_VARIANT = 6, KNOB_FP8_TILE = 7 };
 int knob(int which);
 
 // Record the detail of an error for tbn_last_error() on this thread; returns s.
@@ -208,6 +208,31 @@ hipError_t launch_conv_i8(const ConvI8Args& a, hipStream_t stream);
 // q = clamp(round-half-even(x * inv), -127, 127), NaN -> 0; x bf16 or fp32.
 hipError_t launch_quantize_act_i8(const void* x, int x_f32, int64_t count, float inv, int8_t* q,
                                   hipStream_t stream);
+
+// Forward pass on E4M3 activation codes (scaled fp8 x E2M1 MFMA): y = act(sum f * W~ *
+// fp32(alpha_k * x_scale)), the sum fp32, NHWC, bf16 or fp32 output.  The filters in the
+// E2M1 operand layout (launch_repack_fp4).  Needs C % 16 == 0, R*S <= 63 and tensors below
+// 2 GiB (conv_fp8_eligible); no workspace.
+struct ConvFp8Args {
+    const uint8_t* x;         // NHWC [N][H][W][C] E4M3 codes
+    const uint32_t* codes;    // E2M1-layout codes of K filters of n = R*S*C elements
+    const float* alpha;       // [K]
+    void* y;                  // NHWC [N][P][Q][K]
+    float x_scale;
+    int32_t N, H, W, C, K, R, S, sh, sw, ph, pw, P, Q;
+    int32_t relu, y_f32;
+    FastDiv div_q, div_pq, div_tilesN;
+    uint32_t rep_lo, rep_hi;  // sum_{r < R} 2^(r*S)
+};
+bool conv_fp8_eligible(const ConvFp8Args& a);
+// Tile shape (1: 128 x 256, 2: 128 x 128, 3: 128 x 64, 4: 64 x 128); the fp8 tile knob forces one.
+int conv_fp8_tile(const ConvFp8Args& a);
+hipError_t launch_conv_fp8(const ConvFp8Args& a, hipStream_t stream);
+// q = E4M3(fp32(x * inv)): nearest, ties to even, saturating at +-448, NaN -> 0; x bf16 or fp32.
+hipError_t launch_quantize_act_fp8(const void* x, int x_f32, int64_t count, float inv, uint8_t* q,
+                                   hipStream_t stream);
+// The packed codes (`words` 32-bit words) rewritten in the E2M1 operand layout.
+hipError_t launch_repack_fp4(const uint32_t* codes, int64_t words, uint32_t* out, hipStream_t stream);
 
 struct DenseConvArgs {
     const void* x;

@@ -6,7 +6,7 @@
 #include "tbn_kernels.h"
 
 namespace {
-std::atomic<int32_t> g_knobs[TBN_KNOB_COUNT] = {{-1}, {-1}, {-1}, {-1}, {-1}, {-1}, {-1}};
+std::atomic<int32_t> g_knobs[TBN_KNOB_COUNT] = {{-1}, {-1}, {-1}, {-1}, {-1}, {-1}, {-1}, {-1}};
 }  // namespace
 
 namespace tbn {

@@ -122,6 +122,23 @@ def test_argument_errors_before_launch():
     assert lib.tbn_conv2d_fwd_i8(ctypes.byref(d), good, good, good, 1.0, 0, good, 0, None) == 3  # C = 8
     d_big = tbn.ConvDesc(1, 8, 8, 16, 8, 8, 8, 1, 1)  # R*S = 64 taps
     assert lib.tbn_conv2d_fwd_i8(ctypes.byref(d_big), good, good, good, 1.0, 0, good, 0, None) == 3
+    # fp8-activation variant
+    assert lib.tbn_quantize_act_fp8(None, 0, 16, 1.0, good, None) == 1
+    assert lib.tbn_quantize_act_fp8(good, 0, 0, 1.0, good, None) == 2
+    assert lib.tbn_quantize_act_fp8(good, 0, 16, -1.0, good, None) == 2
+    assert lib.tbn_quantize_act_fp8(good, 0, 16, float("nan"), good, None) == 2
+    assert lib.tbn_quantize_act_fp8(good, 2, 16, 1.0, good, None) == 3
+    assert lib.tbn_quantize_act_fp8(good, 0, 16, 1.0, bad, None) == 4
+    assert lib.tbn_repack_codes_fp4(None, 16, good, None) == 1
+    assert lib.tbn_repack_codes_fp4(good, 0, vp(0x200000), None) == 2
+    assert lib.tbn_repack_codes_fp4(good, 16, vp(0x100002), None) == 4
+    assert lib.tbn_repack_codes_fp4(good, 16, vp(0x100020), None) == 2  # overlapping
+    assert lib.tbn_conv2d_fwd_fp8(ctypes.byref(d16), None, good, good, 1.0, 0, good, 0, None) == 1
+    assert lib.tbn_conv2d_fwd_fp8(ctypes.byref(d16), good, good, good, float("inf"), 0, good, 0, None) == 2
+    assert lib.tbn_conv2d_fwd_fp8(ctypes.byref(d16), bad, good, good, 1.0, 0, good, 0, None) == 4
+    assert lib.tbn_conv2d_fwd_fp8(ctypes.byref(d16), good, good, good, 1.0, 0, good, 5, None) == 3
+    assert lib.tbn_conv2d_fwd_fp8(ctypes.byref(d), good, good, good, 1.0, 0, good, 0, None) == 3  # C = 8
+    assert lib.tbn_conv2d_fwd_fp8(ctypes.byref(d_big), good, good, good, 1.0, 0, good, 0, None) == 3
     # stride-2 backward-data is not implemented
     d2 = tbn.ConvDesc(1, 8, 8, 8, 8, 3, 3, 2, 1)
     assert lib.tbn_conv2d_bwd_data(ctypes.byref(d2), good, good, good, good, 0, good, 1 << 20, None) == 3
