@@ -256,11 +256,13 @@ __global__ __launch_bounds__(256, 2) void conv_fp8_kernel(const ConvFp8Args a) {
         if (il + STAGES - 1 < nst) issue(il + STAGES - 1);
         const uint8_t* st = smem + cslot * L::BYTES;
         cslot = cslot + 1 == STAGES ? 0 : cslot + 1;
-        // the stage's activation operands and filter words up front, then the two steps
+        // step 0's operands first; step 1's are read between step 0's MFMAs
         i32x8 af[2][TM];
         u32x2 bw[2][TN];
+        auto read_step = [&](int s2) {
 #pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
+            for (int t = 0; t < TN; ++t)
+                bw[s2][t] = *reinterpret_cast<const u32x2*>(st + L::B + s2 * NBLK * 1024 + bcol + 32 * 16 * t);
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 const uint8_t* rp = st + L::A + arow + 32 * i * ROWB;
@@ -268,19 +270,27 @@ __global__ __launch_bounds__(256, 2) void conv_fp8_kernel(const ConvFp8Args a) {
                 const i32x4 hi = *reinterpret_cast<const i32x4*>(rp + seg_hi[s2]);
                 af[s2][i] = i32x8{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
             }
-#pragma unroll
-            for (int t = 0; t < TN; ++t)
-                bw[s2][t] = *reinterpret_cast<const u32x2*>(st + L::B + s2 * NBLK * 1024 + bcol + 32 * 16 * t);
-        }
-        __builtin_amdgcn_sched_barrier(0);  // keep the LDS reads ahead of the MFMAs
+        };
+        read_step(0);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
+            if (s2 == 0) read_step(1);
 #pragma unroll
             for (int t = 0; t < TN; ++t) {
                 const i32x8 bf = decode_f4(bw[s2][t].x, bw[s2][t].y);
 #pragma unroll
                 for (int i = 0; i < TM; ++i) acc[i][t] = mfma_f4f8(bf, af[s2][i], acc[i][t]);
             }
+            if (s2 == 0) {
+                // two LDS reads after each MFMA
+#pragma unroll
+                for (int k = 0; k < TM * TN; ++k) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // two LDS reads
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 
