@@ -51,15 +51,24 @@ __device__ __forceinline__ f32x16 mfma_f4f8(i32x8 fil, i32x8 act, f32x16 c) {
     return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fil, act, c, 4, 0, 0, 127, 0, 127);
 }
 
-// The 32 E2M1 values of words w0 (elements 0..15) and w1 (16..31) of the repacked layout.
-__device__ __forceinline__ i32x8 decode_f4(uint32_t w0, uint32_t w1) {
-    i32x8 r;
-    r[0] = (int)((w0 & 0xAAAAAAAAu) + 0x22222222u);
-    r[1] = (int)(((w0 & 0x55555555u) << 1) + 0x22222222u);
-    r[2] = (int)((w1 & 0xAAAAAAAAu) + 0x22222222u);
-    r[3] = (int)(((w1 & 0x55555555u) << 1) + 0x22222222u);
-    r[4] = r[5] = r[6] = r[7] = 0;  // not read by the E2M1 form
+// (t << 1) + c in one v_lshl_add_u32 (c in a scalar register: the three-operand form takes
+// no literal)
+__device__ __forceinline__ uint32_t shl1_add(uint32_t t, uint32_t c) {
+    uint32_t r;
+    asm("v_lshl_add_u32 %0, %1, 1, %2" : "=v"(r) : "v"(t), "s"(c));
     return r;
+}
+
+// The 32 E2M1 values of words w0 (elements 0..15) and w1 (16..31) of the repacked layout;
+// two22 = 0x22222222 (the 2 of every nibble) in a scalar register.
+__device__ __forceinline__ i32x8 decode_f4(uint32_t w0, uint32_t w1, uint32_t two22) {
+    i32x4 r;
+    r[0] = (int)((w0 & 0xAAAAAAAAu) + two22);
+    r[1] = (int)shl1_add(w0 & 0x55555555u, two22);
+    r[2] = (int)((w1 & 0xAAAAAAAAu) + two22);
+    r[3] = (int)shl1_add(w1 & 0x55555555u, two22);
+    // the E2M1 form reads only the low four dwords: the others are left undefined
+    return __builtin_shufflevector(r, r, 0, 1, 2, 3, -1, -1, -1, -1);
 }
 
 // UNI: C % 128 == 0, so all 128 elements of a stage share one tap (r, s) and the tap
@@ -234,6 +243,7 @@ __global__ __launch_bounds__(256, 2) void conv_fp8_kernel(const ConvFp8Args a) {
     }
     const int arow = (wm * WM + l32) * ROWB;
     const int bcol = (wn * WN + l32) * 16 + 8 * half;  // words 2 half, 2 half + 1 of a chunk row
+    const uint32_t two22 = __builtin_amdgcn_readfirstlane(0x22222222u);
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -268,7 +278,7 @@ __global__ __launch_bounds__(256, 2) void conv_fp8_kernel(const ConvFp8Args a) {
                 const uint8_t* rp = st + L::A + arow + 32 * i * ROWB;
                 const i32x4 lo = *reinterpret_cast<const i32x4*>(rp + seg_lo[s2]);
                 const i32x4 hi = *reinterpret_cast<const i32x4*>(rp + seg_hi[s2]);
-                af[s2][i] = i32x8{lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+                af[s2][i] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
             }
         };
         read_step(0);
@@ -278,7 +288,7 @@ __global__ __launch_bounds__(256, 2) void conv_fp8_kernel(const ConvFp8Args a) {
             if (s2 == 0) read_step(1);
 #pragma unroll
             for (int t = 0; t < TN; ++t) {
-                const i32x8 bf = decode_f4(bw[s2][t].x, bw[s2][t].y);
+                const i32x8 bf = decode_f4(bw[s2][t].x, bw[s2][t].y, two22);
 #pragma unroll
                 for (int i = 0; i < TM; ++i) acc[i][t] = mfma_f4f8(bf, af[s2][i], acc[i][t]);
             }
