@@ -1,6 +1,7 @@
 // tbn_conv_direct.hip -- forward pass of a small two-bit layer (Sec. 2 Eq. 1) whose filters
-// have at most 64 elements over few input channels (3x3, 5x5, 7x7 or 1x1 shapes compiled):
-// single-channel MNIST-shaped layers and the first 3x3 layer over RGB.  Such a layer is a few hundred MFLOP at most, so the matrix cores
+// span few input channels (3x3, 5x5, 7x7 or 1x1 shapes compiled, at most 147 elements):
+// single-channel MNIST-shaped layers, the first 3x3 layer over RGB and the 7x7 RGB stem at
+// batch 1.  Such a layer is a few hundred MFLOP at most, so the matrix cores
 // buy nothing; what costs time is latency (filter decode, input gather, output store in
 // sequence).  Here every thread owns one output pixel and 8 consecutive filters:
 //   * a block (four waves) covers 64 pixels and 32 filters; its filters are decoded once
@@ -22,7 +23,7 @@ namespace {
 
 constexpr int DPIX = 64;   // output pixels per block (one per lane)
 constexpr int DFB = 32;    // filters per block (8 per wave)
-constexpr int DMAXN = 64;  // filter elements R*S*C
+constexpr int DMAXN = 147;  // filter elements R*S*C
 
 // R x S filters over C channels (compile-time, so that the gather below is fully unrolled and
 // all of a thread's input loads are in flight together)
@@ -77,17 +78,27 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
 
     // the block's filters: element e of filter kb0 + f is bit (e % 16) / 2 (+ 16 for odd e)
     // of word (e % 64) / 16 of the filter's 16-byte code row in chunk e / 64 (magnitude),
-    // the bit 8 above it the sign; weights of filters past Kf are zero
-    for (int i = tid; i < n * DFB; i += 256) {
-        const int e = i >> 5, f = i & (DFB - 1), k = kb0 + f;
-        float v = 0.0f;
-        if (k < a.Kf) {
-            const uint32_t w = a.codes[((int64_t)((k >> 6) * nchunks + (e >> 6)) * 64 + (k & 63)) * 4 + ((e & 63) >> 4)];
+    // the bit 8 above it the sign; weights of filters past Kf are zero.  All of a thread's
+    // code loads are issued before the first is decoded.
+    constexpr int DITER = (n * DFB + 255) / 256;
+    uint32_t cw[DITER];
+#pragma unroll
+    for (int it = 0; it < DITER; ++it) {
+        const int i = tid + 256 * it;
+        const int e = i >> 5, k = kb0 + (i & (DFB - 1));
+        cw[it] = i < n * DFB && k < a.Kf
+                     ? a.codes[((int64_t)((k >> 6) * nchunks + (e >> 6)) * 64 + (k & 63)) * 4 + ((e & 63) >> 4)]
+                     : 0u;
+    }
+#pragma unroll
+    for (int it = 0; it < DITER; ++it) {
+        const int i = tid + 256 * it;
+        if (i < n * DFB) {
+            const int e = i >> 5, k = kb0 + (i & (DFB - 1));
             const int jj = (e & 15) >> 1, hh = e & 1;
-            const uint32_t mag = (w >> (16 * hh + jj)) & 1u, sg = (w >> (16 * hh + 8 + jj)) & 1u;
-            v = (mag ? 2.0f : 1.0f) * (sg ? -1.0f : 1.0f);
+            const uint32_t mag = (cw[it] >> (16 * hh + jj)) & 1u, sg = (cw[it] >> (16 * hh + 8 + jj)) & 1u;
+            wl[i] = k < a.Kf ? (mag ? 2.0f : 1.0f) * (sg ? -1.0f : 1.0f) : 0.0f;
         }
-        wl[i] = v;
     }
     __syncthreads();
 
@@ -164,15 +175,15 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
 
 }  // namespace
 
-// filter shapes with a compiled kernel: 3x3 over 1..7 channels, 5x5 over 1..2, 7x7 over 1,
-// 1x1 over 1..8
+// filter shapes with a compiled kernel: 3x3 over 1..7 channels, 5x5 over 1..2, 7x7 over 1 and
+// 3, 1x1 over 1..8
 static const void* direct_kernel(int R, int S, int C, bool x32) {
 #define TBN_D(r, s, c) \
     if (R == r && S == s && C == c) \
         return x32 ? reinterpret_cast<const void*>(&conv_direct_kernel<r, s, c, true>) \
                    : reinterpret_cast<const void*>(&conv_direct_kernel<r, s, c, false>);
     TBN_D(3, 3, 1) TBN_D(3, 3, 2) TBN_D(3, 3, 3) TBN_D(3, 3, 4) TBN_D(3, 3, 5) TBN_D(3, 3, 6) TBN_D(3, 3, 7)
-    TBN_D(5, 5, 1) TBN_D(5, 5, 2) TBN_D(7, 7, 1)
+    TBN_D(5, 5, 1) TBN_D(5, 5, 2) TBN_D(7, 7, 1) TBN_D(7, 7, 3)
     TBN_D(1, 1, 1) TBN_D(1, 1, 2) TBN_D(1, 1, 3) TBN_D(1, 1, 4) TBN_D(1, 1, 5) TBN_D(1, 1, 6) TBN_D(1, 1, 7)
     TBN_D(1, 1, 8)
 #undef TBN_D
@@ -180,7 +191,7 @@ static const void* direct_kernel(int R, int S, int C, bool x32) {
 }
 
 bool conv_direct_eligible(const ConvGemmArgs& a) {
-    // forward pass with packed codes, a compiled filter shape (at most 64 elements, C <= 8),
+    // forward pass with packed codes, a compiled filter shape (at most 147 elements, C <= 8),
     // and little work in total (at most 2^28 multiply-adds: beyond that the matrix-core
     // kernels win)
     const int64_t n = (int64_t)a.R * a.S * a.C;

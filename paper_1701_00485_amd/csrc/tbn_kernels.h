@@ -130,7 +130,7 @@ struct ThinGeom {
     int64_t ws_bytes;
 };
 bool conv_thin_plan(const ConvGemmArgs& a, ThinGeom* g);
-// Direct fp32-FMA kernel for small forward layers (at most 64 filter elements, C <= 8).
+// Direct fp32-FMA kernel for small forward layers (at most 147 filter elements, C <= 8).
 bool conv_direct_eligible(const ConvGemmArgs& a);
 hipError_t launch_conv_direct(const ConvGemmArgs& a, hipStream_t stream);
 hipError_t launch_conv_thin(const ConvGemmArgs& a, const ThinGeom& g, hipStream_t stream);

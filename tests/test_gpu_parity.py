@@ -319,9 +319,10 @@ def test_fwd_thin_bordered_copy(tbn, g, xdt, knobs):
                                     ((2, 9, 9, 3, 72, 3, 3, 2, 1), "f32"),      # RGB 3x3 stride 2, two filter blocks
                                     ((1, 13, 11, 7, 40, 3, 3, 1, 1), "bf16"),   # 7 channels (63 elements)
                                     ((2, 10, 9, 1, 8, 7, 7, 1, 3), "bf16"),     # 7x7, one filter group
-                                    ((5, 6, 7, 4, 33, 1, 1, 1, 0), "f32")])     # 1x1, K one past 32
+                                    ((5, 6, 7, 4, 33, 1, 1, 1, 0), "f32"),      # 1x1, K one past 32
+                                    ((1, 37, 35, 3, 64, 7, 7, 2, 3), "bf16")])  # the 7x7 RGB stem, 147 elements
 def test_fwd_direct_small_layers(tbn, g, xdt):
-    """The direct fp32-FMA kernel (few channels, at most 64 filter elements): fused epilogue
+    """The direct fp32-FMA kernel (few channels, at most 147 filter elements): fused epilogue
     (scale, bias, residual, ReLU) with bf16 output and plain fp32 output against the oracle."""
     log("fwd direct %s %s" % (g, xdt))
     n, h, w, c, k, r, s, st, pd = g
