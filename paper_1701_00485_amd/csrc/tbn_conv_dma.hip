@@ -445,6 +445,89 @@ __global__ __launch_bounds__(256 * G, (BM * BN >= 65536 || G > 1) ? 1 : 2) void 
     const int gcol = lane % CG;
     const int grow = lane / CG;
     const int col0 = n0 + wn * WN + 8 * gcol;
+    // bf16 residual: the 16-byte loads of PRE_I tile rows (at most 8 per lane) are issued
+    // together before those rows are processed, so that their memory latency is paid once
+    // per group rather than once per pass
+    constexpr int NPASS = 32 / RPP;
+    constexpr int PRE_I = NPASS >= 8 ? 1 : (8 / NPASS < TM ? 8 / NPASS : TM);
+    static_assert(TM % PRE_I == 0, "residual prefetch groups");
+    const uint16_t* res16 = reinterpret_cast<const uint16_t*>(a.residual);
+
+    // Common case, decided per wave: bf16 output, no reduction split, the wave's tile wholly
+    // inside the output (rows below M, whole 8-column groups below Kf) and 16-byte aligned
+    // column factors.  It needs no per-row or per-column test: the column factors come in
+    // with 16-byte loads and every pass is the same straight-line code.
+    const bool fast = a.splits <= 1 && !a.y_f32 && (Kf % 8) == 0 && n0 + wn * WN + WN <= Kf &&
+                      m0 + wm * WM + WM <= M &&
+                      (((uintptr_t)a.colscale | (uintptr_t)a.scale | (uintptr_t)a.bias) & 15) == 0;
+    if (fast) {
+        f32x4 csl = {1.0f, 1.0f, 1.0f, 1.0f}, csh = csl, bil = {0.0f, 0.0f, 0.0f, 0.0f}, bih = bil;
+        if (a.colscale) {
+            csl = *reinterpret_cast<const f32x4*>(a.colscale + col0);
+            csh = *reinterpret_cast<const f32x4*>(a.colscale + col0 + 4);
+        }
+        if (a.scale) {
+            csl *= *reinterpret_cast<const f32x4*>(a.scale + col0);
+            csh *= *reinterpret_cast<const f32x4*>(a.scale + col0 + 4);
+        }
+        if (a.bias) {
+            bil = *reinterpret_cast<const f32x4*>(a.bias + col0);
+            bih = *reinterpret_cast<const f32x4*>(a.bias + col0 + 4);
+        }
+        const float cs8[8] = {csl.x, csl.y, csl.z, csl.w, csh.x, csh.y, csh.z, csh.w};
+        const float bi8[8] = {bil.x, bil.y, bil.z, bil.w, bih.x, bih.y, bih.z, bih.w};
+        const bool res = a.residual != nullptr, relu = a.relu != 0;
+        uint16_t* const y16 = reinterpret_cast<uint16_t*>(a.y);
+        const int64_t rowb = m0 + wm * WM + grow;  // tile row 0 of this lane's passes
+#pragma unroll
+        for (int i0 = 0; i0 < TM; i0 += PRE_I) {
+            u32x4 rpre[PRE_I][NPASS];
+#pragma unroll
+            for (int ii = 0; ii < PRE_I; ++ii)
+#pragma unroll
+                for (int pass = 0; pass < NPASS; ++pass)
+                    rpre[ii][pass] = res ? *reinterpret_cast<const u32x4*>(res16 + (rowb + 32 * (i0 + ii) + pass * RPP) * Kf + col0)
+                                         : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int ii = 0; ii < PRE_I; ++ii) {
+                const int i = i0 + ii;
+#pragma unroll
+                for (int t = 0; t < TN; ++t)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+                        *reinterpret_cast<f32x4*>(&stage[l32 * PITCH + 32 * t + 8 * g + 4 * half]) =
+                            f32x4{acc[i][t][4 * g], acc[i][t][4 * g + 1], acc[i][t][4 * g + 2], acc[i][t][4 * g + 3]};
+                __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS writes are visible to it
+#pragma unroll
+                for (int pass = 0; pass < NPASS; ++pass) {
+                    const int r = pass * RPP + grow;
+                    const f32x4 lo = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol]);
+                    const f32x4 hi = *reinterpret_cast<const f32x4*>(&stage[r * PITCH + 8 * gcol + 4]);
+                    float v8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v8[e] = v8[e] * cs8[e] + bi8[e];
+                    if (res) {
+                        const u32x4 r8 = rpre[ii][pass];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            v8[2 * e] += bf16_bits_to_f32(r8[e] & 0xFFFFu);
+                            v8[2 * e + 1] += __uint_as_float(r8[e] & 0xFFFF0000u);
+                        }
+                    }
+                    if (relu) {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) v8[e] = fmaxf(v8[e], 0.0f);
+                    }
+                    *reinterpret_cast<u32x4*>(y16 + (rowb + 32 * i + pass * RPP) * Kf + col0) =
+                        u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]), pack_bf16x2(v8[4], v8[5]),
+                              pack_bf16x2(v8[6], v8[7])};
+                }
+                __builtin_amdgcn_s_waitcnt(0xC07F);  // reads of this tile row done before it is overwritten
+            }
+        }
+        return;
+    }
+
     float cs[8], bi[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -459,14 +542,7 @@ __global__ __launch_bounds__(256 * G, (BM * BN >= 65536 || G > 1) ? 1 : 2) void 
     const bool partial_out = a.splits > 1;  // raw fp32 sums of this split, rows of Kp = round_up(Kf, 8)
     const int Kp = (Kf + 7) & ~7;
     float* part = partial_out ? a.partial + (int64_t)split * M * Kp : nullptr;
-    // bf16 residual: the 16-byte loads of PRE_I tile rows (at most 8 per lane) are issued
-    // together before those rows are processed, so that their memory latency is paid once
-    // per group rather than once per pass
-    constexpr int NPASS = 32 / RPP;
-    constexpr int PRE_I = NPASS >= 8 ? 1 : (8 / NPASS < TM ? 8 / NPASS : TM);
-    static_assert(TM % PRE_I == 0, "residual prefetch groups");
     const bool res_pre = a.residual && !a.y_f32 && vec_store && !partial_out && col0 < Kf;
-    const uint16_t* res16 = reinterpret_cast<const uint16_t*>(a.residual);
 #pragma unroll
     for (int i0 = 0; i0 < TM; i0 += PRE_I) {
         u32x4 rpre[PRE_I][NPASS];
