@@ -109,15 +109,34 @@ __global__ __launch_bounds__(256 * G) void fc_stream_kernel(const ConvGemmArgs a
             }
         }
     };
+    // ---- the batch's activations into LDS (zero beyond n, and the zero row).  When they
+    //      fit one pass of 16-byte pieces (8 per thread), their loads are issued before the
+    //      first code loads, so that writing them to LDS waits only for them (loads complete
+    //      in order) and the code loads stay in flight across the barrier ----
+    const int pieces = (N + 1) * xpitch / 8;
+    const int ppr = xpitch / 8;  // pieces per row
+    const bool x_one_pass = !a.x_f32 && n % 8 == 0 && pieces <= 256 * G * 8;
+    u32x4 xv[8];
+    if (x_one_pass) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = tid + 256 * G * u;
+            const int r = i / ppr, e = (i - r * ppr) * 8;
+            const bool ok = i < pieces && r < N && e < n;
+            xv[u] = ok ? *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.x) + (int64_t)r * n + e)
+                       : u32x4{0u, 0u, 0u, 0u};
+        }
+    }
     // nsteps is a multiple of NBUF KU (the host pads the activations in LDS to match); the
     // first code loads are in flight while the activations are staged
 #pragma unroll
     for (int b = 0; b < NBUF; ++b) load(wbuf[b], b * KU);
-    // ---- the batch's activations into LDS (zero beyond n, and the zero row) ----
-    if (!a.x_f32 && n % 8 == 0) {
+    if (x_one_pass) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (tid + 256 * G * u < pieces) reinterpret_cast<u32x4*>(xl)[tid + 256 * G * u] = xv[u];
+    } else if (!a.x_f32 && n % 8 == 0) {
         // 16-byte pieces, the loads of a thread issued together
-        const int pieces = (N + 1) * xpitch / 8;
-        const int ppr = xpitch / 8;  // pieces per row
         for (int i0 = tid; i0 < pieces; i0 += 256 * G * 8) {
             u32x4 v[8];
 #pragma unroll
