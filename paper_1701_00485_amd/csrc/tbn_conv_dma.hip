@@ -47,6 +47,89 @@ struct StageLayout {
     static constexpr int BYTES = P + 256;
 };
 
+// Sum of the split-K partials of outputs (row, col0 .. col0 + 7) in split order, then the
+// epilogue (partial rows are Kp = round_up(Kf, 8) wide; columns past Kf are skipped).
+__device__ __forceinline__ void split_epilogue_group(const ConvGemmArgs& a, int64_t M, int64_t row, int col0) {
+    const int Kf = a.Kf;
+    const int Kp = (Kf + 7) & ~7;
+    const int64_t po = row * Kp + col0;
+    float v8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    auto add = [&](const f32x4& lo, const f32x4& hi) {
+        v8[0] += lo.x; v8[1] += lo.y; v8[2] += lo.z; v8[3] += lo.w;
+        v8[4] += hi.x; v8[5] += hi.y; v8[6] += hi.z; v8[7] += hi.w;
+    };
+    // eight splits' loads in flight at a time, added in split order
+    int z = 0;
+    for (; z + 8 <= a.splits; z += 8) {
+        f32x4 lo[8], hi[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const float* pp = a.partial + (int64_t)(z + u) * M * Kp + po;
+            lo[u] = *reinterpret_cast<const f32x4*>(pp);
+            hi[u] = *reinterpret_cast<const f32x4*>(pp + 4);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) add(lo[u], hi[u]);
+    }
+    for (; z < a.splits; ++z) {
+        const float* pp = a.partial + (int64_t)z * M * Kp + po;
+        add(*reinterpret_cast<const f32x4*>(pp), *reinterpret_cast<const f32x4*>(pp + 4));
+    }
+    const bool full = col0 + 8 <= Kf;  // all 8 columns real (always when Kf % 8 == 0)
+    const int64_t o = row * Kf + col0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int col = col0 + e < Kf ? col0 + e : Kf - 1;  // past Kf: computed, never stored
+        float sc = a.colscale ? a.colscale[col] : 1.0f;
+        if (a.scale) sc *= a.scale[col];
+        v8[e] = v8[e] * sc + (a.bias ? a.bias[col] : 0.0f);
+    }
+    if (a.residual) {
+        if (a.y_f32) {
+            const float* rp = reinterpret_cast<const float*>(a.residual) + o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (col0 + e < Kf) v8[e] += rp[e];
+        } else if (full && (Kf % 8) == 0) {
+            const u32x4 r8 = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.residual) + o);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                v8[2 * e] += bf16_bits_to_f32(r8[e] & 0xFFFFu);
+                v8[2 * e + 1] += bf16_bits_to_f32(r8[e] >> 16);
+            }
+        } else {
+            const uint16_t* rp = reinterpret_cast<const uint16_t*>(a.residual) + o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (col0 + e < Kf) v8[e] += bf16_bits_to_f32(rp[e]);
+        }
+    }
+    if (a.relu) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v8[e] = fmaxf(v8[e], 0.0f);
+    }
+    if ((Kf % 8) == 0) {
+        if (a.y_f32) {
+            float* yp = reinterpret_cast<float*>(a.y) + o;
+            *reinterpret_cast<f32x4*>(yp) = f32x4{v8[0], v8[1], v8[2], v8[3]};
+            *reinterpret_cast<f32x4*>(yp + 4) = f32x4{v8[4], v8[5], v8[6], v8[7]};
+        } else {
+            *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(a.y) + o) =
+                u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]), pack_bf16x2(v8[4], v8[5]),
+                      pack_bf16x2(v8[6], v8[7])};
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            if (col0 + e >= Kf) break;
+            if (a.y_f32)
+                reinterpret_cast<float*>(a.y)[o + e] = v8[e];
+            else
+                reinterpret_cast<uint16_t*>(a.y)[o + e] = (uint16_t)f32_to_bf16_bits(v8[e]);
+        }
+    }
+}
+
 // UNI: C % 64 == 0, so all 64 elements of a stage share one tap (r, s) and the tap
 // bookkeeping is wave-uniform (scalar registers).
 // Tiles of 256 x 256 run one block per CU (one wave per SIMD, 128 x 128 accumulators each);
@@ -636,93 +719,15 @@ __global__ __launch_bounds__(256 * G, (BM * BN >= 65536 || G > 1) ? 1 : 2) void 
     }
 }
 
-// Sum of the split-K partials in split order, then the epilogue; one thread per 8 outputs
-// (partial rows are Kp = round_up(Kf, 8) wide; columns past Kf are skipped).
+// Sum of the split-K partials in split order, then the epilogue; one thread per 8 outputs.
 __global__ __launch_bounds__(256) void conv_split_epilogue_kernel(const ConvGemmArgs a) {
     const int64_t M = (int64_t)a.N * a.P * a.Q;
-    const int Kf = a.Kf;
-    const int Kp = (Kf + 7) & ~7;
+    const int Kp = (a.Kf + 7) & ~7;
     const int64_t groups = M * (Kp / 8);
     const int64_t gi = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (gi >= groups) return;
     const int64_t row = gi / (Kp / 8);
-    const int col0 = (int)(gi - row * (Kp / 8)) * 8;
-    const int64_t po = row * Kp + col0;
-    float v8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    auto add = [&](const f32x4& lo, const f32x4& hi) {
-        v8[0] += lo.x; v8[1] += lo.y; v8[2] += lo.z; v8[3] += lo.w;
-        v8[4] += hi.x; v8[5] += hi.y; v8[6] += hi.z; v8[7] += hi.w;
-    };
-    // eight splits' loads in flight at a time, added in split order
-    int z = 0;
-    for (; z + 8 <= a.splits; z += 8) {
-        f32x4 lo[8], hi[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const float* pp = a.partial + (int64_t)(z + u) * M * Kp + po;
-            lo[u] = *reinterpret_cast<const f32x4*>(pp);
-            hi[u] = *reinterpret_cast<const f32x4*>(pp + 4);
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) add(lo[u], hi[u]);
-    }
-    for (; z < a.splits; ++z) {
-        const float* pp = a.partial + (int64_t)z * M * Kp + po;
-        add(*reinterpret_cast<const f32x4*>(pp), *reinterpret_cast<const f32x4*>(pp + 4));
-    }
-    const bool full = col0 + 8 <= Kf;  // all 8 columns real (always when Kf % 8 == 0)
-    const int64_t o = row * Kf + col0;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const int col = col0 + e < Kf ? col0 + e : Kf - 1;  // past Kf: computed, never stored
-        float sc = a.colscale ? a.colscale[col] : 1.0f;
-        if (a.scale) sc *= a.scale[col];
-        v8[e] = v8[e] * sc + (a.bias ? a.bias[col] : 0.0f);
-    }
-    if (a.residual) {
-        if (a.y_f32) {
-            const float* rp = reinterpret_cast<const float*>(a.residual) + o;
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (col0 + e < Kf) v8[e] += rp[e];
-        } else if (full && (Kf % 8) == 0) {
-            const u32x4 r8 = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.residual) + o);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                v8[2 * e] += bf16_bits_to_f32(r8[e] & 0xFFFFu);
-                v8[2 * e + 1] += bf16_bits_to_f32(r8[e] >> 16);
-            }
-        } else {
-            const uint16_t* rp = reinterpret_cast<const uint16_t*>(a.residual) + o;
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-                if (col0 + e < Kf) v8[e] += bf16_bits_to_f32(rp[e]);
-        }
-    }
-    if (a.relu) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v8[e] = fmaxf(v8[e], 0.0f);
-    }
-    if ((Kf % 8) == 0) {
-        if (a.y_f32) {
-            float* yp = reinterpret_cast<float*>(a.y) + o;
-            *reinterpret_cast<f32x4*>(yp) = f32x4{v8[0], v8[1], v8[2], v8[3]};
-            *reinterpret_cast<f32x4*>(yp + 4) = f32x4{v8[4], v8[5], v8[6], v8[7]};
-        } else {
-            *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(a.y) + o) =
-                u32x4{pack_bf16x2(v8[0], v8[1]), pack_bf16x2(v8[2], v8[3]), pack_bf16x2(v8[4], v8[5]),
-                      pack_bf16x2(v8[6], v8[7])};
-        }
-    } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            if (col0 + e >= Kf) break;
-            if (a.y_f32)
-                reinterpret_cast<float*>(a.y)[o + e] = v8[e];
-            else
-                reinterpret_cast<uint16_t*>(a.y)[o + e] = (uint16_t)f32_to_bf16_bits(v8[e]);
-        }
-    }
+    split_epilogue_group(a, M, row, (int)(gi - row * (Kp / 8)) * 8);
 }
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool BWD, int G = 1>

@@ -206,10 +206,11 @@ __global__ __launch_bounds__(256 * G) void fc_stream_kernel(const ConvGemmArgs a
 }  // namespace
 
 // (loads per buffer, buffers, groups) of each variant; the tuning knob selects one for
-// sweeps.  Measured on the 8192 -> 32768 batch-1 layer (two runs each): two groups with two
-// buffers of four 16-byte loads 17.6 us per call (the default, variant 5), one group with
-// four buffers of two 17.8-18.8 us, the other one- and two-group variants 18.0-19.8 us, four
-// groups 20.1 us (one block per CU).
+// sweeps.  Measured on the 8192 -> 32768 batch-1 layer, graph-replayed, alternating in one
+// process, with the activations staged ahead of the first code loads: one group with four
+// buffers of two 16-byte loads 17.5-17.7 us per call (the default, variant 0), two groups
+// with two buffers of four 17.8-18.4 us, two groups with four buffers of two 18.0-18.7 us,
+// four groups ~20 us (one block per CU).
 constexpr int kNumVariants = 8;
 constexpr int kVariants[kNumVariants][3] = {{2, 4, 1}, {4, 2, 1}, {8, 2, 1}, {4, 3, 1},
                                             {2, 4, 2}, {4, 2, 2}, {2, 2, 4}, {2, 3, 2}};
@@ -219,7 +220,7 @@ bool fc_stream_plan(const ConvGemmArgs& a, FcStreamPlan* p) {
     if (a.apair || a.N > 16 || a.P != 1 || a.Q != 1 || a.R != a.H || a.S != a.W || a.ph != 0 || a.pw != 0)
         return false;
     const int forced = knob(KNOB_FC_VARIANT);
-    p->variant = forced >= 0 && forced < kNumVariants ? forced : 5;
+    p->variant = forced >= 0 && forced < kNumVariants ? forced : 0;
     const int64_t n = (int64_t)a.R * a.S * a.C;
     const int64_t nb = (n + 63) / 64;
     const int G = kVariants[p->variant][2];
