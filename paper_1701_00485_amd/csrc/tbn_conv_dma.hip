@@ -818,6 +818,19 @@ ConvPlan plan_conv_dma(const ConvGemmArgs& a, int cfg) {
         if (p.cfg == 18) {
             const int64_t t18 = ((M + 63) / 64) * ((a.Kf + 127) / 128);
             if (t18 >= 128 && t18 < 256 && nchunks >= 16) p.cfg = 22;
+            // fewer than 128 tiles (batch-1 layers): two or four wave groups per block
+            // splitting the reduction inside the block, instead of a grid split and its
+            // epilogue pass, when every group then has 4 to 10 stages.  Measured on the
+            // ResNet-18 batch-1 layers: 28 x 28 x 128, two groups of 9 stages, 9.0 us against
+            // 12.3 us split three ways plus the epilogue pass; 14 x 14 x 256, four groups of
+            // 9, 12.7 against 13.0 us; 7 x 7 x 512 (18 stages per group with four groups)
+            // stays split: 13.4 against 20.8 us.
+            if (t18 < 128) {
+                if (nchunks >= 8 && (nchunks + 1) / 2 <= 10)
+                    p.cfg = 21;
+                else if (nchunks >= 16 && (nchunks + 3) / 4 <= 10)
+                    p.cfg = 22;
+            }
         }
     }
     cfg_tile(p.cfg, &bm, &bn);
