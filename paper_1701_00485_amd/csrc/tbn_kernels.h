@@ -54,6 +54,9 @@ struct ConvGemmArgs {
     int32_t relu;
     int32_t x_f32;
     int32_t y_f32;
+    // LDS-DMA kernel: write y with non-temporal (streaming) stores -- set by its launcher
+    // for outputs too large to be read back from the last-level cache
+    int32_t y_stream;
     FastDiv div_q, div_pq;    // division by Q and by P*Q (output pixel -> (n, p, q))
     float* partial;           // split-K: fp32 partial sums [splits][M][Kf] (workspace)
     int32_t splits;           // split-K: number of reduction ranges (1 = none)
