@@ -8,10 +8,11 @@
 //     from the packed codes into LDS as fp32 +-1 / +-2 (element-major, so the 8 weights a
 //     thread needs for one element are one 32-byte broadcast read: every lane of a wave
 //     reads the same filters);
-//   * the thread first issues the loads of its R*S*C input values (zero outside the image;
-//     fp32 input rounded to bf16, nearest even, as in every other forward kernel), then the
-//     block decodes its filters while they are in flight, then the values are accumulated
-//     against the weights with fp32 FMAs (products exact, sums fp32);
+//   * the thread issues its loads of the filter codes, then those of the first input rows
+//     (zero outside the image; fp32 input rounded to bf16, nearest even, as in every other
+//     forward kernel); the block decodes its filters as soon as the codes land, the rest of
+//     the input loads go out after the barrier, and the values are accumulated against the
+//     weights with fp32 FMAs (products exact, sums fp32) as they arrive;
 //   * alpha (the column scale) and the optional scale, bias, residual and ReLU are applied
 //     in fp32 and the 8 outputs written with 16-byte stores.
 #include "tbn_device.h"
@@ -38,8 +39,25 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
     constexpr int nchunks = (n + 63) / 64;
     const int kb0 = blockIdx.y * DFB;
 
-    // the input values of this thread's pixel, loaded first so that their latency overlaps
-    // the filter decode (zero outside the image; fp32 input rounded to bf16)
+    // the block's filters: element e of filter kb0 + f is bit (e % 16) / 2 (+ 16 for odd e)
+    // of word (e % 64) / 16 of the filter's 16-byte code row in chunk e / 64 (magnitude),
+    // the bit 8 above it the sign; weights of filters past Kf are zero.  The code loads go
+    // out first, so that the decode waits for them alone (vector loads complete in order).
+    constexpr int DITER = (n * DFB + 255) / 256;
+    uint32_t cw[DITER];
+#pragma unroll
+    for (int it = 0; it < DITER; ++it) {
+        const int i = tid + 256 * it;
+        const int e = i >> 5, k = kb0 + (i & (DFB - 1));
+        cw[it] = i < n * DFB && k < a.Kf
+                     ? a.codes[((int64_t)((k >> 6) * nchunks + (e >> 6)) * 64 + (k & 63)) * 4 + ((e & 63) >> 4)]
+                     : 0u;
+    }
+
+    // the input values of this thread's pixel (zero outside the image), raw bf16 bits (or fp32
+    // bits), converted where they are used: the first R1 filter rows are loaded before the
+    // decode (at most ~60 loads with the code loads, within the hardware's count of loads in
+    // flight), the rest after the barrier, so that the first products start while they land
     const int64_t M = (int64_t)a.N * a.P * a.Q;
     const int64_t m = (int64_t)blockIdx.x * DPIX + lane;
     const bool live = m < M;
@@ -53,43 +71,28 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
     // may be negative here, only in-image taps are used)
     const int32_t pix0 = (((int32_t)img * a.H + h0) * a.W + w0) * C;
     // unconditional gather through a buffer resource: an out-of-image tap gets an offset
-    // beyond the buffer and the hardware returns zero, so no load sits behind a branch and
-    // all of them are in flight together
+    // beyond the buffer and the hardware returns zero, so no load sits behind a branch
     constexpr int ESZ = X32 ? 4 : 2;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<void*>(a.x), (short)0, (int)((int64_t)a.N * a.H * a.W * C * ESZ), 0x00020000);
-    float xv[n];
-#pragma unroll
-    for (int r = 0; r < R; ++r)
+    uint32_t xb[n];
+    auto gather_row = [&](int r) {
 #pragma unroll
         for (int s_ = 0; s_ < S; ++s_) {
             const bool ok = live && (unsigned)(h0 + r) < (unsigned)a.H && (unsigned)(w0 + s_) < (unsigned)a.W;
             const int off = ok ? (pix0 + (r * a.W + s_) * C) * ESZ : (int)0x80000000;
 #pragma unroll
             for (int c = 0; c < C; ++c) {
-                uint32_t b;
                 if constexpr (X32)
-                    b = f32_to_bf16_bits(__uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, off, c * 4, 0)));
+                    xb[(r * S + s_) * C + c] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, c * 4, 0);
                 else
-                    b = __builtin_amdgcn_raw_buffer_load_b16(rs, off, c * 2, 0);
-                xv[(r * S + s_) * C + c] = bf16_bits_to_f32(b);
+                    xb[(r * S + s_) * C + c] = __builtin_amdgcn_raw_buffer_load_b16(rs, off, c * 2, 0);
             }
         }
-
-    // the block's filters: element e of filter kb0 + f is bit (e % 16) / 2 (+ 16 for odd e)
-    // of word (e % 64) / 16 of the filter's 16-byte code row in chunk e / 64 (magnitude),
-    // the bit 8 above it the sign; weights of filters past Kf are zero.  All of a thread's
-    // code loads are issued before the first is decoded.
-    constexpr int DITER = (n * DFB + 255) / 256;
-    uint32_t cw[DITER];
+    };
+    constexpr int R1 = (60 - DITER) / (S * C) < R ? ((60 - DITER) / (S * C) > 0 ? (60 - DITER) / (S * C) : 0) : R;
 #pragma unroll
-    for (int it = 0; it < DITER; ++it) {
-        const int i = tid + 256 * it;
-        const int e = i >> 5, k = kb0 + (i & (DFB - 1));
-        cw[it] = i < n * DFB && k < a.Kf
-                     ? a.codes[((int64_t)((k >> 6) * nchunks + (e >> 6)) * 64 + (k & 63)) * 4 + ((e & 63) >> 4)]
-                     : 0u;
-    }
+    for (int r = 0; r < R1; ++r) gather_row(r);
 #pragma unroll
     for (int it = 0; it < DITER; ++it) {
         const int i = tid + 256 * it;
@@ -101,6 +104,8 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
         }
     }
     __syncthreads();
+#pragma unroll
+    for (int r = R1; r < R; ++r) gather_row(r);
 
     const int k0 = kb0 + 8 * grp;
     if (!live || k0 >= a.Kf) return;  // no barrier follows
@@ -115,14 +120,20 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
         // the 8 weights of element e: the same address in every lane (broadcast)
         const f32x4 lo = *reinterpret_cast<const f32x4*>(wg + e * DFB);
         const f32x4 hi = *reinterpret_cast<const f32x4*>(wg + e * DFB + 4);
-        acc[0] = fmaf(xv[e], lo.x, acc[0]);
-        acc[1] = fmaf(xv[e], lo.y, acc[1]);
-        acc[2] = fmaf(xv[e], lo.z, acc[2]);
-        acc[3] = fmaf(xv[e], lo.w, acc[3]);
-        acc[4] = fmaf(xv[e], hi.x, acc[4]);
-        acc[5] = fmaf(xv[e], hi.y, acc[5]);
-        acc[6] = fmaf(xv[e], hi.z, acc[6]);
-        acc[7] = fmaf(xv[e], hi.w, acc[7]);
+        // fp32 input rounded to bf16 (nearest even), as in every other forward kernel
+        float xv_e;
+        if constexpr (X32)
+            xv_e = bf16_bits_to_f32(f32_to_bf16_bits(__uint_as_float(xb[e])));
+        else
+            xv_e = bf16_bits_to_f32(xb[e]);
+        acc[0] = fmaf(xv_e, lo.x, acc[0]);
+        acc[1] = fmaf(xv_e, lo.y, acc[1]);
+        acc[2] = fmaf(xv_e, lo.z, acc[2]);
+        acc[3] = fmaf(xv_e, lo.w, acc[3]);
+        acc[4] = fmaf(xv_e, hi.x, acc[4]);
+        acc[5] = fmaf(xv_e, hi.y, acc[5]);
+        acc[6] = fmaf(xv_e, hi.z, acc[6]);
+        acc[7] = fmaf(xv_e, hi.w, acc[7]);
         if (e % 4 == 3 || e == n - 1) {
             // the sums so far are materialised here, so the FMAs cannot be moved past the
             // next reads (which would keep every weight of the filter live at once)
