@@ -80,6 +80,63 @@ __global__ __launch_bounds__(256) void maxpool_fwd_kernel(const PoolArgs a, cons
     }
 }
 
+// The same for a compile-time K x K window, 8 channels per thread (C % 8 == 0) and 32-bit
+// indices (the host checks the sizes): the K*K 16-byte loads of a thread are all issued
+// before the first comparison, and the pixel index is split with multiply-shift divisions.
+template <int K>
+__global__ __launch_bounds__(256) void maxpool_fwd8_kernel(const PoolArgs a, const FastDiv div_g, const FastDiv div_q,
+                                                           const FastDiv div_p, const uint32_t groups,
+                                                           const uint16_t* __restrict__ x, uint16_t* __restrict__ y,
+                                                           int32_t* __restrict__ arg) {
+    const uint32_t gi = blockIdx.x * 256u + threadIdx.x;  // (output pixel, 8-channel group)
+    if (gi >= groups) return;
+    const uint32_t pix = fdiv(gi, div_g);
+    const uint32_t c = (gi - pix * (uint32_t)(a.C / 8)) * 8u;
+    const uint32_t nq = fdiv(pix, div_q);
+    const int q = (int)(pix - nq * (uint32_t)a.Q);
+    const uint32_t n = fdiv(nq, div_p);
+    const int p = (int)(nq - n * (uint32_t)a.P);
+    const int h0 = p * a.s - a.pad, w0 = q * a.s - a.pad;
+    u32x4 v[K * K];
+    bool ok[K * K];
+#pragma unroll
+    for (int r = 0; r < K; ++r)
+#pragma unroll
+        for (int t = 0; t < K; ++t) {
+            const int h = h0 + r, w = w0 + t;
+            ok[r * K + t] = (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+            const uint32_t xi = (((n * (uint32_t)a.H + (uint32_t)h) * (uint32_t)a.W + (uint32_t)w) * (uint32_t)a.C + c);
+            v[r * K + t] = ok[r * K + t] ? *reinterpret_cast<const u32x4*>(x + xi) : u32x4{0u, 0u, 0u, 0u};
+        }
+    float best[8];
+    int bi[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        best[e] = 0.0f;
+        bi[e] = -1;
+    }
+#pragma unroll
+    for (int j = 0; j < K * K; ++j) {
+        if (!ok[j]) continue;
+        const int pos = (h0 + j / K) * a.W + (w0 + j % K);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float f = bf16_bits_to_f32((e & 1) ? (v[j][e / 2] >> 16) : (v[j][e / 2] & 0xFFFFu));
+            if (bi[e] < 0 || f > best[e]) {
+                best[e] = f;
+                bi[e] = pos;
+            }
+        }
+    }
+    const uint32_t o = gi * 8u;
+    *reinterpret_cast<u32x4*>(y + o) = u32x4{pack_bf16x2(best[0], best[1]), pack_bf16x2(best[2], best[3]),
+                                              pack_bf16x2(best[4], best[5]), pack_bf16x2(best[6], best[7])};
+    if (arg) {
+        *reinterpret_cast<u32x4*>(arg + o) = u32x4{(uint32_t)bi[0], (uint32_t)bi[1], (uint32_t)bi[2], (uint32_t)bi[3]};
+        *reinterpret_cast<u32x4*>(arg + o + 4) = u32x4{(uint32_t)bi[4], (uint32_t)bi[5], (uint32_t)bi[6], (uint32_t)bi[7]};
+    }
+}
+
 // dx[n,h,w,c] = sum of dy over the windows that chose (h, w); NV channels per thread
 template <int NV>
 __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const PoolArgs a, const uint16_t* __restrict__ dy,
@@ -486,7 +543,18 @@ unsigned blocks_for(int64_t total) { return (unsigned)((total + 255) / 256); }
 
 hipError_t launch_maxpool_fwd(const PoolArgs& a, const uint16_t* x, uint16_t* y, int32_t* arg, hipStream_t s) {
     const int64_t total = (int64_t)a.N * a.P * a.Q * a.C;
-    if (a.C % 8 == 0)
+    const int64_t in_total = (int64_t)a.N * a.H * a.W * a.C;
+    if (a.C % 8 == 0 && (a.k == 2 || a.k == 3) && total < 0x7FFFFFFFll && in_total < 0x7FFFFFFFll) {
+        const uint32_t groups = (uint32_t)(total / 8);
+        const FastDiv dg = make_fastdiv((uint32_t)(a.C / 8)), dq = make_fastdiv((uint32_t)a.Q),
+                      dp = make_fastdiv((uint32_t)a.P);
+        if (a.k == 3)
+            hipLaunchKernelGGL(maxpool_fwd8_kernel<3>, dim3(blocks_for(groups)), dim3(256), 0, s, a, dg, dq, dp, groups,
+                               x, y, arg);
+        else
+            hipLaunchKernelGGL(maxpool_fwd8_kernel<2>, dim3(blocks_for(groups)), dim3(256), 0, s, a, dg, dq, dp, groups,
+                               x, y, arg);
+    } else if (a.C % 8 == 0)
         hipLaunchKernelGGL(maxpool_fwd_kernel<8>, dim3(blocks_for(total / 8)), dim3(256), 0, s, a, x, y, arg);
     else
         hipLaunchKernelGGL(maxpool_fwd_kernel<1>, dim3(blocks_for(total)), dim3(256), 0, s, a, x, y, arg);

@@ -18,7 +18,9 @@ def _bits_to_f64(t):
 
 
 @pytest.mark.parametrize("shape,k,s,p", [((2, 112, 112, 64), 3, 2, 1), ((4, 28, 28, 32), 2, 2, 0),
-                                          ((3, 9, 7, 5), 3, 2, 1), ((2, 14, 14, 64), 2, 2, 0)])
+                                          ((3, 9, 7, 5), 3, 2, 1), ((2, 14, 14, 64), 2, 2, 0),
+                                          ((2, 15, 17, 16), 3, 2, 1), ((3, 7, 9, 8), 3, 1, 1),
+                                          ((2, 11, 13, 24), 2, 2, 0)])
 def test_maxpool(tbn, shape, k, s, p):
     log("maxpool %s k%d s%d p%d" % (shape, k, s, p))
     xb = synth.normal_bf16(10, "mp%s" % (shape,), shape)
