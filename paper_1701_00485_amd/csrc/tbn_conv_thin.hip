@@ -137,13 +137,17 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
     const int NB = (n + 63) / 64;
     const int k0 = blockIdx.y * FB;
 
-    const int64_t PQt = (int64_t)g.tiles_p * g.tiles_q;
+    // tile index -> (image, first output row, first output column), by multiply-shift
+    // divisions (the host checks that the tile count fits 31 bits)
+    const uint32_t PQt = (uint32_t)g.tiles_p * (uint32_t)g.tiles_q;
     auto origin = [&](int64_t tile, int64_t* img, int* p0, int* q0) {
-        *img = tile / PQt;
-        const int rem = (int)(tile - *img * PQt);
-        const int tp = rem / g.tiles_q;
-        *p0 = tp * TP;
-        *q0 = (rem - tp * g.tiles_q) * TQ;
+        const uint32_t t32 = (uint32_t)tile;
+        const uint32_t im = fdiv(t32, g.div_pqt);
+        const uint32_t rem = t32 - im * PQt;
+        const uint32_t tp = fdiv(rem, g.div_tq);
+        *img = (int64_t)im;
+        *p0 = (int)tp * TP;
+        *q0 = (int)(rem - tp * (uint32_t)g.tiles_q) * TQ;
     };
     const uint32_t img_elems = (uint32_t)a.H * a.W * a.C;
     uint32_t desc[kElemsPerThread];
@@ -260,26 +264,32 @@ __global__ __launch_bounds__(256) void conv_thin_kernel(const ConvGemmArgs a, co
         const int arowr = g.PW * CP;             // patch offset of filter row r + 1
         const uint16_t* bbase = wl + l32 * g.WPITCH + 8 * half;
         // flat reduction steps j = r * TT + t (16 elements each); the filters are contiguous
-        // in j, the patch advances a row every TT steps
+        // in j, the patch advances a row every TT steps.  Two operand sets alternate, the
+        // reads of step j + 1 issued before the MFMAs of step j (no copies at the loop edge)
         const int J = R * TT;
-        bf16x8 a0 = load8<CP>(abase), a1 = load8<CP>(abase + arow4);
-        bf16x8 b0 = *reinterpret_cast<const bf16x8*>(bbase);
-        bf16x8 b1 = *reinterpret_cast<const bf16x8*>(bbase + 32 * g.WPITCH);
-        for (int j = 0; j < J; ++j) {
-            const bf16x8 ca0 = a0, ca1 = a1, cb0 = b0, cb1 = b1;
-            if (j + 1 < J) {
-                const int jn = j + 1;
-                const uint16_t* an = abase + (jn / TT) * arowr + 16 * (jn % TT);
-                a0 = load8<CP>(an);
-                a1 = load8<CP>(an + arow4);
-                b0 = *reinterpret_cast<const bf16x8*>(bbase + 16 * jn);
-                b1 = *reinterpret_cast<const bf16x8*>(bbase + 32 * g.WPITCH + 16 * jn);
-            }
-            acc[0][0] = mfma32(cb0, ca0, acc[0][0]);
-            acc[0][1] = mfma32(cb1, ca0, acc[0][1]);
-            acc[1][0] = mfma32(cb0, ca1, acc[1][0]);
-            acc[1][1] = mfma32(cb1, ca1, acc[1][1]);
+        bf16x8 xa[2], xb[2], wa[2], wb[2];
+        auto rd = [&](int j, int s) {
+            const uint16_t* an = abase + (j / TT) * arowr + 16 * (j % TT);
+            xa[s] = load8<CP>(an);
+            xb[s] = load8<CP>(an + arow4);
+            wa[s] = *reinterpret_cast<const bf16x8*>(bbase + 16 * j);
+            wb[s] = *reinterpret_cast<const bf16x8*>(bbase + 32 * g.WPITCH + 16 * j);
+        };
+        auto mm = [&](int s) {
+            acc[0][0] = mfma32(wa[s], xa[s], acc[0][0]);
+            acc[0][1] = mfma32(wb[s], xa[s], acc[0][1]);
+            acc[1][0] = mfma32(wa[s], xb[s], acc[1][0]);
+            acc[1][1] = mfma32(wb[s], xb[s], acc[1][1]);
+        };
+        rd(0, 0);
+        int j = 0;
+        for (; j + 2 <= J; j += 2) {
+            rd(j + 1, 1);
+            mm(0);
+            if (j + 2 < J) rd(j + 2, 0);
+            mm(1);
         }
+        if (j < J) mm(0);  // odd step count: the last step's operands are in set 0
     };
 
     auto tile_epilogue = [&](const f32x16 (&acc)[2][2], int64_t cimg, int cp0, int cq0) {
@@ -470,6 +480,9 @@ bool conv_thin_plan(const ConvGemmArgs& a, ThinGeom* g) {
     t.rowlen = t.PW * a.C;
     t.nelem = t.PH * t.rowlen;
     t.ept = (t.nelem + 255) / 256;
+    if (t.ntiles >= 0x7FFFFFFFll) return false;
+    t.div_pqt = make_fastdiv((uint32_t)(t.tiles_p * t.tiles_q));
+    t.div_tq = make_fastdiv((uint32_t)t.tiles_q);
     t.div_rowlen = make_fastdiv((uint32_t)t.rowlen);
     t.div_c = make_fastdiv((uint32_t)a.C);
     if (t.lds_bytes > 96 * 1024 || a.R > 64 || t.T > 128 || nb * 1024 > 4 * 32 * SPITCH * 4 ||

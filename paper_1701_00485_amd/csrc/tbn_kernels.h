@@ -125,6 +125,7 @@ struct ThinGeom {
     int32_t pbuf;  // bf16 elements per patch buffer (two buffers)
     int32_t rowlen, nelem, ept;  // input elements per patch row, per patch, per thread
     FastDiv div_rowlen, div_c;
+    FastDiv div_pqt, div_tq;  // tile index -> (image, tile row, tile column); ntiles < 2^31
     // large inputs: the input is first written once into workspace as a zero-bordered NHWC
     // copy with CP channels [N][Hp][Wp][CP] bf16, from which every patch is a block of whole
     // 16-byte pieces copied straight into LDS (ppr pieces per patch row, npieces per patch,
