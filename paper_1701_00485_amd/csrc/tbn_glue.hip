@@ -250,9 +250,12 @@ __global__ __launch_bounds__(256) void avgpool8_kernel(int32_t N, int32_t HW, in
 //     cover tpr = 256 / groups rows at a time, then combine their row lanes through LDS in
 //     a fixed order and write partial[b][c];
 //   * finalize: one thread per channel adds partial[0..chunks)[c] in order.
-// Modes: BN_SUM sums x; BN_SQDEV sums (x - mean)^2 (two-pass variance); BN_BWD sums
-// g and g * xhat, with g = dy masked by y > 0 when ReLU followed the normalisation.
-enum { BN_SUM = 0, BN_SQDEV = 1, BN_BWD = 2 };
+// Modes: BN_STATS sums d and d^2 with d = x - x[0][c] (one pass for both statistics: the
+// first row's value of each channel is a shift common to every chunk, so the chunk sums
+// add, and the variance S2/n - (S1/n)^2 of the shifted values does not cancel against a
+// large mean); BN_BWD sums g and g * xhat, with g = dy masked by y > 0 when ReLU followed
+// the normalisation.
+enum { BN_BWD = 2, BN_STATS = 3 };
 
 template <int MODE, bool VEC>
 __global__ __launch_bounds__(256) void bn_partial_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ y,
@@ -261,7 +264,8 @@ __global__ __launch_bounds__(256) void bn_partial_kernel(const uint16_t* __restr
                                                          const float* __restrict__ inv_std, float* __restrict__ p1,
                                                          float* __restrict__ p2) {
     constexpr int NV = VEC ? 8 : 1;
-    __shared__ float s1[256 * NV], s2[MODE == BN_BWD ? 256 * NV : 1];
+    constexpr bool TWO = MODE == BN_BWD || MODE == BN_STATS;  // two sums per channel
+    __shared__ float s1[256 * NV], s2[TWO ? 256 * NV : 1];
     const int G = VEC ? C / 8 : C;
     const int gbase = blockIdx.y * 256;
     const int Gs = min(256, G - gbase);
@@ -276,8 +280,21 @@ __global__ __launch_bounds__(256) void bn_partial_kernel(const uint16_t* __restr
 #pragma unroll
     for (int e = 0; e < NV; ++e) {
         a1[e] = a2[e] = 0.0f;
-        m[e] = MODE != BN_SUM ? mean[c0 + e] : 0.0f;
+        m[e] = MODE == BN_BWD ? mean[c0 + e] : 0.0f;
         is[e] = MODE == BN_BWD ? inv_std[c0 + e] : 0.0f;
+    }
+    if constexpr (MODE == BN_STATS) {
+        // the shift: channel c0 + e of row 0
+        if constexpr (VEC) {
+            const u32x4 kw = *reinterpret_cast<const u32x4*>(x + c0);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                m[2 * e] = bf16_bits_to_f32(kw[e] & 0xFFFFu);
+                m[2 * e + 1] = bf16_bits_to_f32(kw[e] >> 16);
+            }
+        } else {
+            m[0] = bf16_bits_to_f32(x[c0]);
+        }
     }
     if (active) {
         for (int64_t r = rbeg + r0; r < rend; r += tpr) {
@@ -310,11 +327,10 @@ __global__ __launch_bounds__(256) void bn_partial_kernel(const uint16_t* __restr
             }
 #pragma unroll
             for (int e = 0; e < NV; ++e) {
-                if constexpr (MODE == BN_SUM) {
-                    a1[e] += xv[e];
-                } else if constexpr (MODE == BN_SQDEV) {
+                if constexpr (MODE == BN_STATS) {
                     const float d = xv[e] - m[e];
-                    a1[e] += d * d;
+                    a1[e] += d;
+                    a2[e] += d * d;
                 } else {
                     const float gv = (relu && !(yv[e] > 0.0f)) ? 0.0f : dv[e];
                     a1[e] += gv;
@@ -328,7 +344,7 @@ __global__ __launch_bounds__(256) void bn_partial_kernel(const uint16_t* __restr
 #pragma unroll
         for (int e = 0; e < NV; ++e) {
             s1[r0 * W + g * NV + e] = a1[e];
-            if constexpr (MODE == BN_BWD) s2[r0 * W + g * NV + e] = a2[e];
+            if constexpr (TWO) s2[r0 * W + g * NV + e] = a2[e];
         }
     }
     __syncthreads();
@@ -336,20 +352,19 @@ __global__ __launch_bounds__(256) void bn_partial_kernel(const uint16_t* __restr
         float u1 = 0.0f, u2 = 0.0f;
         for (int rr = 0; rr < tpr; ++rr) {
             u1 += s1[rr * W + c];
-            if constexpr (MODE == BN_BWD) u2 += s2[rr * W + c];
+            if constexpr (TWO) u2 += s2[rr * W + c];
         }
         const int64_t o = (int64_t)blockIdx.x * C + gbase * NV + c;
         p1[o] = u1;
-        if constexpr (MODE == BN_BWD) p2[o] = u2;
+        if constexpr (TWO) p2[o] = u2;
     }
 }
 
-// 16 channels x 16 chunk lanes per block: lane j sums chunks j, j + 16, ... in order, then
-// the 16 lane sums are added in lane order.
-template <int MODE>
-__global__ __launch_bounds__(256) void bn_finalize_kernel(const float* __restrict__ p1, const float* __restrict__ p2,
-                                                          int64_t chunks, int32_t C, int64_t rows, float eps,
-                                                          float* __restrict__ out1, float* __restrict__ out2) {
+// Backward sums dbeta = sum g and dgamma = sum g * xhat: 16 channels x 16 chunk lanes per
+// block, lane j sums chunks j, j + 16, ... in order, then the 16 lane sums in lane order.
+__global__ __launch_bounds__(256) void bn_bwd_finalize_kernel(const float* __restrict__ p1, const float* __restrict__ p2,
+                                                              int64_t chunks, int32_t C, float* __restrict__ out1,
+                                                              float* __restrict__ out2) {
     __shared__ float s1[16][17], s2[16][17];
     const int cl = threadIdx.x & 15, part = threadIdx.x >> 4;
     const int c = blockIdx.x * 16 + cl;
@@ -363,7 +378,7 @@ __global__ __launch_bounds__(256) void bn_finalize_kernel(const float* __restric
             u1 += v1;
             u1 += v2;
             u1 += v3;
-            if constexpr (MODE == BN_BWD) {
+            {
                 const float w0 = p2[b * C + c], w1 = p2[(b + 16) * C + c];
                 const float w2 = p2[(b + 32) * C + c], w3 = p2[(b + 48) * C + c];
                 u2 += w0;
@@ -374,7 +389,7 @@ __global__ __launch_bounds__(256) void bn_finalize_kernel(const float* __restric
         }
         for (; b < chunks; b += 16) {
             u1 += p1[b * C + c];
-            if constexpr (MODE == BN_BWD) u2 += p2[b * C + c];
+            u2 += p2[b * C + c];
         }
     }
     s1[part][cl] = u1;
@@ -386,14 +401,42 @@ __global__ __launch_bounds__(256) void bn_finalize_kernel(const float* __restric
         t1 += s1[j][cl];
         t2 += s2[j][cl];
     }
-    if constexpr (MODE == BN_SUM) {
-        out1[c] = t1 / (float)rows;  // mean
-    } else if constexpr (MODE == BN_SQDEV) {
-        out1[c] = 1.0f / sqrtf(t1 / (float)rows + eps);  // inv_std (biased variance)
-    } else {
-        out1[c] = t1;  // dbeta
-        out2[c] = t2;  // dgamma
+    out1[c] = t1;  // dbeta
+    out2[c] = t2;  // dgamma
+}
+
+// One-pass statistics: the chunk sums S1 = sum d, S2 = sum d^2 (d = x - x[0][c]) added in
+// chunk order in fp64 (16 chunk lanes per channel, then the lanes in order), then
+// mean = x[0][c] + S1 / n and inv_std = 1 / sqrt(S2 / n - (S1 / n)^2 + eps) (biased variance,
+// clamped at zero).
+__global__ __launch_bounds__(256) void bn_stats_finalize_kernel(const float* __restrict__ p1, const float* __restrict__ p2,
+                                                                int64_t chunks, int32_t C, int64_t rows, float eps,
+                                                                const uint16_t* __restrict__ x, float* __restrict__ mean,
+                                                                float* __restrict__ inv_std) {
+    __shared__ double s1[16][17], s2[16][17];
+    const int cl = threadIdx.x & 15, part = threadIdx.x >> 4;
+    const int c = blockIdx.x * 16 + cl;
+    double u1 = 0.0, u2 = 0.0;
+    if (c < C)
+        for (int64_t b = part; b < chunks; b += 16) {
+            u1 += (double)p1[b * C + c];
+            u2 += (double)p2[b * C + c];
+        }
+    s1[part][cl] = u1;
+    s2[part][cl] = u2;
+    __syncthreads();
+    if (part != 0 || c >= C) return;
+    double t1 = 0.0, t2 = 0.0;
+    for (int j = 0; j < 16; ++j) {
+        t1 += s1[j][cl];
+        t2 += s2[j][cl];
     }
+    const double n = (double)rows;
+    const double d1 = t1 / n;
+    double var = t2 / n - d1 * d1;
+    if (var < 0.0) var = 0.0;
+    mean[c] = (float)((double)bf16_bits_to_f32(x[c]) + d1);
+    inv_std[c] = 1.0f / sqrtf((float)var + eps);
 }
 
 // y = act(gamma * (x - mean) * inv_std + beta); VEC: 8 channels (16 bytes) per thread
@@ -615,13 +658,12 @@ hipError_t launch_bn_train_fwd(const uint16_t* x, int64_t rows, int32_t C, const
                                hipStream_t s) {
     const BnPlan p = plan_bn(rows, C);
     float* p1 = ws;
+    float* p2 = ws + p.chunks * C;
     const unsigned cb = (unsigned)((C + 15) / 16);
-    bn_partial<BN_SUM>(p, x, nullptr, nullptr, rows, C, 0, nullptr, nullptr, p1, nullptr, s);
-    hipLaunchKernelGGL(bn_finalize_kernel<BN_SUM>, dim3(cb), dim3(256), 0, s, p1, nullptr, p.chunks, C, rows, eps,
-                       mean, nullptr);
-    bn_partial<BN_SQDEV>(p, x, nullptr, nullptr, rows, C, 0, mean, nullptr, p1, nullptr, s);
-    hipLaunchKernelGGL(bn_finalize_kernel<BN_SQDEV>, dim3(cb), dim3(256), 0, s, p1, nullptr, p.chunks, C, rows, eps,
-                       inv_std, nullptr);
+    // one pass over x for both statistics (shifted sums), then the per-channel finalize
+    bn_partial<BN_STATS>(p, x, nullptr, nullptr, rows, C, 0, nullptr, nullptr, p1, p2, s);
+    hipLaunchKernelGGL(bn_stats_finalize_kernel, dim3(cb), dim3(256), 0, s, p1, p2, p.chunks, C, rows, eps, x, mean,
+                       inv_std);
     const int64_t total = rows * C;
     if (p.vec)
         hipLaunchKernelGGL(bn_apply_kernel<true>, dim3(blocks_for(total / 8)), dim3(256), 0, s, x, total, C, mean,
@@ -639,8 +681,8 @@ hipError_t launch_bn_train_bwd(const uint16_t* x, const uint16_t* y, const uint1
     float* p1 = ws;
     float* p2 = ws + p.chunks * C;
     bn_partial<BN_BWD>(p, x, y, dy, rows, C, relu, mean, inv_std, p1, p2, s);
-    hipLaunchKernelGGL(bn_finalize_kernel<BN_BWD>, dim3((unsigned)((C + 15) / 16)), dim3(256), 0, s, p1, p2,
-                       p.chunks, C, rows, 0.0f, dbeta, dgamma);
+    hipLaunchKernelGGL(bn_bwd_finalize_kernel, dim3((unsigned)((C + 15) / 16)), dim3(256), 0, s, p1, p2, p.chunks, C,
+                       dbeta, dgamma);
     const int64_t total = rows * C;
     if (p.vec)
         hipLaunchKernelGGL(bn_bwd_apply_kernel<true>, dim3(blocks_for(total / 8)), dim3(256), 0, s, x, y, dy, total, rows,
