@@ -555,12 +555,18 @@ def batchnorm_train_fwd(x, gamma, beta, eps=1e-5, relu=False, ws=None):
     return y, mean, inv_std
 
 
-def batchnorm_train_bwd(x, y, dy, mean, inv_std, gamma, relu=False, ws=None):
+def batchnorm_train_bwd(x, y, dy, mean, inv_std, gamma, relu=False, ws=None, dgamma=None, dbeta=None):
+    """Returns (dx, dgamma, dbeta); `dgamma` / `dbeta` may be caller-provided fp32 [C] outputs
+    (for example views into one flat gradient buffer)."""
     c = x.shape[-1]
     rows = x.numel() // c
     dx = torch.empty_like(x)
-    dgamma = torch.empty(c, dtype=torch.float32, device=x.device)
-    dbeta = torch.empty(c, dtype=torch.float32, device=x.device)
+    if dgamma is None:
+        dgamma = torch.empty(c, dtype=torch.float32, device=x.device)
+    if dbeta is None:
+        dbeta = torch.empty(c, dtype=torch.float32, device=x.device)
+    _numel(dgamma, c, "dgamma")
+    _numel(dbeta, c, "dbeta")
     ws = _bn_ws(rows, c, ws, x.device)
     _call("tbn_batchnorm_train_bwd", _dev(x, "x", (torch.bfloat16,)), _dev(y, "y", (torch.bfloat16,)),
           _dev(dy, "dy", (torch.bfloat16,)), rows, c, 1 if relu else 0, _dev(mean, "mean"),

@@ -401,6 +401,25 @@ class VGGSmall(_Trainer):
             self.convs.append(layer(name, cin, cout, 3, 1, 1, device, stream))
             self.bns.append(BatchNorm(name, cout, device, stream))
         self.fc = TwoBitLayer("fc", 512, 10, 4, 1, 0, device, stream)
+        # every batch-norm parameter, its momentum and its gradient live in three flat
+        # buffers (gamma then beta of each layer), so that one SGD call updates them all
+        # (they share the hyperparameters: no weight decay); the layers hold views
+        total = sum(2 * bn.gamma.numel() for bn in self.bns)
+        self.bn_flat = torch.empty(total, dtype=torch.float32, device=device)
+        self.bn_vflat = torch.zeros(total, dtype=torch.float32, device=device)
+        self.bn_gflat = torch.zeros(total, dtype=torch.float32, device=device)
+        self.bn_grad_views = []
+        off = 0
+        for bn in self.bns:
+            c = bn.gamma.numel()
+            views = []
+            for f, vf in (("gamma", "vg"), ("beta", "vb")):
+                self.bn_flat[off:off + c].copy_(getattr(bn, f))
+                setattr(bn, f, self.bn_flat[off:off + c])
+                setattr(bn, vf, self.bn_vflat[off:off + c])
+                views.append(self.bn_gflat[off:off + c])
+                off += c
+            self.bn_grad_views.append(tuple(views))
 
     def two_bit_layers(self):
         return self.convs[1:] + [self.fc]
@@ -458,7 +477,8 @@ class VGGSmall(_Trainer):
                 rec(trace, "maxpool_bwd", (2, 2, 0), dy=dh, arg=arg, dx=da)
             else:
                 da = dh
-            dzi, dg, db = tbn.batchnorm_train_bwd(z, a, da, mean, inv_std, bn.gamma, relu=True)
+            dzi, dg, db = tbn.batchnorm_train_bwd(z, a, da, mean, inv_std, bn.gamma, relu=True,
+                                                  dgamma=self.bn_grad_views[i][0], dbeta=self.bn_grad_views[i][1])
             if trace is not None:
                 rec(trace, "bn_bwd", bn, x=z, y=a, dy=da, gamma=bn.gamma.clone(), dx=dzi, dgamma=dg, dbeta=db)
             dh, dw = conv.backward(hin, dzi, need_dx=i > 0)
@@ -471,7 +491,17 @@ class VGGSmall(_Trainer):
                 self._sgd(trace, conv.name, conv.w, conv.v, g.view(conv.w.shape), WEIGHT_DECAY)
         self._update_two_bit(trace, self.fc, dwfc.view(self.fc.w.shape), fused)
         self._codes_current = fused
-        for bn, (dg, db) in zip(self.bns, bn_grads):
-            self._sgd(trace, bn.name + ".gamma", bn.gamma, bn.vg, dg, 0.0)
-            self._sgd(trace, bn.name + ".beta", bn.beta, bn.vb, db, 0.0)
+        # every gamma and beta in one call over the flat buffers (the trace still gets one
+        # record per parameter: the update is element-wise)
+        if trace is not None:
+            w0, v0 = self.bn_flat.clone(), self.bn_vflat.clone()
+        tbn.sgd_step(self.bn_flat, self.bn_vflat, self.bn_gflat, self.lr, MOMENTUM, 0.0)
+        if trace is not None:
+            off = 0
+            for bn, (dg, db) in zip(self.bns, bn_grads):
+                for f, vf, g in (("gamma", "vg", dg), ("beta", "vb", db)):
+                    c = g.numel()
+                    self._rec(trace, "sgd", (bn.name + "." + f, 0.0), w=w0[off:off + c], v=v0[off:off + c], g=g,
+                              w_new=getattr(bn, f), v_new=getattr(bn, vf))
+                    off += c
         return loss
