@@ -5,14 +5,17 @@
 // buy nothing; what costs time is latency (filter decode, input gather, output store in
 // sequence).  Here every thread owns one output pixel and 8 consecutive filters:
 //   * a block (four waves) covers 64 pixels and 32 filters; its filters are decoded once
-//     from the packed codes into LDS as fp32 +-1 / +-2 (element-major, so the 8 weights a
-//     thread needs for one element are one 32-byte broadcast read: every lane of a wave
-//     reads the same filters);
+//     from the packed codes into LDS as bf16 +-1 / +-2, two consecutive elements per 32-bit
+//     word (pair-major, so the 8 weight pairs a thread needs for two elements are one
+//     32-byte broadcast read: every lane of a wave reads the same filters);
 //   * the thread issues its loads of the filter codes, then those of the first input rows
 //     (zero outside the image; fp32 input rounded to bf16, nearest even, as in every other
 //     forward kernel); the block decodes its filters as soon as the codes land, the rest of
 //     the input loads go out after the barrier, and the values are accumulated against the
-//     weights with fp32 FMAs (products exact, sums fp32) as they arrive;
+//     weights two elements at a time with v_dot2_f32_bf16 (the bf16 pair of inputs against
+//     a pair of weights: products exact, sums fp32) as they arrive; against one fp32 FMA per
+//     element this halves both the vector instructions and the LDS broadcast bytes, which
+//     bound the kernel;
 //   * alpha (the column scale) and the optional scale, bias, residual and ReLU are applied
 //     in fp32 and the 8 outputs written with 16-byte stores.
 #include "tbn_device.h"
@@ -21,6 +24,12 @@
 namespace tbn {
 
 namespace {
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// the word as a bf16 pair (taken by value: a bit cast applied to a vector element in place
+// reads the vector's first element)
+__device__ __forceinline__ bf16x2 as_bf16x2(uint32_t v) { return __builtin_bit_cast(bf16x2, v); }
 
 constexpr int DPIX = 64;   // output pixels per block (one per lane)
 constexpr int DFB = 32;    // filters per block (8 per wave)
@@ -31,8 +40,9 @@ constexpr int DMAXN = 147;  // filter elements R*S*C
 template <int R, int S, int C, bool X32>
 __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) {
     constexpr int n = R * S * C;
+    constexpr int np = (n + 1) / 2;  // element pairs (the last one zero-padded for odd n)
     static_assert(n <= DMAXN, "filter elements");
-    __shared__ __attribute__((aligned(16))) float wl[n * DFB];  // [element][filter]
+    __shared__ __attribute__((aligned(16))) uint32_t wl[np * DFB];  // [pair][filter], bf16 x 2
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int grp = __builtin_amdgcn_readfirstlane(tid >> 6);  // filter group of the wave
@@ -41,15 +51,16 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
 
     // the block's filters: element e of filter kb0 + f is bit (e % 16) / 2 (+ 16 for odd e)
     // of word (e % 64) / 16 of the filter's 16-byte code row in chunk e / 64 (magnitude),
-    // the bit 8 above it the sign; weights of filters past Kf are zero.  The code loads go
-    // out first, so that the decode waits for them alone (vector loads complete in order).
-    constexpr int DITER = (n * DFB + 255) / 256;
+    // the bit 8 above it the sign, so both elements of pair j (2 j and 2 j + 1) sit in one
+    // word; weights of filters past Kf are zero.  The code loads go out first, so that the
+    // decode waits for them alone (vector loads complete in order).
+    constexpr int DITER = (np * DFB + 255) / 256;
     uint32_t cw[DITER];
 #pragma unroll
     for (int it = 0; it < DITER; ++it) {
         const int i = tid + 256 * it;
-        const int e = i >> 5, k = kb0 + (i & (DFB - 1));
-        cw[it] = i < n * DFB && k < a.Kf
+        const int e = 2 * (i >> 5), k = kb0 + (i & (DFB - 1));
+        cw[it] = i < np * DFB && k < a.Kf
                      ? a.codes[((int64_t)((k >> 6) * nchunks + (e >> 6)) * 64 + (k & 63)) * 4 + ((e & 63) >> 4)]
                      : 0u;
     }
@@ -96,11 +107,20 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
 #pragma unroll
     for (int it = 0; it < DITER; ++it) {
         const int i = tid + 256 * it;
-        if (i < n * DFB) {
-            const int e = i >> 5, k = kb0 + (i & (DFB - 1));
-            const int jj = (e & 15) >> 1, hh = e & 1;
-            const uint32_t mag = (cw[it] >> (16 * hh + jj)) & 1u, sg = (cw[it] >> (16 * hh + 8 + jj)) & 1u;
-            wl[i] = k < a.Kf ? (mag ? 2.0f : 1.0f) * (sg ? -1.0f : 1.0f) : 0.0f;
+        if (i < np * DFB) {
+            const int e = 2 * (i >> 5);
+            const int jj = (e & 15) >> 1;
+            // bf16 of +-1 / +-2: 0x3F80 or 0x4000 for the magnitude bit, 0x8000 for the sign;
+            // a filter past Kf has an all-zero code word but must weigh zero, as must the
+            // padding element of an odd n
+            auto wbits = [&](int hh) -> uint32_t {
+                const uint32_t mag = (cw[it] >> (16 * hh + jj)) & 1u, sg = (cw[it] >> (16 * hh + 8 + jj)) & 1u;
+                return (mag ? 0x4000u : 0x3F80u) | (sg << 15);
+            };
+            const bool live_k = kb0 + (i & (DFB - 1)) < a.Kf;
+            const uint32_t lo = live_k ? wbits(0) : 0u;
+            const uint32_t hi = live_k && e + 1 < n ? wbits(1) : 0u;
+            wl[i] = lo | (hi << 16);
         }
     }
     __syncthreads();
@@ -111,32 +131,35 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
     if (!live || k0 >= a.Kf) return;  // no barrier follows
 
     float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    const float* wg = wl + 8 * grp;
-#pragma unroll
-    for (int e = 0; e < n; ++e) {
-        // weights read four elements at a time (the fence keeps the compiler from hoisting
-        // all of them, which would cost ~200 registers and occupancy)
-        if (e % 4 == 0) __builtin_amdgcn_sched_barrier(0);
-        // the 8 weights of element e: the same address in every lane (broadcast)
-        const f32x4 lo = *reinterpret_cast<const f32x4*>(wg + e * DFB);
-        const f32x4 hi = *reinterpret_cast<const f32x4*>(wg + e * DFB + 4);
-        // fp32 input rounded to bf16 (nearest even), as in every other forward kernel
-        float xv_e;
+    const uint32_t* wg = wl + 8 * grp;
+    // fp32 input rounded to bf16 (nearest even), as in every other forward kernel
+    auto xbits = [&](int e) -> uint32_t {
+        if (e >= n) return 0u;
         if constexpr (X32)
-            xv_e = bf16_bits_to_f32(f32_to_bf16_bits(__uint_as_float(xb[e])));
+            return f32_to_bf16_bits(__uint_as_float(xb[e]));
         else
-            xv_e = bf16_bits_to_f32(xb[e]);
-        acc[0] = fmaf(xv_e, lo.x, acc[0]);
-        acc[1] = fmaf(xv_e, lo.y, acc[1]);
-        acc[2] = fmaf(xv_e, lo.z, acc[2]);
-        acc[3] = fmaf(xv_e, lo.w, acc[3]);
-        acc[4] = fmaf(xv_e, hi.x, acc[4]);
-        acc[5] = fmaf(xv_e, hi.y, acc[5]);
-        acc[6] = fmaf(xv_e, hi.z, acc[6]);
-        acc[7] = fmaf(xv_e, hi.w, acc[7]);
-        if (e % 4 == 3 || e == n - 1) {
-            // the sums so far are materialised here, so the FMAs cannot be moved past the
-            // next reads (which would keep every weight of the filter live at once)
+            return xb[e];
+    };
+#pragma unroll
+    for (int j2 = 0; j2 < np; ++j2) {
+        // weights read two pairs at a time (the fence keeps the compiler from hoisting all
+        // of them, which would cost ~150 registers and occupancy)
+        if (j2 % 2 == 0) __builtin_amdgcn_sched_barrier(0);
+        // the 8 weight pairs of elements 2 j2, 2 j2 + 1: the same address in every lane
+        const u32x4 lo = *reinterpret_cast<const u32x4*>(wg + j2 * DFB);
+        const u32x4 hi = *reinterpret_cast<const u32x4*>(wg + j2 * DFB + 4);
+        const bf16x2 xp = as_bf16x2(xbits(2 * j2) | (xbits(2 * j2 + 1) << 16));
+        acc[0] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(lo.x), acc[0], false);
+        acc[1] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(lo.y), acc[1], false);
+        acc[2] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(lo.z), acc[2], false);
+        acc[3] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(lo.w), acc[3], false);
+        acc[4] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(hi.x), acc[4], false);
+        acc[5] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(hi.y), acc[5], false);
+        acc[6] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(hi.z), acc[6], false);
+        acc[7] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(hi.w), acc[7], false);
+        if (j2 % 2 == 1 || j2 == np - 1) {
+            // the sums so far are materialised here, so the products cannot be moved past
+            // the next reads (which would keep every weight of the filter live at once)
 #pragma unroll
             for (int j = 0; j < 8; ++j) asm volatile("" : "+v"(acc[j]));
         }
@@ -203,12 +226,13 @@ static const void* direct_kernel(int R, int S, int C, bool x32) {
 
 bool conv_direct_eligible(const ConvGemmArgs& a) {
     // forward pass with packed codes, a compiled filter shape (at most 147 elements, C <= 8),
-    // and little work in total (at most 2^28 multiply-adds: beyond that the matrix-core
-    // kernels win)
+    // and little work in total (at most 2^27 multiply-adds: beyond that the matrix-core
+    // kernels win; the 7x7 RGB stem, 1.2e8 multiply-adds per image, measured 17 against 22 us
+    // at batch 1 and 27 against 22 us at batch 2)
     const int64_t n = (int64_t)a.R * a.S * a.C;
     const int64_t macs = (int64_t)a.N * a.P * a.Q * a.Kf * n;
     return !a.apair && !a.wdense && direct_kernel(a.R, a.S, a.C, a.x_f32 != 0) != nullptr &&
-           macs <= (1ll << 28) && (int64_t)a.N * a.P * a.Q < 0x7FFFFFFFll &&
+           macs <= (1ll << 27) && (int64_t)a.N * a.P * a.Q < 0x7FFFFFFFll &&
            (int64_t)a.N * a.H * a.W * a.C < 0x7FFFFFFFll;
 }
 
