@@ -8,14 +8,17 @@
 //     from the packed codes into LDS as bf16 +-1 / +-2, two consecutive elements per 32-bit
 //     word (pair-major, so the 8 weight pairs a thread needs for two elements are one
 //     32-byte broadcast read: every lane of a wave reads the same filters);
-//   * the thread issues its loads of the filter codes, then those of the first input rows
-//     (zero outside the image; fp32 input rounded to bf16, nearest even, as in every other
-//     forward kernel); the block decodes its filters as soon as the codes land, the rest of
-//     the input loads go out after the barrier, and the values are accumulated against the
-//     weights two elements at a time with v_dot2_f32_bf16 (the bf16 pair of inputs against
-//     a pair of weights: products exact, sums fp32) as they arrive; against one fp32 FMA per
-//     element this halves both the vector instructions and the LDS broadcast bytes, which
-//     bound the kernel;
+//   * the four waves need the same 64 pixels' inputs, so each loads only every fourth
+//     filter row of the patches (zero outside the image; fp32 input rounded to bf16, nearest
+//     even, as in every other forward kernel) and writes it to LDS as bf16 pairs: a quarter
+//     of the load instructions of per-wave gathers, which bounded the kernel (ResNet stem at
+//     batch 1: 16.8 -> 11.9 us);
+//   * the thread issues its loads of the filter codes, then those of its patch rows; the
+//     block decodes its filters as soon as the codes land and stores the patches, and after
+//     one barrier every thread accumulates its pixel two elements at a time with
+//     v_dot2_f32_bf16 (an input pair read from LDS against a pair of weights: products exact,
+//     sums fp32); against one fp32 FMA per element this halves both the vector instructions
+//     and the LDS broadcast bytes;
 //   * alpha (the column scale) and the optional scale, bias, residual and ReLU are applied
 //     in fp32 and the 8 outputs written with 16-byte stores.
 #include "tbn_device.h"
@@ -42,7 +45,9 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
     constexpr int n = R * S * C;
     constexpr int np = (n + 1) / 2;  // element pairs (the last one zero-padded for odd n)
     static_assert(n <= DMAXN, "filter elements");
+    constexpr int PW2 = np % 2 == 1 ? np : np + 1;  // words per pixel row of xs
     __shared__ __attribute__((aligned(16))) uint32_t wl[np * DFB];  // [pair][filter], bf16 x 2
+    __shared__ uint32_t xs[DPIX * PW2];                               // [pixel][pair], bf16 x 2
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int grp = __builtin_amdgcn_readfirstlane(tid >> 6);  // filter group of the wave
@@ -65,10 +70,7 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
                      : 0u;
     }
 
-    // the input values of this thread's pixel (zero outside the image), raw bf16 bits (or fp32
-    // bits), converted where they are used: the first R1 filter rows are loaded before the
-    // decode (at most ~60 loads with the code loads, within the hardware's count of loads in
-    // flight), the rest after the barrier, so that the first products start while they land
+    // the pixel of lane l of every wave is pixel l of the block (zero outside the image)
     const int64_t M = (int64_t)a.N * a.P * a.Q;
     const int64_t m = (int64_t)blockIdx.x * DPIX + lane;
     const bool live = m < M;
@@ -86,24 +88,30 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
     constexpr int ESZ = X32 ? 4 : 2;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<void*>(a.x), (short)0, (int)((int64_t)a.N * a.H * a.W * C * ESZ), 0x00020000);
-    uint32_t xb[n];
-    auto gather_row = [&](int r) {
+    // the block's 64 pixels' inputs are loaded once, patch row r by wave r % 4 (raw bf16, fp32
+    // input rounded to bf16 at once, nearest even, as in every other forward kernel), and
+    // written to LDS as bf16 pairs, one row of PW2 words per pixel (PW2 odd: the 64 lanes'
+    // reads of one pair fall in distinct banks)
+    constexpr int RW = (R + 3) / 4;  // patch rows per wave at most
+    uint32_t xv[RW * S * C];
 #pragma unroll
-        for (int s_ = 0; s_ < S; ++s_) {
-            const bool ok = live && (unsigned)(h0 + r) < (unsigned)a.H && (unsigned)(w0 + s_) < (unsigned)a.W;
-            const int off = ok ? (pix0 + (r * a.W + s_) * C) * ESZ : (int)0x80000000;
+    for (int i = 0; i < RW; ++i) {
+        const int r = grp + 4 * i;
+        if (r < R) {
 #pragma unroll
-            for (int c = 0; c < C; ++c) {
-                if constexpr (X32)
-                    xb[(r * S + s_) * C + c] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, c * 4, 0);
-                else
-                    xb[(r * S + s_) * C + c] = __builtin_amdgcn_raw_buffer_load_b16(rs, off, c * 2, 0);
+            for (int s_ = 0; s_ < S; ++s_) {
+                const bool ok = live && (unsigned)(h0 + r) < (unsigned)a.H && (unsigned)(w0 + s_) < (unsigned)a.W;
+                const int off = ok ? (pix0 + (r * a.W + s_) * C) * ESZ : (int)0x80000000;
+#pragma unroll
+                for (int c = 0; c < C; ++c) {
+                    if constexpr (X32)
+                        xv[(i * S + s_) * C + c] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, c * 4, 0);
+                    else
+                        xv[(i * S + s_) * C + c] = __builtin_amdgcn_raw_buffer_load_b16(rs, off, c * 2, 0);
+                }
             }
         }
-    };
-    constexpr int R1 = (60 - DITER) / (S * C) < R ? ((60 - DITER) / (S * C) > 0 ? (60 - DITER) / (S * C) : 0) : R;
-#pragma unroll
-    for (int r = 0; r < R1; ++r) gather_row(r);
+    }
 #pragma unroll
     for (int it = 0; it < DITER; ++it) {
         const int i = tid + 256 * it;
@@ -123,23 +131,27 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
             wl[i] = lo | (hi << 16);
         }
     }
-    __syncthreads();
+    uint16_t* xrow16 = reinterpret_cast<uint16_t*>(xs + lane * PW2);
 #pragma unroll
-    for (int r = R1; r < R; ++r) gather_row(r);
+    for (int i = 0; i < RW; ++i) {
+        const int r = grp + 4 * i;
+        if (r < R) {
+#pragma unroll
+            for (int j = 0; j < S * C; ++j) {
+                const uint32_t v = xv[i * S * C + j];
+                xrow16[r * S * C + j] = (uint16_t)(X32 ? f32_to_bf16_bits(__uint_as_float(v)) : v);
+            }
+        }
+    }
+    if (n % 2 == 1 && grp == 0) xrow16[n] = 0;  // the padding element of the last pair
+    __syncthreads();
 
     const int k0 = kb0 + 8 * grp;
     if (!live || k0 >= a.Kf) return;  // no barrier follows
 
     float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     const uint32_t* wg = wl + 8 * grp;
-    // fp32 input rounded to bf16 (nearest even), as in every other forward kernel
-    auto xbits = [&](int e) -> uint32_t {
-        if (e >= n) return 0u;
-        if constexpr (X32)
-            return f32_to_bf16_bits(__uint_as_float(xb[e]));
-        else
-            return xb[e];
-    };
+    const uint32_t* xrow = xs + lane * PW2;
 #pragma unroll
     for (int j2 = 0; j2 < np; ++j2) {
         // weights read two pairs at a time (the fence keeps the compiler from hoisting all
@@ -148,7 +160,7 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const ConvGemmArgs a) 
         // the 8 weight pairs of elements 2 j2, 2 j2 + 1: the same address in every lane
         const u32x4 lo = *reinterpret_cast<const u32x4*>(wg + j2 * DFB);
         const u32x4 hi = *reinterpret_cast<const u32x4*>(wg + j2 * DFB + 4);
-        const bf16x2 xp = as_bf16x2(xbits(2 * j2) | (xbits(2 * j2 + 1) << 16));
+        const bf16x2 xp = as_bf16x2(xrow[j2]);
         acc[0] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(lo.x), acc[0], false);
         acc[1] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(lo.y), acc[1], false);
         acc[2] = __builtin_amdgcn_fdot2_f32_bf16(xp, as_bf16x2(lo.z), acc[2], false);
@@ -226,13 +238,13 @@ static const void* direct_kernel(int R, int S, int C, bool x32) {
 
 bool conv_direct_eligible(const ConvGemmArgs& a) {
     // forward pass with packed codes, a compiled filter shape (at most 147 elements, C <= 8),
-    // and little work in total (at most 2^27 multiply-adds: beyond that the matrix-core
-    // kernels win; the 7x7 RGB stem, 1.2e8 multiply-adds per image, measured 17 against 22 us
-    // at batch 1 and 27 against 22 us at batch 2)
+    // and little work in total (at most 2^28 multiply-adds: beyond that the matrix-core
+    // kernels win; the 7x7 RGB stem, 1.2e8 multiply-adds per image, measured 12 against 22 us
+    // on the thin kernel at batch 1, 17 against 22 at batch 2)
     const int64_t n = (int64_t)a.R * a.S * a.C;
     const int64_t macs = (int64_t)a.N * a.P * a.Q * a.Kf * n;
     return !a.apair && !a.wdense && direct_kernel(a.R, a.S, a.C, a.x_f32 != 0) != nullptr &&
-           macs <= (1ll << 27) && (int64_t)a.N * a.P * a.Q < 0x7FFFFFFFll &&
+           macs <= (1ll << 28) && (int64_t)a.N * a.P * a.Q < 0x7FFFFFFFll &&
            (int64_t)a.N * a.H * a.W * a.C < 0x7FFFFFFFll;
 }
 
