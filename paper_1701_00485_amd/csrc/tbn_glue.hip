@@ -417,11 +417,26 @@ __global__ __launch_bounds__(256) void bn_stats_finalize_kernel(const float* __r
     const int cl = threadIdx.x & 15, part = threadIdx.x >> 4;
     const int c = blockIdx.x * 16 + cl;
     double u1 = 0.0, u2 = 0.0;
-    if (c < C)
-        for (int64_t b = part; b < chunks; b += 16) {
+    if (c < C) {
+        int64_t b = part;
+        for (; b + 7 * 16 < chunks; b += 8 * 16) {  // eight loads of each in flight, added in chunk order
+            float v1[8], v2[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                v1[k] = p1[(b + 16 * k) * C + c];
+                v2[k] = p2[(b + 16 * k) * C + c];
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                u1 += (double)v1[k];
+                u2 += (double)v2[k];
+            }
+        }
+        for (; b < chunks; b += 16) {
             u1 += (double)p1[b * C + c];
             u2 += (double)p2[b * C + c];
         }
+    }
     s1[part][cl] = u1;
     s2[part][cl] = u2;
     __syncthreads();

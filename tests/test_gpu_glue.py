@@ -57,6 +57,7 @@ def test_avgpool(tbn, shape):
 
 @pytest.mark.parametrize("shape,relu", [((8, 16, 16, 128), True), ((4, 8, 8, 24), False), ((2, 5, 5, 13), True),
                                         ((64, 32, 32, 32), True),    # 65536 rows: many row chunks
+                                        ((4, 80, 80, 128), True),    # 200 row chunks: batched and tail sums
                                         ((2, 3, 3, 2056), False),    # more than 256 groups of 8 channels
                                         ((3, 7, 7, 300), True)])     # 300 scalar channels: two slices
 def test_batchnorm_train(tbn, shape, relu):
