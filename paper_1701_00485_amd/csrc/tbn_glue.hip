@@ -188,6 +188,52 @@ __global__ __launch_bounds__(256) void maxpool_bwd_kernel(const PoolArgs a, cons
     }
 }
 
+// The same gather over 8-channel groups with 32-bit multiply-shift index splits (sizes below
+// 2^31): the kernel above spends most of its instructions on 64-bit divisions.
+__global__ __launch_bounds__(256) void maxpool_bwd8_kernel(const PoolArgs a, const FastDiv div_g, const FastDiv div_w,
+                                                           const FastDiv div_h, const uint32_t groups,
+                                                           const uint16_t* __restrict__ dy,
+                                                           const int32_t* __restrict__ arg, void* __restrict__ dx,
+                                                           int dx_f32) {
+    const uint32_t gi = blockIdx.x * 256u + threadIdx.x;  // (input pixel, 8-channel group)
+    if (gi >= groups) return;
+    const uint32_t pix = fdiv(gi, div_g);
+    const uint32_t c = (gi - pix * (uint32_t)(a.C / 8)) * 8u;
+    const uint32_t nh = fdiv(pix, div_w);
+    const int w = (int)(pix - nh * (uint32_t)a.W);
+    const uint32_t n = fdiv(nh, div_h);
+    const int h = (int)(nh - n * (uint32_t)a.H);
+    const int me = h * a.W + w;
+    const int p_lo = max(0, (h + a.pad - a.k + a.s) / a.s), p_hi = min(a.P - 1, (h + a.pad) / a.s);
+    const int q_lo = max(0, (w + a.pad - a.k + a.s) / a.s), q_hi = min(a.Q - 1, (w + a.pad) / a.s);
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+    for (int p = p_lo; p <= p_hi; ++p)
+        for (int q = q_lo; q <= q_hi; ++q) {
+            const uint32_t o = ((n * (uint32_t)a.P + (uint32_t)p) * (uint32_t)a.Q + (uint32_t)q) * (uint32_t)a.C + c;
+            const u32x4 a0 = *reinterpret_cast<const u32x4*>(arg + o);
+            const u32x4 a1 = *reinterpret_cast<const u32x4*>(arg + o + 4);
+            const u32x4 d = *reinterpret_cast<const u32x4*>(dy + o);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t ae = e < 4 ? a0[e] : a1[e - 4];
+                const uint32_t db = (e & 1) ? (d[e / 2] >> 16) : (d[e / 2] & 0xFFFFu);
+                if ((int)ae == me) acc[e] += bf16_bits_to_f32(db);
+            }
+        }
+    const uint32_t i = gi * 8u;
+    if (dx_f32) {
+        float* dp = reinterpret_cast<float*>(dx) + i;
+        *reinterpret_cast<f32x4*>(dp) = f32x4{acc[0], acc[1], acc[2], acc[3]};
+        *reinterpret_cast<f32x4*>(dp + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
+    } else {
+        *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(dx) + i) =
+            u32x4{pack_bf16x2(acc[0], acc[1]), pack_bf16x2(acc[2], acc[3]), pack_bf16x2(acc[4], acc[5]),
+                  pack_bf16x2(acc[6], acc[7])};
+    }
+}
+
 // y[n][c] = mean over h, w of x[n][h][w][c]; one thread per (n, c)
 __global__ __launch_bounds__(256) void avgpool_kernel(int32_t N, int32_t HW, int32_t C, const uint16_t* __restrict__ x,
                                                       void* __restrict__ y, int y_f32) {
@@ -622,7 +668,13 @@ hipError_t launch_maxpool_fwd(const PoolArgs& a, const uint16_t* x, uint16_t* y,
 hipError_t launch_maxpool_bwd(const PoolArgs& a, const uint16_t* dy, const int32_t* arg, void* dx, int dx_f32,
                               hipStream_t s) {
     const int64_t total = (int64_t)a.N * a.H * a.W * a.C;
-    if (a.C % 8 == 0)
+    const int64_t out_total = (int64_t)a.N * a.P * a.Q * a.C;
+    if (a.C % 8 == 0 && total < 0x7FFFFFFFll && out_total < 0x7FFFFFFFll) {
+        const uint32_t groups = (uint32_t)(total / 8);
+        hipLaunchKernelGGL(maxpool_bwd8_kernel, dim3(blocks_for(groups)), dim3(256), 0, s, a,
+                           make_fastdiv((uint32_t)(a.C / 8)), make_fastdiv((uint32_t)a.W), make_fastdiv((uint32_t)a.H),
+                           groups, dy, arg, dx, dx_f32);
+    } else if (a.C % 8 == 0)
         hipLaunchKernelGGL(maxpool_bwd_kernel<8>, dim3(blocks_for(total / 8)), dim3(256), 0, s, a, dy, arg, dx, dx_f32);
     else
         hipLaunchKernelGGL(maxpool_bwd_kernel<1>, dim3(blocks_for(total)), dim3(256), 0, s, a, dy, arg, dx, dx_f32);
