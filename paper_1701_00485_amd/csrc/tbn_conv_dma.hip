@@ -48,62 +48,65 @@ struct StageLayout {
 };
 
 // Sum of the split-K partials of outputs (row, col0 .. col0 + 7) in split order, then the
-// epilogue (partial rows are Kp = round_up(Kf, 8) wide; columns past Kf are skipped).
+// epilogue (partial rows are Kp = round_up(Kf, 8) wide; columns past Kf are skipped).  The
+// column factors and the residual are loaded first, then the partials eight splits at a
+// time (the last batch masked, its missing terms zero), so that a thread waits for memory
+// about once per eight splits rather than once per split of the tail.
 __device__ __forceinline__ void split_epilogue_group(const ConvGemmArgs& a, int64_t M, int64_t row, int col0) {
     const int Kf = a.Kf;
     const int Kp = (Kf + 7) & ~7;
     const int64_t po = row * Kp + col0;
-    float v8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    auto add = [&](const f32x4& lo, const f32x4& hi) {
-        v8[0] += lo.x; v8[1] += lo.y; v8[2] += lo.z; v8[3] += lo.w;
-        v8[4] += hi.x; v8[5] += hi.y; v8[6] += hi.z; v8[7] += hi.w;
-    };
-    // eight splits' loads in flight at a time, added in split order
-    int z = 0;
-    for (; z + 8 <= a.splits; z += 8) {
-        f32x4 lo[8], hi[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const float* pp = a.partial + (int64_t)(z + u) * M * Kp + po;
-            lo[u] = *reinterpret_cast<const f32x4*>(pp);
-            hi[u] = *reinterpret_cast<const f32x4*>(pp + 4);
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) add(lo[u], hi[u]);
-    }
-    for (; z < a.splits; ++z) {
-        const float* pp = a.partial + (int64_t)z * M * Kp + po;
-        add(*reinterpret_cast<const f32x4*>(pp), *reinterpret_cast<const f32x4*>(pp + 4));
-    }
-    const bool full = col0 + 8 <= Kf;  // all 8 columns real (always when Kf % 8 == 0)
     const int64_t o = row * Kf + col0;
+    const bool full = col0 + 8 <= Kf;  // all 8 columns real (always when Kf % 8 == 0)
+    float sc[8], bi[8], rs[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         const int col = col0 + e < Kf ? col0 + e : Kf - 1;  // past Kf: computed, never stored
-        float sc = a.colscale ? a.colscale[col] : 1.0f;
-        if (a.scale) sc *= a.scale[col];
-        v8[e] = v8[e] * sc + (a.bias ? a.bias[col] : 0.0f);
+        sc[e] = a.colscale ? a.colscale[col] : 1.0f;
+        if (a.scale) sc[e] *= a.scale[col];
+        bi[e] = a.bias ? a.bias[col] : 0.0f;
+        rs[e] = 0.0f;
     }
     if (a.residual) {
         if (a.y_f32) {
             const float* rp = reinterpret_cast<const float*>(a.residual) + o;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                if (col0 + e < Kf) v8[e] += rp[e];
+                if (col0 + e < Kf) rs[e] = rp[e];
         } else if (full && (Kf % 8) == 0) {
             const u32x4 r8 = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.residual) + o);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                v8[2 * e] += bf16_bits_to_f32(r8[e] & 0xFFFFu);
-                v8[2 * e + 1] += bf16_bits_to_f32(r8[e] >> 16);
+                rs[2 * e] = bf16_bits_to_f32(r8[e] & 0xFFFFu);
+                rs[2 * e + 1] = bf16_bits_to_f32(r8[e] >> 16);
             }
         } else {
             const uint16_t* rp = reinterpret_cast<const uint16_t*>(a.residual) + o;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                if (col0 + e < Kf) v8[e] += bf16_bits_to_f32(rp[e]);
+                if (col0 + e < Kf) rs[e] = bf16_bits_to_f32(rp[e]);
         }
     }
+    float v8[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    for (int z = 0; z < a.splits; z += 8) {
+        f32x4 lo[8], hi[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            lo[u] = hi[u] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            if (z + u < a.splits) {
+                const float* pp = a.partial + (int64_t)(z + u) * M * Kp + po;
+                lo[u] = *reinterpret_cast<const f32x4*>(pp);
+                hi[u] = *reinterpret_cast<const f32x4*>(pp + 4);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            v8[0] += lo[u].x; v8[1] += lo[u].y; v8[2] += lo[u].z; v8[3] += lo[u].w;
+            v8[4] += hi[u].x; v8[5] += hi[u].y; v8[6] += hi[u].z; v8[7] += hi[u].w;
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v8[e] = v8[e] * sc[e] + bi[e] + rs[e];
     if (a.relu) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) v8[e] = fmaxf(v8[e], 0.0f);
